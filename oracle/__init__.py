@@ -1,0 +1,25 @@
+"""CPU oracle of the masked co-adaptive MoE layer -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, obviously correct float64 (NumPy) and pure-Python statement of
+what the masked MoE hot path computes, written from the paper:
+
+* ``routing``  -- router logits and softmax (Section 3.1), Top-K with the
+  plain rule (Eq. 1), the hard binary mask of training (Eq. 2) and the soft
+  prior of inference (Eq. 4), the two gate rules (Section 3.1);
+* ``ffn``      -- the expert FFN (SwiGLU) and the gate-weighted combine with
+  shared experts (Eq. 1 and Section 3.1);
+* ``cache``    -- the per-layer expert cache of the trace simulator and the
+  hit-rate / fetches-per-token metrics (Section 4.1, Eq. 5).
+
+It shares no code with the HIP path and imports nothing from it. Only the
+tests, the smoke check and the benchmark's CPU-baseline leg may import it;
+the product path never does.
+
+Parity pins: every function here is pinned by the CPU test suite
+(brute-force Top-K, closed forms, invariants, library routines and
+hand-worked cache traces). The fetch counts of synthetic traces at
+particular prior strengths have no value printed in the paper to compare
+with; they are pinned only through the cache rules above.
+"""
+
+from . import cache, ffn, routing  # noqa: F401

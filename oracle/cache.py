@@ -1,0 +1,105 @@
+"""Oracle: per-layer expert cache of the trace simulator (pure Python). Test infrastructure only.
+
+Section 4.1 (Simulation): each layer keeps a cache of B routed experts
+(K <= B < E; B >= E is accepted and then never evicts). Caches start empty
+unless a state is given, initial fills count as misses, every miss is one
+fetch, and a full cache evicts one entry per miss. Shared experts are not
+part of the trace. Eq. 5: h_{l,t} counts the selected experts already
+cached, f_{l,t} = K - h_{l,t} counts the misses,
+HR = sum h / (N L K) and Fetches/tok = sum f / N, so Fetches/tok = L K (1 - HR).
+
+Least-recently-used policy, with these readings of what the paper leaves
+open:
+* within one step, the hits are touched first, in ascending expert index,
+  then the misses are inserted in ascending expert index; a miss evicts the
+  least recently used cached expert that is not selected at this step;
+* a trace entry outside [0, E) or repeating an earlier entry of the same
+  step is skipped (it counts neither as hit nor as miss) and reported;
+* a cache state lists the cached experts from least to most recently used.
+"""
+
+from __future__ import annotations
+
+from typing import Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+
+def step_set(entries: Iterable[int], E: int) -> Tuple[List[int], bool]:
+    """Distinct in-range experts of one step, ascending; and whether any entry was skipped."""
+    seen: List[int] = []
+    bad = False
+    for e in entries:
+        e = int(e)
+        if e < 0 or e >= E or e in seen:
+            bad = True
+            continue
+        seen.append(e)
+    return sorted(seen), bad
+
+
+def lru_stream(steps: Sequence[Sequence[int]], E: int, B: int,
+               state: Optional[Sequence[int]] = None):
+    """Replay one (layer, stream) trace through a B-slot LRU cache.
+
+    Returns ``(f, h, final_state, bad)``: per-step miss and hit counts,
+    the final cache (least to most recently used) and whether any entry was
+    skipped.
+    """
+    cache: List[int] = [int(e) for e in (state or []) if int(e) >= 0]
+    f: List[int] = []
+    h: List[int] = []
+    bad_any = False
+    for entries in steps:
+        A, bad = step_set(entries, E)
+        bad_any |= bad
+        hits = [e for e in A if e in cache]
+        misses = [e for e in A if e not in cache]
+        for e in hits:                      # touch: becomes most recently used
+            cache.remove(e)
+            cache.append(e)
+        for e in misses:
+            if len(cache) >= B:
+                victim = next(c for c in cache if c not in A)
+                cache.remove(victim)
+            cache.append(e)
+        h.append(len(hits))
+        f.append(len(misses))
+    return f, h, cache, bad_any
+
+
+def cache_fetches(trace: np.ndarray, E: int, B: int, state: Optional[np.ndarray] = None):
+    """Replay a trace [L,S,N,K] with one independent cache per (layer, stream).
+
+    ``state`` is an optional ``[L,S,B]`` int array of initial caches (least
+    to most recently used, -1 = empty slot). Returns ``fetches [L,S]``,
+    ``hits [L,S]`` (int64), ``f_per_step [L,S,N]`` (uint8), the final state
+    ``[L,S,B]`` and whether any trace entry was skipped.
+    """
+    trace = np.asarray(trace)
+    L, S, N, K = trace.shape
+    fetches = np.zeros((L, S), dtype=np.int64)
+    hits = np.zeros((L, S), dtype=np.int64)
+    fps = np.zeros((L, S, N), dtype=np.uint8)
+    final = np.full((L, S, B), -1, dtype=np.int32)
+    bad_any = False
+    for l in range(L):
+        for s in range(S):
+            init = None if state is None else [int(e) for e in state[l, s] if e >= 0]
+            f, h, c, bad = lru_stream(trace[l, s].tolist(), E, B, init)
+            fetches[l, s] = sum(f)
+            hits[l, s] = sum(h)
+            fps[l, s] = f
+            final[l, s, :len(c)] = c
+            bad_any |= bad
+    return fetches, hits, fps, final, bad_any
+
+
+def hit_rate(total_hits: int, N: int, L: int, K: int) -> float:
+    """HR = (1 / (N L K)) * sum_l sum_t h_{l,t}  (Eq. 5)."""
+    return total_hits / (N * L * K)
+
+
+def fetches_per_token(total_fetches: int, N: int) -> float:
+    """Fetches/tok = (1 / N) * sum_l sum_t f_{l,t}  (Eq. 5): summed over layers, averaged over steps."""
+    return total_fetches / N

@@ -1,0 +1,202 @@
+"""Pins of the cache oracle against things other than itself (CPU only).
+
+* a hand-worked LRU trace (``tests/golden/lru_hand_trace.txt``);
+* closed forms: with B = K a step misses exactly the experts not selected at
+  the previous step; with B >= E only first uses miss;
+* per-step rules of Section 4.1 and Eq. 5: f <= K, f = K - h, the misses
+  are the selected experts absent from the previous cache state, and
+  Fetches/tok = L K (1 - HR); the paper's Table 2 obeys the same identity;
+* a second LRU written here with explicit time stamps agrees on random
+  traces;
+* a trace split in two and resumed from the saved state equals the whole.
+"""
+
+import numpy as np
+import pytest
+
+from conftest import golden_path
+from oracle import cache as C
+from paper_2609_34077_amd import synth
+
+
+def _read_hand_trace():
+    info, steps, section = {}, [], None
+    with open(golden_path("lru_hand_trace.txt")) as fh:
+        for line in fh:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line == "steps:":
+                section = "steps"
+                continue
+            head = line.split()[0]
+            if section == "steps" and head.isdigit():
+                steps.append([int(v) for v in line.split()])
+                continue
+            section = None
+            info[head] = line[len(head):].strip()
+    return info, steps
+
+
+def test_hand_trace_b4():
+    info, steps = _read_hand_trace()
+    E = int(info["E"])
+    states = [[int(v) for v in s.split(",")] for s in info["B4_state"].split("|")]
+    cache = None
+    for t, A in enumerate(steps):
+        f, h, cache, bad = C.lru_stream([A], E, 4, cache)
+        assert cache == states[t]
+        assert f[0] == int(info["B4_f"].split()[t])
+        assert not bad
+    f, h, _, _ = C.lru_stream(steps, E, 4)
+    assert sum(f) == int(info["B4_total"])
+    assert sum(h) == 16 - 11
+    assert C.fetches_per_token(sum(f), len(steps)) == pytest.approx(
+        1 * 2 * (1 - C.hit_rate(sum(h), len(steps), 1, 2)))
+
+
+def test_hand_trace_b2_and_b8():
+    info, steps = _read_hand_trace()
+    E = int(info["E"])
+    assert sum(C.lru_stream(steps, E, 2)[0]) == int(info["B2_total"])
+    assert sum(C.lru_stream(steps, E, 8)[0]) == int(info["B8_total"])
+
+
+def test_within_step_order_matters_on_hand_trace():
+    # Processing a step's experts in rank order (the trace's listing order)
+    # instead of hits-then-misses ascending gives a different count on this
+    # trace, which is why the order is fixed explicitly.
+    info, steps = _read_hand_trace()
+    steps_rank = [list(s) for s in steps]
+    steps_rank[2] = [5, 4]
+    cache, total = [], 0
+    for A in steps_rank:
+        for e in A:           # naive: one expert at a time, in listed order
+            if e in cache:
+                cache.remove(e)
+                cache.append(e)
+            else:
+                total += 1
+                if len(cache) >= 4:
+                    cache.pop(next(i for i, c in enumerate(cache) if c not in A))
+                cache.append(e)
+    assert total == 12 and sum(C.lru_stream(steps, 8, 4)[0]) == 11
+
+
+def _stamp_lru(steps, E, B):
+    """Independent LRU: a dict expert -> last-use time; evict the smallest time."""
+    last, clock, f_all = {}, 0, []
+    for A in steps:
+        A = sorted(set(A))
+        hit = [e for e in A if e in last]
+        for e in hit:
+            last[e] = clock
+            clock += 1
+        miss = 0
+        for e in A:
+            if e in hit:
+                continue
+            miss += 1
+            if len(last) >= B:
+                victim = min((t, c) for c, t in last.items() if c not in A)[1]
+                del last[victim]
+            last[e] = clock
+            clock += 1
+        f_all.append(miss)
+    return f_all
+
+
+@pytest.mark.parametrize("E,K,B", [(8, 2, 4), (8, 2, 2), (8, 2, 7), (16, 3, 5), (64, 6, 12), (5, 5, 5)])
+def test_lru_matches_timestamp_lru(E, K, B):
+    tr = synth.random_trace(1, 6, 200, K, E, seed=E * 100 + B, locality=0.6)
+    for s in range(tr.shape[1]):
+        steps = tr[0, s].tolist()
+        f, h, _, _ = C.lru_stream(steps, E, B)
+        assert f == _stamp_lru(steps, E, B)
+
+
+@pytest.mark.parametrize("E,K", [(8, 2), (16, 4), (64, 6)])
+def test_b_equals_k_closed_form(E, K):
+    tr = synth.random_trace(1, 3, 300, K, E, seed=E + K, locality=0.5)
+    for s in range(3):
+        steps = tr[0, s].tolist()
+        f, _, _, _ = C.lru_stream(steps, E, K)
+        prev = set()
+        for t, A in enumerate(steps):
+            assert f[t] == K - len(set(A) & prev)
+            prev = set(A)
+
+
+@pytest.mark.parametrize("E,K,B", [(8, 2, 8), (8, 2, 12), (16, 3, 16)])
+def test_b_at_least_e_counts_distinct(E, K, B):
+    tr = synth.random_trace(1, 4, 100, K, E, seed=B, locality=0.3)
+    for s in range(4):
+        steps = tr[0, s].tolist()
+        f, _, _, _ = C.lru_stream(steps, E, B)
+        assert sum(f) == len({e for A in steps for e in A})
+
+
+def test_step_rules_and_eq5_identity():
+    E, K, B, L, S, N = 8, 2, 4, 3, 5, 120
+    tr = synth.random_trace(L, S, N, K, E, seed=42, locality=0.7)
+    fetches, hits, fps, final, bad = C.cache_fetches(tr, E, B)
+    assert not bad
+    assert (fps <= K).all()
+    assert (fetches + hits == N * K).all()
+    # misses are the selected experts absent from the previous state
+    for l in range(L):
+        for s in range(S):
+            cache = []
+            for n in range(N):
+                A = tr[l, s, n].tolist()
+                assert fps[l, s, n] == len(set(A) - set(cache))
+                _, _, cache, _ = C.lru_stream([A], E, B, cache)
+            assert cache == [c for c in final[l, s].tolist() if c >= 0]
+    # Eq. 5 over one stream per layer, summed over layers
+    for s in range(S):
+        tot_f, tot_h = int(fetches[:, s].sum()), int(hits[:, s].sum())
+        assert C.fetches_per_token(tot_f, N) == pytest.approx(L * K * (1 - C.hit_rate(tot_h, N, L, K)))
+
+
+def test_paper_table2_satisfies_eq5():
+    rows = []
+    with open(golden_path("table2_cache_simulation.txt")) as fh:
+        for line in fh:
+            if line.startswith("#") or not line.strip():
+                continue
+            model, L, K, B, pol, meth, hr, ft = line.split()
+            rows.append((model, int(L), int(K), pol, meth, float(hr), float(ft)))
+    assert len(rows) == 18
+    for model, L, K, pol, meth, hr, ft in rows:
+        # Fetches/tok summed over layers: L*K*(1-HR), to the printed rounding
+        assert abs(L * K * (1 - hr / 100) - ft) <= 0.011, (model, pol, meth)
+    changes = {}
+    with open(golden_path("table2_relative_changes.txt")) as fh:
+        for line in fh:
+            if line.startswith("#") or not line.strip():
+                continue
+            model, pol, ch = line.split()
+            changes[(model, pol)] = float(ch)
+    ft = {(m, p, me): f for m, L, K, p, me, hr, f in rows}
+    for (model, pol), ch in changes.items():
+        rel = 100 * (ft[(model, pol, "maskcoft")] - ft[(model, pol, "baseline")]) / ft[(model, pol, "baseline")]
+        assert abs(rel - ch) <= 0.051, (model, pol, rel, ch)
+
+
+def test_resume_from_saved_state_equals_whole_trace():
+    E, K, B, L, S, N = 8, 2, 4, 2, 3, 90
+    tr = synth.random_trace(L, S, N, K, E, seed=5, locality=0.6)
+    fw, hw, pw, sw, _ = C.cache_fetches(tr, E, B)
+    f1, h1, p1, s1, _ = C.cache_fetches(tr[:, :, :37], E, B)
+    f2, h2, p2, s2, _ = C.cache_fetches(tr[:, :, 37:], E, B, state=s1)
+    np.testing.assert_array_equal(fw, f1 + f2)
+    np.testing.assert_array_equal(hw, h1 + h2)
+    np.testing.assert_array_equal(pw, np.concatenate([p1, p2], axis=2))
+    np.testing.assert_array_equal(sw, s2)
+
+
+def test_invalid_entries_are_skipped_and_reported():
+    f, h, cache, bad = C.lru_stream([[0, 9], [1, 1], [-1, 2]], 8, 4)
+    assert bad
+    assert f == [1, 1, 1] and h == [0, 0, 0]
+    assert cache == [0, 1, 2]
