@@ -1,0 +1,352 @@
+#!/usr/bin/env python3
+"""Throughput of the masked MoE hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic tokens:
+router + masked/prior Top-K, permutation, SwiGLU expert FFNs, gate-weighted combine
+(maskmoe_layer_forward) and the expert-cache fetch accounting of that step's
+selections (maskmoe_cache_fetches, LRU, one cache per sequence, state carried from
+step to step). Inputs are resident in HBM before timing starts.
+
+Workloads (--workload):
+  decode   (default) Mixtral-shaped decode layer: d=4096, F=14336, 8 experts, top-2,
+           soft prior from a 4-expert set; --batch tokens per step (1, 4 or 16; default 16).
+           Expert weights are rotated over --copies device copies so that no step re-reads
+           weights from the 256 MB Infinity Cache left by the previous one.
+  ft       Mixtral-shaped fine-tuning forward: 8192 tokens, hard mask keeping 4 experts.
+  deepseek DeepSeek-V2-Lite-shaped layer: d=2048, 64 routed (F=1408) + 2 shared experts,
+           top-6, g = p, 4096 tokens (--mode hard|soft).
+  trace    routing-and-fetch trace: 32 routers (4096 -> 8) over 256 AR(1) sequences x 512
+           steps, then one LRU cache of 4 experts per (layer, sequence).
+
+Prints one JSON line (rank 0). The roofline entry is for the dominant kernel, timed with
+HIP events recorded around each stage on the stream the kernels run on; `traffic` is
+filled from rocprofv3 counter runs when given with --traffic-bytes.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "masked-MoE layer tokens/s (bf16) + % MFMA/HBM roofline; fetches/token exact"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
+FP32_VALU_PEAK_TFLOPS = 157.3
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", choices=("decode", "ft", "deepseek", "trace"), default="decode")
+    ap.add_argument("--batch", type=int, default=16, help="decode tokens per step")
+    ap.add_argument("--mode", choices=("hard", "soft"), default="soft", help="deepseek routing mode")
+    ap.add_argument("--copies", type=int, default=3, help="decode: weight copies rotated across steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-bytes", type=float, default=None,
+                    help="HBM bytes per launch of the dominant kernel from rocprofv3 counters")
+    return ap.parse_args()
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+        return int(max(n)) if n else 1
+    except Exception:  # pragma: no cover
+        return 1
+
+
+# ----------------------------------------------------------------------------- layer workloads
+
+def layer_setup(args):
+    import torch
+    from paper_2609_34077_amd import _lib as L
+    from paper_2609_34077_amd import synth
+
+    if args.workload == "decode":
+        cfg = synth.mixtral_decode_config(args.batch)
+    elif args.workload == "ft":
+        cfg = synth.mixtral_ft_config(8192)
+    else:
+        cfg = synth.deepseek_config(L.ROUTE_HARD_MASK if args.mode == "hard" else L.ROUTE_SOFT_PRIOR)
+    log(f"generating {cfg.name} inputs")
+    t0 = time.time()
+    inp = synth.make_layer(cfg)
+    log(f"  inputs ready in {time.time() - t0:.1f}s")
+    n_batches = 8 if args.workload == "decode" else 2
+    xs = [inp["x"]] + [synth.make_tokens(cfg, cfg.T, s) for s in range(1, n_batches)]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).view(torch.bfloat16).cuda()
+    copies = max(1, args.copies) if args.workload == "decode" else 1
+    wgu0, wdn0 = dev(inp["w_gate_up"]), dev(inp["w_down"])
+    wgu = [wgu0] + [wgu0.clone() for _ in range(copies - 1)]
+    wdn = [wdn0] + [wdn0.clone() for _ in range(copies - 1)]
+    st = dict(cfg=cfg, inp=inp, xs_host=xs, xs=[dev(x) for x in xs], w_router=dev(inp["w_router"]), wgu=wgu, wdn=wdn,
+              sgu=dev(inp["ws_gate_up"]) if cfg.n_shared else None,
+              sdn=dev(inp["ws_down"]) if cfg.n_shared else None)
+    desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, cfg.n_shared, L.BF16, cfg.route_mode, cfg.gate_mode)
+    st["ws"] = torch.empty(L.maskmoe_layer_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    st["y"] = torch.empty((cfg.T, cfg.d), dtype=torch.bfloat16, device="cuda")
+    st["idx"] = torch.empty((cfg.T, cfg.K), dtype=torch.int32, device="cuda")
+    st["gate"] = torch.empty((cfg.T, cfg.K), dtype=torch.float32, device="cuda")
+    st["B"] = 4 if cfg.E == 8 else 12
+    st["state"] = torch.full((1, cfg.T, st["B"]), -1, dtype=torch.int32, device="cuda")
+    st["mp"] = dict(mask=inp["mask"]) if cfg.route_mode == L.ROUTE_HARD_MASK else dict(prior=inp["prior"])
+    return st
+
+
+def layer_step(st, i, events=None):
+    from paper_2609_34077_amd import _lib as L
+    cfg = st["cfg"]
+    c = i % len(st["wgu"])
+    L.maskmoe_layer_forward(st["xs"][i % len(st["xs"])], st["w_router"], st["wgu"][c], st["wdn"][c], cfg.K,
+                            cfg.route_mode, cfg.gate_mode, ws_gate_up=st["sgu"], ws_down=st["sdn"],
+                            workspace=st["ws"], y=st["y"], topk_idx=st["idx"], topk_gate=st["gate"],
+                            events=events, **st["mp"])
+    # fetch accounting of this step: every token is one sequence (stream) at one decode step
+    return L.maskmoe_cache_fetches(st["idx"].view(1, cfg.T, 1, cfg.K), cfg.E, st["B"], state=st["state"])
+
+
+def layer_work(st):
+    """Algorithmic work per batch: distinct experts D, bytes of each expert stage, FLOPs."""
+    import torch
+    cfg = st["cfg"]
+    out = []
+    for i in range(len(st["xs"])):
+        layer_step(st, i)
+        torch.cuda.synchronize()
+        sel = st["idx"].cpu().numpy()
+        D = len(np.unique(sel)) + cfg.n_shared
+        rows = cfg.T * (cfg.K + cfg.n_shared)
+        gu_bytes = D * 2 * cfg.F * cfg.d * 2 + cfg.T * cfg.d * 2 + rows * cfg.F * 2
+        dn_bytes = D * cfg.d * cfg.F * 2 + rows * cfg.F * 2 + cfg.T * cfg.d * 2
+        gu_flops = 2.0 * rows * 2 * cfg.F * cfg.d
+        dn_flops = 2.0 * rows * cfg.F * cfg.d
+        out.append(dict(D=D, gu_bytes=gu_bytes, dn_bytes=dn_bytes, gu_flops=gu_flops, dn_flops=dn_flops))
+    return out
+
+
+def layer_cpu_baseline(st, budget_s: float = 10.0):
+    """The oracle on a bounded sample: batches of up to 16 tokens of the workload, one after
+    another (each a full oracle layer call) until about ``budget_s`` seconds have passed."""
+    from oracle import ffn as O
+    from oracle import routing as R
+    from paper_2609_34077_amd import synth
+    cfg, inp = st["cfg"], st["inp"]
+    n = min(16, cfg.T)
+    wr = synth.widen(inp["w_router"], "bf16")
+    done, calls = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        xb = st["xs_host"][calls % len(st["xs_host"])]
+        off = (calls // len(st["xs_host"])) * n % max(1, cfg.T - n + 1)
+        xf = synth.widen(xb[off:off + n], "bf16")
+        idx, gate, _ = R.route(xf, wr, cfg.K, cfg.route_mode, cfg.gate_mode, mask=inp["mask"], prior=inp["prior"])
+        O.moe_layer(xf, idx, gate, inp["w_gate_up"], inp["w_down"],
+                    inp["ws_gate_up"] if cfg.n_shared else None, inp["ws_down"] if cfg.n_shared else None,
+                    widen=lambda a: synth.widen(a, "bf16"))
+        done += n
+        calls += 1
+        dt = time.perf_counter() - t0
+        if dt >= budget_s:
+            break
+    return {"value": round(done / dt, 3), "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{calls} oracle layer calls of {n} tokens ({done} tokens, {dt:.1f} s): fp64 routing + "
+                      f"SwiGLU FFN of every selected expert, weights widened to fp64 per call"}
+
+
+def run_layer(args):
+    import torch
+    from paper_2609_34077_amd import _lib as L
+    st = layer_setup(args)
+    cfg = st["cfg"]
+    work = layer_work(st)
+    steps = args.steps if args.steps is not None else (200 if args.workload == "decode" else 20)
+    warmup = args.warmup if args.warmup is not None else (20 if args.workload == "decode" else 3)
+    for i in range(warmup):
+        layer_step(st, i)
+    nev = L.NUM_STAGES + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(steps)]
+    for row in evs:
+        for e in row:
+            e.record()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        layer_step(st, i, events=evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms = total_ms / steps
+    stage = np.zeros(L.NUM_STAGES)
+    GU = L.STAGES.index("gate_up")
+    gu_ms, gu_bytes, gu_flops = [], 0.0, 0.0
+    for i in range(steps):
+        for s in range(L.NUM_STAGES):
+            stage[s] += evs[i][s].elapsed_time(evs[i][s + 1])
+        gu_ms.append(evs[i][GU].elapsed_time(evs[i][GU + 1]))
+        w = work[i % len(work)]
+        gu_bytes += w["gu_bytes"]
+        gu_flops += w["gu_flops"]
+    gu_s = sum(gu_ms) / 1e3
+    decode = args.workload == "decode"
+    if decode:
+        achieved = gu_bytes / gu_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": args.traffic_bytes,
+                "kernel": "decode_gate_up_kernel",
+                "algorithmic_unit": "bytes per launch = D x 2*F*d*2 (W_gate, W_up of each distinct selected "
+                                    "expert) + x rows + H writes",
+                "avg_launch_us": round(1e3 * np.mean(gu_ms), 2)}
+        tot_bytes = sum(w["gu_bytes"] + w["dn_bytes"] for w in (work[i % len(work)] for i in range(steps)))
+        step_frac = tot_bytes / (total_ms / 1e3) / 1e9 / HBM_PEAK_GBS
+    else:
+        achieved = gu_flops / gu_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": args.traffic_bytes,
+                "kernel": "grouped_gemm_bf16<0> (gate/up + SwiGLU)",
+                "algorithmic_unit": "FLOPs per launch = 2 * T*(K+shared) * 2F * d",
+                "avg_launch_us": round(1e3 * np.mean(gu_ms), 2)}
+        tot_flops = sum(w["gu_flops"] + w["dn_flops"] for w in (work[i % len(work)] for i in range(steps)))
+        step_frac = tot_flops / (total_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS
+    res = {
+        "metric": METRIC, "value": round(cfg.T / (ms / 1e3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": cfg.name, "tokens_per_step": cfg.T, "d": cfg.d, "F": cfg.F, "E": cfg.E,
+                   "K": cfg.K, "n_shared": cfg.n_shared,
+                   "route": {1: "hard_mask", 2: "soft_prior", 0: "plain"}[cfg.route_mode],
+                   "gate": "renorm" if cfg.gate_mode == 1 else "p", "mask_set": list(cfg.mask_set),
+                   "prior_delta": cfg.delta, "cache_slots": st["B"], "weight_copies": len(st["wgu"]),
+                   "distinct_experts_per_step": round(float(np.mean([w["D"] for w in work])), 2)},
+        "roofline": roof,
+        "step_roofline_frac": round(step_frac, 4),
+        "stages_ms": {L.STAGES[s]: round(stage[s] / steps, 4) for s in range(L.NUM_STAGES)},
+    }
+    return res, st
+
+
+# ----------------------------------------------------------------------------- trace workload
+
+def run_trace(args):
+    import torch
+    from paper_2609_34077_amd import _lib as L
+    from paper_2609_34077_amd import synth
+    cfg = synth.TraceConfig()
+    log("generating trace inputs (AR(1) hidden states)")
+    t0 = time.time()
+    inp = synth.make_trace_inputs(cfg)
+    log(f"  inputs ready in {time.time() - t0:.1f}s")
+    xd = torch.from_numpy(inp["x"]).view(torch.bfloat16).cuda()
+    wd = torch.from_numpy(inp["w_router"]).view(torch.bfloat16).cuda()
+    T = cfg.S * cfg.N
+
+    def step(prior, events=None):
+        idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=prior, with_margin=False)
+        if events:
+            events[1].record()
+        res = L.maskmoe_cache_fetches(idx.view(cfg.L, cfg.S, cfg.N, cfg.K), cfg.E, cfg.B)
+        return res
+
+    fetch = {}
+    for name, pr in (("prior", inp["prior"]), ("zero_prior", inp["prior_zero"])):
+        r = step(pr)
+        torch.cuda.synchronize()
+        fetch[name] = float(r["fetches"].sum().item()) / (cfg.S * cfg.N)
+    steps = args.steps if args.steps is not None else 10
+    warmup = args.warmup if args.warmup is not None else 2
+    for _ in range(warmup):
+        step(inp["prior"])
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        evs[i][0].record()
+        step(inp["prior"], evs[i])
+        evs[i][2].record()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    route_ms = np.mean([e[0].elapsed_time(e[1]) for e in evs])
+    cache_ms = np.mean([e[1].elapsed_time(e[2]) for e in evs])
+    flops = 2.0 * T * cfg.L * cfg.E * cfg.d
+    achieved = flops / (route_ms / 1e3) / 1e12
+    x_bytes = T * cfg.d * 2
+    res = {
+        "metric": METRIC, "value": round(T / (ms / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "routing_fetch_trace", "layers": cfg.L, "sequences": cfg.S, "steps_per_seq": cfg.N,
+                   "d": cfg.d, "E": cfg.E, "K": cfg.K, "cache_slots": cfg.B, "prior_delta": cfg.delta},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": args.traffic_bytes,
+                     "kernel": "route_bf16_kernel<2,4,4,1>",
+                     "algorithmic_unit": "FLOPs per launch = 2 * S*N * L*E * d",
+                     "hbm_frac_of_x_read": round(x_bytes / (route_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "avg_launch_us": round(1e3 * route_ms, 2)},
+        "stages_ms": {"route": round(route_ms, 4), "cache": round(cache_ms, 4)},
+        "fetches_per_token": {k: round(v, 4) for k, v in fetch.items()},
+        "fetch_reduction_pct": round(100 * (fetch["prior"] - fetch["zero_prior"]) / fetch["zero_prior"], 2),
+    }
+    return res, dict(cfg=cfg, inp=inp)
+
+
+def trace_cpu_baseline(st):
+    """The oracle on 32 of the 256 sequences (all layers and steps)."""
+    from oracle import cache as C
+    from oracle import routing as R
+    from paper_2609_34077_amd import synth
+    cfg, inp = st["cfg"], st["inp"]
+    S = 32
+    t0 = time.perf_counter()
+    x = synth.widen(inp["x"][: S * cfg.N], "bf16")
+    w = synth.widen(inp["w_router"], "bf16")
+    idx, _, _ = R.route_layers(x, w, cfg.K, R.SOFT_PRIOR, R.GATE_RENORM, priors=inp["prior"])
+    C.cache_fetches(idx.reshape(cfg.L, S, cfg.N, cfg.K), cfg.E, cfg.B)
+    dt = time.perf_counter() - t0
+    return {"value": S * cfg.N / dt, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{S} of {cfg.S} sequences x {cfg.N} steps, 32 layers: fp64 routing + Python LRU ({dt:.1f} s)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build has no multi-GPU path; "
+              "the sharding design is described in the design notes", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    from paper_2609_34077_amd import _lib as L
+    L.load()
+    if args.workload == "trace":
+        res, st = run_trace(args)
+        base = None if args.no_cpu_baseline else trace_cpu_baseline(st)
+    else:
+        res, st = run_layer(args)
+        base = None if args.no_cpu_baseline else layer_cpu_baseline(st)
+    res["cpu_baseline"] = base
+    res["device"] = torch.cuda.get_device_name(0)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

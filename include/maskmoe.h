@@ -1,0 +1,209 @@
+/*
+ * maskmoe.h -- C ABI of the masked co-adaptive MoE hot path on AMD Instinct MI355X (gfx950).
+ *
+ * The library computes, on one GPU, the masked-routing mixture-of-experts layer of
+ * MaskCoFT (Masked Co-Adaptive Fine-Tuning): router logits and softmax, Top-K routing
+ * under a hard binary expert mask (training, Section 3.2 Stage 1, Eq. 2) or a soft
+ * re-ranking prior (inference, Section 3.2 "Evaluation and inference", Eq. 4), gate
+ * values from the full softmax (Section 3.1, Eq. 1), the SwiGLU expert FFNs, the
+ * gate-weighted combine with shared experts (Section 3.1), and the per-layer expert
+ * cache simulation behind the paper's hit rate and fetches-per-token metrics
+ * (Section 4.1, Eq. 5).
+ *
+ * Conventions shared by every entry point
+ *  - Every pointer marked "device" must point to device memory of the current HIP device;
+ *    pointers marked "host" are read synchronously during the call and not kept.
+ *  - The caller owns every buffer. The library allocates nothing, keeps no global state and
+ *    is reentrant. All work is enqueued asynchronously on `stream` (0 = the null stream);
+ *    nothing is synchronised. Outputs are valid once the stream reaches that point.
+ *  - Every argument is validated before anything is enqueued: a non-zero status means that
+ *    nothing was written. MASKMOE_E_HIP reports a failed launch (work enqueued before the
+ *    failing launch may still run).
+ *  - Tensors are dense and row-major in the shapes given. bf16 tensors hold IEEE bfloat16
+ *    bit patterns; arithmetic accumulates in fp32.
+ *  - Results are deterministic: no atomics feed any output, so a repeated call on the same
+ *    inputs gives bit-identical outputs.
+ */
+#ifndef MASKMOE_H_
+#define MASKMOE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes (returned, never thrown) ---- */
+enum {
+  MASKMOE_OK = 0,
+  MASKMOE_E_INVAL = 1,        /* an argument is outside its documented range; nothing enqueued */
+  MASKMOE_E_WORKSPACE = 2,    /* workspace NULL or smaller than maskmoe_layer_workspace_bytes() */
+  MASKMOE_E_HIP = 3,          /* a HIP launch or runtime call failed */
+  MASKMOE_E_UNSUPPORTED = 4   /* valid arguments outside what the kernels implement */
+};
+
+/* ---- routing rule (which keys Top-K ranks) ----
+ * PLAIN:      A = Top-K(p)                      Section 3.1, Eq. 1
+ * HARD_MASK:  A = Top-K(p * m), m binary        Section 3.2 Stage 1, Eq. 2 (training)
+ * SOFT_PRIOR: A = Top-K(p * pi), pi > 0         Section 3.2 inference, Eq. 4
+ * where p = softmax(W x) over all E routed experts. Ranking is done on log-domain keys
+ * (z_i, or z_i + log pi_i; experts with m_i = 0 are never eligible), which order experts
+ * exactly as the products do. Equal keys go to the lower expert index. */
+enum { MASKMOE_ROUTE_PLAIN = 0, MASKMOE_ROUTE_HARD_MASK = 1, MASKMOE_ROUTE_SOFT_PRIOR = 2 };
+
+/* ---- gate rule (Section 3.1); gates always come from the full softmax p, in every
+ * routing mode (Eq. 2 gates equal those of p on the active set; Eq. 4 keeps p's gates) ----
+ * GATE_P:      g_i = p_i                          (DeepSeek-V2-Lite)
+ * GATE_RENORM: g_i = p_i / sum_{j in A} p_j       (Mixtral-8x7B)                     */
+enum { MASKMOE_GATE_P = 0, MASKMOE_GATE_RENORM = 1 };
+
+/* ---- element type of x, router weights, expert weights and y ---- */
+enum { MASKMOE_BF16 = 0, MASKMOE_F32 = 1 };
+
+/* ---- cache replacement policy of maskmoe_cache_fetches ---- */
+enum { MASKMOE_CACHE_LRU = 0 };
+
+/* One masked MoE layer.
+ *  T          tokens (T >= 0; T = 0 is a no-op)
+ *  d          hidden size; F expert FFN width
+ *  E          routed experts, 1 <= E <= 256; K experts per token, 1 <= K <= E, K <= 16
+ *  n_shared   shared experts (0..8): see every token, gate 1, never routed or masked
+ *  dtype      MASKMOE_BF16 or MASKMOE_F32
+ *  route_mode MASKMOE_ROUTE_*; gate_mode MASKMOE_GATE_*                               */
+typedef struct maskmoe_layer_desc {
+  int32_t T, d, E, K, F, n_shared, dtype, route_mode, gate_mode;
+} maskmoe_layer_desc;
+
+/*
+ * maskmoe_route -- router logits, softmax, masked / prior-re-ranked Top-K and gates for
+ * L independent layers that read the same tokens (Section 3.1 Eq. 1; Eq. 2; Eq. 4).
+ *
+ *  desc        T, d, E, K, dtype, route_mode, gate_mode are used (F, n_shared ignored).
+ *  L           number of layers, L >= 1.
+ *  x           device [T, d] tokens (dtype).
+ *  w_router    device [L, E, d] router weights W_l (dtype), no bias.
+ *  mask        host [L, E] uint8, HARD_MASK only (else ignored, may be NULL): 1 keeps the
+ *              expert; each layer must keep at least K experts.
+ *  prior       host [L, E] float, SOFT_PRIOR only (else ignored, may be NULL): every value
+ *              finite and > 0 (the prior excludes no expert).
+ *  topk_idx    device [L, T, K] int32: selected experts of token t at layer l, by decreasing
+ *              key, ties by increasing index.
+ *  topk_gate   device [L, T, K] float: gate of each selected expert (gate_mode).
+ *  topk_margin device [L, T] float or NULL: gap in logit units between the K-th and the
+ *              (K+1)-th largest log-domain key (+inf when fewer than K+1 experts are
+ *              eligible). Index sets are unique wherever the margin is clearly positive.
+ *  Errors: E_INVAL for T < 0, L < 1, d < 1, K/E outside their ranges, an unknown mode, a
+ *  NULL required pointer, a mask row with fewer than K ones, or a prior value that is not
+ *  finite and > 0; E_UNSUPPORTED for bf16 with d % 32 != 0.
+ */
+int maskmoe_route(const maskmoe_layer_desc* desc, int32_t L, const void* x, const void* w_router,
+                  const uint8_t* mask, const float* prior, int32_t* topk_idx, float* topk_gate,
+                  float* topk_margin, hipStream_t stream);
+
+/*
+ * maskmoe_layer_workspace_bytes -- device workspace that maskmoe_layer_forward needs for
+ * `desc` (routing outputs, the expert permutation, the SwiGLU activations and the
+ * per-(token, expert) FFN outputs). Returns 0 for an invalid desc. Monotone in T.
+ */
+size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc);
+
+/*
+ * maskmoe_layer_forward -- one masked MoE layer:
+ *     y_t = sum_{i in A_t} g_{t,i} F_i(x_t) + sum_s F_s(x_t)          (Section 3.1, Eq. 1)
+ * with A_t and g from maskmoe_route's rule (L = 1) and the SwiGLU expert
+ *     F(x) = W_down (SiLU(W_gate x) * (W_up x)),  SiLU(u) = u / (1 + e^-u).
+ *
+ *  x            device [T, d] (dtype).
+ *  w_router     device [E, d] (dtype).   mask / prior: host [E], as in maskmoe_route.
+ *  w_gate_up    device [E, 2F, d] (dtype): rows 0..F-1 = W_gate, rows F..2F-1 = W_up.
+ *  w_down       device [E, d, F] (dtype).
+ *  ws_gate_up   device [n_shared, 2F, d], ws_down device [n_shared, d, F]; NULL when
+ *               n_shared == 0.
+ *  y            device [T, d] (dtype) output.
+ *  topk_idx     device [T, K] int32 or NULL; topk_gate device [T, K] float or NULL:
+ *               when given, the routing decision is also written there.
+ *  workspace    device, at least maskmoe_layer_workspace_bytes(desc) bytes, 256-byte
+ *               aligned; its contents on entry do not matter and are clobbered.
+ *  Rounding (bf16): fp32 accumulation; the SwiGLU activation is rounded to bf16 before the
+ *  down projection; the combine sums the gate-weighted fp32 expert outputs in fp32 and
+ *  rounds once to bf16. f32: no intermediate rounding beyond fp32 arithmetic.
+ *  Errors: as maskmoe_route, plus E_INVAL for F < 1 or n_shared outside 0..8 or a NULL
+ *  shared-weight pointer with n_shared > 0; E_WORKSPACE when the workspace is too small;
+ *  E_UNSUPPORTED for bf16 with d % 64 != 0 or F % 64 != 0.
+ */
+int maskmoe_layer_forward(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                          const uint8_t* mask, const float* prior, const void* w_gate_up,
+                          const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
+                          int32_t* topk_idx, float* topk_gate, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
+
+/* Stages of maskmoe_layer_forward, in launch order. */
+enum {
+  MASKMOE_STAGE_ROUTE = 0,       /* router logits + masked / prior Top-K + gates        */
+  MASKMOE_STAGE_PERMUTE = 1,     /* grouping of (token, slot) pairs by expert           */
+  MASKMOE_STAGE_GATE_UP = 2,     /* H = SiLU(X W_gate^T) * (X W_up^T) per expert        */
+  MASKMOE_STAGE_DOWN = 3,        /* O = H W_down^T per expert (few tokens: with combine) */
+  MASKMOE_STAGE_COMBINE = 4,     /* y = sum_k g O + shared experts                      */
+  MASKMOE_NUM_STAGES = 5
+};
+
+/*
+ * maskmoe_layer_forward_profiled -- maskmoe_layer_forward that also records caller-owned
+ * HIP events on `stream`, for measuring each stage on the device timeline: events[0]
+ * before the first launch and events[s + 1] after stage s (MASKMOE_STAGE_*). A stage that
+ * a path fuses into the previous one (the combine of the few-token path) gets its event
+ * right after that one. Same computation, outputs and errors as maskmoe_layer_forward;
+ * E_INVAL when `events` or any of its MASKMOE_NUM_STAGES + 1 entries is NULL.
+ */
+int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                   const uint8_t* mask, const float* prior, const void* w_gate_up,
+                                   const void* w_down, const void* ws_gate_up, const void* ws_down,
+                                   void* y, int32_t* topk_idx, float* topk_gate, void* workspace,
+                                   size_t workspace_bytes, hipEvent_t* events, hipStream_t stream);
+
+/*
+ * maskmoe_cache_fetches -- replay expert-selection traces through per-layer expert caches
+ * (Section 4.1 "Simulation"; metrics of Eq. 5).
+ *
+ * Each (layer l, stream s) pair is an independent cache of B routed experts that sees the
+ * steps n = 0..N-1 of trace[l, s]. At a step, h = number of selected experts already
+ * cached, f = misses (= K - h for a trace of K distinct valid experts); every miss is one
+ * fetch and, in a full cache, one eviction. LRU: the hits are touched first, in ascending
+ * expert index, then the misses are inserted in ascending expert index, each evicting the
+ * least recently used cached expert not selected at this step.
+ * Eq. 5 then gives HR = sum h / (N L K) and Fetches/tok = sum f / N (per stream).
+ *
+ *  trace       device [L, S, N, K] int32 expert ids. An id outside [0, E) or repeating an
+ *              earlier id of the same step is skipped (neither hit nor miss) and flags
+ *              *dev_error.
+ *  L, S, N, K  sizes, L, S, N >= 0, 1 <= K <= E; E experts, 1 <= E <= 64;
+ *              B cache slots, K <= B (B >= E never evicts); N * K + B < 2^24.
+ *  policy      MASKMOE_CACHE_LRU.
+ *  state       device [L, S, B] int32 in/out or NULL. In: initial cache, least to most
+ *              recently used, -1 = empty slot (entries must be distinct ids in [0, E) or
+ *              -1; bad entries are dropped and flag *dev_error). Out: final cache in the
+ *              same form. NULL: every cache starts empty and the final state is not kept.
+ *  fetches     device [L, S] int64: sum of f over the N steps.
+ *  hits        device [L, S] int64: sum of h over the N steps.
+ *  f_per_step  device [L, S, N] uint8 or NULL: f at every step.
+ *  dev_error   device int32 or NULL: set to 1 (never cleared) when a trace or state entry
+ *              was skipped.
+ *  Errors: E_INVAL for negative sizes, K < 1, K > E, B < K, an unknown policy, NULL
+ *  required pointers; E_UNSUPPORTED for E > 64 or N * K + B >= 2^24.
+ */
+int maskmoe_cache_fetches(const int32_t* trace, int32_t L, int32_t S, int32_t N, int32_t K,
+                          int32_t E, int32_t B, int32_t policy, int32_t* state, int64_t* fetches,
+                          int64_t* hits, uint8_t* f_per_step, int32_t* dev_error,
+                          hipStream_t stream);
+
+/* maskmoe_status_string -- static, NUL-terminated description of a status code. */
+const char* maskmoe_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MASKMOE_H_ */

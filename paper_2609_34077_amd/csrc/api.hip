@@ -1,0 +1,249 @@
+// C-ABI entry points: argument validation, workspace layout and launch sequencing.
+// Nothing here touches the device before every argument has been checked; the only
+// device work is the kernel launches, enqueued on the caller's stream.
+
+#include <math.h>
+#include <stdint.h>
+
+#include "kernels.hpp"
+#include "maskmoe.h"
+
+namespace {
+
+using maskmoe::PermBuffers;
+
+constexpr int kMaxE = 256;
+constexpr int kMaxK = 16;
+constexpr int kMaxShared = 8;
+constexpr int kCacheMaxE = 64;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+size_t round256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
+
+// Checks shared by maskmoe_route and maskmoe_layer_forward (routing part of desc).
+int check_route_desc(const maskmoe_layer_desc* d) {
+  if (!d) return MASKMOE_E_INVAL;
+  if (d->T < 0 || d->d < 1 || d->E < 1 || d->E > kMaxE || d->K < 1 || d->K > d->E || d->K > kMaxK)
+    return MASKMOE_E_INVAL;
+  if (d->dtype != MASKMOE_BF16 && d->dtype != MASKMOE_F32) return MASKMOE_E_INVAL;
+  if (d->route_mode < MASKMOE_ROUTE_PLAIN || d->route_mode > MASKMOE_ROUTE_SOFT_PRIOR) return MASKMOE_E_INVAL;
+  if (d->gate_mode != MASKMOE_GATE_P && d->gate_mode != MASKMOE_GATE_RENORM) return MASKMOE_E_INVAL;
+  if (static_cast<int64_t>(d->T) * d->K >= (int64_t{1} << 31)) return MASKMOE_E_INVAL;
+  return MASKMOE_OK;
+}
+
+// Mask rows need at least K ones (Eq. 2 draws E' >= K experts); prior values must be
+// finite and positive (Eq. 4: the prior excludes no expert).
+int check_mask_prior(int mode, int L, int E, int K, const uint8_t* mask, const float* prior) {
+  if (mode == MASKMOE_ROUTE_HARD_MASK) {
+    if (!mask) return MASKMOE_E_INVAL;
+    for (int l = 0; l < L; ++l) {
+      int ones = 0;
+      for (int e = 0; e < E; ++e) ones += mask[static_cast<size_t>(l) * E + e] != 0;
+      if (ones < K) return MASKMOE_E_INVAL;
+    }
+  } else if (mode == MASKMOE_ROUTE_SOFT_PRIOR) {
+    if (!prior) return MASKMOE_E_INVAL;
+    for (size_t i = 0; i < static_cast<size_t>(L) * E; ++i) {
+      const float v = prior[i];
+      if (!(v > 0.0f) || !isfinite(v)) return MASKMOE_E_INVAL;
+    }
+  }
+  return MASKMOE_OK;
+}
+
+struct Layout {
+  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, H, O, total;
+};
+
+bool uses_decode_path(const maskmoe_layer_desc& d) {
+  return d.dtype == MASKMOE_BF16 && d.T <= maskmoe::kDecodeMaxT;
+}
+
+Layout layout(const maskmoe_layer_desc& d) {
+  Layout w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += round256(bytes);
+    return o;
+  };
+  const size_t TK = static_cast<size_t>(d.T) * d.K;
+  const size_t G = static_cast<size_t>(d.E) + d.n_shared;
+  const size_t rows = static_cast<size_t>(d.T) * (d.K + d.n_shared);
+  const size_t hsz = d.dtype == MASKMOE_BF16 ? 2 : 4;
+  w.idx = take(TK * 4);
+  w.gate = take(TK * 4);
+  w.offsets = take((G + 1) * 4);
+  w.tile_off = take((G + 1) * 4);
+  w.active = take(G * 4);
+  w.n_active = take(4);
+  w.perm = take(TK * 4);
+  w.inv = take(TK * 4);
+  w.row_tok = take(rows * 4);
+  w.H = take(rows * d.F * hsz);
+  w.O = uses_decode_path(d) ? off : take(rows * d.d * 4);
+  w.total = off;
+  return w;
+}
+
+int check_layer_desc(const maskmoe_layer_desc* d) {
+  int st = check_route_desc(d);
+  if (st != MASKMOE_OK) return st;
+  if (d->F < 1 || d->n_shared < 0 || d->n_shared > kMaxShared) return MASKMOE_E_INVAL;
+  if (static_cast<int64_t>(d->T) * (d->K + d->n_shared) >= (int64_t{1} << 31)) return MASKMOE_E_INVAL;
+  return MASKMOE_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? MASKMOE_OK : MASKMOE_E_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* maskmoe_status_string(int status) {
+  switch (status) {
+    case MASKMOE_OK: return "ok";
+    case MASKMOE_E_INVAL: return "invalid argument";
+    case MASKMOE_E_WORKSPACE: return "workspace missing or too small";
+    case MASKMOE_E_HIP: return "HIP launch or runtime error";
+    case MASKMOE_E_UNSUPPORTED: return "unsupported size or configuration";
+    default: return "unknown status";
+  }
+}
+
+int maskmoe_route(const maskmoe_layer_desc* desc, int32_t L, const void* x, const void* w_router,
+                  const uint8_t* mask, const float* prior, int32_t* topk_idx, float* topk_gate,
+                  float* topk_margin, hipStream_t stream) {
+  int st = check_route_desc(desc);
+  if (st != MASKMOE_OK) return st;
+  if (L < 1 || static_cast<int64_t>(L) * desc->T * desc->K >= (int64_t{1} << 31)) return MASKMOE_E_INVAL;
+  st = check_mask_prior(desc->route_mode, L, desc->E, desc->K, mask, prior);
+  if (st != MASKMOE_OK) return st;
+  if (desc->T == 0) return MASKMOE_OK;
+  if (!x || !w_router || !topk_idx || !topk_gate) return MASKMOE_E_INVAL;
+  const bool bf16 = desc->dtype == MASKMOE_BF16;
+  if (bf16 && desc->d % 32 != 0) return MASKMOE_E_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(w_router, 16) || !aligned(topk_idx, 4) || !aligned(topk_gate, 4) ||
+      (topk_margin && !aligned(topk_margin, 4)))
+    return MASKMOE_E_INVAL;
+  return hip_status(maskmoe::launch_route(bf16, x, w_router, desc->T, desc->d, desc->E, desc->K, L,
+                                         desc->route_mode, desc->gate_mode, mask, prior, topk_idx,
+                                         topk_gate, topk_margin, stream));
+}
+
+size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc) {
+  if (check_layer_desc(desc) != MASKMOE_OK) return 0;
+  return layout(*desc).total;
+}
+
+static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                              const uint8_t* mask, const float* prior, const void* w_gate_up,
+                              const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
+                              int32_t* topk_idx, float* topk_gate, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream, hipEvent_t* events) {
+  int st = check_layer_desc(desc);
+  if (st != MASKMOE_OK) return st;
+  const maskmoe_layer_desc& d = *desc;
+  st = check_mask_prior(d.route_mode, 1, d.E, d.K, mask, prior);
+  if (st != MASKMOE_OK) return st;
+  if (d.T == 0) return MASKMOE_OK;
+  if (!x || !w_router || !w_gate_up || !w_down || !y) return MASKMOE_E_INVAL;
+  if (d.n_shared > 0 && (!ws_gate_up || !ws_down)) return MASKMOE_E_INVAL;
+  const bool bf16 = d.dtype == MASKMOE_BF16;
+  if (bf16 && (d.d % 64 != 0 || d.F % 64 != 0)) return MASKMOE_E_UNSUPPORTED;
+  const void* ptrs[] = {x, w_router, w_gate_up, w_down, y};
+  for (const void* p : ptrs)
+    if (!aligned(p, 16)) return MASKMOE_E_INVAL;
+  if (d.n_shared > 0 && (!aligned(ws_gate_up, 16) || !aligned(ws_down, 16))) return MASKMOE_E_INVAL;
+  if ((topk_idx && !aligned(topk_idx, 4)) || (topk_gate && !aligned(topk_gate, 4))) return MASKMOE_E_INVAL;
+  const Layout w = layout(d);
+  if (!workspace || workspace_bytes < w.total || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  int32_t* idx = topk_idx ? topk_idx : reinterpret_cast<int32_t*>(ws + w.idx);
+  float* gate = topk_gate ? topk_gate : reinterpret_cast<float*>(ws + w.gate);
+  PermBuffers pb;
+  pb.offsets = reinterpret_cast<int32_t*>(ws + w.offsets);
+  pb.tile_off = reinterpret_cast<int32_t*>(ws + w.tile_off);
+  pb.active = reinterpret_cast<int32_t*>(ws + w.active);
+  pb.n_active = reinterpret_cast<int32_t*>(ws + w.n_active);
+  pb.perm = reinterpret_cast<int32_t*>(ws + w.perm);
+  pb.inv = reinterpret_cast<int32_t*>(ws + w.inv);
+  pb.row_tok = reinterpret_cast<int32_t*>(ws + w.row_tok);
+
+  maskmoe::record_mark(events, 0, stream);
+  hipError_t e = maskmoe::launch_route(bf16, x, w_router, d.T, d.d, d.E, d.K, 1, d.route_mode, d.gate_mode,
+                                       mask, prior, idx, gate, nullptr, stream);
+  if (e != hipSuccess) return MASKMOE_E_HIP;
+  maskmoe::record_mark(events, 1, stream);
+  e = maskmoe::launch_permute(idx, d.T, d.K, d.E, d.n_shared, maskmoe::kGemmBM, pb, stream);
+  if (e != hipSuccess) return MASKMOE_E_HIP;
+  maskmoe::record_mark(events, 2, stream);
+  hipEvent_t* expert_marks = events ? events + 3 : nullptr;
+
+  maskmoe::ExpertArgs a;
+  a.x = x;
+  a.w_gate_up = w_gate_up;
+  a.w_down = w_down;
+  a.ws_gate_up = ws_gate_up;
+  a.ws_down = ws_down;
+  a.gate = gate;
+  a.T = d.T; a.d = d.d; a.F = d.F; a.E = d.E; a.K = d.K; a.n_shared = d.n_shared;
+  if (!bf16) {
+    e = maskmoe::launch_experts_f32(a, pb, reinterpret_cast<float*>(ws + w.H), reinterpret_cast<float*>(ws + w.O),
+                                    y, stream, expert_marks);
+  } else if (uses_decode_path(d)) {
+    e = maskmoe::launch_experts_bf16_decode(a, pb, reinterpret_cast<uint16_t*>(ws + w.H), y, stream,
+                                            expert_marks);
+  } else {
+    const int64_t TK = static_cast<int64_t>(d.T) * d.K;
+    const int64_t nonempty = TK < d.E ? TK : d.E;
+    const int64_t max_tiles = TK / maskmoe::kGemmBM + nonempty +
+                              static_cast<int64_t>(d.n_shared) * ((d.T + maskmoe::kGemmBM - 1) / maskmoe::kGemmBM);
+    e = maskmoe::launch_experts_bf16(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
+                                     reinterpret_cast<float*>(ws + w.O), y, static_cast<int>(max_tiles), stream,
+                                     expert_marks);
+  }
+  return hip_status(e);
+}
+
+int maskmoe_layer_forward(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                          const uint8_t* mask, const float* prior, const void* w_gate_up,
+                          const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
+                          int32_t* topk_idx, float* topk_gate, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream) {
+  return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
+                            topk_idx, topk_gate, workspace, workspace_bytes, stream, nullptr);
+}
+
+int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                   const uint8_t* mask, const float* prior, const void* w_gate_up,
+                                   const void* w_down, const void* ws_gate_up, const void* ws_down,
+                                   void* y, int32_t* topk_idx, float* topk_gate, void* workspace,
+                                   size_t workspace_bytes, hipEvent_t* events, hipStream_t stream) {
+  if (!events) return MASKMOE_E_INVAL;
+  for (int i = 0; i <= MASKMOE_NUM_STAGES; ++i)
+    if (!events[i]) return MASKMOE_E_INVAL;
+  return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
+                            topk_idx, topk_gate, workspace, workspace_bytes, stream, events);
+}
+
+int maskmoe_cache_fetches(const int32_t* trace, int32_t L, int32_t S, int32_t N, int32_t K, int32_t E,
+                          int32_t B, int32_t policy, int32_t* state, int64_t* fetches, int64_t* hits,
+                          uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream) {
+  if (L < 0 || S < 0 || N < 0 || K < 1 || E < 1 || K > E || B < K) return MASKMOE_E_INVAL;
+  if (policy != MASKMOE_CACHE_LRU) return MASKMOE_E_INVAL;
+  if (E > kCacheMaxE) return MASKMOE_E_UNSUPPORTED;
+  if (static_cast<int64_t>(N) * K + B >= (int64_t{1} << 24)) return MASKMOE_E_UNSUPPORTED;
+  if (static_cast<int64_t>(L) * S >= (int64_t{1} << 31)) return MASKMOE_E_INVAL;
+  if (static_cast<int64_t>(L) * S == 0) return MASKMOE_OK;
+  if (!fetches || !hits || (N > 0 && !trace)) return MASKMOE_E_INVAL;
+  if (!aligned(fetches, 8) || !aligned(hits, 8) || (trace && !aligned(trace, 4)) ||
+      (state && !aligned(state, 4)) || (dev_error && !aligned(dev_error, 4)))
+    return MASKMOE_E_INVAL;
+  return hip_status(maskmoe::launch_cache_lru(trace, L, S, N, K, E, B, state, fetches, hits, f_per_step,
+                                              dev_error, stream));
+}
+
+}  // extern "C"

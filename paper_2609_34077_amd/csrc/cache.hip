@@ -1,0 +1,144 @@
+// Per-layer expert cache replay behind the hit rate and fetches-per-token metrics.
+//
+// Section 4.1 (Simulation): every layer keeps a cache of B routed experts; caches start
+// empty (or from a given state), initial fills are misses, each miss is one fetch and,
+// when the cache is full, one eviction. Eq. 5: h_{l,t} = selected experts already cached,
+// f_{l,t} = K - h_{l,t}; HR = sum h / (N L K), Fetches/tok = sum f / N.
+//
+// One wavefront replays one (layer, stream) trace; lane e owns expert e (E <= 64) and
+// keeps a cached flag and a last-use stamp. A step is a handful of wave-uniform bitmask
+// operations: ballot the cached set, intersect with the selected set for the hits, stamp
+// the hits in ascending expert order, then insert the misses in ascending order, each
+// evicting the cached expert with the smallest stamp. The selected experts always carry
+// the newest stamps, so the smallest stamp is never one of them. The trace is read 64
+// entries at a time, coalesced, and broadcast to the wave with lane shuffles; per-step
+// miss counts are gathered in lanes and written back 64 bytes at a time.
+
+#include <limits.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace maskmoe {
+namespace {
+
+constexpr int kCacheWavesPerBlock = 4;
+
+__global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_lru_kernel(
+    const int32_t* __restrict__ trace, int L, int S, int N, int K, int E, int B,
+    int32_t* __restrict__ state, int64_t* __restrict__ fetches, int64_t* __restrict__ hits,
+    uint8_t* __restrict__ f_per_step, int32_t* __restrict__ dev_error) {
+  const int lane = threadIdx.x & 63;
+  const long stream = static_cast<long>(blockIdx.x) * kCacheWavesPerBlock + (threadIdx.x >> 6);
+  if (stream >= static_cast<long>(L) * S) return;  // whole wavefront exits together
+  const int32_t* tr = trace + stream * static_cast<long>(N) * K;
+
+  bool cached = false;
+  int stamp = INT_MAX;
+  int ncached = 0;
+  int clock = 0;
+  bool bad = false;
+
+  if (state) {  // slots are listed least to most recently used
+    const int32_t* st = state + stream * B;
+    for (int s = 0; s < B; ++s) {
+      const int e = st[s];  // wave-uniform
+      if (e < 0) continue;
+      const bool dup = e < E && ((__ballot(cached) >> e) & 1ull);
+      if (e >= E || dup) {
+        bad = true;
+        continue;
+      }
+      if (lane == e) {
+        cached = true;
+        stamp = s;
+      }
+      ++ncached;
+    }
+    clock = B;
+  }
+
+  long tot_f = 0, tot_h = 0;
+  const int chunk = 64 / K;  // steps per 64-entry load
+  for (int n0 = 0; n0 < N; n0 += chunk) {
+    const int ns = min(chunk, N - n0);
+    const int v = lane < ns * K ? tr[static_cast<long>(n0) * K + lane] : -1;
+    int my_f = 0;
+    for (int j = 0; j < ns; ++j) {
+      uint64_t sel = 0;
+      for (int k = 0; k < K; ++k) {
+        const int e = __shfl(v, j * K + k, kWave);
+        if (e < 0 || e >= E || ((sel >> e) & 1ull)) {
+          bad = true;
+        } else {
+          sel |= 1ull << e;
+        }
+      }
+      const uint64_t cmask = __ballot(cached);
+      const uint64_t hitm = sel & cmask;
+      uint64_t missm = sel & ~cmask;
+      const int h = __popcll(hitm), f = __popcll(missm);
+      if ((hitm >> lane) & 1ull) stamp = clock + __popcll(hitm & lanemask_lt(lane));
+      clock += h;
+      while (missm) {
+        const int e = __ffsll(static_cast<unsigned long long>(missm)) - 1;
+        missm &= missm - 1;
+        if (ncached >= B) {
+          const int key = cached ? stamp : INT_MAX;
+          const int mn = wave_min_int(key);
+          const uint64_t vm = __ballot(cached && key == mn);
+          const int victim = __ffsll(static_cast<unsigned long long>(vm)) - 1;
+          if (lane == victim) {
+            cached = false;
+            stamp = INT_MAX;
+          }
+          --ncached;
+        }
+        if (lane == e) {
+          cached = true;
+          stamp = clock;
+        }
+        ++clock;
+        ++ncached;
+      }
+      tot_h += h;
+      tot_f += f;
+      if (lane == j) my_f = f;
+    }
+    if (f_per_step && lane < ns) f_per_step[stream * N + n0 + lane] = static_cast<uint8_t>(my_f);
+  }
+
+  if (lane == 0) {
+    fetches[stream] = tot_f;
+    hits[stream] = tot_h;
+    if (bad && dev_error) *dev_error = 1;
+  }
+  if (state) {
+    // rank of each cached expert by stamp = its slot, least recently used first
+    int rank = 0;
+    for (int o = 0; o < 64; ++o) {
+      const int so = __shfl(cached ? stamp : INT_MAX, o, kWave);
+      if (cached && so < stamp) ++rank;
+    }
+    int32_t* st = state + stream * B;
+    const int nc = __popcll(__ballot(cached));
+    for (int s = lane; s < B; s += 64)
+      if (s >= nc) st[s] = -1;
+    if (cached) st[rank] = lane;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_cache_lru(const int32_t* trace, int L, int S, int N, int K, int E, int B,
+                            int32_t* state, int64_t* fetches, int64_t* hits, uint8_t* f_per_step,
+                            int32_t* dev_error, hipStream_t stream) {
+  const long streams = static_cast<long>(L) * S;
+  if (streams == 0) return hipSuccess;
+  const long blocks = (streams + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock;
+  hipLaunchKernelGGL(cache_lru_kernel, dim3(static_cast<unsigned>(blocks)), dim3(64 * kCacheWavesPerBlock),
+                     0, stream, trace, L, S, N, K, E, B, state, fetches, hits, f_per_step, dev_error);
+  return hipGetLastError();
+}
+
+}  // namespace maskmoe

@@ -1,0 +1,556 @@
+// Expert FFNs and the gate-weighted combine of the masked MoE layer.
+//
+// Eq. 1 (Section 3.1): y = sum_{i in A} g_i F_i(x), plus the shared experts' outputs
+// with weight 1. Each expert is the SwiGLU FFN F(x) = W_down (SiLU(W_gate x) * W_up x).
+// After the permutation every expert group is a dense row block, so the FFN is a grouped
+// GEMM pair:
+//   H_g = SiLU(X_g W_gate,g^T) * (X_g W_up,g^T)   (rows gathered from x through row_tok)
+//   O_g = H_g W_down,g^T
+// followed by y_t = sum_k g_{t,k} O[inv(t,k)] + sum_s O[shared row of t].
+//
+// bf16, many tokens: 256x256x64 block tiles on v_mfma_f32_32x32x16_bf16, 8 waves (4 x 2),
+// 64x128 per wave, A and B double-buffered in LDS (128 KB) with a 16-byte XOR swizzle so
+// that both the global->LDS stores and the MFMA operand reads are bank-conflict free.
+// The gate/up GEMM holds matching 128-column slices of W_gate and W_up in one tile and
+// applies SwiGLU in registers (H rounded once to bf16). Tiles are enumerated expert-tile
+// fastest so the workgroups that share a weight slice run together, and the linear block
+// id is remapped so each XCD (L2) receives a contiguous range of tiles.
+//
+// bf16, few tokens (decode): the work is reading each selected expert's weights once.
+// The gate/up kernel gives every workgroup a 32-column slab of one active expert and
+// splits d over 4 waves; the down kernel gives every workgroup a 16-column slab of y,
+// loops over the active experts with F split over 8 waves, and applies the gates in LDS,
+// so the combine needs no extra pass. MFMA 16x16x32 with tokens padded to 16 rows.
+//
+// f32: plain fp32 loops (no MFMA), one thread per output element.
+
+#include <math.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace maskmoe {
+namespace {
+
+// ------------------------------------------------------------------ bf16 grouped GEMM
+
+constexpr int BM = kGemmBM, BN = 256, BK = 64, GEMM_THREADS = 512;
+static_assert(BM == 256, "tile mapping assumes 256-row tiles");
+
+struct GemmArgs {
+  const uint16_t* a;        // EPI 0: x [T, d] (rows via row_tok); EPI 1: H [rows, F]
+  const int32_t* row_tok;
+  const uint16_t* w;        // routed weights: EPI 0 [E, 2F, d], EPI 1 [E, d, F]
+  const uint16_t* ws;       // shared weights, same layout with n_shared experts
+  const int32_t* offsets;   // [G+1]
+  const int32_t* tile_off;  // [G+1]
+  void* out;                // EPI 0: H bf16 [rows, F]; EPI 1: O f32 [rows, d]
+  int G, E, F, d;
+  int mt_max;               // grid bound on row tiles
+};
+
+__device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt) {
+  int lo = 0, hi = G;  // tile_off[lo] <= mt < tile_off[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tile_off[mid] <= mt) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
+  __shared__ u32x4 lds_a[2][BM * BK / 8];
+  __shared__ u32x4 lds_b[2][BN * BK / 8];
+
+  // XCD-aware block order: consecutive logical tiles land on the same XCD.
+  const int nwg = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, local = bid >> 3, q = nwg >> 3, rem = nwg & 7;
+  const int lid = xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
+  const int mt = lid % p.mt_max, nt = lid / p.mt_max;
+  if (mt >= p.tile_off[p.G]) return;
+  const int g = find_group(p.tile_off, p.G, mt);
+  const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM;
+  const int row_end = p.offsets[g + 1];
+  const int Kdim = EPI == 0 ? p.d : p.F;
+  const int Ndim = EPI == 0 ? p.F : p.d;
+  const int n0 = nt * (EPI == 0 ? BN / 2 : BN);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // Global -> LDS copy mapping: 4 chunks of 16 B per thread and operand; row (tid>>3)+64i.
+  const int kc = tid & 7;
+  const uint16_t* asrc[4];
+  const uint16_t* bsrc[4];
+  const uint16_t* wg = g < p.E ? p.w + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * Kdim
+                               : p.ws + static_cast<size_t>(g - p.E) * (EPI == 0 ? 2 * p.F : p.d) * Kdim;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = (tid >> 3) + 64 * i;
+    const int row = min(row0 + r, row_end - 1);
+    if (EPI == 0) asrc[i] = p.a + static_cast<size_t>(p.row_tok[row]) * Kdim + kc * 8;
+    else asrc[i] = p.a + static_cast<size_t>(row) * Kdim + kc * 8;
+    int brow;
+    if (EPI == 0) {  // tile rows 0..127: W_gate rows n0.., rows 128..255: W_up rows F+n0..
+      const int n = min(n0 + (r & 127), p.F - 1);
+      brow = r < 128 ? n : p.F + n;
+    } else {
+      brow = min(n0 + r, p.d - 1);
+    }
+    bsrc[i] = wg + static_cast<size_t>(brow) * Kdim + kc * 8;
+  }
+
+  u32x4 ra[4], rb[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ra[i] = *reinterpret_cast<const u32x4*>(asrc[i] + k0);
+      rb[i] = *reinterpret_cast<const u32x4*>(bsrc[i] + k0);
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = (tid >> 3) + 64 * i;
+      lds_a[buf][r * 8 + (kc ^ (r & 7))] = ra[i];
+      lds_b[buf][r * 8 + (kc ^ (r & 7))] = rb[i];
+    }
+  };
+
+  // Wave tile: rows wm*64 + [0,64); B rows: EPI 0 -> gate wn*64+[0,64) and up 128+wn*64+[0,64),
+  // EPI 1 -> wn*128 + [0,128). Fragment j covers 32 B rows.
+  int brow_base[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (EPI == 0) brow_base[j] = (j < 2 ? 0 : 128) + wn * 64 + (j & 1) * 32;
+    else brow_base[j] = wn * 128 + j * 32;
+  }
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = Kdim / BK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * BK);
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int ch = kk * 2 + (lane >> 5);
+      u32x4 af[2], bf[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int r = wm * 64 + i * 32 + (lane & 31);
+        af[i] = lds_a[buf][r * 8 + (ch ^ (r & 7))];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = brow_base[j] + (lane & 31);
+        bf[j] = lds_b[buf][r * 8 + (ch ^ (r & 7))];
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_32x32x16(af[i], bf[j], acc[i][j]);
+    }
+    if (kt + 1 < nk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue. acc[i][j][4*jj+ii] is row wm*64 + i*32 + 8*jj + 4*(lane>>5) + ii,
+  // column (lane & 31) of fragment j.
+  const int col_in = lane & 31;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int row = row0 + wm * 64 + i * 32 + 8 * jj + 4 * (lane >> 5) + ii;
+        if (row >= row_end) continue;
+        const int r = 4 * jj + ii;
+        if (EPI == 0) {
+          uint16_t* H = static_cast<uint16_t*>(p.out);
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const int col = n0 + wn * 64 + j * 32 + col_in;
+            if (col < Ndim) {
+              const float h = silu(acc[i][j][r]) * acc[i][j + 2][r];
+              H[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(h);
+            }
+          }
+        } else {
+          float* O = static_cast<float*>(p.out);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int col = n0 + wn * 128 + j * 32 + col_in;
+            if (col < Ndim) O[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
+          }
+        }
+      }
+    }
+  }
+}
+
+// y_t = sum_k gate[t,k] * O[inv[t*K+k]] + sum_s O[T*K + s*T + t]; fp32 sum in k order, one
+// rounding at the end. One workgroup per token.
+template <bool BF16>
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
+                                                       const int32_t* __restrict__ inv,
+                                                       const float* __restrict__ gate, int T, int K,
+                                                       int n_shared, int d, void* y) {
+  const int t = blockIdx.x;
+  if (BF16) {  // d % 4 == 0
+    for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
+      float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int k = 0; k < K; ++k) {
+        const float gk = gate[t * K + k];
+        const float4 v = *reinterpret_cast<const float4*>(O + static_cast<size_t>(inv[t * K + k]) * d + c);
+        s.x += gk * v.x; s.y += gk * v.y; s.z += gk * v.z; s.w += gk * v.w;
+      }
+      for (int sh = 0; sh < n_shared; ++sh) {
+        const float4 v = *reinterpret_cast<const float4*>(O + (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c);
+        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+      }
+      uint2 packed;
+      packed.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
+      packed.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d + c) = packed;
+    }
+  } else {
+    for (int c = threadIdx.x; c < d; c += 256) {
+      float s = 0.0f;
+      for (int k = 0; k < K; ++k) s += gate[t * K + k] * O[static_cast<size_t>(inv[t * K + k]) * d + c];
+      for (int sh = 0; sh < n_shared; ++sh) s += O[(static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c];
+      static_cast<float*>(y)[static_cast<size_t>(t) * d + c] = s;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ bf16 decode kernels
+
+constexpr int DEC_GU_COLS = 32;     // H columns per workgroup (gate/up kernel)
+constexpr int DEC_GU_WAVES = 4;
+constexpr int DEC_DN_COLS = 16;     // y columns per workgroup (down + combine kernel)
+constexpr int DEC_DN_WAVES = 8;
+
+struct DecodeArgs {
+  const uint16_t* x;
+  const int32_t* row_tok;
+  const int32_t* perm;
+  const float* gate;
+  const int32_t* offsets;
+  const int32_t* active;
+  const int32_t* n_active;
+  const uint16_t* w_gate_up;
+  const uint16_t* w_down;
+  const uint16_t* ws_gate_up;
+  const uint16_t* ws_down;
+  uint16_t* H;
+  uint16_t* y;
+  int T, d, F, E, K;
+};
+
+__global__ __launch_bounds__(64 * DEC_GU_WAVES) void decode_gate_up_kernel(const DecodeArgs p) {
+  __shared__ f32x4 red[DEC_GU_WAVES][4][64];
+  const int slot = blockIdx.y;
+  if (slot >= p.n_active[0]) return;
+  const int g = p.active[slot];
+  const int row0 = p.offsets[g];
+  const int nrows = p.offsets[g + 1] - row0;   // 1..16
+  const int n0 = blockIdx.x * DEC_GU_COLS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kg = (lane >> 4) * 8;
+  const int rr = min(lane & 15, nrows - 1);
+  const uint16_t* ap = p.x + static_cast<size_t>(p.row_tok[row0 + rr]) * p.d + kg;
+  const uint16_t* wg = g < p.E ? p.w_gate_up + static_cast<size_t>(g) * 2 * p.F * p.d
+                               : p.ws_gate_up + static_cast<size_t>(g - p.E) * 2 * p.F * p.d;
+  const uint16_t* bp[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {  // j = 0,1 gate columns; j = 2,3 the matching up columns
+    const int n = n0 + (j & 1) * 16 + (lane & 15);
+    bp[j] = wg + static_cast<size_t>(j < 2 ? n : p.F + n) * p.d + kg;
+  }
+  f32x4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int ksteps = p.d >> 5;
+  constexpr int U = 4;  // k-steps whose loads are issued together
+  int s = wave;
+  for (; s + (U - 1) * DEC_GU_WAVES < ksteps; s += U * DEC_GU_WAVES) {
+    u32x4 a[U], b[U][4];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = (s + u * DEC_GU_WAVES) << 5;
+      a[u] = *reinterpret_cast<const u32x4*>(ap + k);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[u][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp[j] + k));
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = mfma_16x16x32(a[u], b[u][j], acc[j]);
+  }
+  for (; s < ksteps; s += DEC_GU_WAVES) {
+    const int k = s << 5;
+    const u32x4 a = *reinterpret_cast<const u32x4*>(ap + k);
+    u32x4 b[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp[j] + k));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = mfma_16x16x32(a, b[j], acc[j]);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) red[wave][j][lane] = acc[j];
+  __syncthreads();
+  if (tid < 128) {  // (pair j in {0,1}, lane l): gate fragment j with up fragment j+2
+    const int j = tid >> 6, l = tid & 63;
+    f32x4 gs = red[0][j][l], us = red[0][j + 2][l];
+#pragma unroll
+    for (int w = 1; w < DEC_GU_WAVES; ++w) {
+      gs += red[w][j][l];
+      us += red[w][j + 2][l];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * (l >> 4) + i;
+      if (row < nrows) {
+        const int col = n0 + j * 16 + (l & 15);
+        p.H[static_cast<size_t>(row0 + row) * p.F + col] = f32_to_bf16(silu(gs[i]) * us[i]);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(64 * DEC_DN_WAVES) void decode_down_combine_kernel(const DecodeArgs p) {
+  __shared__ f32x4 red[DEC_DN_WAVES][64];
+  __shared__ float yacc[kDecodeMaxT][DEC_DN_COLS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.x * DEC_DN_COLS;
+  const int kg = (lane >> 4) * 8;
+  if (tid < kDecodeMaxT * DEC_DN_COLS) yacc[tid / DEC_DN_COLS][tid % DEC_DN_COLS] = 0.0f;
+  const int na = p.n_active[0];
+  const int ksteps = p.F >> 5;
+  for (int slot = 0; slot < na; ++slot) {
+    const int g = p.active[slot];
+    const int row0 = p.offsets[g];
+    const int nrows = p.offsets[g + 1] - row0;
+    const int rr = min(lane & 15, nrows - 1);
+    const uint16_t* ap = p.H + static_cast<size_t>(row0 + rr) * p.F + kg;
+    const uint16_t* wd = g < p.E ? p.w_down + static_cast<size_t>(g) * p.d * p.F
+                                 : p.ws_down + static_cast<size_t>(g - p.E) * p.d * p.F;
+    const uint16_t* bp = wd + static_cast<size_t>(n0 + (lane & 15)) * p.F + kg;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    constexpr int U = 8;  // k-steps whose loads are issued together
+    int s = wave;
+    for (; s + (U - 1) * DEC_DN_WAVES < ksteps; s += U * DEC_DN_WAVES) {
+      u32x4 a[U], b[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = (s + u * DEC_DN_WAVES) << 5;
+        a[u] = *reinterpret_cast<const u32x4*>(ap + k);
+        b[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp + k));
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) acc = mfma_16x16x32(a[u], b[u], acc);
+    }
+    for (; s < ksteps; s += DEC_DN_WAVES) {
+      const int k = s << 5;
+      const u32x4 a = *reinterpret_cast<const u32x4*>(ap + k);
+      const u32x4 b = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp + k));
+      acc = mfma_16x16x32(a, b, acc);
+    }
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (tid < kDecodeMaxT * DEC_DN_COLS) {
+      const int r = tid / DEC_DN_COLS, c = tid % DEC_DN_COLS;
+      if (r < nrows) {
+        const int l = (r >> 2) * 16 + c, i = r & 3;
+        float v = red[0][l][i];
+#pragma unroll
+        for (int w = 1; w < DEC_DN_WAVES; ++w) v += red[w][l][i];
+        const int pos = row0 + r;
+        float gt = 1.0f;
+        int t;
+        if (g < p.E) {
+          const int j = p.perm[pos];
+          t = j / p.K;
+          gt = p.gate[j];
+        } else {
+          t = p.row_tok[pos];
+        }
+        yacc[t][c] += gt * v;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid < kDecodeMaxT * DEC_DN_COLS) {
+    const int t = tid / DEC_DN_COLS, c = tid % DEC_DN_COLS;
+    if (t < p.T) p.y[static_cast<size_t>(t) * p.d + n0 + c] = f32_to_bf16(yacc[t][c]);
+  }
+}
+
+// ------------------------------------------------------------------ f32 kernels
+
+__device__ __forceinline__ int group_of_row(const int32_t* offsets, int G, int pos) {
+  int lo = 0, hi = G;  // offsets[lo] <= pos < offsets[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (offsets[mid] <= pos) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+struct F32Args {
+  const float* x;
+  const int32_t* row_tok;
+  const int32_t* offsets;
+  const float* w_gate_up;
+  const float* w_down;
+  const float* ws_gate_up;
+  const float* ws_down;
+  float* H;
+  float* O;
+  int rows, d, F, E, G;
+};
+
+__global__ __launch_bounds__(256) void f32_gate_up_kernel(const F32Args p) {
+  const size_t id = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (id >= static_cast<size_t>(p.rows) * p.F) return;
+  const int pos = static_cast<int>(id / p.F), n = static_cast<int>(id % p.F);
+  const int g = group_of_row(p.offsets, p.G, pos);
+  const float* w = g < p.E ? p.w_gate_up + static_cast<size_t>(g) * 2 * p.F * p.d
+                           : p.ws_gate_up + static_cast<size_t>(g - p.E) * 2 * p.F * p.d;
+  const float* xr = p.x + static_cast<size_t>(p.row_tok[pos]) * p.d;
+  const float* wg = w + static_cast<size_t>(n) * p.d;
+  const float* wu = w + static_cast<size_t>(p.F + n) * p.d;
+  float a = 0.0f, b = 0.0f;
+  for (int k = 0; k < p.d; ++k) {
+    a = fmaf(xr[k], wg[k], a);
+    b = fmaf(xr[k], wu[k], b);
+  }
+  p.H[id] = (a / (1.0f + expf(-a))) * b;
+}
+
+__global__ __launch_bounds__(256) void f32_down_kernel(const F32Args p) {
+  const size_t id = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (id >= static_cast<size_t>(p.rows) * p.d) return;
+  const int pos = static_cast<int>(id / p.d), n = static_cast<int>(id % p.d);
+  const int g = group_of_row(p.offsets, p.G, pos);
+  const float* w = g < p.E ? p.w_down + static_cast<size_t>(g) * p.d * p.F
+                           : p.ws_down + static_cast<size_t>(g - p.E) * p.d * p.F;
+  const float* h = p.H + static_cast<size_t>(pos) * p.F;
+  const float* wr = w + static_cast<size_t>(n) * p.F;
+  float a = 0.0f;
+  for (int k = 0; k < p.F; ++k) a = fmaf(h[k], wr[k], a);
+  p.O[id] = a;
+}
+
+}  // namespace
+
+hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
+                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks) {
+  const int G = a.E + a.n_shared;
+  GemmArgs g;
+  g.row_tok = pb.row_tok;
+  g.offsets = pb.offsets;
+  g.tile_off = pb.tile_off;
+  g.G = G; g.E = a.E; g.F = a.F; g.d = a.d;
+  g.mt_max = max_tiles;
+
+  g.a = static_cast<const uint16_t*>(a.x);
+  g.w = static_cast<const uint16_t*>(a.w_gate_up);
+  g.ws = static_cast<const uint16_t*>(a.ws_gate_up);
+  g.out = H;
+  const int nt1 = (a.F + BN / 2 - 1) / (BN / 2);
+  hipLaunchKernelGGL(grouped_gemm_bf16<0>, dim3(max_tiles * nt1), dim3(GEMM_THREADS), 0, stream, g);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  record_mark(marks, 0, stream);
+
+  g.a = H;
+  g.w = static_cast<const uint16_t*>(a.w_down);
+  g.ws = static_cast<const uint16_t*>(a.ws_down);
+  g.out = O;
+  const int nt2 = (a.d + BN - 1) / BN;
+  hipLaunchKernelGGL(grouped_gemm_bf16<1>, dim3(max_tiles * nt2), dim3(GEMM_THREADS), 0, stream, g);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  record_mark(marks, 1, stream);
+
+  hipLaunchKernelGGL(combine_kernel<true>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
+                     a.K, a.n_shared, a.d, y);
+  err = hipGetLastError();
+  record_mark(marks, 2, stream);
+  return err;
+}
+
+hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H,
+                                      void* y, hipStream_t stream, hipEvent_t* marks) {
+  DecodeArgs p;
+  p.x = static_cast<const uint16_t*>(a.x);
+  p.row_tok = pb.row_tok;
+  p.perm = pb.perm;
+  p.gate = a.gate;
+  p.offsets = pb.offsets;
+  p.active = pb.active;
+  p.n_active = pb.n_active;
+  p.w_gate_up = static_cast<const uint16_t*>(a.w_gate_up);
+  p.w_down = static_cast<const uint16_t*>(a.w_down);
+  p.ws_gate_up = static_cast<const uint16_t*>(a.ws_gate_up);
+  p.ws_down = static_cast<const uint16_t*>(a.ws_down);
+  p.H = H;
+  p.y = static_cast<uint16_t*>(y);
+  p.T = a.T; p.d = a.d; p.F = a.F; p.E = a.E; p.K = a.K;
+  const int max_active = (a.T * a.K < a.E ? a.T * a.K : a.E) + a.n_shared;
+  hipLaunchKernelGGL(decode_gate_up_kernel, dim3(a.F / DEC_GU_COLS, max_active), dim3(64 * DEC_GU_WAVES),
+                     0, stream, p);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  record_mark(marks, 0, stream);
+  hipLaunchKernelGGL(decode_down_combine_kernel, dim3(a.d / DEC_DN_COLS), dim3(64 * DEC_DN_WAVES), 0,
+                     stream, p);
+  err = hipGetLastError();
+  record_mark(marks, 1, stream);
+  record_mark(marks, 2, stream);
+  return err;
+}
+
+hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float* H, float* O,
+                              void* y, hipStream_t stream, hipEvent_t* marks) {
+  F32Args p;
+  p.x = static_cast<const float*>(a.x);
+  p.row_tok = pb.row_tok;
+  p.offsets = pb.offsets;
+  p.w_gate_up = static_cast<const float*>(a.w_gate_up);
+  p.w_down = static_cast<const float*>(a.w_down);
+  p.ws_gate_up = static_cast<const float*>(a.ws_gate_up);
+  p.ws_down = static_cast<const float*>(a.ws_down);
+  p.H = H;
+  p.O = O;
+  p.rows = a.T * (a.K + a.n_shared);
+  p.d = a.d; p.F = a.F; p.E = a.E; p.G = a.E + a.n_shared;
+  const size_t n1 = static_cast<size_t>(p.rows) * a.F, n2 = static_cast<size_t>(p.rows) * a.d;
+  hipLaunchKernelGGL(f32_gate_up_kernel, dim3((n1 + 255) / 256), dim3(256), 0, stream, p);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  record_mark(marks, 0, stream);
+  hipLaunchKernelGGL(f32_down_kernel, dim3((n2 + 255) / 256), dim3(256), 0, stream, p);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  record_mark(marks, 1, stream);
+  hipLaunchKernelGGL(combine_kernel<false>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
+                     a.K, a.n_shared, a.d, y);
+  err = hipGetLastError();
+  record_mark(marks, 2, stream);
+  return err;
+}
+
+}  // namespace maskmoe

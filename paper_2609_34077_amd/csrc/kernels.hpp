@@ -1,0 +1,71 @@
+// Internal launchers of the masked-MoE kernels. Every launcher enqueues on `stream` and
+// returns hipSuccess or the launch error; arguments are validated by the C-ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace maskmoe {
+
+// Router logits + softmax + mask/prior Top-K + gates for layers [0, L) of w_router
+// ([L, E, d]); host `mask` [L, E] (HARD_MASK) or `prior` [L, E] (SOFT_PRIOR), unused for
+// PLAIN. Outputs idx/gate [L, T, K], margin [L, T].
+hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
+                        int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
+                        int32_t* idx, float* gate, float* margin, hipStream_t stream);
+
+// Group the T*K routed (token, slot) entries by expert, stably in entry order, and append
+// n_shared groups of all T tokens. Writes offsets/tile_off [G+1], active [G], n_active [1],
+// perm/inv [T*K], row_tok [T*(K+n_shared)], with G = E + n_shared.
+struct PermBuffers {
+  int32_t* offsets;
+  int32_t* tile_off;
+  int32_t* active;
+  int32_t* n_active;
+  int32_t* perm;
+  int32_t* inv;
+  int32_t* row_tok;
+};
+hipError_t launch_permute(const int32_t* idx, int T, int K, int E, int n_shared, int tile_rows,
+                          const PermBuffers& pb, hipStream_t stream);
+
+// Row-tile size of the bf16 grouped GEMMs (the permutation counts tiles of this many rows).
+constexpr int kGemmBM = 256;
+// Tokens at or below which the bf16 layer uses the weight-streaming decode kernels.
+constexpr int kDecodeMaxT = 16;
+
+struct ExpertArgs {
+  const void* x;           // [T, d]
+  const void* w_gate_up;   // [E, 2F, d]
+  const void* w_down;      // [E, d, F]
+  const void* ws_gate_up;  // [n_shared, 2F, d]
+  const void* ws_down;     // [n_shared, d, F]
+  const float* gate;       // [T, K]
+  int T, d, F, E, K, n_shared;
+};
+
+// Optional stage markers: when `marks` is non-null, marks[i] is recorded on the stream after
+// the i-th of the three expert stages (gate/up, down, combine); a stage that a path fuses
+// away is marked right after the previous one.
+inline void record_mark(hipEvent_t* marks, int i, hipStream_t stream) {
+  if (marks) (void)hipEventRecord(marks[i], stream);
+}
+
+// bf16, T > kDecodeMaxT: H = SwiGLU(X_g W_gate,up^T) per group; O = H W_down^T; y = combine.
+hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
+                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks);
+// bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel, then down projection fused with
+// the gate-weighted combine.
+hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H,
+                                      void* y, hipStream_t stream, hipEvent_t* marks);
+// f32 path (no MFMA; fp32 end to end).
+hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float* H, float* O,
+                              void* y, hipStream_t stream, hipEvent_t* marks);
+
+// Per-(layer, stream) expert cache replay (LRU), one wavefront per stream.
+hipError_t launch_cache_lru(const int32_t* trace, int L, int S, int N, int K, int E, int B,
+                            int32_t* state, int64_t* fetches, int64_t* hits, uint8_t* f_per_step,
+                            int32_t* dev_error, hipStream_t stream);
+
+}  // namespace maskmoe

@@ -1,0 +1,291 @@
+// Router logits + softmax + hard-mask / soft-prior Top-K + gates, fused in one kernel.
+//
+// Section 3.1 (Eq. 1): z = W x, p = softmax(z), A = Top-K(p), gates g_i = p_i or
+// p_i / sum_{j in A} p_j. Section 3.2, Stage 1 (Eq. 2): A = Top-K(p * m) with a binary
+// mask m; the gates computed from p * m equal those of p on A. Section 3.2, inference
+// (Eq. 4): A = Top-K(p * pi) with a prior pi > 0; gates stay those of p.
+//
+// Experts are ranked on log-domain keys z_i + c_i, with c_i = 0 (plain), 0 or -inf
+// (mask), log pi_i (prior); softmax is monotone with a shared normaliser, so these order
+// experts exactly as the products do and avoid ties from exp underflow. Equal keys go to
+// the lower expert index.
+//
+// bf16 logits use v_mfma_f32_16x16x32_bf16: a workgroup computes a tile of
+// (16*MB tokens) x (16*NB*WN outputs), where outputs are the rows of [L*E, d] router
+// weights of whole layers; its WN*WK waves split the outputs (WN) and the k-steps (WK)
+// and the WK partial tiles are summed in LDS in a fixed order. Small token counts
+// (decode) use WK = 8..16 so all of d is in flight at once; large token counts stream x.
+// The selection runs one thread per (token, layer) on the fp32 logits in LDS.
+
+#include <math.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace maskmoe {
+namespace {
+
+constexpr int kMaxK = 16;
+constexpr int kMaxModeParams = 512;
+
+struct RouteParams {
+  const void* x;
+  const void* w;       // [L, E, d] router weights of this launch's first layer
+  int32_t* idx;        // [L, T, K]
+  float* gate;         // [L, T, K]
+  float* margin;       // [L, T] or null
+  int T, d, E, K, L, lpw, mode, gate_mode;
+  float modep[kMaxModeParams];  // [L, E]: mask (0/1) or prior values of this launch
+};
+
+__device__ __forceinline__ float key_offset(int mode, float v) {
+  if (mode == 1) return v != 0.0f ? 0.0f : -INFINITY;  // hard mask
+  if (mode == 2) return logf(v);                        // soft prior
+  return 0.0f;                                          // plain
+}
+
+// Selection and gates for every (token, layer) pair of the tile. logits[tt * ld + lw*E + e]
+// are the fp32 router logits, lo[lw*E + e] the key offsets.
+__device__ void route_finalize(const RouteParams& p, const float* logits, int ld, const float* lo,
+                               int t0, int TT, int lg0, int nl) {
+  const int E = p.E, K = p.K;
+  for (int pi = threadIdx.x; pi < TT * nl; pi += blockDim.x) {
+    const int tt = pi / nl, lw = pi - tt * nl;
+    const int t = t0 + tt;
+    if (t >= p.T) continue;
+    const float* z = logits + tt * ld + lw * E;
+    const float* o = lo + lw * E;
+    const size_t obase = (static_cast<size_t>(lg0 + lw) * p.T + t);
+
+    uint64_t tk0 = 0, tk1 = 0, tk2 = 0, tk3 = 0;
+    int sel[kMaxK];
+    float selz[kMaxK];
+    float kth = -INFINITY, nxt = -INFINITY;
+#pragma unroll
+    for (int j = 0; j <= kMaxK; ++j) {
+      if (j <= K) {
+        float best = -INFINITY;
+        int bi = -1;
+        for (int e = 0; e < E; ++e) {
+          const uint64_t word = e < 64 ? tk0 : e < 128 ? tk1 : e < 192 ? tk2 : tk3;
+          if ((word >> (e & 63)) & 1ull) continue;
+          const float key = z[e] + o[e];
+          if (key > best) {
+            best = key;
+            bi = e;
+          }
+        }
+        if (j < K) {
+          if (bi < 0) {  // only reachable with non-finite logits: keep the output well formed
+            for (int e = 0; e < E && bi < 0; ++e) {
+              const uint64_t word = e < 64 ? tk0 : e < 128 ? tk1 : e < 192 ? tk2 : tk3;
+              if (!((word >> (e & 63)) & 1ull)) bi = e;
+            }
+          }
+          const uint64_t bit = 1ull << (bi & 63);
+          if (bi < 64) tk0 |= bit; else if (bi < 128) tk1 |= bit; else if (bi < 192) tk2 |= bit; else tk3 |= bit;
+          sel[j] = bi;
+          selz[j] = z[bi];
+          kth = best;
+        } else {
+          nxt = best;
+        }
+      }
+    }
+
+    float zref, norm = 0.0f;
+    if (p.gate_mode == 0) {  // g = p_i: full softmax over all E experts
+      zref = z[0];
+      for (int e = 1; e < E; ++e) zref = fmaxf(zref, z[e]);
+      for (int e = 0; e < E; ++e) norm += expf(z[e] - zref);
+    } else {  // g = p_i / sum_{j in A} p_j
+      zref = selz[0];
+#pragma unroll
+      for (int j = 1; j < kMaxK; ++j)
+        if (j < K) zref = fmaxf(zref, selz[j]);
+#pragma unroll
+      for (int j = 0; j < kMaxK; ++j)
+        if (j < K) norm += expf(selz[j] - zref);
+    }
+    const float inv = 1.0f / norm;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      if (j < K) {
+        p.idx[obase * K + j] = sel[j];
+        p.gate[obase * K + j] = expf(selz[j] - zref) * inv;
+      }
+    }
+    if (p.margin) p.margin[obase] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+  }
+}
+
+template <int MB, int NB, int WN, int WK>
+__global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RouteParams p) {
+  constexpr int TT = 16 * MB, NO = 16 * NB * WN, NT = 64 * WN * WK;
+  __shared__ float red[WK * TT * NO];
+  __shared__ float lo[NO];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wn = wave % WN, wk = wave / WN;
+  const int t0 = blockIdx.x * TT;
+  const int lg0 = blockIdx.y * p.lpw;
+  const int nl = min(p.lpw, p.L - lg0);
+  const int nout = nl * p.E;
+  const uint16_t* x = static_cast<const uint16_t*>(p.x);
+  const uint16_t* w = static_cast<const uint16_t*>(p.w) + static_cast<size_t>(lg0) * p.E * p.d;
+  const int ksteps = p.d >> 5;
+  const int kg = (lane >> 4) * 8;
+
+  // Rows past the last token / output are clamped onto valid rows; their results are
+  // never written, and MFMA rows and columns do not mix.
+  const uint16_t* ap[MB];
+  const uint16_t* bp[NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int t = min(t0 + mb * 16 + (lane & 15), p.T - 1);
+    ap[mb] = x + static_cast<size_t>(t) * p.d + kg;
+  }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int o = min((wn * NB + nb) * 16 + (lane & 15), nout - 1);
+    bp[nb] = w + static_cast<size_t>(o) * p.d + kg;
+  }
+  f32x4 acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // k-steps wk, wk+WK, ...; groups of U steps are loaded before any is multiplied.
+  constexpr int U = (MB + NB) <= 2 ? 8 : 4;
+  int s = wk;
+  for (; s + (U - 1) * WK < ksteps; s += U * WK) {
+    u32x4 av[U][MB], bv[U][NB];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = (s + u * WK) << 5;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) av[u][mb] = *reinterpret_cast<const u32x4*>(ap[mb] + k);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) bv[u][nb] = *reinterpret_cast<const u32x4*>(bp[nb] + k);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma_16x16x32(av[u][mb], bv[u][nb], acc[mb][nb]);
+  }
+  for (; s < ksteps; s += WK) {
+    const int k = s << 5;
+    u32x4 av[MB], bv[NB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) av[mb] = *reinterpret_cast<const u32x4*>(ap[mb] + k);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) bv[nb] = *reinterpret_cast<const u32x4*>(bp[nb] + k);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma_16x16x32(av[mb], bv[nb], acc[mb][nb]);
+  }
+
+  float* r = red + wk * TT * NO;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        r[(mb * 16 + (lane >> 4) * 4 + i) * NO + (wn * NB + nb) * 16 + (lane & 15)] = acc[mb][nb][i];
+  for (int i = threadIdx.x; i < nout; i += NT) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
+  __syncthreads();
+  if (WK > 1) {
+    for (int i = threadIdx.x; i < TT * NO; i += NT) {
+      float s = red[i];
+#pragma unroll
+      for (int q = 1; q < WK; ++q) s += red[q * TT * NO + i];
+      red[i] = s;
+    }
+    __syncthreads();
+  }
+  route_finalize(p, red, NO, lo, t0, TT, lg0, nl);
+}
+
+// fp32 router: plain fp32 dot products (no MFMA), one thread per (token, output).
+constexpr int kF32TT = 16;
+__global__ __launch_bounds__(256) void route_f32_kernel(const RouteParams p) {
+  __shared__ float logits[kF32TT * 256];
+  __shared__ float lo[256];
+  const int t0 = blockIdx.x * kF32TT;
+  const int lg0 = blockIdx.y * p.lpw;
+  const int nl = min(p.lpw, p.L - lg0);
+  const int nout = nl * p.E;
+  const float* x = static_cast<const float*>(p.x);
+  const float* w = static_cast<const float*>(p.w) + static_cast<size_t>(lg0) * p.E * p.d;
+  for (int i = threadIdx.x; i < kF32TT * nout; i += blockDim.x) {
+    const int tt = i / nout, o = i - tt * nout;
+    const int t = min(t0 + tt, p.T - 1);
+    const float* xr = x + static_cast<size_t>(t) * p.d;
+    const float* wr = w + static_cast<size_t>(o) * p.d;
+    float s = 0.0f;
+    for (int k = 0; k < p.d; ++k) s = fmaf(xr[k], wr[k], s);
+    logits[tt * 256 + o] = s;
+  }
+  for (int i = threadIdx.x; i < nout; i += blockDim.x) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
+  __syncthreads();
+  route_finalize(p, logits, 256, lo, t0, kF32TT, lg0, nl);
+}
+
+template <int MB, int NB, int WN, int WK>
+hipError_t launch_bf16(RouteParams& p, hipStream_t stream) {
+  constexpr int TT = 16 * MB, NO = 16 * NB * WN;
+  p.lpw = NO / p.E < 1 ? 1 : NO / p.E;
+  if (p.lpw > p.L) p.lpw = p.L;
+  dim3 grid((p.T + TT - 1) / TT, (p.L + p.lpw - 1) / p.lpw);
+  hipLaunchKernelGGL((route_bf16_kernel<MB, NB, WN, WK>), grid, dim3(64 * WN * WK), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
+                        int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
+                        int32_t* idx, float* gate, float* margin, hipStream_t stream) {
+  if (T == 0 || L == 0) return hipSuccess;
+  // Layers are processed in launches whose (layer, expert) parameters fit in the kernel
+  // arguments; every launch covers whole layers.
+  const int max_layers = kMaxModeParams / E;
+  const size_t esz = bf16 ? 2 : 4;
+  for (int l0 = 0; l0 < L; l0 += max_layers) {
+    RouteParams p;
+    p.x = x;
+    p.w = static_cast<const char*>(w_router) + static_cast<size_t>(l0) * E * d * esz;
+    p.idx = idx + static_cast<size_t>(l0) * T * K;
+    p.gate = gate + static_cast<size_t>(l0) * T * K;
+    p.margin = margin ? margin + static_cast<size_t>(l0) * T : nullptr;
+    p.T = T; p.d = d; p.E = E; p.K = K;
+    p.L = L - l0 < max_layers ? L - l0 : max_layers;
+    p.mode = mode; p.gate_mode = gate_mode;
+    for (int i = 0; i < p.L * E; ++i) {
+      const size_t gi = static_cast<size_t>(l0) * E + i;
+      p.modep[i] = mode == 1 ? (mask[gi] ? 1.0f : 0.0f) : mode == 2 ? prior[gi] : 1.0f;
+    }
+    hipError_t err;
+    if (!bf16) {
+      p.lpw = 256 / E < 1 ? 1 : 256 / E;
+      if (p.lpw > p.L) p.lpw = p.L;
+      dim3 grid((T + kF32TT - 1) / kF32TT, (p.L + p.lpw - 1) / p.lpw);
+      hipLaunchKernelGGL(route_f32_kernel, grid, dim3(256), 0, stream, p);
+      err = hipGetLastError();
+    } else {
+      const int need = p.L * E < 256 ? p.L * E : 256;
+      const bool small = T <= 128;
+      if (need <= 16) err = small ? launch_bf16<1, 1, 1, 16>(p, stream) : launch_bf16<1, 1, 1, 4>(p, stream);
+      else if (need <= 64) err = small ? launch_bf16<1, 4, 1, 8>(p, stream) : launch_bf16<2, 4, 1, 4>(p, stream);
+      else err = small ? launch_bf16<1, 4, 4, 2>(p, stream) : launch_bf16<2, 4, 4, 1>(p, stream);
+    }
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
+}
+
+}  // namespace maskmoe

@@ -1,0 +1,141 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared entry point,
+and rejects invalid arguments before touching the device; workspace sizing is monotone."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT
+from paper_2609_34077_amd import _lib as L
+
+HEADER = os.path.join(ROOT, "include", "maskmoe.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="libmaskmoe.so not built")
+
+FAKE = 0x10000  # a 256-byte aligned non-null address; only used where validation must fail
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(maskmoe_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert set(names) == set(L.EXPORTS)
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    lib = L.load()
+    for code in range(6):
+        assert lib.maskmoe_status_string(code)
+    assert lib.maskmoe_status_string(99) == b"unknown status"
+
+
+def _route(desc, Lyr=1, x=FAKE, w=FAKE, mask=None, prior=None, idx=FAKE, gate=FAKE, margin=None):
+    lib = L.load()
+    return lib.maskmoe_route(ctypes.byref(desc), Lyr, x, w, mask, prior, idx, gate, margin, None)
+
+
+def test_route_rejects_invalid_arguments():
+    good = dict(T=4, d=64, E=8, K=2, dtype=L.BF16, route_mode=L.ROUTE_PLAIN, gate_mode=L.GATE_RENORM)
+    bad = [dict(T=-1), dict(d=0), dict(E=0), dict(E=257), dict(K=0), dict(K=9), dict(E=32, K=17),
+           dict(dtype=7), dict(route_mode=3), dict(gate_mode=2)]
+    for b in bad:
+        desc = L.make_desc(**{**good, **b})
+        assert _route(desc) == L.E_INVAL, b
+    desc = L.make_desc(**good)
+    assert _route(desc, Lyr=0) == L.E_INVAL
+    assert _route(desc, x=None) == L.E_INVAL
+    assert _route(desc, idx=None) == L.E_INVAL
+    assert _route(desc, x=FAKE + 2) == L.E_INVAL          # misaligned
+    assert _route(L.make_desc(**{**good, "d": 48})) == L.E_UNSUPPORTED
+
+
+def test_route_rejects_bad_mask_and_prior():
+    E, K = 8, 2
+    hard = L.make_desc(T=4, d=64, E=E, K=K, route_mode=L.ROUTE_HARD_MASK)
+    m = np.array([1, 0, 0, 0, 0, 0, 0, 0], np.uint8)                  # one expert < K
+    assert _route(hard, mask=m.ctypes.data_as(ctypes.c_void_p)) == L.E_INVAL
+    assert _route(hard, mask=None) == L.E_INVAL
+    m2 = np.array([[1, 1, 0, 0, 0, 0, 0, 0], [0, 0, 0, 0, 0, 0, 0, 1]], np.uint8)   # second layer bad
+    assert _route(hard, Lyr=2, mask=m2.ctypes.data_as(ctypes.c_void_p)) == L.E_INVAL
+    soft = L.make_desc(T=4, d=64, E=E, K=K, route_mode=L.ROUTE_SOFT_PRIOR)
+    for badv in (0.0, -0.1, np.inf, np.nan):
+        p = np.full(E, 1.0 / E, np.float32)
+        p[3] = badv
+        assert _route(soft, prior=p.ctypes.data_as(ctypes.c_void_p)) == L.E_INVAL
+    assert _route(soft, prior=None) == L.E_INVAL
+
+
+def test_route_with_no_tokens_is_a_no_op():
+    desc = L.make_desc(T=0, d=64, E=8, K=2)
+    assert _route(desc, x=None, w=None, idx=None, gate=None) == L.OK
+
+
+def _fwd(desc, ws_bytes=None, **kw):
+    lib = L.load()
+    a = dict(x=FAKE, w=FAKE, mask=None, prior=None, wgu=FAKE, wdn=FAKE, sgu=None, sdn=None, y=FAKE,
+             idx=None, gate=None, ws=FAKE)
+    a.update(kw)
+    if ws_bytes is None:
+        ws_bytes = lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+    return lib.maskmoe_layer_forward(ctypes.byref(desc), a["x"], a["w"], a["mask"], a["prior"], a["wgu"],
+                                     a["wdn"], a["sgu"], a["sdn"], a["y"], a["idx"], a["gate"], a["ws"],
+                                     ws_bytes, None)
+
+
+def test_layer_forward_rejects_invalid_arguments():
+    lib = L.load()
+    good = dict(T=32, d=128, E=8, K=2, F=256, n_shared=0, dtype=L.BF16, route_mode=L.ROUTE_PLAIN,
+                gate_mode=L.GATE_RENORM)
+    for b in (dict(F=0), dict(n_shared=-1), dict(n_shared=9), dict(K=0)):
+        assert _fwd(L.make_desc(**{**good, **b}), ws_bytes=1 << 30) == L.E_INVAL, b
+    desc = L.make_desc(**good)
+    assert _fwd(desc, y=None) == L.E_INVAL
+    assert _fwd(desc, wgu=None) == L.E_INVAL
+    assert _fwd(desc, x=FAKE + 8) == L.E_INVAL
+    assert _fwd(L.make_desc(**{**good, "n_shared": 1})) == L.E_INVAL       # shared weights missing
+    need = lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+    assert _fwd(desc, ws_bytes=need - 1) == L.E_WORKSPACE
+    assert _fwd(desc, ws=None) == L.E_WORKSPACE
+    assert _fwd(desc, ws=FAKE + 64) == L.E_WORKSPACE                        # not 256-byte aligned
+    assert _fwd(L.make_desc(**{**good, "F": 96}), ws_bytes=1 << 30) == L.E_UNSUPPORTED
+    assert _fwd(L.make_desc(**{**good, "d": 96}), ws_bytes=1 << 30) == L.E_UNSUPPORTED
+
+
+def test_workspace_bytes_monotone_in_tokens():
+    lib = L.load()
+    for (d, E, K, F, ns, dt) in ((4096, 8, 2, 14336, 0, L.BF16), (2048, 64, 6, 1408, 2, L.BF16),
+                                 (256, 8, 2, 512, 0, L.F32)):
+        prev = 0
+        for T in list(range(0, 40)) + [100, 1000, 8192]:
+            desc = L.make_desc(T, d, E, K, F, ns, dt)
+            b = lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+            assert b >= prev and b % 256 == 0
+            prev = b
+    assert lib.maskmoe_layer_workspace_bytes(ctypes.byref(L.make_desc(-1, 64, 8, 2, 64))) == 0
+
+
+def _cache(L_=1, S=1, N=4, K=2, E=8, B=4, policy=0, trace=FAKE, state=None, fetches=FAKE, hits=FAKE):
+    lib = L.load()
+    return lib.maskmoe_cache_fetches(trace, L_, S, N, K, E, B, policy, state, fetches, hits, None, None, None)
+
+
+def test_cache_rejects_invalid_arguments():
+    assert _cache(B=1) == L.E_INVAL          # B < K
+    assert _cache(K=0) == L.E_INVAL
+    assert _cache(K=9) == L.E_INVAL          # K > E
+    assert _cache(N=-1) == L.E_INVAL
+    assert _cache(policy=1) == L.E_INVAL
+    assert _cache(E=65, K=2) == L.E_UNSUPPORTED
+    assert _cache(N=1 << 23, K=2) == L.E_UNSUPPORTED
+    assert _cache(fetches=None) == L.E_INVAL
+    assert _cache(trace=None) == L.E_INVAL
+    assert _cache(L_=0, trace=None, fetches=None, hits=None) == L.OK   # nothing to do

@@ -1,0 +1,146 @@
+"""GPU parity of maskmoe_route against the oracle (Section 3.1 Eq. 1, Eq. 2, Eq. 4)."""
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_util as U
+from oracle import routing as R
+from paper_2609_34077_amd import _lib as L
+from paper_2609_34077_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(T, d, E, dtype, seed, Lyr=None):
+    g = np.random.default_rng(seed)
+    shape_w = (E, d) if Lyr is None else (Lyr, E, d)
+    x = g.standard_normal((T, d)).astype(np.float32)
+    w = (0.02 * g.standard_normal(shape_w)).astype(np.float32)
+    if dtype == "bf16":
+        return synth.bf16_bits(x), synth.bf16_bits(w)
+    return x, w
+
+
+def _run_and_check(T, d, E, K, mode, gate_mode, dtype, seed, mask=None, prior=None, max_near_frac=0.05):
+    U.say(f"route T={T} d={d} E={E} K={K} mode={mode} gate={gate_mode} {dtype} seed={seed}")
+    x, w = _inputs(T, d, E, dtype, seed)
+    idx, gate, margin = L.maskmoe_route(U.dev(x), U.dev(w), K, mode, gate_mode, mask=mask, prior=prior)
+    torch.cuda.synchronize()
+    z = R.router_logits(U.f64(x, dtype), U.f64(w, dtype))
+    near = U.check_routing(z, idx.cpu().numpy(), gate.cpu().numpy(), margin.cpu().numpy(), K, mode,
+                           gate_mode, mask, prior)
+    assert near <= max(2, int(T * max_near_frac))
+    U.say(f"  near-tie tokens {near} of {T}")
+    return idx, gate, margin
+
+
+MODES = [(L.ROUTE_PLAIN, None), (L.ROUTE_HARD_MASK, "mask"), (L.ROUTE_SOFT_PRIOR, "prior")]
+
+
+def _mp(kind, E, keep, delta=1.0):
+    if kind == "mask":
+        return dict(mask=synth.binary_mask(E, keep))
+    if kind == "prior":
+        return dict(prior=synth.concentrated_prior(E, keep, delta))
+    return {}
+
+
+@pytest.mark.parametrize("mode,kind", MODES)
+@pytest.mark.parametrize("gate_mode", [L.GATE_P, L.GATE_RENORM])
+def test_tiny_f32(mode, kind, gate_mode):
+    _run_and_check(64, 256, 8, 2, mode, gate_mode, "f32", 0, **_mp(kind, 8, [0, 2, 5, 7]))
+
+
+@pytest.mark.parametrize("T", [1, 4, 16, 17, 129, 1000])
+@pytest.mark.parametrize("mode,kind", MODES)
+def test_mixtral_shaped(T, mode, kind):
+    _run_and_check(T, 4096, 8, 2, mode, L.GATE_RENORM, "bf16", T, **_mp(kind, 8, [0, 2, 5, 7]))
+
+
+@pytest.mark.parametrize("T", [3, 333])
+@pytest.mark.parametrize("mode,kind", MODES)
+def test_deepseek_shaped(T, mode, kind):
+    _run_and_check(T, 2048, 64, 6, mode, L.GATE_P, "bf16", 100 + T, **_mp(kind, 64, synth.deepseek_mask_set()))
+
+
+@pytest.mark.parametrize("E,K,T", [(256, 16, 70), (256, 1, 200), (16, 16, 40), (5, 3, 33), (1, 1, 9)])
+def test_extreme_expert_counts(E, K, T):
+    # 256 experts with d = 128 put many keys within 1e-3 of each other: near-ties are common
+    _run_and_check(T, 128, E, K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, "bf16", E * 31 + K,
+                   prior=synth.concentrated_prior(E, list(range(0, E, 3)), 0.7), max_near_frac=0.6)
+
+
+@pytest.mark.parametrize("T", [5, 300])
+def test_multi_layer_trace_router(T):
+    Lyr, E, K, d = 32, 8, 2, 4096
+    U.say(f"route multi-layer L={Lyr} T={T}")
+    x, w = _inputs(T, d, E, "bf16", 77 + T, Lyr=Lyr)
+    cfg = synth.TraceConfig(L=Lyr)
+    sets = synth.trace_layer_sets(cfg)
+    prior = np.stack([synth.concentrated_prior(E, s, 1.0) for s in sets])
+    idx, gate, margin = L.maskmoe_route(U.dev(x), U.dev(w), K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=prior)
+    torch.cuda.synchronize()
+    xf = U.f64(x, "bf16")
+    wf = U.f64(w, "bf16")
+    idx, gate, margin = idx.cpu().numpy(), gate.cpu().numpy(), margin.cpu().numpy()
+    for l in range(Lyr):
+        z = R.router_logits(xf, wf[l])
+        U.check_routing(z, idx[l], gate[l], margin[l], K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=prior[l])
+
+
+def test_mode_equivalences_bit_exact():
+    T, d, E, K = 500, 1024, 8, 2
+    x, w = _inputs(T, d, E, "bf16", 5)
+    xd, wd = U.dev(x), U.dev(w)
+    ip, gp, mp = L.maskmoe_route(xd, wd, K, L.ROUTE_PLAIN, L.GATE_RENORM)
+    ih, gh, mh = L.maskmoe_route(xd, wd, K, L.ROUTE_HARD_MASK, L.GATE_RENORM, mask=np.ones(E, np.uint8))
+    iu, gu, mu = L.maskmoe_route(xd, wd, K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=np.full(E, 0.125, np.float32))
+    assert torch.equal(ip, ih) and torch.equal(gp, gh) and torch.equal(mp, mh)
+    # a uniform prior shifts every key by the same constant: same order up to sub-ulp ties
+    assert torch.equal(ip, iu) and torch.equal(gp, gu)
+    keep = [1, 6]
+    ik, gk, mk = L.maskmoe_route(xd, wd, K, L.ROUTE_HARD_MASK, L.GATE_RENORM, mask=synth.binary_mask(E, keep))
+    assert (ik.sort(dim=1).values.cpu() == torch.tensor(keep, dtype=torch.int32)).all()
+    assert torch.isinf(mk).all()
+
+
+def test_deterministic_repeat():
+    x, w = _inputs(777, 2048, 64, "bf16", 9)
+    xd, wd = U.dev(x), U.dev(w)
+    prior = synth.concentrated_prior(64, synth.deepseek_mask_set(), 1.0)
+    a = L.maskmoe_route(xd, wd, 6, L.ROUTE_SOFT_PRIOR, L.GATE_P, prior=prior)
+    b = L.maskmoe_route(xd, wd, 6, L.ROUTE_SOFT_PRIOR, L.GATE_P, prior=prior)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
+
+
+def test_empty_tokens():
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((8, 64), dtype=torch.bfloat16, device="cuda")
+    idx, gate, margin = L.maskmoe_route(x, w, 2, L.ROUTE_PLAIN, L.GATE_RENORM)
+    assert idx.shape == (0, 2)
+
+
+def test_full_trace_router_sampled():
+    """Routing-and-fetch trace router at full size (32 layers, 131072 AR(1) tokens); the
+    oracle checks a random sample of 1024 tokens in every layer."""
+    cfg = synth.TraceConfig()
+    U.say("route full trace: generating AR(1) inputs")
+    inp = synth.make_trace_inputs(cfg)
+    xd, wd = U.dev(inp["x"]), U.dev(inp["w_router"])
+    U.say("route full trace: running")
+    idx, gate, margin = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=inp["prior"])
+    torch.cuda.synchronize()
+    sample = np.sort(np.random.default_rng(3).choice(cfg.S * cfg.N, 1024, replace=False))
+    xs = U.f64(inp["x"][sample], "bf16")
+    ws = U.f64(inp["w_router"], "bf16")
+    sd = torch.from_numpy(sample).cuda()
+    ig, gg, mg = idx[:, sd].cpu().numpy(), gate[:, sd].cpu().numpy(), margin[:, sd].cpu().numpy()
+    for l in range(cfg.L):
+        U.check_routing(R.router_logits(xs, ws[l]), ig[l], gg[l], mg[l], cfg.K, L.ROUTE_SOFT_PRIOR,
+                        L.GATE_RENORM, prior=inp["prior"][l])
+    # properties at every token: distinct in-range experts, renormalised gates sum to 1
+    ia = idx.cpu().numpy()
+    assert ((ia >= 0) & (ia < cfg.E)).all() and (ia[..., 0] != ia[..., 1]).all()
+    np.testing.assert_allclose(gate.sum(-1).cpu().numpy(), 1.0, atol=1e-5)
