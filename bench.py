@@ -344,7 +344,8 @@ def main():
         res, st = run_layer(args)
         base = None if args.no_cpu_baseline else layer_cpu_baseline(st)
     res["cpu_baseline"] = base
-    res["device"] = torch.cuda.get_device_name(0)
+    pr = torch.cuda.get_device_properties(0)
+    res["device"] = f"{pr.name} ({pr.gcnArchName}, {pr.multi_processor_count} CUs, {pr.total_memory / 2**30:.0f} GiB)"
     print(json.dumps(res), flush=True)
 
 

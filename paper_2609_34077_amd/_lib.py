@@ -223,9 +223,10 @@ def maskmoe_cache_fetches(trace, E: int, B: int, state=None, with_f_per_step: bo
                           dev_error=None, policy: int = CACHE_LRU):
     """Replay traces [L,S,N,K] (int32 device) through per-(layer, stream) caches.
 
-    ``state`` [L,S,B] int32 device (in/out) or None. Returns a dict with
-    ``fetches``/``hits`` [L,S] int64, ``f_per_step`` [L,S,N] uint8 (or None)
-    and ``dev_error`` (int32 [1]).
+    ``state`` [L,S,B] int32 device (in/out) or None; ``dev_error`` an int32
+    device tensor that the kernel sets to 1 when it skips an entry (never
+    cleared), or None. Returns a dict with ``fetches``/``hits`` [L,S] int64,
+    ``f_per_step`` [L,S,N] uint8 (or None) and ``dev_error``.
     """
     import torch
     lib = load()
@@ -238,8 +239,6 @@ def maskmoe_cache_fetches(trace, E: int, B: int, state=None, with_f_per_step: bo
     fetches = torch.empty((L, S), dtype=torch.int64, device=dev)
     hits = torch.empty((L, S), dtype=torch.int64, device=dev)
     fps = torch.empty((L, S, N), dtype=torch.uint8, device=dev) if with_f_per_step else None
-    if dev_error is None:
-        dev_error = torch.zeros(1, dtype=torch.int32, device=dev)
     if state is not None and (state.dtype != torch.int32 or tuple(state.shape) != (L, S, B)):
         raise ValueError("state must be int32 [L,S,B]")
     _check("maskmoe_cache_fetches", lib.maskmoe_cache_fetches(

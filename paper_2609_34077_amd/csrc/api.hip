@@ -82,7 +82,11 @@ Layout layout(const maskmoe_layer_desc& d) {
   w.inv = take(TK * 4);
   w.row_tok = take(rows * 4);
   w.H = take(rows * d.F * hsz);
-  w.O = uses_decode_path(d) ? off : take(rows * d.d * 4);
+  // O holds the expert outputs: [rows, d], or [split, rows, d] on the few-token path. It is
+  // sized for the largest split (8) of up to kDecodeMaxT tokens so the total stays monotone in T.
+  const size_t dec_T = static_cast<size_t>(d.T < maskmoe::kDecodeMaxT ? d.T : maskmoe::kDecodeMaxT);
+  const size_t dec_rows = 8 * dec_T * (d.K + d.n_shared);
+  w.O = take((rows > dec_rows ? rows : dec_rows) * d.d * 4);
   w.total = off;
   return w;
 }
@@ -194,8 +198,8 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
     e = maskmoe::launch_experts_f32(a, pb, reinterpret_cast<float*>(ws + w.H), reinterpret_cast<float*>(ws + w.O),
                                     y, stream, expert_marks);
   } else if (uses_decode_path(d)) {
-    e = maskmoe::launch_experts_bf16_decode(a, pb, reinterpret_cast<uint16_t*>(ws + w.H), y, stream,
-                                            expert_marks);
+    e = maskmoe::launch_experts_bf16_decode(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
+                                            reinterpret_cast<float*>(ws + w.O), y, stream, expert_marks);
   } else {
     const int64_t TK = static_cast<int64_t>(d.T) * d.K;
     const int64_t nonempty = TK < d.E ? TK : d.E;

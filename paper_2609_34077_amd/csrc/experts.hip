@@ -16,11 +16,10 @@
 // fastest so the workgroups that share a weight slice run together, and the linear block
 // id is remapped so each XCD (L2) receives a contiguous range of tiles.
 //
-// bf16, few tokens (decode): the work is reading each selected expert's weights once.
-// The gate/up kernel gives every workgroup a 32-column slab of one active expert and
-// splits d over 4 waves; the down kernel gives every workgroup a 16-column slab of y,
-// loops over the active experts with F split over 8 waves, and applies the gates in LDS,
-// so the combine needs no extra pass. MFMA 16x16x32 with tokens padded to 16 rows.
+// bf16, few tokens (decode): the work is reading each selected expert's weights once; the
+// kernels stream weight rows through LDS in cache-line-sized row segments (see the decode
+// section below) and a split-K down projection keeps every CU busy when only two experts
+// are active. MFMA 16x16x32 with the token rows padded to 16.
 //
 // f32: plain fp32 loops (no MFMA), one thread per output element.
 
@@ -200,23 +199,34 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
 }
 
 // y_t = sum_k gate[t,k] * O[inv[t*K+k]] + sum_s O[T*K + s*T + t]; fp32 sum in k order, one
-// rounding at the end. One workgroup per token.
+// rounding at the end. O holds `split` partial slices [split, rows, d] that are added first,
+// in slice order. One workgroup per token.
+__device__ __forceinline__ float4 sum_slices(const float* O, int split, size_t slice, size_t off) {
+  float4 v = *reinterpret_cast<const float4*>(O + off);
+  for (int z = 1; z < split; ++z) {
+    const float4 u = *reinterpret_cast<const float4*>(O + z * slice + off);
+    v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+  }
+  return v;
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
                                                        const int32_t* __restrict__ inv,
                                                        const float* __restrict__ gate, int T, int K,
-                                                       int n_shared, int d, void* y) {
+                                                       int n_shared, int d, void* y, int split) {
   const int t = blockIdx.x;
   if (BF16) {  // d % 4 == 0
+    const size_t slice = static_cast<size_t>(T) * (K + n_shared) * d;
     for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
       float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int k = 0; k < K; ++k) {
         const float gk = gate[t * K + k];
-        const float4 v = *reinterpret_cast<const float4*>(O + static_cast<size_t>(inv[t * K + k]) * d + c);
+        const float4 v = sum_slices(O, split, slice, static_cast<size_t>(inv[t * K + k]) * d + c);
         s.x += gk * v.x; s.y += gk * v.y; s.z += gk * v.z; s.w += gk * v.w;
       }
       for (int sh = 0; sh < n_shared; ++sh) {
-        const float4 v = *reinterpret_cast<const float4*>(O + (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c);
+        const float4 v = sum_slices(O, split, slice, (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c);
         s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
       }
       uint2 packed;
@@ -235,17 +245,24 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 }
 
 // ------------------------------------------------------------------ bf16 decode kernels
+//
+// With few tokens the FFN is a weight stream: each selected expert's matrices are read once
+// and every row meets at most 16 token rows. A workgroup owns DEC_NT tiles of 16 weight rows
+// (gate/up kernel: DEC_NT gate tiles and the DEC_NT matching up tiles) and walks the
+// reduction dimension in chunks of DEC_CK values. Each chunk is loaded with 16-byte loads in
+// which a wavefront covers whole 128-byte row segments (full cache lines), stored to LDS with
+// a 16-byte row pad (conflict-free MFMA operand reads), and multiplied on MFMA 16x16x32 with
+// the token rows padded to 16. The next chunk's loads are in flight while the current one is
+// multiplied. The down projection splits its reduction over F into `split` slices so that
+// enough workgroups stream at once; the combine adds the slices in order.
 
-constexpr int DEC_GU_COLS = 32;     // H columns per workgroup (gate/up kernel)
-constexpr int DEC_GU_WAVES = 4;
-constexpr int DEC_DN_COLS = 16;     // y columns per workgroup (down + combine kernel)
-constexpr int DEC_DN_WAVES = 8;
+constexpr int DEC_NT = 4;        // 16-row weight tiles per operand per workgroup
+constexpr int DEC_CK = 64;       // reduction values per chunk (128 bytes per row)
+constexpr int DEC_THREADS = 256;
 
 struct DecodeArgs {
   const uint16_t* x;
   const int32_t* row_tok;
-  const int32_t* perm;
-  const float* gate;
   const int32_t* offsets;
   const int32_t* active;
   const int32_t* n_active;
@@ -253,147 +270,139 @@ struct DecodeArgs {
   const uint16_t* w_down;
   const uint16_t* ws_gate_up;
   const uint16_t* ws_down;
-  uint16_t* H;
-  uint16_t* y;
-  int T, d, F, E, K;
+  uint16_t* H;        // [rows, F] bf16
+  float* O;           // [split, rows, d] fp32
+  int T, d, F, E, K, rows, split;
 };
 
-__global__ __launch_bounds__(64 * DEC_GU_WAVES) void decode_gate_up_kernel(const DecodeArgs p) {
-  __shared__ f32x4 red[DEC_GU_WAVES][4][64];
+// Streams R = 16 * NTILE weight rows (row r starts at wrow(r)) over k in [k0, k0 + klen) and
+// accumulates tile (wave + 4q) of A(16 x k) * W^T into acc[q]. A row (lane & 15) is `arow`.
+template <int NTILE, class RowPtr>
+__device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* arow, int k0, int klen,
+                                            unsigned char (*lds)[16 * NTILE * (DEC_CK * 2 + 16)],
+                                            f32x4* acc) {
+  constexpr int R = 16 * NTILE;
+  constexpr int PITCH = DEC_CK * 2 + 16;
+  constexpr int UPR = DEC_CK * 2 / 16;
+  constexpr int PER = R * UPR / DEC_THREADS;
+  constexpr int TPW = (NTILE + 3) / 4;
+  static_assert(R * UPR % DEC_THREADS == 0, "chunk must split evenly over the threads");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint16_t* src[PER];
+  int dst[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int u = tid + DEC_THREADS * i;
+    const int r = u / UPR, piece = u % UPR;
+    src[i] = wrow(r) + k0 + piece * 8;
+    dst[i] = r * PITCH + piece * 16;
+  }
+  const uint16_t* ap = arow + k0 + (lane >> 4) * 8;
+  const int nc = klen / DEC_CK;
+  u32x4 reg[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) reg[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i]));
+#pragma unroll
+  for (int i = 0; i < PER; ++i) *reinterpret_cast<u32x4*>(&lds[0][dst[i]]) = reg[i];
+  __syncthreads();
+  for (int c = 0; c < nc; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < nc) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        reg[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i] + (c + 1) * DEC_CK));
+    }
+#pragma unroll
+    for (int ks = 0; ks < DEC_CK / 32; ++ks) {
+      const u32x4 a = *reinterpret_cast<const u32x4*>(ap + c * DEC_CK + ks * 32);
+#pragma unroll
+      for (int q = 0; q < TPW; ++q) {
+        const int tile = wave + 4 * q;
+        if (tile < NTILE) {
+          const int r = tile * 16 + (lane & 15);
+          const u32x4 b = *reinterpret_cast<const u32x4*>(&lds[buf][r * PITCH + ks * 64 + (lane >> 4) * 16]);
+          acc[q] = mfma_16x16x32(a, b, acc[q]);
+        }
+      }
+    }
+    if (c + 1 < nc) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) *reinterpret_cast<u32x4*>(&lds[buf ^ 1][dst[i]]) = reg[i];
+    }
+    __syncthreads();
+  }
+}
+
+// H[row0 + r, n0 + j] = SiLU(x_r . W_gate[n0 + j]) * (x_r . W_up[n0 + j]) for the rows of one
+// active expert; grid (F / (16 * DEC_NT), max active experts).
+__global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const DecodeArgs p) {
+  constexpr int NTILE = 2 * DEC_NT;
+  constexpr int TPW = (NTILE + 3) / 4;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2][16 * NTILE * (DEC_CK * 2 + 16)];
   const int slot = blockIdx.y;
   if (slot >= p.n_active[0]) return;
   const int g = p.active[slot];
   const int row0 = p.offsets[g];
   const int nrows = p.offsets[g + 1] - row0;   // 1..16
-  const int n0 = blockIdx.x * DEC_GU_COLS;
+  const int n0 = blockIdx.x * 16 * DEC_NT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kg = (lane >> 4) * 8;
-  const int rr = min(lane & 15, nrows - 1);
-  const uint16_t* ap = p.x + static_cast<size_t>(p.row_tok[row0 + rr]) * p.d + kg;
   const uint16_t* wg = g < p.E ? p.w_gate_up + static_cast<size_t>(g) * 2 * p.F * p.d
                                : p.ws_gate_up + static_cast<size_t>(g - p.E) * 2 * p.F * p.d;
-  const uint16_t* bp[4];
+  const int F = p.F, d = p.d;
+  auto wrow = [=](int r) {  // rows 0..16*DEC_NT-1: W_gate, then the matching W_up rows
+    const int n = n0 + (r % (16 * DEC_NT));
+    return wg + static_cast<size_t>(r < 16 * DEC_NT ? n : F + n) * d;
+  };
+  const uint16_t* arow = p.x + static_cast<size_t>(p.row_tok[row0 + min(lane & 15, nrows - 1)]) * p.d;
+  f32x4 acc[TPW];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {  // j = 0,1 gate columns; j = 2,3 the matching up columns
-    const int n = n0 + (j & 1) * 16 + (lane & 15);
-    bp[j] = wg + static_cast<size_t>(j < 2 ? n : p.F + n) * p.d + kg;
+  for (int q = 0; q < TPW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  stream_rows<NTILE>(wrow, arow, 0, p.d, lds, acc);
+  // gate tile j pairs with up tile j + DEC_NT: exchange through LDS
+  f32x4* ex = reinterpret_cast<f32x4*>(&lds[0][0]);
+#pragma unroll
+  for (int q = 0; q < TPW; ++q) {
+    const int tile = wave + 4 * q;
+    if (tile < NTILE) ex[tile * 64 + lane] = acc[q];
   }
-  f32x4 acc[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int ksteps = p.d >> 5;
-  constexpr int U = 4;  // k-steps whose loads are issued together
-  int s = wave;
-  for (; s + (U - 1) * DEC_GU_WAVES < ksteps; s += U * DEC_GU_WAVES) {
-    u32x4 a[U], b[U][4];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = (s + u * DEC_GU_WAVES) << 5;
-      a[u] = *reinterpret_cast<const u32x4*>(ap + k);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[u][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp[j] + k));
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = mfma_16x16x32(a[u], b[u][j], acc[j]);
-  }
-  for (; s < ksteps; s += DEC_GU_WAVES) {
-    const int k = s << 5;
-    const u32x4 a = *reinterpret_cast<const u32x4*>(ap + k);
-    u32x4 b[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp[j] + k));
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = mfma_16x16x32(a, b[j], acc[j]);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) red[wave][j][lane] = acc[j];
   __syncthreads();
-  if (tid < 128) {  // (pair j in {0,1}, lane l): gate fragment j with up fragment j+2
-    const int j = tid >> 6, l = tid & 63;
-    f32x4 gs = red[0][j][l], us = red[0][j + 2][l];
+  const int j = tid >> 6, l = tid & 63;   // DEC_NT = 4 gate tiles over 256 threads
+  const f32x4 gs = ex[j * 64 + l], us = ex[(j + DEC_NT) * 64 + l];
 #pragma unroll
-    for (int w = 1; w < DEC_GU_WAVES; ++w) {
-      gs += red[w][j][l];
-      us += red[w][j + 2][l];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = 4 * (l >> 4) + i;
-      if (row < nrows) {
-        const int col = n0 + j * 16 + (l & 15);
-        p.H[static_cast<size_t>(row0 + row) * p.F + col] = f32_to_bf16(silu(gs[i]) * us[i]);
-      }
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * (l >> 4) + i;
+    if (row < nrows)
+      p.H[static_cast<size_t>(row0 + row) * p.F + n0 + j * 16 + (l & 15)] = f32_to_bf16(silu(gs[i]) * us[i]);
   }
 }
 
-__global__ __launch_bounds__(64 * DEC_DN_WAVES) void decode_down_combine_kernel(const DecodeArgs p) {
-  __shared__ f32x4 red[DEC_DN_WAVES][64];
-  __shared__ float yacc[kDecodeMaxT][DEC_DN_COLS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n0 = blockIdx.x * DEC_DN_COLS;
-  const int kg = (lane >> 4) * 8;
-  if (tid < kDecodeMaxT * DEC_DN_COLS) yacc[tid / DEC_DN_COLS][tid % DEC_DN_COLS] = 0.0f;
-  const int na = p.n_active[0];
-  const int ksteps = p.F >> 5;
-  for (int slot = 0; slot < na; ++slot) {
-    const int g = p.active[slot];
-    const int row0 = p.offsets[g];
-    const int nrows = p.offsets[g + 1] - row0;
-    const int rr = min(lane & 15, nrows - 1);
-    const uint16_t* ap = p.H + static_cast<size_t>(row0 + rr) * p.F + kg;
-    const uint16_t* wd = g < p.E ? p.w_down + static_cast<size_t>(g) * p.d * p.F
-                                 : p.ws_down + static_cast<size_t>(g - p.E) * p.d * p.F;
-    const uint16_t* bp = wd + static_cast<size_t>(n0 + (lane & 15)) * p.F + kg;
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    constexpr int U = 8;  // k-steps whose loads are issued together
-    int s = wave;
-    for (; s + (U - 1) * DEC_DN_WAVES < ksteps; s += U * DEC_DN_WAVES) {
-      u32x4 a[U], b[U];
+// O[z, row0 + r, n0 + j] = sum over k in slice z of H[row0 + r, k] * W_down[n0 + j, k];
+// grid (d / (16 * DEC_NT), max active experts, split).
+__global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeArgs p) {
+  constexpr int NTILE = DEC_NT;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2][16 * NTILE * (DEC_CK * 2 + 16)];
+  const int slot = blockIdx.y;
+  if (slot >= p.n_active[0]) return;
+  const int g = p.active[slot];
+  const int row0 = p.offsets[g];
+  const int nrows = p.offsets[g + 1] - row0;
+  const int n0 = blockIdx.x * 16 * DEC_NT;
+  const int z = blockIdx.z;
+  const int klen = p.F / p.split;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint16_t* wd = g < p.E ? p.w_down + static_cast<size_t>(g) * p.d * p.F
+                               : p.ws_down + static_cast<size_t>(g - p.E) * p.d * p.F;
+  const int F = p.F;
+  auto wrow = [=](int r) { return wd + static_cast<size_t>(n0 + r) * F; };
+  const uint16_t* arow = p.H + static_cast<size_t>(row0 + min(lane & 15, nrows - 1)) * p.F;
+  f32x4 acc[1] = {f32x4{0.f, 0.f, 0.f, 0.f}};
+  stream_rows<NTILE>(wrow, arow, z * klen, klen, lds, acc);
+  // wave w holds tile w: rows 4*(lane>>4)+i, column lane & 15
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int k = (s + u * DEC_DN_WAVES) << 5;
-        a[u] = *reinterpret_cast<const u32x4*>(ap + k);
-        b[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp + k));
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) acc = mfma_16x16x32(a[u], b[u], acc);
-    }
-    for (; s < ksteps; s += DEC_DN_WAVES) {
-      const int k = s << 5;
-      const u32x4 a = *reinterpret_cast<const u32x4*>(ap + k);
-      const u32x4 b = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(bp + k));
-      acc = mfma_16x16x32(a, b, acc);
-    }
-    red[wave][lane] = acc;
-    __syncthreads();
-    if (tid < kDecodeMaxT * DEC_DN_COLS) {
-      const int r = tid / DEC_DN_COLS, c = tid % DEC_DN_COLS;
-      if (r < nrows) {
-        const int l = (r >> 2) * 16 + c, i = r & 3;
-        float v = red[0][l][i];
-#pragma unroll
-        for (int w = 1; w < DEC_DN_WAVES; ++w) v += red[w][l][i];
-        const int pos = row0 + r;
-        float gt = 1.0f;
-        int t;
-        if (g < p.E) {
-          const int j = p.perm[pos];
-          t = j / p.K;
-          gt = p.gate[j];
-        } else {
-          t = p.row_tok[pos];
-        }
-        yacc[t][c] += gt * v;
-      }
-    }
-    __syncthreads();
-  }
-  if (tid < kDecodeMaxT * DEC_DN_COLS) {
-    const int t = tid / DEC_DN_COLS, c = tid % DEC_DN_COLS;
-    if (t < p.T) p.y[static_cast<size_t>(t) * p.d + n0 + c] = f32_to_bf16(yacc[t][c]);
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * (lane >> 4) + i;
+    if (row < nrows)
+      p.O[(static_cast<size_t>(z) * p.rows + row0 + row) * p.d + n0 + wave * 16 + (lane & 15)] = acc[0][i];
   }
 }
 
@@ -486,19 +495,30 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   record_mark(marks, 1, stream);
 
   hipLaunchKernelGGL(combine_kernel<true>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                     a.K, a.n_shared, a.d, y);
+                     a.K, a.n_shared, a.d, y, 1);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
 }
 
-hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H,
+int decode_split(int T, int d, int F, int E, int K, int n_shared) {
+  // enough (expert, column-slab, slice) workgroups for every CU to stream several at once
+  const int max_active = (T * K < E ? T * K : E) + n_shared;
+  const int slabs = d / (16 * DEC_NT) * max_active;
+  if (slabs <= 0) return 1;  // no tokens: nothing is launched
+  const int target = (1024 + slabs - 1) / slabs;
+  const int chunks = F / DEC_CK;
+  int best = 1;  // at most 8: the workspace reserves 8 slices
+  for (int s = 1; s <= 8 && s <= target; ++s)
+    if (chunks % s == 0) best = s;
+  return best;
+}
+
+hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
                                       void* y, hipStream_t stream, hipEvent_t* marks) {
   DecodeArgs p;
   p.x = static_cast<const uint16_t*>(a.x);
   p.row_tok = pb.row_tok;
-  p.perm = pb.perm;
-  p.gate = a.gate;
   p.offsets = pb.offsets;
   p.active = pb.active;
   p.n_active = pb.n_active;
@@ -507,18 +527,23 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
   p.ws_gate_up = static_cast<const uint16_t*>(a.ws_gate_up);
   p.ws_down = static_cast<const uint16_t*>(a.ws_down);
   p.H = H;
-  p.y = static_cast<uint16_t*>(y);
+  p.O = O;
   p.T = a.T; p.d = a.d; p.F = a.F; p.E = a.E; p.K = a.K;
+  p.rows = a.T * (a.K + a.n_shared);
+  p.split = decode_split(a.T, a.d, a.F, a.E, a.K, a.n_shared);
   const int max_active = (a.T * a.K < a.E ? a.T * a.K : a.E) + a.n_shared;
-  hipLaunchKernelGGL(decode_gate_up_kernel, dim3(a.F / DEC_GU_COLS, max_active), dim3(64 * DEC_GU_WAVES),
-                     0, stream, p);
+  hipLaunchKernelGGL(decode_gate_up_kernel, dim3(a.F / (16 * DEC_NT), max_active), dim3(DEC_THREADS), 0, stream, p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
-  hipLaunchKernelGGL(decode_down_combine_kernel, dim3(a.d / DEC_DN_COLS), dim3(64 * DEC_DN_WAVES), 0,
+  hipLaunchKernelGGL(decode_down_kernel, dim3(a.d / (16 * DEC_NT), max_active, p.split), dim3(DEC_THREADS), 0,
                      stream, p);
   err = hipGetLastError();
+  if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
+  hipLaunchKernelGGL(combine_kernel<true>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T, a.K,
+                     a.n_shared, a.d, y, p.split);
+  err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
 }
@@ -547,7 +572,7 @@ hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float*
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
   hipLaunchKernelGGL(combine_kernel<false>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                     a.K, a.n_shared, a.d, y);
+                     a.K, a.n_shared, a.d, y, 1);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;

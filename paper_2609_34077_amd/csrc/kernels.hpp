@@ -55,9 +55,10 @@ inline void record_mark(hipEvent_t* marks, int i, hipStream_t stream) {
 // bf16, T > kDecodeMaxT: H = SwiGLU(X_g W_gate,up^T) per group; O = H W_down^T; y = combine.
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
                                void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks);
-// bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel, then down projection fused with
-// the gate-weighted combine.
-hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H,
+// bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel, split-K down projection into
+// O [split, rows, d], then the combine. decode_split() gives the split for a layer.
+int decode_split(int T, int d, int F, int E, int K, int n_shared);
+hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
                                       void* y, hipStream_t stream, hipEvent_t* marks);
 // f32 path (no MFMA; fp32 end to end).
 hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float* H, float* O,

@@ -16,8 +16,9 @@ pytestmark = pytest.mark.gpu
 
 def _gpu(trace, E, B, state=None, fps=True):
     st = None if state is None else torch.from_numpy(np.ascontiguousarray(state, dtype=np.int32)).cuda()
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = L.maskmoe_cache_fetches(torch.from_numpy(np.ascontiguousarray(trace, dtype=np.int32)).cuda(), E, B,
-                                  state=st, with_f_per_step=fps)
+                                  state=st, with_f_per_step=fps, dev_error=err)
     torch.cuda.synchronize()
     res = {k: (v.cpu().numpy() if v is not None else None) for k, v in out.items()}
     res["state"] = None if st is None else st.cpu().numpy()
