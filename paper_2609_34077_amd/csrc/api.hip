@@ -156,6 +156,11 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   if (d.n_shared > 0 && (!ws_gate_up || !ws_down)) return MASKMOE_E_INVAL;
   const bool bf16 = d.dtype == MASKMOE_BF16;
   if (bf16 && (d.d % 64 != 0 || d.F % 64 != 0)) return MASKMOE_E_UNSUPPORTED;
+  // the grouped GEMMs address x, H and one expert's matrices with 32-bit element offsets
+  const int64_t rows64 = static_cast<int64_t>(d.T) * (d.K + d.n_shared);
+  if (bf16 && (static_cast<int64_t>(d.T) * d.d >= (int64_t{1} << 31) || rows64 * d.F >= (int64_t{1} << 31) ||
+               int64_t{2} * d.F * d.d >= (int64_t{1} << 31)))
+    return MASKMOE_E_UNSUPPORTED;
   const void* ptrs[] = {x, w_router, w_gate_up, w_down, y};
   for (const void* p : ptrs)
     if (!aligned(p, 16)) return MASKMOE_E_INVAL;

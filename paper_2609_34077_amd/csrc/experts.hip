@@ -8,9 +8,9 @@
 //   O_g = H_g W_down,g^T
 // followed by y_t = sum_k g_{t,k} O[inv(t,k)] + sum_s O[shared row of t].
 //
-// bf16, many tokens: 256x256x64 block tiles on v_mfma_f32_32x32x16_bf16, 8 waves (4 x 2),
-// 64x128 per wave, A and B double-buffered in LDS (128 KB) with a 16-byte XOR swizzle so
-// that both the global->LDS stores and the MFMA operand reads are bank-conflict free.
+// bf16, many tokens: 256x256x64 block tiles on v_mfma_f32_32x32x16_bf16, 8 waves (2 x 4),
+// 128x64 per wave, A and B double-buffered in LDS (128 KB) with a 16-byte XOR swizzle so
+// that the MFMA operand reads are bank-conflict free; global loads run two k-tiles ahead.
 // The gate/up GEMM holds matching 128-column slices of W_gate and W_up in one tile and
 // applies SwiGLU in registers (H rounded once to bf16). Tiles are enumerated expert-tile
 // fastest so the workgroups that share a weight slice run together, and the linear block
@@ -59,10 +59,15 @@ __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt
 
 template <int EPI>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
-  __shared__ u32x4 lds_a[2][BM * BK / 8];
-  __shared__ u32x4 lds_b[2][BN * BK / 8];
+  constexpr int WN = 4;                 // waves: 2 along rows x 4 along columns
+  constexpr int TM = 4, TN = 2;         // 32x32 fragments per wave: 128 rows x 64 B-rows
+  constexpr int NT = GEMM_THREADS;
+  constexpr int U = BM * 8 / NT;        // 16-byte units per thread per operand and stage (= 4)
+  __shared__ u32x4 lds_a[2][BM * 8];
+  __shared__ u32x4 lds_b[2][BN * 8];
 
-  // XCD-aware block order: consecutive logical tiles land on the same XCD.
+  // XCD-aware block order: consecutive logical tiles land on the same XCD; row tiles vary
+  // fastest so the workgroups sharing a weight slice run together.
   const int nwg = gridDim.x, bid = blockIdx.x;
   const int xcd = bid & 7, local = bid >> 3, q = nwg >> 3, rem = nwg & 7;
   const int lid = xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
@@ -76,121 +81,135 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   const int n0 = nt * (EPI == 0 ? BN / 2 : BN);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
 
-  // Global -> LDS copy mapping: 4 chunks of 16 B per thread and operand; row (tid>>3)+64i.
-  const int kc = tid & 7;
-  const uint16_t* asrc[4];
-  const uint16_t* bsrc[4];
+  // Global -> LDS mapping: thread tid loads rows (tid >> 3) + 64 i (i < U) of each operand;
+  // LDS slot u = tid + NT * i (row u >> 3, physical chunk u & 7) receives the logical chunk
+  // (u & 7) ^ (row & 7), an XOR swizzle that keeps the MFMA operand reads conflict free.
+  // The swizzle term is the same for all i (64 rows apart), so one chunk offset serves all.
+  const int r0 = tid >> 3;
+  const int chunk = ((tid & 7) ^ (r0 & 7)) * 8;
   const uint16_t* wg = g < p.E ? p.w + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * Kdim
                                : p.ws + static_cast<size_t>(g - p.E) * (EPI == 0 ? 2 * p.F : p.d) * Kdim;
+  int aoffs[U], boffs[U];   // element offsets (< 2^31, checked by the host)
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = (tid >> 3) + 64 * i;
+  for (int i = 0; i < U; ++i) {
+    const int r = r0 + 64 * i;
     const int row = min(row0 + r, row_end - 1);
-    if (EPI == 0) asrc[i] = p.a + static_cast<size_t>(p.row_tok[row]) * Kdim + kc * 8;
-    else asrc[i] = p.a + static_cast<size_t>(row) * Kdim + kc * 8;
+    aoffs[i] = (EPI == 0 ? p.row_tok[row] : row) * Kdim + chunk;
     int brow;
-    if (EPI == 0) {  // tile rows 0..127: W_gate rows n0.., rows 128..255: W_up rows F+n0..
+    if (EPI == 0) {  // tile rows 0..127: W_gate rows n0.., rows 128..255: the matching W_up rows
       const int n = min(n0 + (r & 127), p.F - 1);
       brow = r < 128 ? n : p.F + n;
     } else {
       brow = min(n0 + r, p.d - 1);
     }
-    bsrc[i] = wg + static_cast<size_t>(brow) * Kdim + kc * 8;
+    boffs[i] = brow * Kdim + chunk;
   }
 
-  u32x4 ra[4], rb[4];
-  auto gload = [&](int k0) {
+  // Fragment rows: A rows wm*128 + i*32 + (lane & 31); B rows: EPI 0 -> gate wn*32 + ... and
+  // the matching up row 128 + wn*32 + ...; EPI 1 -> wn*64 + j*32 + ...
+  int aoff[TM], boff[TN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = *reinterpret_cast<const u32x4*>(asrc[i] + k0);
-      rb[i] = *reinterpret_cast<const u32x4*>(bsrc[i] + k0);
+  for (int i = 0; i < TM; ++i) aoff[i] = (wm * 128 + i * 32 + (lane & 31)) * 8;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int br = EPI == 0 ? (j == 0 ? 0 : 128) + wn * 32 : wn * 64 + j * 32;
+    boff[j] = (br + (lane & 31)) * 8;
+  }
+  const int sw = lane & 7;   // (fragment row & 7) == (lane & 7)
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  u32x4 ra[U], rb[U];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      ra[i] = *reinterpret_cast<const u32x4*>(p.a + (aoffs[i] + kt * BK));
+      rb[i] = *reinterpret_cast<const u32x4*>(wg + (boffs[i] + kt * BK));
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = (tid >> 3) + 64 * i;
-      lds_a[buf][r * 8 + (kc ^ (r & 7))] = ra[i];
-      lds_b[buf][r * 8 + (kc ^ (r & 7))] = rb[i];
+    for (int i = 0; i < U; ++i) {
+      lds_a[buf][tid + NT * i] = ra[i];
+      lds_b[buf][tid + NT * i] = rb[i];
     }
   };
+  u32x4 af[2][TM], bf[2][TN];
+  auto read_frags = [&](int buf, int kk, int slot) {
+    const int ch = (kk * 2 + (lane >> 5)) ^ sw;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[slot][i] = lds_a[buf][aoff[i] + ch];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bf[slot][j] = lds_b[buf][boff[j] + ch];
+  };
 
-  // Wave tile: rows wm*64 + [0,64); B rows: EPI 0 -> gate wn*64+[0,64) and up 128+wn*64+[0,64),
-  // EPI 1 -> wn*128 + [0,128). Fragment j covers 32 B rows.
-  int brow_base[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (EPI == 0) brow_base[j] = (j < 2 ? 0 : 128) + wn * 64 + (j & 1) * 32;
-    else brow_base[j] = wn * 128 + j * 32;
-  }
-  f32x16 acc[2][4];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
+  // Pipeline: tile kt is in LDS buffer kt & 1, tile kt + 1 in registers. Right after the
+  // first k16 step of tile kt the registers go to the other LDS buffer and are refilled with
+  // tile kt + 2, so every global load has a whole k-tile of MFMA work to arrive. Operand
+  // fragments for the next k16 step are read while the current one multiplies.
   const int nk = Kdim / BK;
   gload(0);
   lstore(0);
+  if (nk > 1) gload(1);
   __syncthreads();
+  read_frags(0, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int ch = kk * 2 + (lane >> 5);
-      u32x4 af[2], bf[4];
+      const int cur = kk & 1;
+      if (kk + 1 < BK / 16) read_frags(buf, kk + 1, cur ^ 1);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int r = wm * 64 + i * 32 + (lane & 31);
-        af[i] = lds_a[buf][r * 8 + (ch ^ (r & 7))];
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_32x32x16(af[cur][i], bf[cur][j], acc[i][j]);
+      if (kk + 1 < BK / 16) {
+#pragma unroll
+        for (int s = 0; s < TM + TN; ++s) {   // interleave one operand read per MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = brow_base[j] + (lane & 31);
-        bf[j] = lds_b[buf][r * 8 + (ch ^ (r & 7))];
+      if (kk == 0) {
+        if (kt + 1 < nk) lstore(buf ^ 1);
+        if (kt + 2 < nk) gload(kt + 2);
       }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_32x32x16(af[i], bf[j], acc[i][j]);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
+    if (kt + 1 < nk) read_frags(buf ^ 1, 0, 0);
   }
 
-  // Epilogue. acc[i][j][4*jj+ii] is row wm*64 + i*32 + 8*jj + 4*(lane>>5) + ii,
-  // column (lane & 31) of fragment j.
+  // Epilogue. acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column
+  // (lane & 31) of fragment j.
   const int col_in = lane & 31;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        const int row = row0 + wm * 64 + i * 32 + 8 * jj + 4 * (lane >> 5) + ii;
+        const int row = row0 + wm * 128 + i * 32 + 8 * jj + 4 * (lane >> 5) + ii;
         if (row >= row_end) continue;
         const int r = 4 * jj + ii;
         if (EPI == 0) {
-          uint16_t* H = static_cast<uint16_t*>(p.out);
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const int col = n0 + wn * 64 + j * 32 + col_in;
-            if (col < Ndim) {
-              const float h = silu(acc[i][j][r]) * acc[i][j + 2][r];
-              H[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(h);
-            }
+          const int col = n0 + wn * 32 + col_in;
+          if (col < Ndim) {
+            const float h = silu(acc[i][0][r]) * acc[i][1][r];
+            static_cast<uint16_t*>(p.out)[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(h);
           }
         } else {
-          float* O = static_cast<float*>(p.out);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int col = n0 + wn * 128 + j * 32 + col_in;
-            if (col < Ndim) O[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
+          for (int j = 0; j < TN; ++j) {
+            const int col = n0 + wn * 64 + j * 32 + col_in;
+            if (col < Ndim) static_cast<float*>(p.out)[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
           }
         }
       }
