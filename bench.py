@@ -19,8 +19,9 @@ Workloads (--workload):
            steps, then one LRU cache of 4 experts per (layer, sequence).
 
 Prints one JSON line (rank 0). The roofline entry is for the dominant kernel, timed with
-HIP events recorded around each stage on the stream the kernels run on; `traffic` is
-filled from rocprofv3 counter runs when given with --traffic-bytes.
+HIP events recorded around each stage on the stream the kernels run on; `traffic` comes from
+the committed rocprofv3 counter summary (profiles/<workload>_traffic.md) and is reported only
+while that summary's kernel-source hash matches the current source, else null.
 """
 
 from __future__ import annotations
@@ -57,9 +58,50 @@ def parse():
     ap.add_argument("--mode", choices=("hard", "soft"), default="soft", help="deepseek routing mode")
     ap.add_argument("--copies", type=int, default=3, help="decode: weight copies rotated across steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--traffic-bytes", type=float, default=None,
-                    help="HBM bytes per launch of the dominant kernel from rocprofv3 counters")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="run one plain 512 MiB device copy before timing (reference for counter runs)")
     return ap.parse_args()
+
+
+KERNEL_SOURCES = {"decode": "paper_2609_34077_amd/csrc/experts.hip", "ft": "paper_2609_34077_amd/csrc/experts.hip",
+                  "deepseek": "paper_2609_34077_amd/csrc/experts.hip", "trace": "paper_2609_34077_amd/csrc/route.hip"}
+
+
+def source_hash(rel: str) -> str:
+    import hashlib
+    with open(os.path.join(ROOT, rel), "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def recorded_traffic(workload: str, config_name: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter summary, if the
+    summary was taken on the current kernel source (matching hash); else None."""
+    path = os.path.join(ROOT, "profiles", f"{config_name}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].split(": ", 1)
+                vals[k.strip().strip("`")] = v.strip().strip("`")
+    if vals.get("kernel source hash") != source_hash(KERNEL_SOURCES[workload]):
+        return None
+    try:
+        return float(vals["traffic bytes per launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def calibration_copy():
+    """One plain device copy of 512 MiB (reads 512 MiB, writes 512 MiB)."""
+    import torch
+    src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def blas_threads() -> int:
@@ -208,7 +250,7 @@ def run_layer(args):
     if decode:
         achieved = gu_bytes / gu_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": args.traffic_bytes,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(args.workload, cfg.name),
                 "kernel": "decode_gate_up_kernel",
                 "algorithmic_unit": "bytes per launch = D x 2*F*d*2 (W_gate, W_up of each distinct selected "
                                     "expert) + x rows + H writes",
@@ -218,7 +260,7 @@ def run_layer(args):
     else:
         achieved = gu_flops / gu_s / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": args.traffic_bytes,
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": recorded_traffic(args.workload, cfg.name),
                 "kernel": "grouped_gemm_bf16<0> (gate/up + SwiGLU)",
                 "algorithmic_unit": "FLOPs per launch = 2 * T*(K+shared) * 2F * d",
                 "avg_launch_us": round(1e3 * np.mean(gu_ms), 2)}
@@ -295,7 +337,8 @@ def run_trace(args):
         "config": {"workload": "routing_fetch_trace", "layers": cfg.L, "sequences": cfg.S, "steps_per_seq": cfg.N,
                    "d": cfg.d, "E": cfg.E, "K": cfg.K, "cache_slots": cfg.B, "prior_delta": cfg.delta},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": args.traffic_bytes,
+                     "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                     "traffic": recorded_traffic("trace", "routing_fetch_trace"),
                      "kernel": "route_bf16_kernel<2,4,4,1>",
                      "algorithmic_unit": "FLOPs per launch = 2 * S*N * L*E * d",
                      "hbm_frac_of_x_read": round(x_bytes / (route_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -337,6 +380,8 @@ def main():
     torch.cuda.set_device(0)
     from paper_2609_34077_amd import _lib as L
     L.load()
+    if args.calibrate:
+        calibration_copy()
     if args.workload == "trace":
         res, st = run_trace(args)
         base = None if args.no_cpu_baseline else trace_cpu_baseline(st)

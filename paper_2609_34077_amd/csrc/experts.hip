@@ -46,6 +46,7 @@ struct GemmArgs {
   void* out;                // EPI 0: H bf16 [rows, F]; EPI 1: O f32 [rows, d]
   int G, E, F, d;
   int mt_max;               // grid bound on row tiles
+  int n_tiles;              // column tiles
 };
 
 __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt) {
@@ -66,12 +67,20 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   __shared__ u32x4 lds_a[2][BM * 8];
   __shared__ u32x4 lds_b[2][BN * 8];
 
-  // XCD-aware block order: consecutive logical tiles land on the same XCD; row tiles vary
-  // fastest so the workgroups sharing a weight slice run together.
+  // XCD-aware block order: the hardware deals block ids round-robin over the 8 XCDs, so ids
+  // are remapped to give each XCD a contiguous range of logical tiles. Logical tiles come in
+  // groups of GN column tiles; inside a group the column tile varies fastest, so the ~32
+  // workgroups an XCD runs at once cover about 8 row tiles x 4 column tiles and share both
+  // operands in its L2.
+  constexpr int GN = 4;
   const int nwg = gridDim.x, bid = blockIdx.x;
   const int xcd = bid & 7, local = bid >> 3, q = nwg >> 3, rem = nwg & 7;
   const int lid = xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
-  const int mt = lid % p.mt_max, nt = lid / p.mt_max;
+  const int per_group = GN * p.mt_max;
+  const int first_n = (lid / per_group) * GN;
+  const int gsize = min(p.n_tiles - first_n, GN);
+  const int within = lid % per_group;
+  const int nt = first_n + within % gsize, mt = within / gsize;
   if (mt >= p.tile_off[p.G]) return;
   const int g = find_group(p.tile_off, p.G, mt);
   const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM;
@@ -498,6 +507,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   g.ws = static_cast<const uint16_t*>(a.ws_gate_up);
   g.out = H;
   const int nt1 = (a.F + BN / 2 - 1) / (BN / 2);
+  g.n_tiles = nt1;
   hipLaunchKernelGGL(grouped_gemm_bf16<0>, dim3(max_tiles * nt1), dim3(GEMM_THREADS), 0, stream, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
@@ -508,6 +518,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   g.ws = static_cast<const uint16_t*>(a.ws_down);
   g.out = O;
   const int nt2 = (a.d + BN - 1) / BN;
+  g.n_tiles = nt2;
   hipLaunchKernelGGL(grouped_gemm_bf16<1>, dim3(max_tiles * nt2), dim3(GEMM_THREADS), 0, stream, g);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
