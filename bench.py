@@ -305,11 +305,19 @@ def run_trace(args):
         res = L.maskmoe_cache_fetches(idx.view(cfg.L, cfg.S, cfg.N, cfg.K), cfg.E, cfg.B)
         return res
 
-    fetch = {}
+    # Fetches/tok (Eq. 5, summed over layers) with the prior and with the zero prior, for each
+    # eviction policy and a sweep of cache budgets (outside the timed region).
+    sweep = {}
     for name, pr in (("prior", inp["prior"]), ("zero_prior", inp["prior_zero"])):
-        r = step(pr)
-        torch.cuda.synchronize()
-        fetch[name] = float(r["fetches"].sum().item()) / (cfg.S * cfg.N)
+        idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=pr, with_margin=False)
+        tr = idx.view(cfg.L, cfg.S, cfg.N, cfg.K)
+        for pol_name, pol in (("LRU", L.CACHE_LRU), ("LFU", L.CACHE_LFU), ("FIFO", L.CACHE_FIFO)):
+            for B in (2, 4, 6):
+                r = L.maskmoe_cache_fetches(tr, cfg.E, B, policy=pol)
+                sweep.setdefault(pol_name, {}).setdefault(f"B{B}", {})[name] = round(
+                    float(r["fetches"].sum().item()) / (cfg.S * cfg.N), 4)
+    torch.cuda.synchronize()
+    fetch = {k: sweep["LRU"][f"B{cfg.B}"][k] for k in ("prior", "zero_prior")}
     steps = args.steps if args.steps is not None else 10
     warmup = args.warmup if args.warmup is not None else 2
     for _ in range(warmup):
@@ -346,6 +354,9 @@ def run_trace(args):
         "stages_ms": {"route": round(route_ms, 4), "cache": round(cache_ms, 4)},
         "fetches_per_token": {k: round(v, 4) for k, v in fetch.items()},
         "fetch_reduction_pct": round(100 * (fetch["prior"] - fetch["zero_prior"]) / fetch["zero_prior"], 2),
+        "fetches_per_token_sweep": sweep,
+        "fetch_reduction_pct_sweep": {p: {b: round(100 * (v["prior"] - v["zero_prior"]) / v["zero_prior"], 2)
+                                          for b, v in d.items()} for p, d in sweep.items()},
     }
     return res, dict(cfg=cfg, inp=inp)
 

@@ -63,8 +63,8 @@ enum { MASKMOE_GATE_P = 0, MASKMOE_GATE_RENORM = 1 };
 /* ---- element type of x, router weights, expert weights and y ---- */
 enum { MASKMOE_BF16 = 0, MASKMOE_F32 = 1 };
 
-/* ---- cache replacement policy of maskmoe_cache_fetches ---- */
-enum { MASKMOE_CACHE_LRU = 0 };
+/* ---- cache replacement policy of maskmoe_cache_fetches (Section 4.1, Table 2) ---- */
+enum { MASKMOE_CACHE_LRU = 0, MASKMOE_CACHE_LFU = 1, MASKMOE_CACHE_FIFO = 2 };
 
 /* One masked MoE layer.
  *  T          tokens (T >= 0; T = 0 is a no-op)
@@ -132,7 +132,8 @@ size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc);
  *  rounds once to bf16. f32: no intermediate rounding beyond fp32 arithmetic.
  *  Errors: as maskmoe_route, plus E_INVAL for F < 1 or n_shared outside 0..8 or a NULL
  *  shared-weight pointer with n_shared > 0; E_WORKSPACE when the workspace is too small;
- *  E_UNSUPPORTED for bf16 with d % 64 != 0 or F % 64 != 0.
+ *  E_UNSUPPORTED for bf16 with d % 64 != 0 or F % 64 != 0, or with T*d, T*(K+n_shared)*F or
+ *  2*F*d at or above 2^31 elements.
  */
 int maskmoe_layer_forward(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                           const uint8_t* mask, const float* prior, const void* w_gate_up,
@@ -166,14 +167,18 @@ int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x
 
 /*
  * maskmoe_cache_fetches -- replay expert-selection traces through per-layer expert caches
- * (Section 4.1 "Simulation"; metrics of Eq. 5).
+ * (Section 4.1 "Simulation", its LRU / LFU / FIFO policies; metrics of Eq. 5).
  *
  * Each (layer l, stream s) pair is an independent cache of B routed experts that sees the
  * steps n = 0..N-1 of trace[l, s]. At a step, h = number of selected experts already
  * cached, f = misses (= K - h for a trace of K distinct valid experts); every miss is one
- * fetch and, in a full cache, one eviction. LRU: the hits are touched first, in ascending
- * expert index, then the misses are inserted in ascending expert index, each evicting the
- * least recently used cached expert not selected at this step.
+ * fetch and, in a full cache, one eviction. The hits are handled first, in ascending expert
+ * index, then the misses are inserted in ascending expert index; each miss evicts one cached
+ * expert not selected at this step:
+ *   LRU  the least recently used one;
+ *   FIFO the one inserted earliest (hits do not refresh it);
+ *   LFU  the one with the fewest accesses so far in this stream (every selection counts, and
+ *        counts survive eviction), ties to the least recently used.
  * Eq. 5 then gives HR = sum h / (N L K) and Fetches/tok = sum f / N (per stream).
  *
  *  trace       device [L, S, N, K] int32 expert ids. An id outside [0, E) or repeating an
@@ -181,11 +186,14 @@ int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x
  *              *dev_error.
  *  L, S, N, K  sizes, L, S, N >= 0, 1 <= K <= E; E experts, 1 <= E <= 64;
  *              B cache slots, K <= B (B >= E never evicts); N * K + B < 2^24.
- *  policy      MASKMOE_CACHE_LRU.
- *  state       device [L, S, B] int32 in/out or NULL. In: initial cache, least to most
- *              recently used, -1 = empty slot (entries must be distinct ids in [0, E) or
- *              -1; bad entries are dropped and flag *dev_error). Out: final cache in the
- *              same form. NULL: every cache starts empty and the final state is not kept.
+ *  policy      MASKMOE_CACHE_LRU, MASKMOE_CACHE_LFU or MASKMOE_CACHE_FIFO.
+ *  state       device [L, S, B] int32 in/out or NULL. In: initial cache, oldest first (least
+ *              recently used first for LRU and LFU, first inserted first for FIFO), -1 = empty
+ *              slot (entries must be distinct ids in [0, E) or -1; bad entries are dropped and
+ *              flag *dev_error). Out: final cache in the same form. NULL: every cache starts
+ *              empty and the final state is not kept.
+ *  counts      device [L, S, E] int32 in/out or NULL: LFU access counts per expert (ignored
+ *              by LRU and FIFO). NULL: counts start at zero and are not kept.
  *  fetches     device [L, S] int64: sum of f over the N steps.
  *  hits        device [L, S] int64: sum of h over the N steps.
  *  f_per_step  device [L, S, N] uint8 or NULL: f at every step.
@@ -195,8 +203,8 @@ int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x
  *  required pointers; E_UNSUPPORTED for E > 64 or N * K + B >= 2^24.
  */
 int maskmoe_cache_fetches(const int32_t* trace, int32_t L, int32_t S, int32_t N, int32_t K,
-                          int32_t E, int32_t B, int32_t policy, int32_t* state, int64_t* fetches,
-                          int64_t* hits, uint8_t* f_per_step, int32_t* dev_error,
+                          int32_t E, int32_t B, int32_t policy, int32_t* state, int32_t* counts,
+                          int64_t* fetches, int64_t* hits, uint8_t* f_per_step, int32_t* dev_error,
                           hipStream_t stream);
 
 /* maskmoe_status_string -- static, NUL-terminated description of a status code. */

@@ -22,7 +22,7 @@ OK, E_INVAL, E_WORKSPACE, E_HIP, E_UNSUPPORTED = 0, 1, 2, 3, 4
 ROUTE_PLAIN, ROUTE_HARD_MASK, ROUTE_SOFT_PRIOR = 0, 1, 2
 GATE_P, GATE_RENORM = 0, 1
 BF16, F32 = 0, 1
-CACHE_LRU = 0
+CACHE_LRU, CACHE_LFU, CACHE_FIFO = 0, 1, 2
 
 EXPORTS = ("maskmoe_route", "maskmoe_layer_workspace_bytes", "maskmoe_layer_forward",
            "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string")
@@ -70,7 +70,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                    _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp]
     lib.maskmoe_layer_forward_profiled.restype = ctypes.c_int
     lib.maskmoe_cache_fetches.argtypes = [_vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp,
-                                          _vp, _vp, _vp]
+                                          _vp, _vp, _vp, _vp]
     lib.maskmoe_cache_fetches.restype = ctypes.c_int
     lib.maskmoe_status_string.argtypes = [ctypes.c_int]
     lib.maskmoe_status_string.restype = ctypes.c_char_p
@@ -220,8 +220,10 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
 
 
 def maskmoe_cache_fetches(trace, E: int, B: int, state=None, with_f_per_step: bool = False,
-                          dev_error=None, policy: int = CACHE_LRU):
-    """Replay traces [L,S,N,K] (int32 device) through per-(layer, stream) caches.
+                          dev_error=None, policy: int = CACHE_LRU, counts=None):
+    """Replay traces [L,S,N,K] (int32 device) through per-(layer, stream) caches under
+    ``policy`` (CACHE_LRU, CACHE_LFU or CACHE_FIFO); ``counts`` [L,S,E] int32 device holds
+    LFU access counts (in/out) or is None.
 
     ``state`` [L,S,B] int32 device (in/out) or None; ``dev_error`` an int32
     device tensor that the kernel sets to 1 when it skips an entry (never
@@ -241,7 +243,10 @@ def maskmoe_cache_fetches(trace, E: int, B: int, state=None, with_f_per_step: bo
     fps = torch.empty((L, S, N), dtype=torch.uint8, device=dev) if with_f_per_step else None
     if state is not None and (state.dtype != torch.int32 or tuple(state.shape) != (L, S, B)):
         raise ValueError("state must be int32 [L,S,B]")
+    _dev(counts, "counts")
+    if counts is not None and (counts.dtype != torch.int32 or tuple(counts.shape) != (L, S, E)):
+        raise ValueError("counts must be int32 [L,S,E]")
     _check("maskmoe_cache_fetches", lib.maskmoe_cache_fetches(
-        _ptr(trace), L, S, N, K, E, B, policy, _ptr(state), _ptr(fetches), _ptr(hits), _ptr(fps),
+        _ptr(trace), L, S, N, K, E, B, policy, _ptr(state), _ptr(counts), _ptr(fetches), _ptr(hits), _ptr(fps),
         _ptr(dev_error), _stream()))
     return {"fetches": fetches, "hits": hits, "f_per_step": fps, "dev_error": dev_error}

@@ -239,20 +239,22 @@ int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x
 }
 
 int maskmoe_cache_fetches(const int32_t* trace, int32_t L, int32_t S, int32_t N, int32_t K, int32_t E,
-                          int32_t B, int32_t policy, int32_t* state, int64_t* fetches, int64_t* hits,
-                          uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream) {
+                          int32_t B, int32_t policy, int32_t* state, int32_t* counts, int64_t* fetches,
+                          int64_t* hits, uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream) {
   if (L < 0 || S < 0 || N < 0 || K < 1 || E < 1 || K > E || B < K) return MASKMOE_E_INVAL;
-  if (policy != MASKMOE_CACHE_LRU) return MASKMOE_E_INVAL;
+  if (policy != MASKMOE_CACHE_LRU && policy != MASKMOE_CACHE_LFU && policy != MASKMOE_CACHE_FIFO)
+    return MASKMOE_E_INVAL;
   if (E > kCacheMaxE) return MASKMOE_E_UNSUPPORTED;
   if (static_cast<int64_t>(N) * K + B >= (int64_t{1} << 24)) return MASKMOE_E_UNSUPPORTED;
   if (static_cast<int64_t>(L) * S >= (int64_t{1} << 31)) return MASKMOE_E_INVAL;
   if (static_cast<int64_t>(L) * S == 0) return MASKMOE_OK;
   if (!fetches || !hits || (N > 0 && !trace)) return MASKMOE_E_INVAL;
   if (!aligned(fetches, 8) || !aligned(hits, 8) || (trace && !aligned(trace, 4)) ||
-      (state && !aligned(state, 4)) || (dev_error && !aligned(dev_error, 4)))
+      (state && !aligned(state, 4)) || (counts && !aligned(counts, 4)) || (dev_error && !aligned(dev_error, 4)))
     return MASKMOE_E_INVAL;
-  return hip_status(maskmoe::launch_cache_lru(trace, L, S, N, K, E, B, state, fetches, hits, f_per_step,
-                                              dev_error, stream));
+  return hip_status(maskmoe::launch_cache(policy, trace, L, S, N, K, E, B, state,
+                                          policy == MASKMOE_CACHE_LFU ? counts : nullptr, fetches, hits,
+                                          f_per_step, dev_error, stream));
 }
 
 }  // extern "C"

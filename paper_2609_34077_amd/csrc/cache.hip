@@ -2,17 +2,18 @@
 //
 // Section 4.1 (Simulation): every layer keeps a cache of B routed experts; caches start
 // empty (or from a given state), initial fills are misses, each miss is one fetch and,
-// when the cache is full, one eviction. Eq. 5: h_{l,t} = selected experts already cached,
-// f_{l,t} = K - h_{l,t}; HR = sum h / (N L K), Fetches/tok = sum f / N.
+// when the cache is full, one eviction under LRU, LFU or FIFO. Eq. 5: h_{l,t} = selected
+// experts already cached, f_{l,t} = K - h_{l,t}; HR = sum h / (N L K), Fetches/tok = sum f / N.
 //
-// One wavefront replays one (layer, stream) trace; lane e owns expert e (E <= 64) and
-// keeps a cached flag and a last-use stamp. A step is a handful of wave-uniform bitmask
-// operations: ballot the cached set, intersect with the selected set for the hits, stamp
-// the hits in ascending expert order, then insert the misses in ascending order, each
-// evicting the cached expert with the smallest stamp. The selected experts always carry
-// the newest stamps, so the smallest stamp is never one of them. The trace is read 64
-// entries at a time, coalesced, and broadcast to the wave with lane shuffles; per-step
-// miss counts are gathered in lanes and written back 64 bytes at a time.
+// One wavefront replays one (layer, stream) trace; lane e owns expert e (E <= 64) and keeps
+// a cached flag, a stamp (last use for LRU and LFU, insertion time for FIFO) and, for LFU,
+// its access count. A step is a handful of wave-uniform bitmask operations: ballot the
+// cached set, intersect with the selected set for the hits, count the accesses (LFU), stamp
+// the hits in ascending expert order (LRU, LFU), then insert the misses in ascending order,
+// each evicting, among the cached experts not selected at this step, the smallest stamp
+// (LRU, FIFO) or the smallest (count, stamp) (LFU). The trace is read 64 entries at a time,
+// coalesced, and broadcast with lane shuffles; per-step miss counts are gathered in lanes
+// and written 64 bytes at a time.
 
 #include <limits.h>
 
@@ -24,10 +25,11 @@ namespace {
 
 constexpr int kCacheWavesPerBlock = 4;
 
-__global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_lru_kernel(
+template <int POLICY>  // 0 LRU, 1 LFU, 2 FIFO
+__global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_kernel(
     const int32_t* __restrict__ trace, int L, int S, int N, int K, int E, int B,
-    int32_t* __restrict__ state, int64_t* __restrict__ fetches, int64_t* __restrict__ hits,
-    uint8_t* __restrict__ f_per_step, int32_t* __restrict__ dev_error) {
+    int32_t* __restrict__ state, int32_t* __restrict__ counts, int64_t* __restrict__ fetches,
+    int64_t* __restrict__ hits, uint8_t* __restrict__ f_per_step, int32_t* __restrict__ dev_error) {
   const int lane = threadIdx.x & 63;
   const long stream = static_cast<long>(blockIdx.x) * kCacheWavesPerBlock + (threadIdx.x >> 6);
   if (stream >= static_cast<long>(L) * S) return;  // whole wavefront exits together
@@ -35,11 +37,13 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_lru_kernel(
 
   bool cached = false;
   int stamp = INT_MAX;
+  int count = 0;
   int ncached = 0;
   int clock = 0;
   bool bad = false;
 
-  if (state) {  // slots are listed least to most recently used
+  if (POLICY == 1 && counts && lane < E) count = counts[stream * E + lane];
+  if (state) {  // slots are listed oldest first
     const int32_t* st = state + stream * B;
     for (int s = 0; s < B; ++s) {
       const int e = st[s];  // wave-uniform
@@ -74,19 +78,30 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_lru_kernel(
           sel |= 1ull << e;
         }
       }
+      const bool mine = (sel >> lane) & 1ull;
+      if (POLICY == 1 && mine) ++count;
       const uint64_t cmask = __ballot(cached);
       const uint64_t hitm = sel & cmask;
       uint64_t missm = sel & ~cmask;
       const int h = __popcll(hitm), f = __popcll(missm);
-      if ((hitm >> lane) & 1ull) stamp = clock + __popcll(hitm & lanemask_lt(lane));
-      clock += h;
+      if (POLICY != 2) {  // a hit becomes the most recently used
+        if ((hitm >> lane) & 1ull) stamp = clock + __popcll(hitm & lanemask_lt(lane));
+        clock += h;
+      }
       while (missm) {
         const int e = __ffsll(static_cast<unsigned long long>(missm)) - 1;
         missm &= missm - 1;
         if (ncached >= B) {
-          const int key = cached ? stamp : INT_MAX;
+          const bool eligible = cached && !mine;
+          int key;
+          if (POLICY == 1) {  // lowest count first, then oldest stamp
+            const int low = wave_min_int(eligible ? count : INT_MAX);
+            key = (eligible && count == low) ? stamp : INT_MAX;
+          } else {
+            key = eligible ? stamp : INT_MAX;
+          }
           const int mn = wave_min_int(key);
-          const uint64_t vm = __ballot(cached && key == mn);
+          const uint64_t vm = __ballot(eligible && key == mn);
           const int victim = __ffsll(static_cast<unsigned long long>(vm)) - 1;
           if (lane == victim) {
             cached = false;
@@ -113,8 +128,9 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_lru_kernel(
     hits[stream] = tot_h;
     if (bad && dev_error) *dev_error = 1;
   }
+  if (POLICY == 1 && counts && lane < E) counts[stream * E + lane] = count;
   if (state) {
-    // rank of each cached expert by stamp = its slot, least recently used first
+    // rank of each cached expert by stamp = its slot, oldest first
     int rank = 0;
     for (int o = 0; o < 64; ++o) {
       const int so = __shfl(cached ? stamp : INT_MAX, o, kWave);
@@ -130,14 +146,22 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_lru_kernel(
 
 }  // namespace
 
-hipError_t launch_cache_lru(const int32_t* trace, int L, int S, int N, int K, int E, int B,
-                            int32_t* state, int64_t* fetches, int64_t* hits, uint8_t* f_per_step,
-                            int32_t* dev_error, hipStream_t stream) {
+hipError_t launch_cache(int policy, const int32_t* trace, int L, int S, int N, int K, int E, int B,
+                        int32_t* state, int32_t* counts, int64_t* fetches, int64_t* hits,
+                        uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream) {
   const long streams = static_cast<long>(L) * S;
   if (streams == 0) return hipSuccess;
-  const long blocks = (streams + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock;
-  hipLaunchKernelGGL(cache_lru_kernel, dim3(static_cast<unsigned>(blocks)), dim3(64 * kCacheWavesPerBlock),
-                     0, stream, trace, L, S, N, K, E, B, state, fetches, hits, f_per_step, dev_error);
+  const dim3 grid(static_cast<unsigned>((streams + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock));
+  const dim3 block(64 * kCacheWavesPerBlock);
+  if (policy == 1)
+    hipLaunchKernelGGL(cache_kernel<1>, grid, block, 0, stream, trace, L, S, N, K, E, B, state, counts, fetches,
+                       hits, f_per_step, dev_error);
+  else if (policy == 2)
+    hipLaunchKernelGGL(cache_kernel<2>, grid, block, 0, stream, trace, L, S, N, K, E, B, state, counts, fetches,
+                       hits, f_per_step, dev_error);
+  else
+    hipLaunchKernelGGL(cache_kernel<0>, grid, block, 0, stream, trace, L, S, N, K, E, B, state, counts, fetches,
+                       hits, f_per_step, dev_error);
   return hipGetLastError();
 }
 

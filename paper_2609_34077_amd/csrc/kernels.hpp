@@ -64,9 +64,10 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
 hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float* H, float* O,
                               void* y, hipStream_t stream, hipEvent_t* marks);
 
-// Per-(layer, stream) expert cache replay (LRU), one wavefront per stream.
-hipError_t launch_cache_lru(const int32_t* trace, int L, int S, int N, int K, int E, int B,
-                            int32_t* state, int64_t* fetches, int64_t* hits, uint8_t* f_per_step,
-                            int32_t* dev_error, hipStream_t stream);
+// Per-(layer, stream) expert cache replay (policy 0 LRU, 1 LFU, 2 FIFO), one wavefront per
+// stream.
+hipError_t launch_cache(int policy, const int32_t* trace, int L, int S, int N, int K, int E, int B,
+                        int32_t* state, int32_t* counts, int64_t* fetches, int64_t* hits,
+                        uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream);
 
 }  // namespace maskmoe

@@ -125,7 +125,7 @@ def test_workspace_bytes_monotone_in_tokens():
 
 def _cache(L_=1, S=1, N=4, K=2, E=8, B=4, policy=0, trace=FAKE, state=None, fetches=FAKE, hits=FAKE):
     lib = L.load()
-    return lib.maskmoe_cache_fetches(trace, L_, S, N, K, E, B, policy, state, fetches, hits, None, None, None)
+    return lib.maskmoe_cache_fetches(trace, L_, S, N, K, E, B, policy, state, None, fetches, hits, None, None, None)
 
 
 def test_cache_rejects_invalid_arguments():
@@ -133,7 +133,8 @@ def test_cache_rejects_invalid_arguments():
     assert _cache(K=0) == L.E_INVAL
     assert _cache(K=9) == L.E_INVAL          # K > E
     assert _cache(N=-1) == L.E_INVAL
-    assert _cache(policy=1) == L.E_INVAL
+    assert _cache(policy=3) == L.E_INVAL
+    assert _cache(policy=-1) == L.E_INVAL
     assert _cache(E=65, K=2) == L.E_UNSUPPORTED
     assert _cache(N=1 << 23, K=2) == L.E_UNSUPPORTED
     assert _cache(fetches=None) == L.E_INVAL

@@ -14,26 +14,31 @@ from paper_2609_34077_amd import synth
 pytestmark = pytest.mark.gpu
 
 
-def _gpu(trace, E, B, state=None, fps=True):
+def _gpu(trace, E, B, state=None, fps=True, policy=L.CACHE_LRU, counts=None):
     st = None if state is None else torch.from_numpy(np.ascontiguousarray(state, dtype=np.int32)).cuda()
+    ct = None if counts is None else torch.from_numpy(np.ascontiguousarray(counts, dtype=np.int32)).cuda()
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = L.maskmoe_cache_fetches(torch.from_numpy(np.ascontiguousarray(trace, dtype=np.int32)).cuda(), E, B,
-                                  state=st, with_f_per_step=fps, dev_error=err)
+                                  state=st, with_f_per_step=fps, dev_error=err, policy=policy, counts=ct)
     torch.cuda.synchronize()
     res = {k: (v.cpu().numpy() if v is not None else None) for k, v in out.items()}
     res["state"] = None if st is None else st.cpu().numpy()
+    res["counts"] = None if ct is None else ct.cpu().numpy()
     return res
 
 
-def _compare(trace, E, B, state=None):
-    g = _gpu(trace, E, B, state)
-    f, h, fps, final, bad = C.cache_fetches(trace, E, B, state)
+def _compare(trace, E, B, state=None, policy=L.CACHE_LRU, counts=None):
+    g = _gpu(trace, E, B, state, policy=policy, counts=counts)
+    out = C.cache_fetches(trace, E, B, state, policy=policy, counts=counts)
+    f, h, fps, final, bad = out[:5]
     np.testing.assert_array_equal(g["fetches"], f)
     np.testing.assert_array_equal(g["hits"], h)
     np.testing.assert_array_equal(g["f_per_step"], fps)
     assert int(g["dev_error"][0]) == int(bad)
     if state is not None:
         np.testing.assert_array_equal(g["state"], final)
+    if counts is not None and policy == L.CACHE_LFU:
+        np.testing.assert_array_equal(g["counts"], out[5])
     return g
 
 
@@ -143,3 +148,46 @@ def test_route_then_replay_end_to_end(delta):
     g2 = _gpu(trace_o, cfg.E, cfg.B)
     np.testing.assert_array_equal(g2["fetches"], f_o)
     np.testing.assert_array_equal(g2["hits"], h_o)
+
+
+POLICIES = [L.CACHE_LRU, L.CACHE_LFU, L.CACHE_FIFO]
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+@pytest.mark.parametrize("E,K,B,N", [(8, 2, 4, 300), (8, 2, 3, 65), (64, 6, 12, 200), (16, 3, 16, 40),
+                                     (6, 1, 2, 130), (64, 64, 64, 5)])
+def test_policies_bit_exact(policy, E, K, B, N):
+    U.say(f"cache policy={policy} E={E} K={K} B={B} N={N}")
+    tr = synth.random_trace(2, 9, N, K, E, seed=E * 31 + B * 7 + K + policy, locality=0.55)
+    _compare(tr, E, B, policy=policy)
+    st = np.full((2, 9, B), -1, np.int32)
+    cnt = np.random.default_rng(policy).integers(0, 5, size=(2, 9, E)).astype(np.int32)
+    _compare(tr, E, B, st, policy=policy, counts=cnt)
+
+
+def test_policy_hand_traces():
+    steps = [[0, 1], [2, 3], [4, 5], [2, 6], [2, 7], [0, 5], [2, 3], [1, 5]]
+    tr = np.array(steps, np.int32)[None, None]
+    for policy, total, final in ((L.CACHE_FIFO, 13, [2, 3, 1, 5]), (L.CACHE_LFU, 11, [2, 3, 5, 1])):
+        g = _compare(tr, 8, 4, np.full((1, 1, 4), -1, np.int32), policy=policy, counts=np.zeros((1, 1, 8), np.int32))
+        assert int(g["fetches"][0, 0]) == total and g["state"][0, 0].tolist() == final
+    tr2 = np.array([0, 0, 0, 1, 2, 0], np.int32).reshape(1, 1, 6, 1)
+    for policy, fexp in ((L.CACHE_LRU, [1, 0, 0, 1, 1, 1]), (L.CACHE_FIFO, [1, 0, 0, 1, 1, 1]),
+                         (L.CACHE_LFU, [1, 0, 0, 1, 1, 0])):
+        g = _compare(tr2, 3, 2, policy=policy)
+        assert g["f_per_step"][0, 0].tolist() == fexp
+
+
+@pytest.mark.parametrize("policy", [L.CACHE_LFU, L.CACHE_FIFO])
+def test_resume_with_state_and_counts(policy):
+    E, K, B = 8, 2, 4
+    tr = synth.random_trace(2, 5, 200, K, E, seed=12 + policy, locality=0.5)
+    z = lambda: (np.full((2, 5, B), -1, np.int32), np.zeros((2, 5, E), np.int32))
+    s0, c0 = z()
+    whole = _gpu(tr, E, B, s0, policy=policy, counts=c0)
+    s1, c1 = z()
+    first = _gpu(tr[:, :, :61], E, B, s1, policy=policy, counts=c1)
+    second = _gpu(tr[:, :, 61:], E, B, first["state"], policy=policy, counts=first["counts"])
+    np.testing.assert_array_equal(whole["fetches"], first["fetches"] + second["fetches"])
+    np.testing.assert_array_equal(whole["state"], second["state"])
+    np.testing.assert_array_equal(whole["counts"], second["counts"])

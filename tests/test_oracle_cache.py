@@ -1,13 +1,14 @@
 """Pins of the cache oracle against things other than itself (CPU only).
 
-* a hand-worked LRU trace (``tests/golden/lru_hand_trace.txt``);
+* hand-worked traces for LRU, FIFO and LFU (``tests/golden/lru_hand_trace.txt``,
+  ``tests/golden/cache_policy_hand_trace.txt``);
 * closed forms: with B = K a step misses exactly the experts not selected at
   the previous step; with B >= E only first uses miss;
 * per-step rules of Section 4.1 and Eq. 5: f <= K, f = K - h, the misses
   are the selected experts absent from the previous cache state, and
   Fetches/tok = L K (1 - HR); the paper's Table 2 obeys the same identity;
-* a second LRU written here with explicit time stamps agrees on random
-  traces;
+* second implementations written here with explicit time stamps and
+  counters (LRU, FIFO, LFU) agree on random traces;
 * a trace split in two and resumed from the saved state equals the whole.
 """
 
@@ -200,3 +201,111 @@ def test_invalid_entries_are_skipped_and_reported():
     assert bad
     assert f == [1, 1, 1] and h == [0, 0, 0]
     assert cache == [0, 1, 2]
+
+
+def test_hand_trace_fifo_and_lfu():
+    info, steps = _read_hand_trace()
+    E = int(info["E"])
+    for pol, name in ((C.FIFO, "FIFO"), (C.LFU, "LFU")):
+        states = [[int(v) for v in st.split(",")] for st in info[f"{name}_B4_state"].split("|")]
+        fexp = [int(v) for v in info[f"{name}_B4_f"].split()]
+        cache, counts = None, None
+        for t, A in enumerate(steps):
+            f, h, cache, counts, bad = C.replay_stream([A], E, 4, pol, cache, counts)
+            assert cache == states[t], (name, t)
+            assert f[0] == fexp[t]
+        f, _, _, counts, _ = C.replay_stream(steps, E, 4, pol)
+        assert sum(f) == int(info[f"{name}_B4_total"])
+        if pol == C.LFU:
+            assert counts == [int(v) for v in info["LFU_B4_counts"].split()]
+
+
+def test_policies_disagree_on_constructed_trace():
+    info = {}
+    with open(golden_path("cache_policy_hand_trace.txt")) as fh:
+        for line in fh:
+            if line.startswith("#") or not line.strip():
+                continue
+            k, v = line.split(None, 1)
+            info[k] = v.strip()
+    E, B = int(info["E"]), int(info["B"])
+    steps = [[int(v)] for v in info["steps"].split()]
+    for name, pol in C.POLICIES.items():
+        f, h, cache, counts, _ = C.replay_stream(steps, E, B, pol)
+        assert f == [int(v) for v in info[f"{name}_f"].split()], name
+        assert cache == [int(v) for v in info[f"{name}_state"].split(",")], name
+        if pol == C.LFU:
+            assert counts == [int(v) for v in info["LFU_counts"].split()]
+
+
+def _stamp_cache(steps, E, B, policy):
+    """Independent replay: dicts of last-use time, insertion time and access count."""
+    last, inserted, count, clock, f_all = {}, {}, [0] * E, 0, []
+    for A in steps:
+        A = sorted(set(A))
+        for e in A:
+            count[e] += 1
+        hit = [e for e in A if e in last]
+        for e in hit:
+            if policy != C.FIFO:
+                last[e] = clock
+            clock += 1
+        miss = 0
+        for e in A:
+            if e in hit:
+                continue
+            miss += 1
+            if len(last) >= B:
+                cand = [c for c in last if c not in A]
+                if policy == C.LRU:
+                    victim = min(cand, key=lambda c: last[c])
+                elif policy == C.FIFO:
+                    victim = min(cand, key=lambda c: inserted[c])
+                else:
+                    victim = min(cand, key=lambda c: (count[c], last[c]))
+                del last[victim]
+                del inserted[victim]
+            last[e] = clock
+            inserted[e] = clock
+            clock += 1
+        f_all.append(miss)
+    return f_all
+
+
+@pytest.mark.parametrize("policy", [C.LRU, C.FIFO, C.LFU])
+@pytest.mark.parametrize("E,K,B", [(8, 2, 4), (8, 2, 3), (16, 3, 5), (64, 6, 12), (6, 1, 2)])
+def test_policy_matches_stamp_implementation(policy, E, K, B):
+    tr = synth.random_trace(1, 5, 150, K, E, seed=E * 7 + B + policy, locality=0.5)
+    for s in range(tr.shape[1]):
+        steps = tr[0, s].tolist()
+        f, _, _, _, _ = C.replay_stream(steps, E, B, policy)
+        assert f == _stamp_cache(steps, E, B, policy)
+
+
+@pytest.mark.parametrize("policy", [C.LRU, C.FIFO, C.LFU])
+def test_closed_forms_hold_for_every_policy(policy):
+    E, K = 8, 2
+    tr = synth.random_trace(1, 3, 200, K, E, seed=90 + policy, locality=0.6)
+    for s in range(3):
+        steps = tr[0, s].tolist()
+        f, _, _, _, _ = C.replay_stream(steps, E, K, policy)           # B = K
+        prev = set()
+        for t, A in enumerate(steps):
+            assert f[t] == K - len(set(A) & prev)
+            prev = set(A)
+        f, _, _, _, _ = C.replay_stream(steps, E, E, policy)           # B = E
+        assert sum(f) == len({e for A in steps for e in A})
+
+
+@pytest.mark.parametrize("policy", [C.FIFO, C.LFU])
+def test_resume_with_state_and_counts(policy):
+    E, K, B, L, S, N = 8, 2, 4, 2, 3, 80
+    tr = synth.random_trace(L, S, N, K, E, seed=77, locality=0.5)
+    whole = C.cache_fetches(tr, E, B, policy=policy)
+    first = C.cache_fetches(tr[:, :, :31], E, B, policy=policy)
+    second = C.cache_fetches(tr[:, :, 31:], E, B, state=first[3], policy=policy,
+                             counts=first[5] if policy == C.LFU else None)
+    np.testing.assert_array_equal(whole[0], first[0] + second[0])
+    np.testing.assert_array_equal(whole[3], second[3])
+    if policy == C.LFU:
+        np.testing.assert_array_equal(whole[5], second[5])
