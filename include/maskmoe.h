@@ -155,9 +155,12 @@ enum {
  * maskmoe_layer_forward_profiled -- maskmoe_layer_forward that also records caller-owned
  * HIP events on `stream`, for measuring each stage on the device timeline: events[0]
  * before the first launch and events[s + 1] after stage s (MASKMOE_STAGE_*). A stage that
- * a path fuses into the previous one (the combine of the few-token path) gets its event
- * right after that one. Same computation, outputs and errors as maskmoe_layer_forward;
- * E_INVAL when `events` or any of its MASKMOE_NUM_STAGES + 1 entries is NULL.
+ * a path fuses into the previous one (the permutation of the few-token path, done by the
+ * routing kernel) gets its event right after that one; the few-token path's SwiGLU pass
+ * over split gate/up partial sums is timed with the DOWN stage. `events` holds
+ * MASKMOE_NUM_STAGES + 1 entries; a NULL entry is skipped, so a caller can bracket one
+ * stage without adding event records elsewhere. Same computation, outputs and errors as
+ * maskmoe_layer_forward; E_INVAL when `events` is NULL.
  */
 int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                                    const uint8_t* mask, const float* prior, const void* w_gate_up,

@@ -176,9 +176,9 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
 
     Returns y [T,d] (dtype of x). ``workspace`` (uint8 device tensor) is
     allocated when not given; ``topk_idx``/``topk_gate`` [T,K] receive the
-    routing decision when given. ``events``: NUM_STAGES + 1 already-recorded
-    ``torch.cuda.Event(enable_timing=True)`` objects; when given, the profiled
-    entry point re-records them around the stages.
+    routing decision when given. ``events``: NUM_STAGES + 1 entries, each None or an
+    already-recorded ``torch.cuda.Event(enable_timing=True)``; when given, the
+    profiled entry point re-records the non-None ones around the stages.
     """
     import torch
     lib = load()
@@ -213,7 +213,7 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
     else:
         if len(events) != NUM_STAGES + 1:
             raise ValueError(f"need {NUM_STAGES + 1} events")
-        handles = (ctypes.c_void_p * len(events))(*[ev.cuda_event for ev in events])
+        handles = (ctypes.c_void_p * len(events))(*[None if ev is None else ev.cuda_event for ev in events])
         _check("maskmoe_layer_forward_profiled", lib.maskmoe_layer_forward_profiled(*args, handles, _stream()))
     del m_arr, p_arr
     return y

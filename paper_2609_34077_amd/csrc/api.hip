@@ -53,8 +53,11 @@ int check_mask_prior(int mode, int L, int E, int K, const uint8_t* mask, const f
 }
 
 struct Layout {
-  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, H, O, total;
+  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, H, P, O, total;
 };
+
+static_assert(maskmoe::kDecodeMaxT <= maskmoe::kRouteOneBlockT,
+              "the few-token path routes and permutes in one workgroup");
 
 bool uses_decode_path(const maskmoe_layer_desc& d) {
   return d.dtype == MASKMOE_BF16 && d.T <= maskmoe::kDecodeMaxT;
@@ -82,11 +85,14 @@ Layout layout(const maskmoe_layer_desc& d) {
   w.inv = take(TK * 4);
   w.row_tok = take(rows * 4);
   w.H = take(rows * d.F * hsz);
-  // O holds the expert outputs: [rows, d], or [split, rows, d] on the few-token path. It is
-  // sized for the largest split (8) of up to kDecodeMaxT tokens so the total stays monotone in T.
+  // O holds the expert outputs: [rows, d], or [split, rows, d] on the few-token path; P the
+  // few-token partial gate/up sums [split_gu, rows, 2F]. Both are sized for the largest
+  // splits of up to kDecodeMaxT tokens so the total stays monotone in T.
   const size_t dec_T = static_cast<size_t>(d.T < maskmoe::kDecodeMaxT ? d.T : maskmoe::kDecodeMaxT);
-  const size_t dec_rows = 8 * dec_T * (d.K + d.n_shared);
-  w.O = take((rows > dec_rows ? rows : dec_rows) * d.d * 4);
+  const size_t dec_rows = dec_T * (d.K + d.n_shared);
+  w.P = take(maskmoe::kDecodeMaxSplitGateUp * dec_rows * 2 * d.F * 4);
+  const size_t o_rows = maskmoe::kDecodeMaxSplit * dec_rows;
+  w.O = take((rows > o_rows ? rows : o_rows) * d.d * 4);
   w.total = off;
   return w;
 }
@@ -182,12 +188,20 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   pb.row_tok = reinterpret_cast<int32_t*>(ws + w.row_tok);
 
   maskmoe::record_mark(events, 0, stream);
-  hipError_t e = maskmoe::launch_route(bf16, x, w_router, d.T, d.d, d.E, d.K, 1, d.route_mode, d.gate_mode,
-                                       mask, prior, idx, gate, nullptr, stream);
-  if (e != hipSuccess) return MASKMOE_E_HIP;
-  maskmoe::record_mark(events, 1, stream);
-  e = maskmoe::launch_permute(idx, d.T, d.K, d.E, d.n_shared, maskmoe::kGemmBM, pb, stream);
-  if (e != hipSuccess) return MASKMOE_E_HIP;
+  hipError_t e;
+  if (uses_decode_path(d)) {  // one workgroup routes every token and then permutes them
+    e = maskmoe::launch_route_permute(x, w_router, d.T, d.d, d.E, d.K, d.route_mode, d.gate_mode, mask, prior, idx,
+                                      gate, d.n_shared, maskmoe::kGemmBM, pb, stream);
+    if (e != hipSuccess) return MASKMOE_E_HIP;
+    maskmoe::record_mark(events, 1, stream);
+  } else {
+    e = maskmoe::launch_route(bf16, x, w_router, d.T, d.d, d.E, d.K, 1, d.route_mode, d.gate_mode, mask, prior,
+                              idx, gate, nullptr, stream);
+    if (e != hipSuccess) return MASKMOE_E_HIP;
+    maskmoe::record_mark(events, 1, stream);
+    e = maskmoe::launch_permute(idx, d.T, d.K, d.E, d.n_shared, maskmoe::kGemmBM, pb, stream);
+    if (e != hipSuccess) return MASKMOE_E_HIP;
+  }
   maskmoe::record_mark(events, 2, stream);
   hipEvent_t* expert_marks = events ? events + 3 : nullptr;
 
@@ -204,7 +218,8 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
                                     y, stream, expert_marks);
   } else if (uses_decode_path(d)) {
     e = maskmoe::launch_experts_bf16_decode(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
-                                            reinterpret_cast<float*>(ws + w.O), y, stream, expert_marks);
+                                            reinterpret_cast<float*>(ws + w.P), reinterpret_cast<float*>(ws + w.O), y,
+                                            stream, expert_marks);
   } else {
     const int64_t TK = static_cast<int64_t>(d.T) * d.K;
     const int64_t nonempty = TK < d.E ? TK : d.E;
@@ -232,8 +247,6 @@ int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x
                                    void* y, int32_t* topk_idx, float* topk_gate, void* workspace,
                                    size_t workspace_bytes, hipEvent_t* events, hipStream_t stream) {
   if (!events) return MASKMOE_E_INVAL;
-  for (int i = 0; i <= MASKMOE_NUM_STAGES; ++i)
-    if (!events[i]) return MASKMOE_E_INVAL;
   return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
                             topk_idx, topk_gate, workspace, workspace_bytes, stream, events);
 }

@@ -18,12 +18,14 @@
 //
 // bf16, few tokens (decode): the work is reading each selected expert's weights once; the
 // kernels stream weight rows through LDS in cache-line-sized row segments (see the decode
-// section below) and a split-K down projection keeps every CU busy when only two experts
-// are active. MFMA 16x16x32 with the token rows padded to 16.
+// section below); both projections split their reduction dimension when few experts are
+// active so that every CU keeps streaming. MFMA 16x16x32 with the token rows padded to 16.
 //
 // f32: plain fp32 loops (no MFMA), one thread per output element.
 
-#include <math.h>
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -229,41 +231,59 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
 // y_t = sum_k gate[t,k] * O[inv[t*K+k]] + sum_s O[T*K + s*T + t]; fp32 sum in k order, one
 // rounding at the end. O holds `split` partial slices [split, rows, d] that are added first,
 // in slice order. One workgroup per token.
+// Sum of the `split` slices at offset off, added in slice order; groups of four loads are
+// issued together so that a long split costs a few memory round trips, not one per slice.
 __device__ __forceinline__ float4 sum_slices(const float* O, int split, size_t slice, size_t off) {
   float4 v = *reinterpret_cast<const float4*>(O + off);
-  for (int z = 1; z < split; ++z) {
+  int z = 1;
+  for (; z + 3 < split; z += 4) {
+    float4 u[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) u[i] = *reinterpret_cast<const float4*>(O + (z + i) * slice + off);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v.x += u[i].x; v.y += u[i].y; v.z += u[i].z; v.w += u[i].w;
+    }
+  }
+  for (; z < split; ++z) {
     const float4 u = *reinterpret_cast<const float4*>(O + z * slice + off);
     v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
   }
   return v;
 }
 
+// y[t, c] = sum_k gate[t, k] O[inv[t K + k], c] + sum over shared experts of their rows, with
+// O's slices added first. One workgroup of 256 threads per (token, block of kCombineCols
+// columns), token-major in a 1-D grid.
+constexpr int kCombineCols = 1024;
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
                                                        const int32_t* __restrict__ inv,
                                                        const float* __restrict__ gate, int T, int K,
                                                        int n_shared, int d, void* y, int split) {
-  const int t = blockIdx.x;
+  const int nb = (d + kCombineCols - 1) / kCombineCols;
+  const int t = blockIdx.x / nb, cb = blockIdx.x % nb;
   if (BF16) {  // d % 4 == 0
     const size_t slice = static_cast<size_t>(T) * (K + n_shared) * d;
-    for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
-      float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int k = 0; k < K; ++k) {
-        const float gk = gate[t * K + k];
-        const float4 v = sum_slices(O, split, slice, static_cast<size_t>(inv[t * K + k]) * d + c);
-        s.x += gk * v.x; s.y += gk * v.y; s.z += gk * v.z; s.w += gk * v.w;
-      }
-      for (int sh = 0; sh < n_shared; ++sh) {
-        const float4 v = sum_slices(O, split, slice, (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c);
-        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-      }
-      uint2 packed;
-      packed.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
-      packed.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
-      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d + c) = packed;
+    const int c = cb * kCombineCols + threadIdx.x * 4;
+    if (c >= d) return;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k = 0; k < K; ++k) {
+      const float gk = gate[t * K + k];
+      const float4 v = sum_slices(O, split, slice, static_cast<size_t>(inv[t * K + k]) * d + c);
+      s.x += gk * v.x; s.y += gk * v.y; s.z += gk * v.z; s.w += gk * v.w;
     }
+    for (int sh = 0; sh < n_shared; ++sh) {
+      const float4 v = sum_slices(O, split, slice, (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c);
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+    uint2 packed;
+    packed.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
+    packed.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d + c) = packed;
   } else {
-    for (int c = threadIdx.x; c < d; c += 256) {
+    for (int c = cb * kCombineCols + threadIdx.x; c < d && c < (cb + 1) * kCombineCols; c += 256) {
       float s = 0.0f;
       for (int k = 0; k < K; ++k) s += gate[t * K + k] * O[static_cast<size_t>(inv[t * K + k]) * d + c];
       for (int sh = 0; sh < n_shared; ++sh) s += O[(static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c];
@@ -271,6 +291,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     }
   }
 }
+
+static dim3 combine_grid(int T, int d) { return dim3(T * ((d + kCombineCols - 1) / kCombineCols)); }
 
 // ------------------------------------------------------------------ bf16 decode kernels
 //
@@ -281,8 +303,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 // which a wavefront covers whole 128-byte row segments (full cache lines), stored to LDS with
 // a 16-byte row pad (conflict-free MFMA operand reads), and multiplied on MFMA 16x16x32 with
 // the token rows padded to 16. The next chunk's loads are in flight while the current one is
-// multiplied. The down projection splits its reduction over F into `split` slices so that
-// enough workgroups stream at once; the combine adds the slices in order.
+// multiplied. Both projections split their reduction dimension into slices when few experts
+// are active, so that enough workgroups stream at once: the gate/up slices are added by a
+// small SwiGLU pass, the down slices by the combine, always in slice order. (Letting the
+// last workgroup of a column slab do the combine needs a device-scope release per
+// workgroup, which on this multi-XCD part costs more than the separate small launch.)
 
 constexpr int DEC_NT = 4;        // 16-row weight tiles per operand per workgroup
 constexpr int DEC_CK = 64;       // reduction values per chunk (128 bytes per row)
@@ -299,8 +324,9 @@ struct DecodeArgs {
   const uint16_t* ws_gate_up;
   const uint16_t* ws_down;
   uint16_t* H;        // [rows, F] bf16
+  float* P;           // [split_gu, rows, 2F] fp32 partial gate/up sums (split_gu > 1)
   float* O;           // [split, rows, d] fp32
-  int T, d, F, E, K, rows, split;
+  int T, d, F, E, K, rows, split, split_gu;
 };
 
 // Streams R = 16 * NTILE weight rows (row r starts at wrow(r)) over k in [k0, k0 + klen) and
@@ -362,7 +388,9 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
 }
 
 // H[row0 + r, n0 + j] = SiLU(x_r . W_gate[n0 + j]) * (x_r . W_up[n0 + j]) for the rows of one
-// active expert; grid (F / (16 * DEC_NT), max active experts).
+// active expert; grid (F / (16 * DEC_NT), max active experts, split_gu). With split_gu > 1
+// each workgroup covers one slice of d and writes its partial dot products to P instead;
+// decode_swiglu_kernel then adds the slices and applies SwiGLU.
 __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const DecodeArgs p) {
   constexpr int NTILE = 2 * DEC_NT;
   constexpr int TPW = (NTILE + 3) / 4;
@@ -385,7 +413,21 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const Decod
   f32x4 acc[TPW];
 #pragma unroll
   for (int q = 0; q < TPW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  stream_rows<NTILE>(wrow, arow, 0, p.d, lds, acc);
+  const int klen = p.d / p.split_gu, z = blockIdx.z;
+  stream_rows<NTILE>(wrow, arow, z * klen, klen, lds, acc);
+  if (p.split_gu > 1) {  // partial sums: wave w holds tiles w and w + 4 (gate tile j, up tile j)
+#pragma unroll
+    for (int q = 0; q < TPW; ++q) {
+      const int tile = wave + 4 * q;
+      const int col = n0 + (tile % DEC_NT) * 16 + (lane & 15) + (tile < DEC_NT ? 0 : F);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 4 * (lane >> 4) + i;
+        if (row < nrows) p.P[(static_cast<size_t>(z) * p.rows + row0 + row) * 2 * F + col] = acc[q][i];
+      }
+    }
+    return;
+  }
   // gate tile j pairs with up tile j + DEC_NT: exchange through LDS
   f32x4* ex = reinterpret_cast<f32x4*>(&lds[0][0]);
 #pragma unroll
@@ -402,6 +444,40 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const Decod
     if (row < nrows)
       p.H[static_cast<size_t>(row0 + row) * p.F + n0 + j * 16 + (l & 15)] = f32_to_bf16(silu(gs[i]) * us[i]);
   }
+}
+
+// H[r, c] = SiLU(sum_z P[z, r, c]) * (sum_z P[z, r, F + c]), slices added in order. One
+// thread per four columns (F % 64 == 0); the loads of all slices are issued together.
+__global__ __launch_bounds__(256) void decode_swiglu_kernel(const float* __restrict__ P, uint16_t* __restrict__ H,
+                                                            int rows, int F, int split) {
+  const int i = blockIdx.x * 256 + threadIdx.x;   // index of a group of four columns
+  const int per_row = F / 4;
+  if (i >= rows * per_row) return;
+  const int r = i / per_row, c = (i - r * per_row) * 4;
+  const size_t slice = static_cast<size_t>(rows) * 2 * F;
+  const float* src = P + static_cast<size_t>(r) * 2 * F + c;
+  float4 g[kDecodeMaxSplitGateUp], u[kDecodeMaxSplitGateUp];
+#pragma unroll
+  for (int z = 0; z < kDecodeMaxSplitGateUp; ++z) {
+    if (z < split) {
+      g[z] = *reinterpret_cast<const float4*>(src + z * slice);
+      u[z] = *reinterpret_cast<const float4*>(src + z * slice + F);
+    }
+  }
+  float4 gs = g[0], us = u[0];
+#pragma unroll
+  for (int z = 1; z < kDecodeMaxSplitGateUp; ++z) {
+    if (z < split) {
+      gs.x += g[z].x; gs.y += g[z].y; gs.z += g[z].z; gs.w += g[z].w;
+      us.x += u[z].x; us.y += u[z].y; us.z += u[z].z; us.w += u[z].w;
+    }
+  }
+  uint2 packed;
+  packed.x = static_cast<uint32_t>(f32_to_bf16(silu(gs.x) * us.x)) |
+             (static_cast<uint32_t>(f32_to_bf16(silu(gs.y) * us.y)) << 16);
+  packed.y = static_cast<uint32_t>(f32_to_bf16(silu(gs.z) * us.z)) |
+             (static_cast<uint32_t>(f32_to_bf16(silu(gs.w) * us.w)) << 16);
+  *reinterpret_cast<uint2*>(H + static_cast<size_t>(r) * F + c) = packed;
 }
 
 // O[z, row0 + r, n0 + j] = sum over k in slice z of H[row0 + r, k] * W_down[n0 + j, k];
@@ -432,6 +508,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeAr
     if (row < nrows)
       p.O[(static_cast<size_t>(z) * p.rows + row0 + row) * p.d + n0 + wave * 16 + (lane & 15)] = acc[0][i];
   }
+
 }
 
 // ------------------------------------------------------------------ f32 kernels
@@ -524,27 +601,59 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
 
-  hipLaunchKernelGGL(combine_kernel<true>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
+  hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
                      a.K, a.n_shared, a.d, y, 1);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
 }
 
-int decode_split(int T, int d, int F, int E, int K, int n_shared) {
-  // enough (expert, column-slab, slice) workgroups for every CU to stream several at once
-  const int max_active = (T * K < E ? T * K : E) + n_shared;
-  const int slabs = d / (16 * DEC_NT) * max_active;
-  if (slabs <= 0) return 1;  // no tokens: nothing is launched
-  const int target = (1024 + slabs - 1) / slabs;
-  const int chunks = F / DEC_CK;
-  int best = 1;  // at most 8: the workspace reserves 8 slices
-  for (int s = 1; s <= 8 && s <= target; ++s)
-    if (chunks % s == 0) best = s;
+// Slices of the reduction dimension for the two streaming kernels. Measured on MI355X, a
+// weight stream of this shape runs best with about 1800 workgroups in flight: fewer leave
+// HBM channels idle, and a count just past one full residency wave leaves a ragged second
+// wave. The split is the power of two (dividing the chunk count) whose workgroup count is
+// closest to that target, for the number of experts a batch of T tokens is expected to
+// activate under uniform routing, E (1 - (1 - K/E)^T), plus the shared experts. The grid is
+// still sized for the most experts that can be active; the estimate only picks the split.
+constexpr int kDecodeTargetWGs = 1792;
+
+static int best_split(int per_slice_wgs, int chunks, int max_split) {
+  if (per_slice_wgs <= 0) return 1;  // no tokens: nothing is launched
+  int best = 1, best_gap = 1 << 30;
+  for (int s = 1; s <= max_split; s *= 2) {
+    if (chunks % s) break;
+    const int gap = std::abs(per_slice_wgs * s - kDecodeTargetWGs);
+    if (gap < best_gap) {
+      best_gap = gap;
+      best = s;
+    }
+  }
   return best;
 }
 
-hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
+static int max_active_groups(int T, int E, int K, int n_shared) {
+  return (T * K < E ? T * K : E) + n_shared;
+}
+
+static int expected_active_groups(int T, int E, int K, int n_shared) {
+  if (T <= 0) return 0;
+  const double routed = E * (1.0 - std::pow(1.0 - static_cast<double>(K) / E, T));
+  int a = static_cast<int>(std::lround(routed));
+  a = std::max(a, K);
+  a = std::min(a, T * K < E ? T * K : E);
+  return a + n_shared;
+}
+
+int decode_split(int T, int d, int F, int E, int K, int n_shared) {
+  return best_split(d / (16 * DEC_NT) * expected_active_groups(T, E, K, n_shared), F / DEC_CK, kDecodeMaxSplit);
+}
+
+int decode_split_gate_up(int T, int d, int F, int E, int K, int n_shared) {
+  return best_split(F / (16 * DEC_NT) * expected_active_groups(T, E, K, n_shared), d / DEC_CK,
+                    kDecodeMaxSplitGateUp);
+}
+
+hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* P, float* O,
                                       void* y, hipStream_t stream, hipEvent_t* marks) {
   DecodeArgs p;
   p.x = static_cast<const uint16_t*>(a.x);
@@ -557,21 +666,31 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
   p.ws_gate_up = static_cast<const uint16_t*>(a.ws_gate_up);
   p.ws_down = static_cast<const uint16_t*>(a.ws_down);
   p.H = H;
+  p.P = P;
   p.O = O;
   p.T = a.T; p.d = a.d; p.F = a.F; p.E = a.E; p.K = a.K;
   p.rows = a.T * (a.K + a.n_shared);
   p.split = decode_split(a.T, a.d, a.F, a.E, a.K, a.n_shared);
-  const int max_active = (a.T * a.K < a.E ? a.T * a.K : a.E) + a.n_shared;
-  hipLaunchKernelGGL(decode_gate_up_kernel, dim3(a.F / (16 * DEC_NT), max_active), dim3(DEC_THREADS), 0, stream, p);
+  p.split_gu = decode_split_gate_up(a.T, a.d, a.F, a.E, a.K, a.n_shared);
+  const int max_active = max_active_groups(a.T, a.E, a.K, a.n_shared);
+  hipLaunchKernelGGL(decode_gate_up_kernel, dim3(a.F / (16 * DEC_NT), max_active, p.split_gu), dim3(DEC_THREADS),
+                     0, stream, p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
+  if (p.split_gu > 1) {  // timed with the down stage
+    const int groups = p.rows * (p.F / 4);   // rows <= 16 (K + n_shared): no overflow
+    const unsigned blocks = static_cast<unsigned>((groups + 255) / 256);
+    hipLaunchKernelGGL(decode_swiglu_kernel, dim3(blocks), dim3(256), 0, stream, P, H, p.rows, p.F, p.split_gu);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
   hipLaunchKernelGGL(decode_down_kernel, dim3(a.d / (16 * DEC_NT), max_active, p.split), dim3(DEC_THREADS), 0,
                      stream, p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
-  hipLaunchKernelGGL(combine_kernel<true>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T, a.K,
+  hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T, a.K,
                      a.n_shared, a.d, y, p.split);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
@@ -601,7 +720,7 @@ hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float*
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
-  hipLaunchKernelGGL(combine_kernel<false>, dim3(a.T), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
+  hipLaunchKernelGGL(combine_kernel<false>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
                      a.K, a.n_shared, a.d, y, 1);
   err = hipGetLastError();
   record_mark(marks, 2, stream);

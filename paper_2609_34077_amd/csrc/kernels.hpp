@@ -8,13 +8,6 @@
 
 namespace maskmoe {
 
-// Router logits + softmax + mask/prior Top-K + gates for layers [0, L) of w_router
-// ([L, E, d]); host `mask` [L, E] (HARD_MASK) or `prior` [L, E] (SOFT_PRIOR), unused for
-// PLAIN. Outputs idx/gate [L, T, K], margin [L, T].
-hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
-                        int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
-                        int32_t* idx, float* gate, float* margin, hipStream_t stream);
-
 // Group the T*K routed (token, slot) entries by expert, stably in entry order, and append
 // n_shared groups of all T tokens. Writes offsets/tile_off [G+1], active [G], n_active [1],
 // perm/inv [T*K], row_tok [T*(K+n_shared)], with G = E + n_shared.
@@ -27,6 +20,23 @@ struct PermBuffers {
   int32_t* inv;
   int32_t* row_tok;
 };
+// Router logits + softmax + mask/prior Top-K + gates for layers [0, L) of w_router
+// ([L, E, d]); host `mask` [L, E] (HARD_MASK) or `prior` [L, E] (SOFT_PRIOR), unused for
+// PLAIN. Outputs idx/gate [L, T, K], margin [L, T].
+hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
+                        int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
+                        int32_t* idx, float* gate, float* margin, hipStream_t stream);
+
+// Tokens at or below which one bf16 routing workgroup covers every token, so the routing
+// kernel can also perform the permutation (launch_route_permute).
+constexpr int kRouteOneBlockT = 16;
+// Routing of one layer (L = 1, bf16, T <= kRouteOneBlockT) followed, in the same workgroup,
+// by the permutation into `pb` (rows tiled by tile_rows, n_shared shared groups).
+hipError_t launch_route_permute(const void* x, const void* w_router, int T, int d, int E, int K, int mode,
+                                int gate_mode, const uint8_t* mask, const float* prior, int32_t* idx,
+                                float* gate, int n_shared, int tile_rows, const PermBuffers& pb,
+                                hipStream_t stream);
+
 hipError_t launch_permute(const int32_t* idx, int T, int K, int E, int n_shared, int tile_rows,
                           const PermBuffers& pb, hipStream_t stream);
 
@@ -49,16 +59,20 @@ struct ExpertArgs {
 // the i-th of the three expert stages (gate/up, down, combine); a stage that a path fuses
 // away is marked right after the previous one.
 inline void record_mark(hipEvent_t* marks, int i, hipStream_t stream) {
-  if (marks) (void)hipEventRecord(marks[i], stream);
+  if (marks && marks[i]) (void)hipEventRecord(marks[i], stream);
 }
 
 // bf16, T > kDecodeMaxT: H = SwiGLU(X_g W_gate,up^T) per group; O = H W_down^T; y = combine.
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
                                void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks);
-// bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel, split-K down projection into
-// O [split, rows, d], then the combine. decode_split() gives the split for a layer.
+// bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel (split-K into P [split_gu, rows, 2F]
+// plus a SwiGLU pass when decode_split_gate_up() > 1), split-K down projection into
+// O [split, rows, d] with split = decode_split(), then the combine.
+constexpr int kDecodeMaxSplit = 16;
+constexpr int kDecodeMaxSplitGateUp = 8;
 int decode_split(int T, int d, int F, int E, int K, int n_shared);
-hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
+int decode_split_gate_up(int T, int d, int F, int E, int K, int n_shared);
+hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* P, float* O,
                                       void* y, hipStream_t stream, hipEvent_t* marks);
 // f32 path (no MFMA; fp32 end to end).
 hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float* H, float* O,

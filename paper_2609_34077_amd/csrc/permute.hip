@@ -1,96 +1,17 @@
-// Token permutation by expert.
-//
-// The combine of Eq. 1 (Section 3.1) sums, for every token, the outputs of the experts it
-// selected. To run each expert as one dense GEMM over the tokens that chose it, the T*K
-// (token, slot) entries j = t*K + k are grouped by expert, keeping entry order inside a
-// group (a stable counting sort), and n_shared groups holding every token are appended
-// for the shared experts (Section 3.1). Outputs, with G = E + n_shared groups:
-//   offsets[g]   first row of group g (offsets[G] = T*(K + n_shared))
-//   tile_off[g]  first row-tile of group g in units of `tile_rows` (tile_off[G] = total)
-//   active[i]    the i-th non-empty group, n_active[0] their count
-//   perm[pos]    entry j placed at row pos (routed rows only), inv[j] = pos
-//   row_tok[pos] token of row pos (routed and shared rows)
-// One workgroup of 1024 threads: LDS histogram, scan, then a chunked stable scatter where
-// the rank of an entry among equal experts inside a wavefront comes from ballots on the
-// expert id bits. Integer only, deterministic.
+// Token permutation by expert (see permute_block.hpp): one workgroup of 1024 threads.
 
-#include "common.hpp"
-#include "kernels.hpp"
+#include "permute_block.hpp"
 
 namespace maskmoe {
 namespace {
 
 constexpr int kPermThreads = 1024;
-constexpr int kPermWaves = kPermThreads / kWave;
-constexpr int kMaxGroups = 256 + 8;
 
-__global__ __launch_bounds__(kPermThreads) void permute_kernel(const int32_t* __restrict__ idx, int T,
-                                                              int K, int E, int n_shared,
-                                                              int tile_rows, PermBuffers pb) {
-  __shared__ int hist[kMaxGroups];
-  __shared__ int running[kMaxGroups];
-  __shared__ int wcnt[kPermWaves][kMaxGroups];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n = T * K;
-  const int G = E + n_shared;
-
-  for (int g = tid; g < G; g += kPermThreads) hist[g] = 0;
-  __syncthreads();
-  for (int j = tid; j < n; j += kPermThreads) {
-    const int e = idx[j];
-    if (e >= 0 && e < E) atomicAdd(&hist[e], 1);  // LDS integer counts: order-independent
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int off = 0, toff = 0, na = 0;
-    for (int g = 0; g < G; ++g) {
-      const int c = g < E ? hist[g] : T;
-      pb.offsets[g] = off;
-      pb.tile_off[g] = toff;
-      running[g] = off;
-      if (c > 0) pb.active[na++] = g;
-      off += c;
-      toff += (c + tile_rows - 1) / tile_rows;
-    }
-    pb.offsets[G] = off;
-    pb.tile_off[G] = toff;
-    pb.n_active[0] = na;
-  }
-  // shared-expert rows: token t of shared expert s sits at row n + s*T + t
-  for (int r = tid; r < n_shared * T; r += kPermThreads) pb.row_tok[n + r] = r % T;
-  __syncthreads();
-
-  for (int base = 0; base < n; base += kPermThreads) {
-    const int j = base + tid;
-    const int e = (j < n) ? idx[j] : -1;
-    const bool valid = e >= 0 && e < E;
-    // lanes of this wavefront holding the same expert
-    uint64_t same = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < 9; ++b) {
-      const uint64_t bb = __ballot(valid && ((e >> b) & 1));
-      same &= ((e >> b) & 1) ? bb : ~bb;
-    }
-    for (int g = lane; g < G; g += kWave) wcnt[wave][g] = 0;
-    __syncthreads();
-    const uint64_t lower = same & lanemask_lt(lane);
-    if (valid && lower == 0) wcnt[wave][e] = __popcll(same);
-    __syncthreads();
-    if (valid) {
-      int pos = running[e] + __popcll(lower);
-      for (int w = 0; w < wave; ++w) pos += wcnt[w][e];
-      pb.perm[pos] = j;
-      pb.inv[j] = pos;
-      pb.row_tok[pos] = j / K;
-    }
-    __syncthreads();
-    for (int g = tid; g < E; g += kPermThreads) {
-      int s = 0;
-      for (int w = 0; w < kPermWaves; ++w) s += wcnt[w][g];
-      running[g] += s;
-    }
-    __syncthreads();
-  }
+__global__ __launch_bounds__(kPermThreads) void permute_kernel(const int32_t* __restrict__ idx, int T, int K,
+                                                              int E, int n_shared, int tile_rows,
+                                                              PermBuffers pb) {
+  __shared__ PermLds lds;
+  permute_block(idx, T, K, E, n_shared, tile_rows, pb, lds);
 }
 
 }  // namespace

@@ -21,6 +21,7 @@
 
 #include "common.hpp"
 #include "kernels.hpp"
+#include "permute_block.hpp"
 
 namespace maskmoe {
 namespace {
@@ -35,6 +36,8 @@ struct RouteParams {
   float* gate;         // [L, T, K]
   float* margin;       // [L, T] or null
   int T, d, E, K, L, lpw, mode, gate_mode;
+  PermBuffers pb;               // fused permutation (single-workgroup launches only)
+  int n_shared, tile_rows;
   float modep[kMaxModeParams];  // [L, E]: mask (0/1) or prior values of this launch
 };
 
@@ -119,7 +122,9 @@ __device__ void route_finalize(const RouteParams& p, const float* logits, int ld
   }
 }
 
-template <int MB, int NB, int WN, int WK>
+// FUSE: the grid is one workgroup holding every token of one layer; after the selection it
+// also groups the (token, slot) pairs by expert (permute_block).
+template <int MB, int NB, int WN, int WK, bool FUSE>
 __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RouteParams p) {
   constexpr int TT = 16 * MB, NO = 16 * NB * WN, NT = 64 * WN * WK;
   __shared__ float red[WK * TT * NO];
@@ -208,6 +213,11 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
     __syncthreads();
   }
   route_finalize(p, red, NO, lo, t0, TT, lg0, nl);
+  if (FUSE) {
+    __shared__ PermLds plds;
+    __syncthreads();   // the selections written above are read back by other threads
+    permute_block(p.idx, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb, plds);
+  }
 }
 
 // fp32 router: plain fp32 dot products (no MFMA), one thread per (token, output).
@@ -235,14 +245,35 @@ __global__ __launch_bounds__(256) void route_f32_kernel(const RouteParams p) {
   route_finalize(p, logits, 256, lo, t0, kF32TT, lg0, nl);
 }
 
-template <int MB, int NB, int WN, int WK>
+template <int MB, int NB, int WN, int WK, bool FUSE = false>
 hipError_t launch_bf16(RouteParams& p, hipStream_t stream) {
   constexpr int TT = 16 * MB, NO = 16 * NB * WN;
   p.lpw = NO / p.E < 1 ? 1 : NO / p.E;
   if (p.lpw > p.L) p.lpw = p.L;
   dim3 grid((p.T + TT - 1) / TT, (p.L + p.lpw - 1) / p.lpw);
-  hipLaunchKernelGGL((route_bf16_kernel<MB, NB, WN, WK>), grid, dim3(64 * WN * WK), 0, stream, p);
+  if (FUSE && (grid.x != 1 || grid.y != 1)) return hipErrorInvalidValue;  // needs one workgroup
+  hipLaunchKernelGGL((route_bf16_kernel<MB, NB, WN, WK, FUSE>), grid, dim3(64 * WN * WK), 0, stream, p);
   return hipGetLastError();
+}
+
+void fill_params(RouteParams& p, const void* x, const void* w_router, int T, int d, int E, int K, int L, int l0,
+                 int mode, int gate_mode, const uint8_t* mask, const float* prior, int32_t* idx, float* gate,
+                 float* margin, size_t esz) {
+  p.x = x;
+  p.w = static_cast<const char*>(w_router) + static_cast<size_t>(l0) * E * d * esz;
+  p.idx = idx + static_cast<size_t>(l0) * T * K;
+  p.gate = gate + static_cast<size_t>(l0) * T * K;
+  p.margin = margin ? margin + static_cast<size_t>(l0) * T : nullptr;
+  p.T = T; p.d = d; p.E = E; p.K = K;
+  p.L = L;
+  p.mode = mode; p.gate_mode = gate_mode;
+  p.pb = PermBuffers{};
+  p.n_shared = 0;
+  p.tile_rows = 1;
+  for (int i = 0; i < p.L * E; ++i) {
+    const size_t gi = static_cast<size_t>(l0) * E + i;
+    p.modep[i] = mode == 1 ? (mask[gi] ? 1.0f : 0.0f) : mode == 2 ? prior[gi] : 1.0f;
+  }
 }
 
 }  // namespace
@@ -257,18 +288,8 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
   const size_t esz = bf16 ? 2 : 4;
   for (int l0 = 0; l0 < L; l0 += max_layers) {
     RouteParams p;
-    p.x = x;
-    p.w = static_cast<const char*>(w_router) + static_cast<size_t>(l0) * E * d * esz;
-    p.idx = idx + static_cast<size_t>(l0) * T * K;
-    p.gate = gate + static_cast<size_t>(l0) * T * K;
-    p.margin = margin ? margin + static_cast<size_t>(l0) * T : nullptr;
-    p.T = T; p.d = d; p.E = E; p.K = K;
-    p.L = L - l0 < max_layers ? L - l0 : max_layers;
-    p.mode = mode; p.gate_mode = gate_mode;
-    for (int i = 0; i < p.L * E; ++i) {
-      const size_t gi = static_cast<size_t>(l0) * E + i;
-      p.modep[i] = mode == 1 ? (mask[gi] ? 1.0f : 0.0f) : mode == 2 ? prior[gi] : 1.0f;
-    }
+    fill_params(p, x, w_router, T, d, E, K, L - l0 < max_layers ? L - l0 : max_layers, l0, mode, gate_mode, mask,
+                prior, idx, gate, margin, esz);
     hipError_t err;
     if (!bf16) {
       p.lpw = 256 / E < 1 ? 1 : 256 / E;
@@ -286,6 +307,22 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
     if (err != hipSuccess) return err;
   }
   return hipSuccess;
+}
+
+hipError_t launch_route_permute(const void* x, const void* w_router, int T, int d, int E, int K, int mode,
+                                int gate_mode, const uint8_t* mask, const float* prior, int32_t* idx,
+                                float* gate, int n_shared, int tile_rows, const PermBuffers& pb,
+                                hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  if (T > kRouteOneBlockT) return hipErrorInvalidValue;
+  RouteParams p;
+  fill_params(p, x, w_router, T, d, E, K, 1, 0, mode, gate_mode, mask, prior, idx, gate, nullptr, 2);
+  p.pb = pb;
+  p.n_shared = n_shared;
+  p.tile_rows = tile_rows;
+  if (E <= 16) return launch_bf16<1, 1, 1, 16, true>(p, stream);
+  if (E <= 64) return launch_bf16<1, 4, 1, 8, true>(p, stream);
+  return launch_bf16<1, 4, 4, 2, true>(p, stream);
 }
 
 }  // namespace maskmoe

@@ -110,6 +110,14 @@ def test_layer_forward_rejects_invalid_arguments():
     assert _fwd(L.make_desc(**{**good, "d": 96}), ws_bytes=1 << 30) == L.E_UNSUPPORTED
 
 
+def test_profiled_forward_needs_an_event_array():
+    lib = L.load()
+    desc = L.make_desc(T=32, d=128, E=8, K=2, F=256)
+    ws = lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+    assert lib.maskmoe_layer_forward_profiled(ctypes.byref(desc), FAKE, FAKE, None, None, FAKE, FAKE, None, None,
+                                              FAKE, None, None, FAKE, ws, None, None) == L.E_INVAL
+
+
 def test_workspace_bytes_monotone_in_tokens():
     lib = L.load()
     for (d, E, K, F, ns, dt) in ((4096, 8, 2, 14336, 0, L.BF16), (2048, 64, 6, 1408, 2, L.BF16),

@@ -44,14 +44,15 @@ def _mp(cfg, inp):
     return {}
 
 
-def run_gpu(cfg, inp, dd=None, workspace=None):
+def run_gpu(cfg, inp, dd=None, workspace=None, events=None):
     dd = dd or _upload(inp, cfg)
     T, K = cfg.T, cfg.K
     idx = torch.empty((T, K), dtype=torch.int32, device="cuda")
     gate = torch.empty((T, K), dtype=torch.float32, device="cuda")
     y = L.maskmoe_layer_forward(dd["x"], dd["w_router"], dd["w_gate_up"], dd["w_down"], K, cfg.route_mode,
                                 cfg.gate_mode, ws_gate_up=dd.get("ws_gate_up"), ws_down=dd.get("ws_down"),
-                                topk_idx=idx, topk_gate=gate, workspace=workspace, **_mp(cfg, inp))
+                                topk_idx=idx, topk_gate=gate, workspace=workspace, events=events,
+                                **_mp(cfg, inp))
     torch.cuda.synchronize()
     return y, idx, gate
 
@@ -175,3 +176,22 @@ def test_mixtral_ft_forward_full_sampled():
 @pytest.mark.parametrize("mode", [L.ROUTE_HARD_MASK, L.ROUTE_SOFT_PRIOR])
 def test_deepseek_full_sampled(mode):
     check_layer(synth.deepseek_config(mode), n_sample=64)
+
+
+@pytest.mark.gpu
+def test_profiled_entry_matches_plain_forward():
+    """The profiled entry point records events (NULL entries skipped) and changes nothing else."""
+    for cfg in (DECODE_SMALL[0], SMALL_BF16[0]):
+        inp = _inputs(cfg)
+        y0, i0, g0 = run_gpu(cfg, inp)
+        for which in (range(L.NUM_STAGES + 1), (2, 3)):
+            evs = [torch.cuda.Event(enable_timing=True) if s in which else None for s in range(L.NUM_STAGES + 1)]
+            for e in evs:
+                if e is not None:
+                    e.record()
+            y1, i1, g1 = run_gpu(cfg, inp, events=evs)
+            torch.cuda.synchronize()
+            assert torch.equal(y0, y1) and torch.equal(i0, i1) and torch.equal(g0, g1)
+            for s in which:
+                if s + 1 in which:
+                    assert evs[s].elapsed_time(evs[s + 1]) >= 0.0
