@@ -12,8 +12,10 @@
 // the hits in ascending expert order (LRU, LFU), then insert the misses in ascending order,
 // each evicting, among the cached experts not selected at this step, the smallest stamp
 // (LRU, FIFO) or the smallest (count, stamp) (LFU). The trace is read 64 entries at a time,
-// coalesced, and broadcast with lane shuffles; per-step miss counts are gathered in lanes
-// and written 64 bytes at a time.
+// coalesced; once per chunk, lane j turns the entries of step j into that step's selected-set
+// bitmask (and flags invalid entries), and each step then reads its mask back as one
+// wave-uniform value (readlane). Per-step miss counts are gathered in lanes and written 64
+// bytes at a time.
 
 #include <limits.h>
 
@@ -64,20 +66,35 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_kernel(
 
   long tot_f = 0, tot_h = 0;
   const int chunk = 64 / K;  // steps per 64-entry load
+  // entries of the steps n0 .. n0 + ns - 1 in lanes 0 .. ns K - 1; the next chunk's load is
+  // issued before the current chunk is replayed
+  auto load_chunk = [&](int n0) {
+    const int ns = min(chunk, N - n0);
+    return (n0 < N && lane < ns * K) ? tr[static_cast<long>(n0) * K + lane] : -1;
+  };
+  int v_next = load_chunk(0);
   for (int n0 = 0; n0 < N; n0 += chunk) {
     const int ns = min(chunk, N - n0);
-    const int v = lane < ns * K ? tr[static_cast<long>(n0) * K + lane] : -1;
+    const int v = v_next;
+    v_next = load_chunk(n0 + chunk);
+    // lane j < ns builds the selected set of step n0 + j from its K entries, once per chunk
+    uint64_t my_sel = 0;
+    bool my_bad = false;
+    for (int k = 0; k < K; ++k) {
+      const int e = __shfl(v, (lane * K + k) & 63, kWave);
+      if (lane < ns) {
+        if (e < 0 || e >= E || ((my_sel >> e) & 1ull)) my_bad = true;
+        else my_sel |= 1ull << e;
+      }
+    }
+    if (__ballot(my_bad)) bad = true;
+    const int sel_lo = static_cast<int>(my_sel & 0xffffffffull);
+    const int sel_hi = static_cast<int>(my_sel >> 32);
     int my_f = 0;
     for (int j = 0; j < ns; ++j) {
-      uint64_t sel = 0;
-      for (int k = 0; k < K; ++k) {
-        const int e = __shfl(v, j * K + k, kWave);
-        if (e < 0 || e >= E || ((sel >> e) & 1ull)) {
-          bad = true;
-        } else {
-          sel |= 1ull << e;
-        }
-      }
+      // the step's set, read back as a wave-uniform (scalar) value
+      const uint64_t sel = (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readlane(sel_hi, j))) << 32) |
+                           static_cast<uint32_t>(__builtin_amdgcn_readlane(sel_lo, j));
       const bool mine = (sel >> lane) & 1ull;
       if (POLICY == 1 && mine) ++count;
       const uint64_t cmask = __ballot(cached);

@@ -61,4 +61,10 @@ __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
+// XOR swizzle of the eight 16-byte chunks of a 128-byte LDS operand row: row bits 0..2, with
+// row bit 3 flipping chunk bit 0. A 16-byte operand read whose lanes walk 16 consecutive rows
+// at one logical chunk then touches 16 distinct bank groups, for 32 or 64 four-byte banks; rows
+// 64 apart share the swizzle term.
+__device__ __forceinline__ int lds_swizzle(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
 }  // namespace maskmoe

@@ -60,9 +60,6 @@ __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt
   return lo;
 }
 
-// LDS chunk swizzle of a 128-byte operand row: row bits 0..2, and bit 3 flipping chunk bit 0.
-__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
-
 template <int EPI>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
   constexpr int WN = 4;                 // waves: 2 along rows x 4 along columns
@@ -99,11 +96,10 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
 
   // Global -> LDS mapping: thread tid loads rows (tid >> 3) + 64 i (i < U) of each operand;
   // LDS slot u = tid + NT * i (row u >> 3, physical chunk u & 7) receives the logical chunk
-  // (u & 7) ^ swz(row), an XOR swizzle under which the 16 rows that one pass of a 16-byte
-  // operand read touches fall into distinct banks for 32 or 64 four-byte LDS banks alike.
+  // (u & 7) ^ lds_swizzle(row), which keeps the MFMA operand reads free of bank conflicts.
   // The swizzle term is the same for all i (64 rows apart), so one chunk offset serves all.
   const int r0 = tid >> 3;
-  const int chunk = ((tid & 7) ^ swz(r0)) * 8;
+  const int chunk = ((tid & 7) ^ lds_swizzle(r0)) * 8;
   const uint16_t* wg = g < p.E ? p.w + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * Kdim
                                : p.ws + static_cast<size_t>(g - p.E) * (EPI == 0 ? 2 * p.F : p.d) * Kdim;
   int aoffs[U], boffs[U];   // element offsets (< 2^31, checked by the host)
@@ -132,7 +128,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     const int br = EPI == 0 ? (j == 0 ? 0 : 128) + wn * 32 : wn * 64 + j * 32;
     boff[j] = (br + (lane & 31)) * 8;
   }
-  const int sw = swz(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
+  const int sw = lds_swizzle(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
 
   f32x16 acc[TM][TN];
 #pragma unroll

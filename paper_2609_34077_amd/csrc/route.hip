@@ -10,11 +10,13 @@
 // experts exactly as the products do and avoid ties from exp underflow. Equal keys go to
 // the lower expert index.
 //
-// bf16 logits use v_mfma_f32_16x16x32_bf16: a workgroup computes a tile of
+// bf16 logits use v_mfma_f32_16x16x32_bf16 (route_bf16_kernel): a workgroup computes a tile of
 // (16*MB tokens) x (16*NB*WN outputs), where outputs are the rows of [L*E, d] router
 // weights of whole layers; its WN*WK waves split the outputs (WN) and the k-steps (WK)
 // and the WK partial tiles are summed in LDS in a fixed order. Small token counts
 // (decode) use WK = 8..16 so all of d is in flight at once; large token counts stream x.
+// Many tokens routed through many layers at once use route_gemm_kernel instead, which stages
+// both operands through LDS.
 // The selection runs one thread per (token, layer) on the fp32 logits in LDS.
 
 #include <math.h>
@@ -28,6 +30,10 @@ namespace {
 
 constexpr int kMaxK = 16;
 constexpr int kMaxModeParams = 512;
+// The LDS-tiled router GEMM (route_gemm_kernel) pays off once a launch has many tokens and
+// enough router outputs to fill its 256-wide tile.
+constexpr int kRouteGemmMinT = 1024;
+constexpr int kRouteGemmMinOutputs = 128;
 
 struct RouteParams {
   const void* x;
@@ -220,6 +226,128 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
   }
 }
 
+// Many tokens and many router outputs (tens of layers routed from the same tokens): a
+// 128-token x 256-output tile of whole layers, both operands staged through LDS in 64-wide
+// k-steps (the same load pipeline and swizzle as the expert GEMM: every token row is read
+// from HBM once, the router rows are shared by all workgroups through L2), accumulated on
+// v_mfma_f32_32x32x16_bf16. After the k-loop the staging LDS holds the fp32 logits and the
+// selection runs as in route_bf16_kernel.
+constexpr int kRgBM = 128, kRgBN = 256, kRgBK = 64, kRgThreads = 512;
+
+__global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParams p) {
+  constexpr int BM = kRgBM, BN = kRgBN, BK = kRgBK, NT = kRgThreads;
+  constexpr int WN = 4;                        // waves: 2 along tokens x 4 along outputs
+  constexpr int TM = 2, TN = 2;                // 32x32 fragments per wave: 64 tokens x 64 outputs
+  constexpr int UA = BM * 8 / NT, UB = BN * 8 / NT;   // 16-byte units per thread and stage
+  constexpr int SA = BM * 8, SB = BN * 8;             // 16-byte slots per stage
+  constexpr int STAGING = 2 * (SA + SB) * 16;
+  constexpr int LOGITS = BM * BN * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[STAGING > LOGITS ? STAGING : LOGITS];
+  __shared__ float lo[BN];
+  u32x4* lds_a = reinterpret_cast<u32x4*>(smem);   // [2][SA]
+  u32x4* lds_b = lds_a + 2 * SA;                    // [2][SB]
+  float* logits = reinterpret_cast<float*>(smem);   // [BM][BN], after the k-loop
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int t0 = blockIdx.x * BM;
+  const int lg0 = blockIdx.y * p.lpw;
+  const int nl = min(p.lpw, p.L - lg0);
+  const int nout = nl * p.E;
+  const uint16_t* x = static_cast<const uint16_t*>(p.x);
+  const uint16_t* w = static_cast<const uint16_t*>(p.w) + static_cast<size_t>(lg0) * p.E * p.d;
+
+  // Thread tid loads rows (tid >> 3) + 64 i of each operand; rows past the last token or
+  // output are clamped onto valid rows and their results never written.
+  const int r0 = tid >> 3;
+  const int chunk = ((tid & 7) ^ lds_swizzle(r0)) * 8;
+  const uint16_t* asrc[UA];
+  const uint16_t* bsrc[UB];
+#pragma unroll
+  for (int i = 0; i < UA; ++i) asrc[i] = x + static_cast<size_t>(min(t0 + r0 + 64 * i, p.T - 1)) * p.d + chunk;
+#pragma unroll
+  for (int i = 0; i < UB; ++i) bsrc[i] = w + static_cast<size_t>(min(r0 + 64 * i, nout - 1)) * p.d + chunk;
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) aoff[i] = (wm * 64 + i * 32 + (lane & 31)) * 8;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) boff[j] = (wn * 64 + j * 32 + (lane & 31)) * 8;
+  const int sw = lds_swizzle(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  u32x4 ra[UA], rb[UB];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < UA; ++i) ra[i] = *reinterpret_cast<const u32x4*>(asrc[i] + kt * BK);
+#pragma unroll
+    for (int i = 0; i < UB; ++i) rb[i] = *reinterpret_cast<const u32x4*>(bsrc[i] + kt * BK);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < UA; ++i) lds_a[buf * SA + tid + NT * i] = ra[i];
+#pragma unroll
+    for (int i = 0; i < UB; ++i) lds_b[buf * SB + tid + NT * i] = rb[i];
+  };
+  u32x4 af[2][TM], bf[2][TN];
+  auto read_frags = [&](int buf, int kk, int slot) {
+    const int ch = (kk * 2 + (lane >> 5)) ^ sw;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[slot][i] = lds_a[buf * SA + aoff[i] + ch];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bf[slot][j] = lds_b[buf * SB + boff[j] + ch];
+  };
+
+  // k-tile kt sits in LDS buffer kt & 1 and tile kt + 1 in registers; after the first k16 step
+  // of tile kt the registers go to the other buffer and are refilled with tile kt + 2.
+  const int nk = p.d / BK;
+  gload(0);
+  lstore(0);
+  if (nk > 1) gload(1);
+  __syncthreads();
+  read_frags(0, 0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int cur = kk & 1;
+      if (kk + 1 < BK / 16) read_frags(buf, kk + 1, cur ^ 1);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_32x32x16(af[cur][i], bf[cur][j], acc[i][j]);
+      if (kk == 0) {
+        if (kt + 1 < nk) lstore(buf ^ 1);
+        if (kt + 2 < nk) gload(kt + 2);
+      }
+    }
+    __syncthreads();
+    if (kt + 1 < nk) read_frags(buf ^ 1, 0, 0);
+  }
+
+  // The last barrier of the loop ends every read of the staging buffers: write the logits.
+  // acc[i][j][4 jj + ii] is token row wm*64 + i*32 + 8 jj + 4 (lane >> 5) + ii, output column
+  // wn*64 + j*32 + (lane & 31).
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        logits[row * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+      }
+  for (int i = tid; i < nout; i += NT) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
+  __syncthreads();
+  route_finalize(p, logits, BN, lo, t0, BM, lg0, nl);
+}
+
 // fp32 router: plain fp32 dot products (no MFMA), one thread per (token, output).
 constexpr int kF32TT = 16;
 __global__ __launch_bounds__(256) void route_f32_kernel(const RouteParams p) {
@@ -296,6 +424,12 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
       if (p.lpw > p.L) p.lpw = p.L;
       dim3 grid((T + kF32TT - 1) / kF32TT, (p.L + p.lpw - 1) / p.lpw);
       hipLaunchKernelGGL(route_f32_kernel, grid, dim3(256), 0, stream, p);
+      err = hipGetLastError();
+    } else if (T >= kRouteGemmMinT && d % kRgBK == 0 && p.L * E >= kRouteGemmMinOutputs) {
+      p.lpw = kRgBN / E;
+      if (p.lpw > p.L) p.lpw = p.L;
+      dim3 grid((T + kRgBM - 1) / kRgBM, (p.L + p.lpw - 1) / p.lpw);
+      hipLaunchKernelGGL(route_gemm_kernel, grid, dim3(kRgThreads), 0, stream, p);
       err = hipGetLastError();
     } else {
       const int need = p.L * E < 256 ? p.L * E : 256;

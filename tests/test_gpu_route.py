@@ -89,6 +89,38 @@ def test_multi_layer_trace_router(T):
         U.check_routing(z, idx[l], gate[l], margin[l], K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=prior[l])
 
 
+# Many tokens x many router outputs: the LDS-tiled router GEMM path. Ragged token tiles, a
+# second block of layers (40 x 8 outputs), a 240-output tile (E = 48), and E = 256.
+ROUTE_GEMM_CASES = [
+    (1100, 4096, 8, 2, 32, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM),
+    (1024, 256, 8, 2, 40, L.ROUTE_HARD_MASK, L.GATE_RENORM),
+    (1500, 512, 64, 6, 4, L.ROUTE_SOFT_PRIOR, L.GATE_P),
+    (1030, 192, 48, 4, 5, L.ROUTE_PLAIN, L.GATE_RENORM),
+    (1024, 128, 256, 16, 1, L.ROUTE_HARD_MASK, L.GATE_P),
+]
+
+
+@pytest.mark.parametrize("T,d,E,K,Lyr,mode,gate_mode", ROUTE_GEMM_CASES,
+                         ids=lambda v: str(v))
+def test_many_tokens_many_layers(T, d, E, K, Lyr, mode, gate_mode):
+    U.say(f"route gemm path T={T} d={d} E={E} K={K} L={Lyr} mode={mode} gate={gate_mode}")
+    x, w = _inputs(T, d, E, "bf16", 1000 + T + Lyr, Lyr=Lyr)
+    rng = np.random.default_rng(T + E)
+    keep = [sorted(rng.choice(E, max(K, E // 2), replace=False)) for _ in range(Lyr)]
+    mask = np.stack([synth.binary_mask(E, k) for k in keep]) if mode == L.ROUTE_HARD_MASK else None
+    prior = np.stack([synth.concentrated_prior(E, k, 1.0) for k in keep]) if mode == L.ROUTE_SOFT_PRIOR else None
+    idx, gate, margin = L.maskmoe_route(U.dev(x), U.dev(w), K, mode, gate_mode, mask=mask, prior=prior)
+    torch.cuda.synchronize()
+    xf, wf = U.f64(x, "bf16"), U.f64(w, "bf16")
+    idx, gate, margin = idx.cpu().numpy(), gate.cpu().numpy(), margin.cpu().numpy()
+    near = 0
+    for l in range(Lyr):
+        near += U.check_routing(R.router_logits(xf, wf[l]), idx[l], gate[l], margin[l], K, mode, gate_mode,
+                                None if mask is None else mask[l], None if prior is None else prior[l])
+    U.say(f"  near-tie (token, layer) pairs {near} of {T * Lyr}")
+    assert near <= max(2, int(T * Lyr * (0.6 if E == 256 else 0.05)))
+
+
 def test_mode_equivalences_bit_exact():
     T, d, E, K = 500, 1024, 8, 2
     x, w = _inputs(T, d, E, "bf16", 5)
