@@ -227,26 +227,27 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
 }
 
 // Many tokens and many router outputs (tens of layers routed from the same tokens): a
-// 128-token x 256-output tile of whole layers, both operands staged through LDS in 64-wide
+// 256-token x 256-output tile of whole layers, both operands staged through LDS in 64-wide
 // k-steps (the same load pipeline and swizzle as the expert GEMM: every token row is read
 // from HBM once, the router rows are shared by all workgroups through L2), accumulated on
-// v_mfma_f32_32x32x16_bf16. After the k-loop the staging LDS holds the fp32 logits and the
-// selection runs as in route_bf16_kernel.
-constexpr int kRgBM = 128, kRgBN = 256, kRgBK = 64, kRgThreads = 512;
+// v_mfma_f32_32x32x16_bf16. After the k-loop the staging LDS holds the fp32 logits of one
+// half of the tokens at a time, and the selection runs on them as in route_bf16_kernel.
+constexpr int kRgBM = 256, kRgBN = 256, kRgBK = 64, kRgThreads = 512;
 
 __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParams p) {
   constexpr int BM = kRgBM, BN = kRgBN, BK = kRgBK, NT = kRgThreads;
   constexpr int WN = 4;                        // waves: 2 along tokens x 4 along outputs
-  constexpr int TM = 2, TN = 2;                // 32x32 fragments per wave: 64 tokens x 64 outputs
+  constexpr int TM = 4, TN = 2;                // 32x32 fragments per wave: 128 tokens x 64 outputs
+  constexpr int HALF = BM / 2;                 // token rows per selection phase (one wave row)
   constexpr int UA = BM * 8 / NT, UB = BN * 8 / NT;   // 16-byte units per thread and stage
   constexpr int SA = BM * 8, SB = BN * 8;             // 16-byte slots per stage
   constexpr int STAGING = 2 * (SA + SB) * 16;
-  constexpr int LOGITS = BM * BN * 4;
+  constexpr int LOGITS = HALF * BN * 4;
   __shared__ __attribute__((aligned(16))) unsigned char smem[STAGING > LOGITS ? STAGING : LOGITS];
   __shared__ float lo[BN];
   u32x4* lds_a = reinterpret_cast<u32x4*>(smem);   // [2][SA]
   u32x4* lds_b = lds_a + 2 * SA;                    // [2][SB]
-  float* logits = reinterpret_cast<float*>(smem);   // [BM][BN], after the k-loop
+  float* logits = reinterpret_cast<float*>(smem);   // [HALF][BN], after the k-loop
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -269,7 +270,7 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
   for (int i = 0; i < UB; ++i) bsrc[i] = w + static_cast<size_t>(min(r0 + 64 * i, nout - 1)) * p.d + chunk;
   int aoff[TM], boff[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) aoff[i] = (wm * 64 + i * 32 + (lane & 31)) * 8;
+  for (int i = 0; i < TM; ++i) aoff[i] = (wm * 128 + i * 32 + (lane & 31)) * 8;
 #pragma unroll
   for (int j = 0; j < TN; ++j) boff[j] = (wn * 64 + j * 32 + (lane & 31)) * 8;
   const int sw = lds_swizzle(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
@@ -331,21 +332,28 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
     if (kt + 1 < nk) read_frags(buf ^ 1, 0, 0);
   }
 
-  // The last barrier of the loop ends every read of the staging buffers: write the logits.
-  // acc[i][j][4 jj + ii] is token row wm*64 + i*32 + 8 jj + 4 (lane >> 5) + ii, output column
-  // wn*64 + j*32 + (lane & 31).
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        logits[row * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
-      }
+  // The last barrier of the loop ends every read of the staging buffers. Phase h: the waves
+  // of token half h write their logits, then every thread selects for those tokens.
+  // acc[i][j][4 jj + ii] is token row wm*128 + i*32 + 8 jj + 4 (lane >> 5) + ii, output
+  // column wn*64 + j*32 + (lane & 31).
   for (int i = tid; i < nout; i += NT) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
-  __syncthreads();
-  route_finalize(p, logits, BN, lo, t0, BM, lg0, nl);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (wm == h) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            logits[row * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+          }
+    }
+    __syncthreads();
+    route_finalize(p, logits, BN, lo, t0 + h * HALF, HALF, lg0, nl);
+    __syncthreads();   // the next phase overwrites the logits
+  }
 }
 
 // fp32 router: plain fp32 dot products (no MFMA), one thread per (token, output).
