@@ -9,17 +9,21 @@ what the masked MoE hot path computes, written from the paper:
 * ``ffn``      -- the expert FFN (SwiGLU) and the gate-weighted combine with
   shared experts (Eq. 1 and Section 3.1);
 * ``cache``    -- the per-layer expert cache of the trace simulator and the
-  hit-rate / fetches-per-token metrics (Section 4.1, Eq. 5).
+  hit-rate / fetches-per-token metrics (Section 4.1, Eq. 5);
+* ``train``    -- Stage 1 of the fine-tuning: mask sampling without
+  replacement (Eq. 2), the gradients of the gate values with respect to the
+  mask and the router, and the straight-through mask-logit gradient (Eq. 3).
 
 It shares no code with the HIP path and imports nothing from it. Only the
 tests, the smoke check and the benchmark's CPU-baseline leg may import it;
 the product path never does.
 
 Parity pins: every function here is pinned by the CPU test suite
-(brute-force Top-K, closed forms, invariants, library routines and
-hand-worked cache traces). The fetch counts of synthetic traces at
+(brute-force Top-K, closed forms, invariants, library routines,
+hand-worked cache traces, finite differences of the forward for the
+gradients and exact enumerated inclusion probabilities for the sampler). The fetch counts of synthetic traces at
 particular prior strengths have no value printed in the paper to compare
 with; they are pinned only through the cache rules above.
 """
 
-from . import cache, ffn, routing  # noqa: F401
+from . import cache, ffn, routing, train  # noqa: F401
