@@ -301,6 +301,50 @@ def run_layer(args):
     return res, st
 
 
+def run_stage1_backward(st, args):
+    """Stage 1 mask and router gradients of the fine-tuning layer (Eq. 2, Eq. 3), timed on their
+    own: one maskmoe_layer_forward_train supplies the routing, logits and expert outputs, then
+    maskmoe_stage1_backward runs `steps` times on a seeded cotangent, accumulating the
+    mask-logit gradient. HBM-bound: its algorithmic bytes are the expert outputs (T K d fp32),
+    dy and x (T d each, read once), the router rows, and the router's dx written (T d fp32)."""
+    import torch
+    from paper_2609_34077_amd import _lib as L
+    from paper_2609_34077_amd import synth
+    cfg, inp = st["cfg"], st["inp"]
+    x = st["xs"][0]
+    y, idx, gate, logits, eo = L.maskmoe_layer_forward_train(x, st["w_router"], st["wgu"][0], st["wdn"][0], cfg.K,
+                                                             cfg.route_mode, cfg.gate_mode, mask=inp["mask"],
+                                                             workspace=st["ws"])
+    g = np.random.default_rng(123)
+    dy = torch.from_numpy(synth.bf16_bits(g.standard_normal((cfg.T, cfg.d)).astype(np.float32))).view(
+        torch.bfloat16).cuda()
+    ml = np.zeros(cfg.E, np.float32)          # equal mask logits, as at initialisation
+    acc = torch.zeros(cfg.E, dtype=torch.float32, device="cuda")
+    desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, 1, 0, L.BF16, L.ROUTE_HARD_MASK, cfg.gate_mode)
+    ws = torch.empty(int(L.load().maskmoe_stage1_backward_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
+    run = lambda: L.maskmoe_stage1_backward(x, st["w_router"], cfg.K, cfg.gate_mode, inp["mask"], idx, logits, dy,
+                                            eo, mask_logits=ml, d_mask_logits=acc, workspace=ws)
+    for _ in range(3):
+        run()
+    steps = max(10, args.steps if args.steps is not None else 20)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(steps):
+        run()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    T, d, E, K = cfg.T, cfg.d, cfg.E, cfg.K
+    bytes_ = T * K * d * 4 + 2 * T * d * 2 + E * d * 2 + T * d * 4 + T * E * 4 + E * d * 4
+    gbs = bytes_ / (ms / 1e3) / 1e9
+    return {"ms": round(ms, 4), "tokens_per_s": round(T / (ms / 1e3), 1), "bound": "hbm",
+            "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes": bytes_,
+            "computes": "gate cotangents, dL/dm, accumulated dL/dm~ (Eq. 3), dL/dW_router and the router's dL/dx; "
+                        "the expert FFN weights' gradients are not part of it"}
+
+
 # ----------------------------------------------------------------------------- trace workload
 
 def run_trace(args):
@@ -416,6 +460,8 @@ def main():
         base = None if args.no_cpu_baseline else trace_cpu_baseline(st)
     else:
         res, st = run_layer(args)
+        if args.workload == "ft":
+            res["stage1_backward"] = run_stage1_backward(st, args)
         base = None if args.no_cpu_baseline else layer_cpu_baseline(st)
     res["cpu_baseline"] = base
     pr = torch.cuda.get_device_properties(0)

@@ -210,6 +210,89 @@ int maskmoe_cache_fetches(const int32_t* trace, int32_t L, int32_t S, int32_t N,
                           int64_t* fetches, int64_t* hits, uint8_t* f_per_step, int32_t* dev_error,
                           hipStream_t stream);
 
+/* ---- Stage 1 of fine-tuning (Section 3.2, Stage 1 and Mask optimization) ---- */
+
+/*
+ * maskmoe_sample_mask -- the binary masks of Eq. 2: for each of L layers, e_keep = E'
+ * distinct experts drawn without replacement from pi = softmax(m~). Draw s takes, among the
+ * experts not yet drawn and in increasing index order, the first whose running sum of pi
+ * exceeds uniforms[s] times their total (all in double precision). Host function; nothing is
+ * enqueued.
+ *
+ *  mask_logits host [L, E] float m~ (finite).
+ *  uniforms    host [L, e_keep] double in [0, 1): the random draws, supplied by the caller.
+ *  mask        host [L, E] uint8 output: exactly e_keep ones per layer.
+ *  Errors: E_INVAL for L < 1, E outside 1..256, e_keep outside 1..E, a NULL pointer, a
+ *  non-finite logit or a uniform outside [0, 1).
+ */
+int maskmoe_sample_mask(const float* mask_logits, const double* uniforms, int32_t L, int32_t E,
+                        int32_t e_keep, uint8_t* mask);
+
+/*
+ * maskmoe_layer_forward_train -- maskmoe_layer_forward that also returns what the Stage 1
+ * backward reads: the routing decision, the fp32 router logits and every selected expert's
+ * output before gating (Section 3.1, Eq. 1: y_t = sum_k g_{t,k} F_{A_t[k]}(x_t) + shared).
+ *
+ *  topk_idx      device [T, K] int32, required.   topk_gate device [T, K] float, required.
+ *  router_logits device [T, E] float, required: z = W x in fp32.
+ *  expert_out    device [T, K, d] float, required, 16-byte aligned: F_{A_t[k]}(x_t) in fp32
+ *                (for bf16 layers: from the bf16-rounded SwiGLU activation, as in y).
+ *  Other arguments, rounding, workspace and errors as maskmoe_layer_forward, plus E_INVAL
+ *  for a NULL output above when T > 0.
+ */
+int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                const uint8_t* mask, const float* prior, const void* w_gate_up,
+                                const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
+                                int32_t* topk_idx, float* topk_gate, float* router_logits,
+                                float* expert_out, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/*
+ * maskmoe_stage1_backward_workspace_bytes -- device workspace of maskmoe_stage1_backward for
+ * `desc` (T, d, E used). Returns 0 for an invalid desc.
+ */
+size_t maskmoe_stage1_backward_workspace_bytes(const maskmoe_layer_desc* desc);
+
+/*
+ * maskmoe_stage1_backward -- the gradients that reach the mask and the router through the
+ * gate values of a hard-mask layer (Section 3.2, Eq. 2 and Eq. 3), for a cotangent dy of y:
+ *   dg_{t,k} = <dy_t, F_{A_t[k]}(x_t)>                                      (from Eq. 1)
+ *   gates from p * m, A fixed, m = 1 on A:
+ *     GATE_P:      dL/dm_e = sum_t p_e dg_e [e in A_t];  dz = p (dp - <p, dp>), dp = dg on A
+ *     GATE_RENORM: dL/dm_e = sum_t g_e (dg_e - gbar_t) [e in A_t] = sum_t dz_{t,e},
+ *                  gbar_t = sum_{A_t} g dg
+ *   dL/dm~ += (diag(pi) - pi pi^T) dL/dm, pi = softmax(m~)            (Eq. 3, straight-through)
+ *   dL/dW = dz^T x,  router share of dL/dx = dz W                      (z = W x)
+ * All tokens share the mask (Stage 1), so dL/dm sums over the batch. The expert FFN weights'
+ * own gradients are not computed here.
+ *
+ *  desc          route_mode must be MASKMOE_ROUTE_HARD_MASK; T, d, E, K, dtype, gate_mode
+ *                are used.
+ *  x, w_router   device [T, d], [E, d] (dtype), as given to the forward.
+ *  mask          host [E] uint8, the step's binary mask; must be 1 on every expert in
+ *                topk_idx (as the forward's routing guarantees).
+ *  mask_logits   host [E] float m~; required when d_mask_logits is given.
+ *  topk_idx      device [T, K] int32 and router_logits device [T, E] float from
+ *                maskmoe_layer_forward_train.
+ *  dy            device [T, d] (dtype).  expert_out device [T, K, d] float from the forward.
+ *  d_gate        device [T, K] float output (dg) or NULL.
+ *  d_mask        device [E] float output (dL/dm) or NULL.
+ *  d_mask_logits device [E] float, ACCUMULATED: dL/dm~ of this step is added to it, so a
+ *                caller sums T steps before one update (Stage 1); or NULL.
+ *  d_w_router    device [E, d] float output, required.
+ *  d_x           device [T, d] float output (the router's share of dL/dx) or NULL.
+ *  workspace     device, maskmoe_stage1_backward_workspace_bytes(desc) bytes, 256-byte aligned.
+ *  Reductions run in a fixed order: results are deterministic. T = 0 writes nothing.
+ *  Errors: E_INVAL for an invalid desc, a mode other than HARD_MASK, a mask row with fewer
+ *  than K ones, a NULL required pointer, a misaligned pointer or a non-finite mask logit;
+ *  E_UNSUPPORTED for T*E at or above 2^31; E_WORKSPACE when the workspace is too small.
+ */
+int maskmoe_stage1_backward(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                            const uint8_t* mask, const float* mask_logits, const int32_t* topk_idx,
+                            const float* router_logits, const void* dy, const float* expert_out,
+                            float* d_gate, float* d_mask, float* d_mask_logits, float* d_w_router,
+                            float* d_x, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* maskmoe_status_string -- static, NUL-terminated description of a status code. */
 const char* maskmoe_status_string(int status);
 

@@ -25,7 +25,9 @@ BF16, F32 = 0, 1
 CACHE_LRU, CACHE_LFU, CACHE_FIFO = 0, 1, 2
 
 EXPORTS = ("maskmoe_route", "maskmoe_layer_workspace_bytes", "maskmoe_layer_forward",
-           "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string")
+           "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string",
+           "maskmoe_sample_mask", "maskmoe_layer_forward_train", "maskmoe_stage1_backward_workspace_bytes",
+           "maskmoe_stage1_backward")
 NUM_STAGES = 5
 STAGES = ("route", "permute", "gate_up", "down", "combine")
 
@@ -74,6 +76,16 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.maskmoe_cache_fetches.restype = ctypes.c_int
     lib.maskmoe_status_string.argtypes = [ctypes.c_int]
     lib.maskmoe_status_string.restype = ctypes.c_char_p
+    lib.maskmoe_sample_mask.argtypes = [_vp, _vp, _i32, _i32, _i32, _vp]
+    lib.maskmoe_sample_mask.restype = ctypes.c_int
+    lib.maskmoe_layer_forward_train.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                                _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.maskmoe_layer_forward_train.restype = ctypes.c_int
+    lib.maskmoe_stage1_backward_workspace_bytes.argtypes = [ctypes.POINTER(LayerDesc)]
+    lib.maskmoe_stage1_backward_workspace_bytes.restype = _sz
+    lib.maskmoe_stage1_backward.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                            _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.maskmoe_stage1_backward.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -168,20 +180,10 @@ def maskmoe_layer_workspace_bytes(desc: LayerDesc) -> int:
     return int(load().maskmoe_layer_workspace_bytes(ctypes.byref(desc)))
 
 
-def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int,
-                          mask=None, prior=None, ws_gate_up=None, ws_down=None, workspace=None, y=None,
-                          topk_idx=None, topk_gate=None, events=None):
-    """One masked MoE layer. Shapes: x [T,d], w_router [E,d], w_gate_up [E,2F,d],
-    w_down [E,d,F], ws_gate_up [S,2F,d], ws_down [S,d,F]; mask/prior host [E].
-
-    Returns y [T,d] (dtype of x). ``workspace`` (uint8 device tensor) is
-    allocated when not given; ``topk_idx``/``topk_gate`` [T,K] receive the
-    routing decision when given. ``events``: NUM_STAGES + 1 entries, each None or an
-    already-recorded ``torch.cuda.Event(enable_timing=True)``; when given, the
-    profiled entry point re-records the non-None ones around the stages.
-    """
+def _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask, prior, ws_gate_up, ws_down,
+                  workspace, y, topk_idx, topk_gate):
+    """Checks shapes and dtypes of a layer call and marshals its leading arguments."""
     import torch
-    lib = load()
     for t, n in ((x, "x"), (w_router, "w_router"), (w_gate_up, "w_gate_up"), (w_down, "w_down"),
                  (ws_gate_up, "ws_gate_up"), (ws_down, "ws_down"), (y, "y"), (workspace, "workspace"),
                  (topk_idx, "topk_idx"), (topk_gate, "topk_gate")):
@@ -205,9 +207,27 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
         y = torch.empty((T, d), dtype=x.dtype, device=x.device)
     m_arr, m_p = _host_u8(mask, E) if route_mode == ROUTE_HARD_MASK else (None, None)
     p_arr, p_p = _host_f32(prior, E) if route_mode == ROUTE_SOFT_PRIOR else (None, None)
-    args = (ctypes.byref(desc), _ptr(x), _ptr(w_router), m_p, p_p, _ptr(w_gate_up), _ptr(w_down),
-            _ptr(ws_gate_up), _ptr(ws_down), _ptr(y), _ptr(topk_idx), _ptr(topk_gate), _ptr(workspace),
-            workspace.numel())
+    head = (ctypes.byref(desc), _ptr(x), _ptr(w_router), m_p, p_p, _ptr(w_gate_up), _ptr(w_down),
+            _ptr(ws_gate_up), _ptr(ws_down), _ptr(y), _ptr(topk_idx), _ptr(topk_gate))
+    return desc, workspace, y, (m_arr, p_arr), head
+
+
+def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int,
+                          mask=None, prior=None, ws_gate_up=None, ws_down=None, workspace=None, y=None,
+                          topk_idx=None, topk_gate=None, events=None):
+    """One masked MoE layer. Shapes: x [T,d], w_router [E,d], w_gate_up [E,2F,d],
+    w_down [E,d,F], ws_gate_up [S,2F,d], ws_down [S,d,F]; mask/prior host [E].
+
+    Returns y [T,d] (dtype of x). ``workspace`` (uint8 device tensor) is
+    allocated when not given; ``topk_idx``/``topk_gate`` [T,K] receive the
+    routing decision when given. ``events``: NUM_STAGES + 1 entries, each None or an
+    already-recorded ``torch.cuda.Event(enable_timing=True)``; when given, the
+    profiled entry point re-records the non-None ones around the stages.
+    """
+    lib = load()
+    desc, workspace, y, keep, head = _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask,
+                                                   prior, ws_gate_up, ws_down, workspace, y, topk_idx, topk_gate)
+    args = head + (_ptr(workspace), workspace.numel())
     if events is None:
         _check("maskmoe_layer_forward", lib.maskmoe_layer_forward(*args, _stream()))
     else:
@@ -215,8 +235,84 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
             raise ValueError(f"need {NUM_STAGES + 1} events")
         handles = (ctypes.c_void_p * len(events))(*[None if ev is None else ev.cuda_event for ev in events])
         _check("maskmoe_layer_forward_profiled", lib.maskmoe_layer_forward_profiled(*args, handles, _stream()))
-    del m_arr, p_arr
+    del keep
     return y
+
+
+def maskmoe_layer_forward_train(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int,
+                                mask=None, prior=None, ws_gate_up=None, ws_down=None, workspace=None):
+    """maskmoe_layer_forward plus what the Stage 1 backward reads. Returns
+    ``(y [T,d], topk_idx [T,K], topk_gate [T,K], router_logits [T,E] fp32, expert_out [T,K,d] fp32)``."""
+    import torch
+    lib = load()
+    T, d = x.shape
+    E = w_router.shape[0]
+    idx = torch.empty((T, K), dtype=torch.int32, device=x.device)
+    gate = torch.empty((T, K), dtype=torch.float32, device=x.device)
+    logits = torch.empty((T, E), dtype=torch.float32, device=x.device)
+    eo = torch.empty((T, K, d), dtype=torch.float32, device=x.device)
+    desc, workspace, y, keep, head = _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask,
+                                                   prior, ws_gate_up, ws_down, workspace, None, idx, gate)
+    _check("maskmoe_layer_forward_train",
+           lib.maskmoe_layer_forward_train(*head, _ptr(logits), _ptr(eo), _ptr(workspace), workspace.numel(),
+                                           _stream()))
+    del keep
+    return y, idx, gate, logits, eo
+
+
+def maskmoe_sample_mask(mask_logits, uniforms, e_keep: int) -> np.ndarray:
+    """Binary masks [L,E] (or [E]) with e_keep ones, drawn without replacement from
+    softmax(mask_logits) using the given uniforms [L,e_keep] (or [e_keep]) in [0, 1)."""
+    lib = load()
+    ml = np.ascontiguousarray(np.asarray(mask_logits, dtype=np.float32))
+    squeeze = ml.ndim == 1
+    ml2 = ml.reshape(1, -1) if squeeze else ml
+    L, E = ml2.shape
+    u = np.ascontiguousarray(np.asarray(uniforms, dtype=np.float64).reshape(L, e_keep))
+    out = np.zeros((L, E), dtype=np.uint8)
+    _check("maskmoe_sample_mask", lib.maskmoe_sample_mask(ml2.ctypes.data_as(ctypes.c_void_p),
+                                                          u.ctypes.data_as(ctypes.c_void_p), L, E, e_keep,
+                                                          out.ctypes.data_as(ctypes.c_void_p)))
+    return out[0] if squeeze else out
+
+
+def maskmoe_stage1_backward(x, w_router, K: int, gate_mode: int, mask, topk_idx, router_logits, dy, expert_out,
+                            mask_logits=None, d_mask_logits=None, with_d_x: bool = True, workspace=None):
+    """Mask and router gradients of one hard-mask step (Eq. 2, Eq. 3). ``d_mask_logits`` (fp32
+    device [E]) is accumulated in place when given (mask_logits host [E] then required).
+    Returns dict(d_gate [T,K], d_mask [E], d_w_router [E,d], d_x [T,d] or None), fp32."""
+    import torch
+    lib = load()
+    for t, n in ((x, "x"), (w_router, "w_router"), (topk_idx, "topk_idx"), (router_logits, "router_logits"),
+                 (dy, "dy"), (expert_out, "expert_out"), (d_mask_logits, "d_mask_logits"),
+                 (workspace, "workspace")):
+        _dev(t, n)
+    T, d = x.shape
+    E = w_router.shape[0]
+    if tuple(w_router.shape) != (E, d) or tuple(dy.shape) != (T, d) or tuple(expert_out.shape) != (T, K, d) \
+            or tuple(topk_idx.shape) != (T, K) or tuple(router_logits.shape) != (T, E):
+        raise ValueError("inconsistent shapes")
+    if w_router.dtype != x.dtype or dy.dtype != x.dtype:
+        raise ValueError("x, w_router and dy must share a dtype")
+    if expert_out.dtype != torch.float32 or router_logits.dtype != torch.float32 or topk_idx.dtype != torch.int32:
+        raise ValueError("expert_out and router_logits are float32, topk_idx int32")
+    desc = make_desc(T, d, E, K, 1, 0, _dtype_code(x), ROUTE_HARD_MASK, gate_mode)
+    need = int(lib.maskmoe_stage1_backward_workspace_bytes(ctypes.byref(desc)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    m_arr, m_p = _host_u8(mask, E)
+    ml_arr, ml_p = _host_f32(mask_logits, E)
+    out = dict(d_gate=torch.empty((T, K), dtype=torch.float32, device=x.device),
+               d_mask=torch.empty(E, dtype=torch.float32, device=x.device),
+               d_w_router=torch.empty((E, d), dtype=torch.float32, device=x.device),
+               d_x=torch.empty((T, d), dtype=torch.float32, device=x.device) if with_d_x else None)
+    _check("maskmoe_stage1_backward",
+           lib.maskmoe_stage1_backward(ctypes.byref(desc), _ptr(x), _ptr(w_router), m_p, ml_p, _ptr(topk_idx),
+                                       _ptr(router_logits), _ptr(dy), _ptr(expert_out), _ptr(out["d_gate"]),
+                                       _ptr(out["d_mask"]), _ptr(d_mask_logits), _ptr(out["d_w_router"]),
+                                       _ptr(out["d_x"]), _ptr(workspace), workspace.numel(), _stream()))
+    del m_arr, ml_arr
+    return out
 
 
 def maskmoe_cache_fetches(trace, E: int, B: int, state=None, with_f_per_step: bool = False,

@@ -139,7 +139,7 @@ int maskmoe_route(const maskmoe_layer_desc* desc, int32_t L, const void* x, cons
     return MASKMOE_E_INVAL;
   return hip_status(maskmoe::launch_route(bf16, x, w_router, desc->T, desc->d, desc->E, desc->K, L,
                                          desc->route_mode, desc->gate_mode, mask, prior, topk_idx,
-                                         topk_gate, topk_margin, stream));
+                                         topk_gate, topk_margin, nullptr, stream));
 }
 
 size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc) {
@@ -150,8 +150,8 @@ size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc) {
 static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                               const uint8_t* mask, const float* prior, const void* w_gate_up,
                               const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
-                              int32_t* topk_idx, float* topk_gate, void* workspace,
-                              size_t workspace_bytes, hipStream_t stream, hipEvent_t* events) {
+                              int32_t* topk_idx, float* topk_gate, float* router_logits, float* expert_out,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream, hipEvent_t* events) {
   int st = check_layer_desc(desc);
   if (st != MASKMOE_OK) return st;
   const maskmoe_layer_desc& d = *desc;
@@ -172,6 +172,7 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
     if (!aligned(p, 16)) return MASKMOE_E_INVAL;
   if (d.n_shared > 0 && (!aligned(ws_gate_up, 16) || !aligned(ws_down, 16))) return MASKMOE_E_INVAL;
   if ((topk_idx && !aligned(topk_idx, 4)) || (topk_gate && !aligned(topk_gate, 4))) return MASKMOE_E_INVAL;
+  if ((router_logits && !aligned(router_logits, 4)) || (expert_out && !aligned(expert_out, 16))) return MASKMOE_E_INVAL;
   const Layout w = layout(d);
   if (!workspace || workspace_bytes < w.total || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
 
@@ -191,12 +192,12 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   hipError_t e;
   if (uses_decode_path(d)) {  // one workgroup routes every token and then permutes them
     e = maskmoe::launch_route_permute(x, w_router, d.T, d.d, d.E, d.K, d.route_mode, d.gate_mode, mask, prior, idx,
-                                      gate, d.n_shared, maskmoe::kGemmBM, pb, stream);
+                                      gate, router_logits, d.n_shared, maskmoe::kGemmBM, pb, stream);
     if (e != hipSuccess) return MASKMOE_E_HIP;
     maskmoe::record_mark(events, 1, stream);
   } else {
     e = maskmoe::launch_route(bf16, x, w_router, d.T, d.d, d.E, d.K, 1, d.route_mode, d.gate_mode, mask, prior,
-                              idx, gate, nullptr, stream);
+                              idx, gate, nullptr, router_logits, stream);
     if (e != hipSuccess) return MASKMOE_E_HIP;
     maskmoe::record_mark(events, 1, stream);
     e = maskmoe::launch_permute(idx, d.T, d.K, d.E, d.n_shared, maskmoe::kGemmBM, pb, stream);
@@ -212,6 +213,7 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   a.ws_gate_up = ws_gate_up;
   a.ws_down = ws_down;
   a.gate = gate;
+  a.expert_out = expert_out;
   a.T = d.T; a.d = d.d; a.F = d.F; a.E = d.E; a.K = d.K; a.n_shared = d.n_shared;
   if (!bf16) {
     e = maskmoe::launch_experts_f32(a, pb, reinterpret_cast<float*>(ws + w.H), reinterpret_cast<float*>(ws + w.O),
@@ -238,7 +240,18 @@ int maskmoe_layer_forward(const maskmoe_layer_desc* desc, const void* x, const v
                           int32_t* topk_idx, float* topk_gate, void* workspace,
                           size_t workspace_bytes, hipStream_t stream) {
   return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
-                            topk_idx, topk_gate, workspace, workspace_bytes, stream, nullptr);
+                            topk_idx, topk_gate, nullptr, nullptr, workspace, workspace_bytes, stream, nullptr);
+}
+
+int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                const uint8_t* mask, const float* prior, const void* w_gate_up,
+                                const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
+                                int32_t* topk_idx, float* topk_gate, float* router_logits, float* expert_out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (desc && desc->T > 0 && (!topk_idx || !topk_gate || !router_logits || !expert_out)) return MASKMOE_E_INVAL;
+  return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
+                            topk_idx, topk_gate, router_logits, expert_out, workspace, workspace_bytes, stream,
+                            nullptr);
 }
 
 int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
@@ -248,7 +261,76 @@ int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x
                                    size_t workspace_bytes, hipEvent_t* events, hipStream_t stream) {
   if (!events) return MASKMOE_E_INVAL;
   return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
-                            topk_idx, topk_gate, workspace, workspace_bytes, stream, events);
+                            topk_idx, topk_gate, nullptr, nullptr, workspace, workspace_bytes, stream, events);
+}
+
+size_t maskmoe_stage1_backward_workspace_bytes(const maskmoe_layer_desc* desc) {
+  if (check_route_desc(desc) != MASKMOE_OK) return 0;
+  return maskmoe::stage1_workspace_bytes(desc->T, desc->d, desc->E);
+}
+
+int maskmoe_stage1_backward(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                            const uint8_t* mask, const float* mask_logits, const int32_t* topk_idx,
+                            const float* router_logits, const void* dy, const float* expert_out, float* d_gate,
+                            float* d_mask, float* d_mask_logits, float* d_w_router, float* d_x, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  int st = check_route_desc(desc);
+  if (st != MASKMOE_OK) return st;
+  const maskmoe_layer_desc& d = *desc;
+  if (d.route_mode != MASKMOE_ROUTE_HARD_MASK) return MASKMOE_E_INVAL;   // Stage 1 trains under the mask
+  if (d.K > maskmoe::kMaxKTrain || d.E > maskmoe::kMaxETrain) return MASKMOE_E_UNSUPPORTED;
+  st = check_mask_prior(d.route_mode, 1, d.E, d.K, mask, nullptr);
+  if (st != MASKMOE_OK) return st;
+  if (d_mask_logits) {
+    if (!mask_logits) return MASKMOE_E_INVAL;
+    for (int e = 0; e < d.E; ++e)
+      if (!isfinite(mask_logits[e])) return MASKMOE_E_INVAL;
+  }
+  if (!d_w_router) return MASKMOE_E_INVAL;
+  if (static_cast<int64_t>(d.T) * d.E >= (int64_t{1} << 31)) return MASKMOE_E_UNSUPPORTED;
+  if (d.T == 0) return MASKMOE_OK;   // no token: no gradient is written or accumulated
+  if (!x || !w_router || !topk_idx || !router_logits || !dy || !expert_out) return MASKMOE_E_INVAL;
+  const size_t el = d.dtype == MASKMOE_BF16 ? 2 : 4;
+  const void* in[] = {x, w_router, dy};
+  for (const void* p : in)
+    if (!aligned(p, el)) return MASKMOE_E_INVAL;
+  const void* f4[] = {topk_idx, router_logits, expert_out, d_w_router};
+  for (const void* p : f4)
+    if (!aligned(p, 4)) return MASKMOE_E_INVAL;
+  if ((d_gate && !aligned(d_gate, 4)) || (d_mask && !aligned(d_mask, 4)) ||
+      (d_mask_logits && !aligned(d_mask_logits, 4)) || (d_x && !aligned(d_x, 4)))
+    return MASKMOE_E_INVAL;
+  const size_t need = maskmoe::stage1_workspace_bytes(d.T, d.d, d.E);
+  if (!workspace || workspace_bytes < need || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
+
+  double pi[maskmoe::kMaxETrain];
+  if (mask_logits) maskmoe::softmax_f64(mask_logits, d.E, pi);
+  else for (int e = 0; e < d.E; ++e) pi[e] = 0.0;
+  char* ws = static_cast<char*>(workspace);
+  const size_t tok = (static_cast<size_t>(d.T) * d.E * 4 + 255) / 256 * 256;
+  maskmoe::Stage1Args a;
+  a.x = x; a.w_router = w_router; a.dy = dy; a.expert_out = expert_out; a.router_logits = router_logits;
+  a.idx = topk_idx; a.pi = pi; a.d_gate = d_gate; a.d_mask = d_mask; a.d_mask_logits = d_mask_logits;
+  a.d_w_router = d_w_router; a.d_x = d_x;
+  a.dz = reinterpret_cast<float*>(ws);
+  a.dm_tok = reinterpret_cast<float*>(ws + tok);
+  a.wgrad_partial = reinterpret_cast<float*>(ws + 2 * tok);
+  a.T = d.T; a.d = d.d; a.E = d.E; a.K = d.K; a.gate_mode = d.gate_mode;
+  return hip_status(maskmoe::launch_stage1_backward(a, d.dtype == MASKMOE_BF16, stream));
+}
+
+int maskmoe_sample_mask(const float* mask_logits, const double* uniforms, int32_t L, int32_t E, int32_t e_keep,
+                        uint8_t* mask) {
+  if (L < 1 || E < 1 || E > maskmoe::kMaxETrain || e_keep < 1 || e_keep > E) return MASKMOE_E_INVAL;
+  if (!mask_logits || !uniforms || !mask) return MASKMOE_E_INVAL;
+  for (size_t i = 0; i < static_cast<size_t>(L) * E; ++i)
+    if (!isfinite(mask_logits[i])) return MASKMOE_E_INVAL;
+  for (size_t i = 0; i < static_cast<size_t>(L) * e_keep; ++i)
+    if (!(uniforms[i] >= 0.0 && uniforms[i] < 1.0)) return MASKMOE_E_INVAL;
+  for (int l = 0; l < L; ++l)
+    maskmoe::sample_mask_host(mask_logits + static_cast<size_t>(l) * E, uniforms + static_cast<size_t>(l) * e_keep,
+                              E, e_keep, mask + static_cast<size_t>(l) * E);
+  return MASKMOE_OK;
 }
 
 int maskmoe_cache_fetches(const int32_t* trace, int32_t L, int32_t S, int32_t N, int32_t K, int32_t E,

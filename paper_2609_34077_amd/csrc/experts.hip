@@ -253,15 +253,17 @@ __device__ __forceinline__ float4 sum_slices(const float* O, int split, size_t s
 }
 
 // y[t, c] = sum_k gate[t, k] O[inv[t K + k], c] + sum over shared experts of their rows, with
-// O's slices added first. One workgroup of 256 threads per (token, block of kCombineCols
-// columns), token-major in a 1-D grid.
+// O's slices added first; when eo is given, eo[t, k, c] also receives the slice sum of row
+// inv[t K + k] (the selected expert's output before gating). One workgroup of 256 threads
+// per (token, block of kCombineCols columns), token-major in a 1-D grid.
 constexpr int kCombineCols = 1024;
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
                                                        const int32_t* __restrict__ inv,
                                                        const float* __restrict__ gate, int T, int K,
-                                                       int n_shared, int d, void* y, int split) {
+                                                       int n_shared, int d, void* y, int split,
+                                                       float* __restrict__ eo) {
   const int nb = (d + kCombineCols - 1) / kCombineCols;
   const int t = blockIdx.x / nb, cb = blockIdx.x % nb;
   if (BF16) {  // d % 4 == 0
@@ -273,6 +275,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
       const float gk = gate[t * K + k];
       const float4 v = sum_slices(O, split, slice, static_cast<size_t>(inv[t * K + k]) * d + c);
       s.x += gk * v.x; s.y += gk * v.y; s.z += gk * v.z; s.w += gk * v.w;
+      if (eo) *reinterpret_cast<float4*>(eo + (static_cast<size_t>(t) * K + k) * d + c) = v;
     }
     for (int sh = 0; sh < n_shared; ++sh) {
       const float4 v = sum_slices(O, split, slice, (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c);
@@ -285,7 +288,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   } else {
     for (int c = cb * kCombineCols + threadIdx.x; c < d && c < (cb + 1) * kCombineCols; c += 256) {
       float s = 0.0f;
-      for (int k = 0; k < K; ++k) s += gate[t * K + k] * O[static_cast<size_t>(inv[t * K + k]) * d + c];
+      for (int k = 0; k < K; ++k) {
+        const float v = O[static_cast<size_t>(inv[t * K + k]) * d + c];
+        s += gate[t * K + k] * v;
+        if (eo) eo[(static_cast<size_t>(t) * K + k) * d + c] = v;
+      }
       for (int sh = 0; sh < n_shared; ++sh) s += O[(static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c];
       static_cast<float*>(y)[static_cast<size_t>(t) * d + c] = s;
     }
@@ -602,7 +609,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   record_mark(marks, 1, stream);
 
   hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                     a.K, a.n_shared, a.d, y, 1);
+                     a.K, a.n_shared, a.d, y, 1, a.expert_out);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
@@ -691,7 +698,7 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
   hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T, a.K,
-                     a.n_shared, a.d, y, p.split);
+                     a.n_shared, a.d, y, p.split, a.expert_out);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
@@ -721,7 +728,7 @@ hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float*
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
   hipLaunchKernelGGL(combine_kernel<false>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                     a.K, a.n_shared, a.d, y, 1);
+                     a.K, a.n_shared, a.d, y, 1, a.expert_out);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;

@@ -23,9 +23,10 @@ struct PermBuffers {
 // Router logits + softmax + mask/prior Top-K + gates for layers [0, L) of w_router
 // ([L, E, d]); host `mask` [L, E] (HARD_MASK) or `prior` [L, E] (SOFT_PRIOR), unused for
 // PLAIN. Outputs idx/gate [L, T, K], margin [L, T].
+// logits (fp32 [L, T, E]) and margin ([L, T]) are optional outputs (null: not written).
 hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
                         int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
-                        int32_t* idx, float* gate, float* margin, hipStream_t stream);
+                        int32_t* idx, float* gate, float* margin, float* logits, hipStream_t stream);
 
 // Tokens at or below which one bf16 routing workgroup covers every token, so the routing
 // kernel can also perform the permutation (launch_route_permute).
@@ -34,7 +35,7 @@ constexpr int kRouteOneBlockT = 16;
 // by the permutation into `pb` (rows tiled by tile_rows, n_shared shared groups).
 hipError_t launch_route_permute(const void* x, const void* w_router, int T, int d, int E, int K, int mode,
                                 int gate_mode, const uint8_t* mask, const float* prior, int32_t* idx,
-                                float* gate, int n_shared, int tile_rows, const PermBuffers& pb,
+                                float* gate, float* logits, int n_shared, int tile_rows, const PermBuffers& pb,
                                 hipStream_t stream);
 
 hipError_t launch_permute(const int32_t* idx, int T, int K, int E, int n_shared, int tile_rows,
@@ -52,6 +53,7 @@ struct ExpertArgs {
   const void* ws_gate_up;  // [n_shared, 2F, d]
   const void* ws_down;     // [n_shared, d, F]
   const float* gate;       // [T, K]
+  float* expert_out;       // [T, K, d] fp32 output of each selected expert before gating, or null
   int T, d, F, E, K, n_shared;
 };
 
@@ -83,5 +85,35 @@ hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float*
 hipError_t launch_cache(int policy, const int32_t* trace, int L, int S, int N, int K, int E, int B,
                         int32_t* state, int32_t* counts, int64_t* fetches, int64_t* hits,
                         uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream);
+
+// ---- Stage 1 training: mask and router gradients (train.hip)
+constexpr int kMaxKTrain = 16;
+constexpr int kMaxETrain = 256;
+constexpr int kMaxWgradSlices = 64;
+
+struct Stage1Args {
+  const void* x;              // [T, d] layer dtype
+  const void* w_router;       // [E, d] layer dtype
+  const void* dy;             // [T, d] layer dtype
+  const float* expert_out;    // [T, K, d]
+  const float* router_logits; // [T, E]
+  const int32_t* idx;         // [T, K]
+  const double* pi;           // host [E]: softmax of the mask logits
+  float* d_gate;              // [T, K] or null
+  float* d_mask;              // [E] or null
+  float* d_mask_logits;       // [E] accumulated (+=), or null
+  float* d_w_router;          // [E, d]
+  float* d_x;                 // [T, d] or null
+  float* dz;                  // workspace [T, E]
+  float* dm_tok;              // workspace [T, E]
+  float* wgrad_partial;       // workspace [slices, E, d]
+  int T, d, E, K, gate_mode;
+};
+size_t stage1_workspace_bytes(int T, int d, int E);
+hipError_t launch_stage1_backward(const Stage1Args& a, bool bf16, hipStream_t stream);
+// Host helpers: softmax in double precision; mask sampling without replacement (one uniform
+// per draw, inverse CDF over the remaining experts in index order).
+void softmax_f64(const float* logits, int E, double* pi);
+void sample_mask_host(const float* mask_logits, const double* uniforms, int E, int e_keep, uint8_t* mask);
 
 }  // namespace maskmoe

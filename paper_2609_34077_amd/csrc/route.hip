@@ -41,6 +41,7 @@ struct RouteParams {
   int32_t* idx;        // [L, T, K]
   float* gate;         // [L, T, K]
   float* margin;       // [L, T] or null
+  float* logits;       // [L, T, E] fp32 router logits or null
   int T, d, E, K, L, lpw, mode, gate_mode;
   PermBuffers pb;               // fused permutation (single-workgroup launches only)
   int n_shared, tile_rows;
@@ -125,6 +126,8 @@ __device__ void route_finalize(const RouteParams& p, const float* logits, int ld
       }
     }
     if (p.margin) p.margin[obase] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+    if (p.logits)
+      for (int e = 0; e < E; ++e) p.logits[obase * E + e] = z[e];
   }
 }
 
@@ -394,12 +397,13 @@ hipError_t launch_bf16(RouteParams& p, hipStream_t stream) {
 
 void fill_params(RouteParams& p, const void* x, const void* w_router, int T, int d, int E, int K, int L, int l0,
                  int mode, int gate_mode, const uint8_t* mask, const float* prior, int32_t* idx, float* gate,
-                 float* margin, size_t esz) {
+                 float* margin, float* logits, size_t esz) {
   p.x = x;
   p.w = static_cast<const char*>(w_router) + static_cast<size_t>(l0) * E * d * esz;
   p.idx = idx + static_cast<size_t>(l0) * T * K;
   p.gate = gate + static_cast<size_t>(l0) * T * K;
   p.margin = margin ? margin + static_cast<size_t>(l0) * T : nullptr;
+  p.logits = logits ? logits + static_cast<size_t>(l0) * T * E : nullptr;
   p.T = T; p.d = d; p.E = E; p.K = K;
   p.L = L;
   p.mode = mode; p.gate_mode = gate_mode;
@@ -416,7 +420,7 @@ void fill_params(RouteParams& p, const void* x, const void* w_router, int T, int
 
 hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
                         int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
-                        int32_t* idx, float* gate, float* margin, hipStream_t stream) {
+                        int32_t* idx, float* gate, float* margin, float* logits, hipStream_t stream) {
   if (T == 0 || L == 0) return hipSuccess;
   // Layers are processed in launches whose (layer, expert) parameters fit in the kernel
   // arguments; every launch covers whole layers.
@@ -425,7 +429,7 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
   for (int l0 = 0; l0 < L; l0 += max_layers) {
     RouteParams p;
     fill_params(p, x, w_router, T, d, E, K, L - l0 < max_layers ? L - l0 : max_layers, l0, mode, gate_mode, mask,
-                prior, idx, gate, margin, esz);
+                prior, idx, gate, margin, logits, esz);
     hipError_t err;
     if (!bf16) {
       p.lpw = 256 / E < 1 ? 1 : 256 / E;
@@ -453,12 +457,12 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
 
 hipError_t launch_route_permute(const void* x, const void* w_router, int T, int d, int E, int K, int mode,
                                 int gate_mode, const uint8_t* mask, const float* prior, int32_t* idx,
-                                float* gate, int n_shared, int tile_rows, const PermBuffers& pb,
+                                float* gate, float* logits, int n_shared, int tile_rows, const PermBuffers& pb,
                                 hipStream_t stream) {
   if (T == 0) return hipSuccess;
   if (T > kRouteOneBlockT) return hipErrorInvalidValue;
   RouteParams p;
-  fill_params(p, x, w_router, T, d, E, K, 1, 0, mode, gate_mode, mask, prior, idx, gate, nullptr, 2);
+  fill_params(p, x, w_router, T, d, E, K, 1, 0, mode, gate_mode, mask, prior, idx, gate, nullptr, logits, 2);
   p.pb = pb;
   p.n_shared = n_shared;
   p.tile_rows = tile_rows;

@@ -1,0 +1,102 @@
+"""Host-side Stage 1 checks that need no GPU: the library's mask sampler against the oracle's
+(bit-exact masks: both draw in double precision with the same uniforms, Eq. 2), and the argument
+validation of the training entry points (nothing reaches the device)."""
+
+import ctypes
+import os
+
+import numpy as np
+import pytest
+
+from oracle import train as TR
+from paper_2609_34077_amd import _lib as L
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="libmaskmoe.so not built")
+
+FAKE = 0x10000
+
+
+@pytest.mark.parametrize("E,e_keep", [(8, 4), (8, 2), (64, 12), (64, 64), (5, 1), (256, 40)])
+def test_sampler_matches_oracle(E, e_keep):
+    g = np.random.default_rng(E * 1000 + e_keep)
+    for trial in range(60):
+        scale = [0.0, 0.3, 2.0, 8.0][trial % 4]
+        ml = (scale * g.standard_normal(E)).astype(np.float32)
+        u = g.random(e_keep)
+        got = L.maskmoe_sample_mask(ml, u, e_keep)
+        want = TR.sample_mask(ml.astype(np.float64), u, e_keep)
+        assert np.array_equal(got, want), (trial, np.nonzero(got)[0], np.nonzero(want)[0])
+
+
+def test_sampler_layers_are_independent():
+    g = np.random.default_rng(9)
+    ml = g.standard_normal((5, 16)).astype(np.float32)
+    u = g.random((5, 6))
+    got = L.maskmoe_sample_mask(ml, u, 6)
+    for l in range(5):
+        assert np.array_equal(got[l], TR.sample_mask(ml[l].astype(np.float64), u[l], 6))
+
+
+def test_sampler_rejects_invalid_arguments():
+    lib = L.load()
+    ml = np.zeros(8, np.float32)
+    u = np.full(8, 0.5)
+    out = np.zeros(8, np.uint8)
+    P = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    assert lib.maskmoe_sample_mask(P(ml), P(u), 1, 8, 4, P(out)) == L.OK
+    assert lib.maskmoe_sample_mask(P(ml), P(u), 1, 8, 0, P(out)) == L.E_INVAL
+    assert lib.maskmoe_sample_mask(P(ml), P(u), 1, 8, 9, P(out)) == L.E_INVAL
+    assert lib.maskmoe_sample_mask(P(ml), P(u), 0, 8, 4, P(out)) == L.E_INVAL
+    assert lib.maskmoe_sample_mask(P(ml), P(u), 1, 257, 4, P(out)) == L.E_INVAL
+    assert lib.maskmoe_sample_mask(None, P(u), 1, 8, 4, P(out)) == L.E_INVAL
+    bad_u = u.copy()
+    bad_u[2] = 1.0
+    assert lib.maskmoe_sample_mask(P(ml), P(bad_u), 1, 8, 4, P(out)) == L.E_INVAL
+    bad_ml = ml.copy()
+    bad_ml[3] = np.inf
+    assert lib.maskmoe_sample_mask(P(bad_ml), P(u), 1, 8, 4, P(out)) == L.E_INVAL
+
+
+def _bwd(desc, mask, ml=None, dml=None, ws=None, wbytes=None, dw=FAKE, **kw):
+    lib = L.load()
+    a = dict(x=FAKE, w=FAKE, idx=FAKE, logits=FAKE, dy=FAKE, eo=FAKE)
+    a.update(kw)
+    if wbytes is None:
+        wbytes = lib.maskmoe_stage1_backward_workspace_bytes(ctypes.byref(desc))
+    mp = None if mask is None else mask.ctypes.data_as(ctypes.c_void_p)
+    mlp = None if ml is None else ml.ctypes.data_as(ctypes.c_void_p)
+    return lib.maskmoe_stage1_backward(ctypes.byref(desc), a["x"], a["w"], mp, mlp, a["idx"], a["logits"], a["dy"],
+                                       a["eo"], None, None, dml, dw, None, FAKE if ws is None else ws, wbytes, None)
+
+
+def test_stage1_backward_rejects_invalid_arguments():
+    mask = np.array([1, 0, 1, 1, 0, 0, 1, 0], np.uint8)
+    hard = L.make_desc(T=64, d=128, E=8, K=2, route_mode=L.ROUTE_HARD_MASK)
+    assert _bwd(L.make_desc(T=64, d=128, E=8, K=2, route_mode=L.ROUTE_SOFT_PRIOR), mask) == L.E_INVAL
+    assert _bwd(L.make_desc(T=64, d=128, E=8, K=2, route_mode=L.ROUTE_PLAIN), mask) == L.E_INVAL
+    assert _bwd(hard, np.array([1, 0, 0, 0, 0, 0, 0, 0], np.uint8)) == L.E_INVAL   # fewer than K kept
+    assert _bwd(hard, None) == L.E_INVAL
+    assert _bwd(hard, mask, dw=None) == L.E_INVAL
+    assert _bwd(hard, mask, dy=None) == L.E_INVAL
+    assert _bwd(hard, mask, eo=None) == L.E_INVAL
+    assert _bwd(hard, mask, dml=FAKE) == L.E_INVAL                              # logits needed
+    assert _bwd(hard, mask, ml=np.array([0, 0, np.nan, 0, 0, 0, 0, 0], np.float32), dml=FAKE) == L.E_INVAL
+    assert _bwd(hard, mask, eo=FAKE + 2) == L.E_INVAL                           # misaligned
+    need = L.load().maskmoe_stage1_backward_workspace_bytes(ctypes.byref(hard))
+    assert need > 0
+    assert _bwd(hard, mask, wbytes=need - 1) == L.E_WORKSPACE
+    assert _bwd(hard, mask, ws=FAKE + 64) == L.E_WORKSPACE
+    assert _bwd(L.make_desc(T=0, d=128, E=8, K=2, route_mode=L.ROUTE_HARD_MASK), mask,
+                x=None, w=None, idx=None, logits=None, dy=None, eo=None) == L.OK
+
+
+def test_forward_train_requires_its_outputs():
+    lib = L.load()
+    desc = L.make_desc(T=32, d=128, E=8, K=2, F=256)
+    ws = lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+    base = [ctypes.byref(desc), FAKE, FAKE, None, None, FAKE, FAKE, None, None, FAKE]
+    outs = [FAKE, FAKE, FAKE, FAKE]
+    for miss in range(4):
+        o = list(outs)
+        o[miss] = None
+        assert lib.maskmoe_layer_forward_train(*base, *o, FAKE, ws, None) == L.E_INVAL
