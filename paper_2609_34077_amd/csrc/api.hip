@@ -312,10 +312,14 @@ int maskmoe_stage1_backward(const maskmoe_layer_desc* desc, const void* x, const
   a.x = x; a.w_router = w_router; a.dy = dy; a.expert_out = expert_out; a.router_logits = router_logits;
   a.idx = topk_idx; a.pi = pi; a.d_gate = d_gate; a.d_mask = d_mask; a.d_mask_logits = d_mask_logits;
   a.d_w_router = d_w_router; a.d_x = d_x;
+  const size_t dmb = (static_cast<size_t>(d.E) * 4 + 255) / 256 * 256;
   a.dz = reinterpret_cast<float*>(ws);
   a.dm_tok = reinterpret_cast<float*>(ws + tok);
-  a.wgrad_partial = reinterpret_cast<float*>(ws + 2 * tok);
+  a.dm = reinterpret_cast<float*>(ws + 2 * tok);
+  a.wgrad_partial = reinterpret_cast<float*>(ws + 2 * tok + dmb);
   a.T = d.T; a.d = d.d; a.E = d.E; a.K = d.K; a.gate_mode = d.gate_mode;
+  a.vec_rows = d.d % 4 == 0 && aligned(expert_out, 16) && aligned(dy, 4 * el);
+  a.vec_x = (d.d * el) % 16 == 0 && aligned(x, 16);
   return hip_status(maskmoe::launch_stage1_backward(a, d.dtype == MASKMOE_BF16, stream));
 }
 

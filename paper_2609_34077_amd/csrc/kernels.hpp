@@ -106,8 +106,11 @@ struct Stage1Args {
   float* d_x;                 // [T, d] or null
   float* dz;                  // workspace [T, E]
   float* dm_tok;              // workspace [T, E]
+  float* dm;                  // workspace [E]: dL/dm before Eq. 3
   float* wgrad_partial;       // workspace [slices, E, d]
   int T, d, E, K, gate_mode;
+  bool vec_rows;              // d % 4 == 0 and dy, expert_out rows allow 4-element vector loads
+  bool vec_x;                 // rows of x are 16-byte aligned: 16-byte loads of x
 };
 size_t stage1_workspace_bytes(int T, int d, int E);
 hipError_t launch_stage1_backward(const Stage1Args& a, bool bf16, hipStream_t stream);

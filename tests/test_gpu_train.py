@@ -80,6 +80,7 @@ BACKWARD_CASES = [
     ("deepseek_shaped_small", 200, 512, 64, 6, R.GATE_P, "bf16", tuple(synth.deepseek_mask_set())),
     ("tiny_f32", 64, 256, 8, 2, R.GATE_RENORM, "f32", (0, 2, 5, 7)),
     ("gate_p_f32_ragged", 77, 96, 16, 3, R.GATE_P, "f32", tuple(range(0, 16, 2))),
+    ("scalar_load_paths_bf16", 70, 98, 8, 2, R.GATE_RENORM, "bf16", (0, 2, 5, 7)),   # rows not vector aligned
 ]
 
 
