@@ -14,6 +14,10 @@ Mixtral, 100 for DeepSeek-V2-Lite in Appendix B).
 
 Eq. 1 gives y_t = sum_{i in A_t} g_i F_i(x_t) (+ shared experts), so for a cotangent dy the
 gate cotangent is dL/dg_{t,i} = <dy_t, F_i(x_t)>; the router is z = W x, p = softmax(z).
+The experts are fine-tuned too (the routers and experts update at every step, Stage 1; Stage 2
+continues with them): with the gates held fixed, expert i receives dL/dF_i(x_t) = g_i dy_t,
+and the chain rule through its SwiGLU F(x) = W_down (SiLU(W_gate x) * W_up x) gives its
+weight gradients and its share of dL/dx (``expert_backward``, ``moe_layer_backward``).
 
 Readings where the paper is silent:
 * the sampler draws one expert per uniform u in [0, 1): among the experts not yet drawn, in
@@ -150,3 +154,74 @@ def stage1_backward(x, w_router, mask, mask_logits, idx, dy, expert_out, gate_mo
     d_mask, dz = mask_router_grad(z, idx, dg, gate_mode, mask)
     return dict(dg=dg, d_mask=d_mask, d_mask_logits=ste_mask_logits_grad(d_mask, mask_logits), dz=dz,
                 d_w_router=router_weight_grad(dz, x), d_x_router=router_input_grad(dz, w_router))
+
+
+def silu_grad(a):
+    """d SiLU(a) / da = s (1 + a (1 - s)), s = 1 / (1 + e^-a)."""
+    a = np.asarray(a, dtype=np.float64)
+    s = 1.0 / (1.0 + np.exp(-a))
+    return s * (1.0 + a * (1.0 - s))
+
+
+def expert_backward(x, dout, w_gate_up, w_down):
+    """Gradients of sum_r <dout_r, F(x_r)> for one SwiGLU expert on rows x [n,d].
+
+    a = x W_gate^T, b = x W_up^T, h = SiLU(a) * b, F = h W_down^T; then
+    dh = dout W_down, dW_down = dout^T h, da = dh * b * SiLU'(a), db = dh * SiLU(a),
+    dx = da W_gate + db W_up, dW_gate = da^T x, dW_up = db^T x.
+    Returns (dx [n,d], dW_gate_up [2F,d], dW_down [d,F]), float64.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    dout = np.asarray(dout, dtype=np.float64)
+    wgu = np.asarray(w_gate_up, dtype=np.float64)
+    wd = np.asarray(w_down, dtype=np.float64)
+    F = wd.shape[1]
+    wg, wu = wgu[:F], wgu[F:]
+    a = x @ wg.T
+    b = x @ wu.T
+    sa = a / (1.0 + np.exp(-a))
+    h = sa * b
+    dh = dout @ wd
+    d_wd = dout.T @ h
+    da = dh * b * silu_grad(a)
+    db = dh * sa
+    dx = da @ wg + db @ wu
+    return dx, np.concatenate([da.T @ x, db.T @ x], axis=0), d_wd
+
+
+def moe_layer_backward(x, idx, gate, dy, w_gate_up, w_down, ws_gate_up=None, ws_down=None, widen=None):
+    """Expert-side gradients of L = sum_t <dy_t, y_t> for the layer of Eq. 1 with the routing
+    (idx, gate) held fixed: routed expert e gets dout = gate * dy on the tokens that chose it,
+    a shared expert dout = dy on every token.
+
+    Returns dict(dx [T,d] (the experts' share of dL/dx), d_w_gate_up [E,2F,d], d_w_down [E,d,F],
+    d_ws_gate_up, d_ws_down (None without shared experts)), float64.
+    """
+    wdn = widen if widen is not None else (lambda a: np.asarray(a, dtype=np.float64))
+    x = np.asarray(x, dtype=np.float64)
+    dy = np.asarray(dy, dtype=np.float64)
+    idx = np.asarray(idx)
+    gate = np.asarray(gate, dtype=np.float64)
+    T, d = x.shape
+    E, F2, _ = w_gate_up.shape
+    F = F2 // 2
+    dx = np.zeros((T, d))
+    d_wgu = np.zeros((E, F2, d))
+    d_wd = np.zeros((E, d, F))
+    for e in range(E):
+        rows, slots = np.nonzero(idx == e)
+        if rows.size == 0:
+            continue
+        dout = gate[rows, slots][:, None] * dy[rows]
+        gx, d_wgu[e], d_wd[e] = expert_backward(x[rows], dout, wdn(w_gate_up[e]), wdn(w_down[e]))
+        np.add.at(dx, rows, gx)
+    out = dict(dx=dx, d_w_gate_up=d_wgu, d_w_down=d_wd, d_ws_gate_up=None, d_ws_down=None)
+    if ws_gate_up is not None:
+        S = ws_gate_up.shape[0]
+        out["d_ws_gate_up"] = np.zeros((S, F2, d))
+        out["d_ws_down"] = np.zeros((S, d, F))
+        for s in range(S):
+            gx, out["d_ws_gate_up"][s], out["d_ws_down"][s] = expert_backward(x, dy, wdn(ws_gate_up[s]),
+                                                                              wdn(ws_down[s]))
+            dx += gx
+    return out

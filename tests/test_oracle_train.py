@@ -9,7 +9,11 @@
 * the sampler: exactly E' distinct experts, E' = E takes all, a dominant logit is always drawn,
   and the empirical inclusion frequencies over many uniform draws match the exact inclusion
   probabilities of sequential sampling without replacement (enumerated over all draw orders);
-* accumulation over steps is the sum of the per-step gradients.
+* accumulation over steps is the sum of the per-step gradients;
+* the expert-side backward: central finite differences of the Eq. 1 loss (through the oracle's
+  own forward, oracle.ffn.moe_layer) for weight entries of routed and shared experts and for
+  input entries; SiLU' against finite differences of SiLU; K = E with all gates equal to 1
+  and one expert reduces to a dense SwiGLU MLP whose gradient torch's autograd gives.
 """
 
 import itertools
@@ -159,3 +163,70 @@ def test_sampler_inclusion_frequencies(E, e_keep):
 def test_uniform_logits_include_each_expert_with_probability_ratio():
     exact = TR.inclusion_probabilities(np.zeros(6), 4)
     np.testing.assert_allclose(exact, 4 / 6, atol=1e-12)
+
+
+def _moe_problem(seed=0, T=7, d=6, F=5, E=4, K=2, S=1):
+    g = np.random.default_rng(seed)
+    x = g.standard_normal((T, d))
+    wgu = 0.5 * g.standard_normal((E, 2 * F, d))
+    wd = 0.5 * g.standard_normal((E, d, F))
+    sgu = 0.5 * g.standard_normal((S, 2 * F, d)) if S else None
+    sd = 0.5 * g.standard_normal((S, d, F)) if S else None
+    idx = np.stack([g.choice(E, K, replace=False) for _ in range(T)])
+    gate = g.random((T, K))
+    dy = g.standard_normal((T, d))
+    return x, wgu, wd, sgu, sd, idx, gate, dy
+
+
+def test_silu_grad_matches_finite_differences():
+    from oracle import ffn as O
+    a = np.linspace(-6, 6, 41)
+    h = 1e-6
+    np.testing.assert_allclose(TR.silu_grad(a), (O.silu(a + h) - O.silu(a - h)) / (2 * h), atol=1e-9)
+
+
+def test_moe_backward_matches_finite_differences():
+    from oracle import ffn as O
+    x, wgu, wd, sgu, sd, idx, gate, dy = _moe_problem()
+    out = TR.moe_layer_backward(x, idx, gate, dy, wgu, wd, sgu, sd)
+    def loss(x, wgu, wd, sgu, sd):
+        return float(np.sum(dy * O.moe_layer(x, idx, gate, wgu, wd, sgu, sd)))
+    h = 1e-6
+    g = np.random.default_rng(1)
+    checks = [("x", x, out["dx"]), ("wgu", wgu, out["d_w_gate_up"]), ("wd", wd, out["d_w_down"]),
+              ("sgu", sgu, out["d_ws_gate_up"]), ("sd", sd, out["d_ws_down"])]
+    for name, arr, grad in checks:
+        for _ in range(12):
+            pos = tuple(g.integers(0, n) for n in arr.shape)
+            args = dict(x=x, wgu=wgu, wd=wd, sgu=sgu, sd=sd)
+            plus, minus = arr.copy(), arr.copy()
+            plus[pos] += h
+            minus[pos] -= h
+            fp = loss(**{**args, name: plus})
+            fm = loss(**{**args, name: minus})
+            fd = (fp - fm) / (2 * h)
+            assert abs(fd - grad[pos]) < 1e-6 * max(1.0, abs(fd)), (name, pos, fd, grad[pos])
+
+
+def test_moe_backward_unselected_expert_gets_zero():
+    x, wgu, wd, sgu, sd, idx, gate, dy = _moe_problem(seed=2, E=5, S=0)
+    idx[idx == 4] = 0           # expert 4 never chosen
+    idx[:, 1] = np.where(idx[:, 0] == idx[:, 1], (idx[:, 0] + 1) % 4, idx[:, 1])
+    out = TR.moe_layer_backward(x, idx, gate, dy, wgu, wd)
+    assert np.all(out["d_w_gate_up"][4] == 0) and np.all(out["d_w_down"][4] == 0)
+
+
+def test_dense_mlp_reduction_against_autograd():
+    import torch
+    x, wgu, wd, _, _, _, _, dy = _moe_problem(seed=3, E=1, K=1, S=0)
+    T = x.shape[0]
+    out = TR.moe_layer_backward(x, np.zeros((T, 1), int), np.ones((T, 1)), dy, wgu, wd)
+    xt = torch.tensor(x, requires_grad=True)
+    gu = torch.tensor(wgu[0], requires_grad=True)
+    dn = torch.tensor(wd[0], requires_grad=True)
+    F = wd.shape[2]
+    y = (torch.nn.functional.silu(xt @ gu[:F].T) * (xt @ gu[F:].T)) @ dn.T
+    y.backward(torch.tensor(dy))
+    np.testing.assert_allclose(out["dx"], xt.grad.numpy(), atol=1e-12)
+    np.testing.assert_allclose(out["d_w_gate_up"][0], gu.grad.numpy(), atol=1e-12)
+    np.testing.assert_allclose(out["d_w_down"][0], dn.grad.numpy(), atol=1e-12)
