@@ -313,8 +313,7 @@ def run_stage1_backward(st, args):
     cfg, inp = st["cfg"], st["inp"]
     x = st["xs"][0]
     y, idx, gate, logits, eo = L.maskmoe_layer_forward_train(x, st["w_router"], st["wgu"][0], st["wdn"][0], cfg.K,
-                                                             cfg.route_mode, cfg.gate_mode, mask=inp["mask"],
-                                                             workspace=st["ws"])
+                                                             cfg.route_mode, cfg.gate_mode, mask=inp["mask"])
     g = np.random.default_rng(123)
     dy = torch.from_numpy(synth.bf16_bits(g.standard_normal((cfg.T, cfg.d)).astype(np.float32))).view(
         torch.bfloat16).cuda()
@@ -343,6 +342,46 @@ def run_stage1_backward(st, args):
             "algorithmic_bytes": bytes_,
             "computes": "gate cotangents, dL/dm, accumulated dL/dm~ (Eq. 3), dL/dW_router and the router's dL/dx; "
                         "the expert FFN weights' gradients are not part of it"}
+
+
+def run_layer_backward(st, args):
+    """The experts' side of the layer backward (dgrad and wgrad of every selected expert,
+    maskmoe_layer_backward) on the fine-tuning layer, timed on its own after one training forward.
+    MFMA-bound: FLOPs = 2 x the forward's expert FLOPs (dgrad and wgrad of both projections,
+    4 x 2 rows F d x 2 in all); the transposes and row sums it also runs are not counted."""
+    import torch
+    from paper_2609_34077_amd import _lib as L
+    from paper_2609_34077_amd import synth
+    cfg, inp = st["cfg"], st["inp"]
+    x = st["xs"][0]
+    desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, cfg.n_shared, L.BF16, L.ROUTE_HARD_MASK, cfg.gate_mode)
+    lib = L.load()
+    tw = torch.empty(int(lib.maskmoe_layer_train_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
+    bw = torch.empty(int(lib.maskmoe_layer_backward_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
+    _, idx, gate, _, _ = L.maskmoe_layer_forward_train(x, st["w_router"], st["wgu"][0], st["wdn"][0], cfg.K,
+                                                       cfg.route_mode, cfg.gate_mode, mask=inp["mask"], workspace=tw)
+    g = np.random.default_rng(321)
+    dy = torch.from_numpy(synth.bf16_bits(g.standard_normal((cfg.T, cfg.d)).astype(np.float32))).view(
+        torch.bfloat16).cuda()
+    run = lambda: L.maskmoe_layer_backward(x, st["wgu"][0], st["wdn"][0], cfg.K, cfg.gate_mode, gate, dy, tw,
+                                           workspace=bw)
+    run()
+    steps = max(3, min(10, args.steps if args.steps is not None else 5))
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(steps):
+        run()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    rows = cfg.T * (cfg.K + cfg.n_shared)
+    flops = 2.0 * (2.0 * rows * 2 * cfg.F * cfg.d + 2.0 * rows * cfg.F * cfg.d)
+    tf = flops / (ms / 1e3) / 1e12
+    return {"ms": round(ms, 3), "tokens_per_s": round(cfg.T / (ms / 1e3), 1), "bound": "mfma", "achieved": round(tf, 1),
+            "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4), "flops": flops,
+            "computes": "dgrad and wgrad of every selected expert's SwiGLU FFN (dL/dx experts' share, dL/dW_gate_up, "
+                        "dL/dW_down), including the weight and activation transposes it runs"}
 
 
 # ----------------------------------------------------------------------------- trace workload
@@ -462,6 +501,7 @@ def main():
         res, st = run_layer(args)
         if args.workload == "ft":
             res["stage1_backward"] = run_stage1_backward(st, args)
+            res["layer_backward"] = run_layer_backward(st, args)
         base = None if args.no_cpu_baseline else layer_cpu_baseline(st)
     res["cpu_baseline"] = base
     pr = torch.cuda.get_device_properties(0)

@@ -237,8 +237,11 @@ int maskmoe_sample_mask(const float* mask_logits, const double* uniforms, int32_
  *  router_logits device [T, E] float, required: z = W x in fp32.
  *  expert_out    device [T, K, d] float, required, 16-byte aligned: F_{A_t[k]}(x_t) in fp32
  *                (for bf16 layers: from the bf16-rounded SwiGLU activation, as in y).
- *  Other arguments, rounding, workspace and errors as maskmoe_layer_forward, plus E_INVAL
- *  for a NULL output above when T > 0.
+ *  workspace     at least maskmoe_layer_train_workspace_bytes(desc) bytes; for bf16 layers it
+ *                keeps what maskmoe_layer_backward reads (the permutation, the SwiGLU
+ *                activations and the gate / up pre-activations, bf16).
+ *  Other arguments, rounding and errors as maskmoe_layer_forward (whatever T, bf16 layers take
+ *  the grouped-GEMM path), plus E_INVAL for a NULL output above when T > 0.
  */
 int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                                 const uint8_t* mask, const float* prior, const void* w_gate_up,
@@ -246,6 +249,57 @@ int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, c
                                 int32_t* topk_idx, float* topk_gate, float* router_logits,
                                 float* expert_out, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
+
+/*
+ * maskmoe_layer_train_workspace_bytes -- device workspace that maskmoe_layer_forward_train needs
+ * for `desc`: that of maskmoe_layer_forward plus, for bf16 layers, the gate / up pre-activations
+ * [T (K + n_shared), 2F] that maskmoe_layer_backward reads. Returns 0 for an invalid desc.
+ */
+size_t maskmoe_layer_train_workspace_bytes(const maskmoe_layer_desc* desc);
+
+/*
+ * maskmoe_layer_backward_workspace_bytes -- device workspace of maskmoe_layer_backward for
+ * `desc` (transposed weights and activations, dO, [da db], per-row dx). Returns 0 for an
+ * invalid desc.
+ */
+size_t maskmoe_layer_backward_workspace_bytes(const maskmoe_layer_desc* desc);
+
+/*
+ * maskmoe_layer_backward -- the experts' side of the layer backward for a cotangent dy of y,
+ * with the routing held fixed (the routers and experts update at every step: Section 3.2,
+ * Stage 1; Stage 2 continues with them). By Eq. 1 routed expert i receives g dy on the tokens
+ * that chose it, a shared expert dy on every token; through its SwiGLU
+ * F(x) = W_down (SiLU(W_gate x) * (W_up x)), with a = W_gate x, b = W_up x, h = SiLU(a) b:
+ *   dh = dO W_down,  da = dh * b * SiLU'(a),  db = dh * SiLU(a),
+ *   dL/dx (experts' share) = sum over the token's rows of da W_gate + db W_up,
+ *   dL/dW_down = dO^T h,  dL/dW_gate = da^T x,  dL/dW_up = db^T x.
+ * The gates' own gradient and the router's share of dL/dx come from maskmoe_stage1_backward.
+ *
+ *  desc            as given to maskmoe_layer_forward_train; bf16 only.
+ *  x, w_gate_up, w_down, ws_gate_up, ws_down: as given to the forward.
+ *  topk_gate       device [T, K] float, the forward's gates.
+ *  dy              device [T, d] bf16.
+ *  train_workspace the workspace of the maskmoe_layer_forward_train call with the same
+ *                  arguments, unchanged since (it holds the permutation, h and a, b), at least
+ *                  maskmoe_layer_train_workspace_bytes(desc) bytes.
+ *  d_x             device [T, d] float output: the experts' share of dL/dx.
+ *  d_w_gate_up     device [E, 2F, d] float output (zero for experts no token chose).
+ *  d_w_down        device [E, d, F] float output.
+ *  d_ws_gate_up, d_ws_down: the shared experts' gradients, [n_shared, ...]; NULL when
+ *                  n_shared == 0.
+ *  workspace       device, maskmoe_layer_backward_workspace_bytes(desc) bytes, 256-byte aligned.
+ *  Rounding: dO = g dy and [da db] are rounded to bf16 before their products, a and b are the
+ *  forward's bf16-rounded pre-activations; accumulation and all outputs are fp32.
+ *  Errors: as maskmoe_layer_forward; E_UNSUPPORTED for f32 layers or index ranges at or above
+ *  2^31 elements; E_WORKSPACE for a missing, small or misaligned workspace of either kind.
+ *  T = 0 writes nothing.
+ */
+int maskmoe_layer_backward(const maskmoe_layer_desc* desc, const void* x, const void* w_gate_up,
+                           const void* w_down, const void* ws_gate_up, const void* ws_down,
+                           const float* topk_gate, const void* dy, const void* train_workspace,
+                           size_t train_workspace_bytes, float* d_x, float* d_w_gate_up, float* d_w_down,
+                           float* d_ws_gate_up, float* d_ws_down, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream);
 
 /*
  * maskmoe_stage1_backward_workspace_bytes -- device workspace of maskmoe_stage1_backward for

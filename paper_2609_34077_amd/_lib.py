@@ -27,7 +27,8 @@ CACHE_LRU, CACHE_LFU, CACHE_FIFO = 0, 1, 2
 EXPORTS = ("maskmoe_route", "maskmoe_layer_workspace_bytes", "maskmoe_layer_forward",
            "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string",
            "maskmoe_sample_mask", "maskmoe_layer_forward_train", "maskmoe_stage1_backward_workspace_bytes",
-           "maskmoe_stage1_backward")
+           "maskmoe_stage1_backward", "maskmoe_layer_train_workspace_bytes",
+           "maskmoe_layer_backward_workspace_bytes", "maskmoe_layer_backward")
 NUM_STAGES = 5
 STAGES = ("route", "permute", "gate_up", "down", "combine")
 
@@ -86,6 +87,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.maskmoe_stage1_backward.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                             _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.maskmoe_stage1_backward.restype = ctypes.c_int
+    lib.maskmoe_layer_train_workspace_bytes.argtypes = [ctypes.POINTER(LayerDesc)]
+    lib.maskmoe_layer_train_workspace_bytes.restype = _sz
+    lib.maskmoe_layer_backward_workspace_bytes.argtypes = [ctypes.POINTER(LayerDesc)]
+    lib.maskmoe_layer_backward_workspace_bytes.restype = _sz
+    lib.maskmoe_layer_backward.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
+                                           _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.maskmoe_layer_backward.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -241,12 +249,20 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
 
 def maskmoe_layer_forward_train(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int,
                                 mask=None, prior=None, ws_gate_up=None, ws_down=None, workspace=None):
-    """maskmoe_layer_forward plus what the Stage 1 backward reads. Returns
-    ``(y [T,d], topk_idx [T,K], topk_gate [T,K], router_logits [T,E] fp32, expert_out [T,K,d] fp32)``."""
+    """maskmoe_layer_forward plus what the backward passes read. Returns
+    ``(y [T,d], topk_idx [T,K], topk_gate [T,K], router_logits [T,E] fp32, expert_out [T,K,d] fp32)``;
+    ``workspace`` (allocated with maskmoe_layer_train_workspace_bytes when not given) then holds
+    what maskmoe_layer_backward reads: pass the same tensor there, unchanged."""
     import torch
     lib = load()
     T, d = x.shape
     E = w_router.shape[0]
+    if workspace is None:
+        F = w_gate_up.shape[1] // 2
+        ns = 0 if ws_gate_up is None else ws_gate_up.shape[0]
+        desc0 = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode)
+        workspace = torch.empty(max(int(lib.maskmoe_layer_train_workspace_bytes(ctypes.byref(desc0))), 1),
+                                dtype=torch.uint8, device=x.device)
     idx = torch.empty((T, K), dtype=torch.int32, device=x.device)
     gate = torch.empty((T, K), dtype=torch.float32, device=x.device)
     logits = torch.empty((T, E), dtype=torch.float32, device=x.device)
@@ -346,3 +362,38 @@ def maskmoe_cache_fetches(trace, E: int, B: int, state=None, with_f_per_step: bo
         _ptr(trace), L, S, N, K, E, B, policy, _ptr(state), _ptr(counts), _ptr(fetches), _ptr(hits), _ptr(fps),
         _ptr(dev_error), _stream()))
     return {"fetches": fetches, "hits": hits, "f_per_step": fps, "dev_error": dev_error}
+
+
+def maskmoe_layer_backward(x, w_gate_up, w_down, K: int, gate_mode: int, topk_gate, dy, train_workspace,
+                           ws_gate_up=None, ws_down=None, route_mode: int = ROUTE_HARD_MASK, workspace=None):
+    """Experts' side of the layer backward (bf16). ``train_workspace`` is the workspace of the
+    maskmoe_layer_forward_train call with the same arguments. Returns dict(d_x [T,d],
+    d_w_gate_up [E,2F,d], d_w_down [E,d,F], d_ws_gate_up, d_ws_down), fp32."""
+    import torch
+    lib = load()
+    for t, n in ((x, "x"), (w_gate_up, "w_gate_up"), (w_down, "w_down"), (ws_gate_up, "ws_gate_up"),
+                 (ws_down, "ws_down"), (topk_gate, "topk_gate"), (dy, "dy"), (train_workspace, "train_workspace"),
+                 (workspace, "workspace")):
+        _dev(t, n)
+    T, d = x.shape
+    E, F2, _ = w_gate_up.shape
+    F = F2 // 2
+    ns = 0 if ws_gate_up is None else ws_gate_up.shape[0]
+    if tuple(dy.shape) != (T, d) or tuple(topk_gate.shape) != (T, K) or tuple(w_down.shape) != (E, d, F):
+        raise ValueError("inconsistent shapes")
+    desc = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode)
+    need = int(lib.maskmoe_layer_backward_workspace_bytes(ctypes.byref(desc)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    f32 = dict(dtype=torch.float32, device=x.device)
+    out = dict(d_x=torch.empty((T, d), **f32), d_w_gate_up=torch.empty((E, F2, d), **f32),
+               d_w_down=torch.empty((E, d, F), **f32),
+               d_ws_gate_up=torch.empty((ns, F2, d), **f32) if ns else None,
+               d_ws_down=torch.empty((ns, d, F), **f32) if ns else None)
+    _check("maskmoe_layer_backward",
+           lib.maskmoe_layer_backward(ctypes.byref(desc), _ptr(x), _ptr(w_gate_up), _ptr(w_down), _ptr(ws_gate_up),
+                                      _ptr(ws_down), _ptr(topk_gate), _ptr(dy), _ptr(train_workspace),
+                                      train_workspace.numel(), _ptr(out["d_x"]), _ptr(out["d_w_gate_up"]),
+                                      _ptr(out["d_w_down"]), _ptr(out["d_ws_gate_up"]), _ptr(out["d_ws_down"]),
+                                      _ptr(workspace), workspace.numel(), _stream()))
+    return out

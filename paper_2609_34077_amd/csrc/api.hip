@@ -54,6 +54,7 @@ int check_mask_prior(int mode, int L, int E, int K, const uint8_t* mask, const f
 
 struct Layout {
   size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, H, P, O, total;
+  size_t AB, train_total;   // training (bf16): gate / up pre-activations [rows, 2F] after `total`
 };
 
 static_assert(maskmoe::kDecodeMaxT <= maskmoe::kRouteOneBlockT,
@@ -94,6 +95,8 @@ Layout layout(const maskmoe_layer_desc& d) {
   const size_t o_rows = maskmoe::kDecodeMaxSplit * dec_rows;
   w.O = take((rows > o_rows ? rows : o_rows) * d.d * 4);
   w.total = off;
+  w.AB = take(d.dtype == MASKMOE_BF16 ? rows * 2 * d.F * 2 : 0);
+  w.train_total = off;
   return w;
 }
 
@@ -147,6 +150,11 @@ size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc) {
   return layout(*desc).total;
 }
 
+size_t maskmoe_layer_train_workspace_bytes(const maskmoe_layer_desc* desc) {
+  if (check_layer_desc(desc) != MASKMOE_OK) return 0;
+  return layout(*desc).train_total;
+}
+
 static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                               const uint8_t* mask, const float* prior, const void* w_gate_up,
                               const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
@@ -174,7 +182,9 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   if ((topk_idx && !aligned(topk_idx, 4)) || (topk_gate && !aligned(topk_gate, 4))) return MASKMOE_E_INVAL;
   if ((router_logits && !aligned(router_logits, 4)) || (expert_out && !aligned(expert_out, 16))) return MASKMOE_E_INVAL;
   const Layout w = layout(d);
-  if (!workspace || workspace_bytes < w.total || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
+  const bool train = expert_out != nullptr;   // the training forward also keeps what the backward reads
+  const size_t need = train ? w.train_total : w.total;
+  if (!workspace || workspace_bytes < need || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
 
   char* ws = static_cast<char*>(workspace);
   int32_t* idx = topk_idx ? topk_idx : reinterpret_cast<int32_t*>(ws + w.idx);
@@ -190,7 +200,10 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
 
   maskmoe::record_mark(events, 0, stream);
   hipError_t e;
-  if (uses_decode_path(d)) {  // one workgroup routes every token and then permutes them
+  // Training always takes the grouped-GEMM path, whose gate/up epilogue can keep the
+  // pre-activations for the backward.
+  const bool decode = uses_decode_path(d) && !train;
+  if (decode) {  // one workgroup routes every token and then permutes them
     e = maskmoe::launch_route_permute(x, w_router, d.T, d.d, d.E, d.K, d.route_mode, d.gate_mode, mask, prior, idx,
                                       gate, router_logits, d.n_shared, maskmoe::kGemmBM, pb, stream);
     if (e != hipSuccess) return MASKMOE_E_HIP;
@@ -218,7 +231,7 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   if (!bf16) {
     e = maskmoe::launch_experts_f32(a, pb, reinterpret_cast<float*>(ws + w.H), reinterpret_cast<float*>(ws + w.O),
                                     y, stream, expert_marks);
-  } else if (uses_decode_path(d)) {
+  } else if (decode) {
     e = maskmoe::launch_experts_bf16_decode(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
                                             reinterpret_cast<float*>(ws + w.P), reinterpret_cast<float*>(ws + w.O), y,
                                             stream, expert_marks);
@@ -229,7 +242,7 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
                               static_cast<int64_t>(d.n_shared) * ((d.T + maskmoe::kGemmBM - 1) / maskmoe::kGemmBM);
     e = maskmoe::launch_experts_bf16(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
                                      reinterpret_cast<float*>(ws + w.O), y, static_cast<int>(max_tiles), stream,
-                                     expert_marks);
+                                     expert_marks, train ? reinterpret_cast<uint16_t*>(ws + w.AB) : nullptr);
   }
   return hip_status(e);
 }
@@ -262,6 +275,78 @@ int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x
   if (!events) return MASKMOE_E_INVAL;
   return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
                             topk_idx, topk_gate, nullptr, nullptr, workspace, workspace_bytes, stream, events);
+}
+
+size_t maskmoe_layer_backward_workspace_bytes(const maskmoe_layer_desc* desc) {
+  if (check_layer_desc(desc) != MASKMOE_OK) return 0;
+  const maskmoe_layer_desc& d = *desc;
+  return maskmoe::backward_layout(d.T, d.d, d.F, d.E, d.K, d.n_shared).total;
+}
+
+int maskmoe_layer_backward(const maskmoe_layer_desc* desc, const void* x, const void* w_gate_up,
+                           const void* w_down, const void* ws_gate_up, const void* ws_down, const float* topk_gate,
+                           const void* dy, const void* train_workspace, size_t train_workspace_bytes, float* d_x,
+                           float* d_w_gate_up, float* d_w_down, float* d_ws_gate_up, float* d_ws_down,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = check_layer_desc(desc);
+  if (st != MASKMOE_OK) return st;
+  const maskmoe_layer_desc& d = *desc;
+  if (d.dtype != MASKMOE_BF16) return MASKMOE_E_UNSUPPORTED;
+  if (d.d % 64 != 0 || d.F % 64 != 0) return MASKMOE_E_UNSUPPORTED;
+  if (d.T == 0) return MASKMOE_OK;
+  if (!x || !w_gate_up || !w_down || !topk_gate || !dy || !d_x || !d_w_gate_up || !d_w_down) return MASKMOE_E_INVAL;
+  if (d.n_shared > 0 && (!ws_gate_up || !ws_down || !d_ws_gate_up || !d_ws_down)) return MASKMOE_E_INVAL;
+  const void* p16[] = {x, w_gate_up, w_down, dy, d_x};
+  for (const void* p : p16)
+    if (!aligned(p, 16)) return MASKMOE_E_INVAL;
+  if (!aligned(topk_gate, 4) || !aligned(d_w_gate_up, 4) || !aligned(d_w_down, 4)) return MASKMOE_E_INVAL;
+  if (d.n_shared > 0 && (!aligned(ws_gate_up, 16) || !aligned(ws_down, 16) || !aligned(d_ws_gate_up, 4) ||
+                         !aligned(d_ws_down, 4)))
+    return MASKMOE_E_INVAL;
+  const maskmoe::BwdLayout bl = maskmoe::backward_layout(d.T, d.d, d.F, d.E, d.K, d.n_shared);
+  // the GEMMs address rows with 32-bit element offsets
+  const int64_t rows = static_cast<int64_t>(d.T) * (d.K + d.n_shared);
+  const int64_t widest = 2 * static_cast<int64_t>(d.F) > d.d ? 2 * static_cast<int64_t>(d.F) : d.d;
+  if (rows * 2 * d.F >= (int64_t{1} << 31) || rows * d.d >= (int64_t{1} << 31) ||
+      widest * bl.P >= (int64_t{1} << 31) || static_cast<int64_t>(d.T) * d.d >= (int64_t{1} << 31) ||
+      int64_t{2} * d.F * d.d >= (int64_t{1} << 31))
+    return MASKMOE_E_UNSUPPORTED;
+  const Layout w = layout(d);
+  if (!train_workspace || train_workspace_bytes < w.train_total || !aligned(train_workspace, 256))
+    return MASKMOE_E_WORKSPACE;
+  if (!workspace || workspace_bytes < bl.total || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
+
+  char* tw = static_cast<char*>(const_cast<void*>(train_workspace));
+  maskmoe::BwdArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.w_gate_up = static_cast<const uint16_t*>(w_gate_up);
+  a.w_down = static_cast<const uint16_t*>(w_down);
+  a.ws_gate_up = static_cast<const uint16_t*>(ws_gate_up);
+  a.ws_down = static_cast<const uint16_t*>(ws_down);
+  a.gate = topk_gate;
+  a.dy = static_cast<const uint16_t*>(dy);
+  a.pb.offsets = reinterpret_cast<int32_t*>(tw + w.offsets);
+  a.pb.tile_off = reinterpret_cast<int32_t*>(tw + w.tile_off);
+  a.pb.active = reinterpret_cast<int32_t*>(tw + w.active);
+  a.pb.n_active = reinterpret_cast<int32_t*>(tw + w.n_active);
+  a.pb.perm = reinterpret_cast<int32_t*>(tw + w.perm);
+  a.pb.inv = reinterpret_cast<int32_t*>(tw + w.inv);
+  a.pb.row_tok = reinterpret_cast<int32_t*>(tw + w.row_tok);
+  a.h = reinterpret_cast<const uint16_t*>(tw + w.H);
+  a.ab = reinterpret_cast<const uint16_t*>(tw + w.AB);
+  a.d_x = d_x;
+  a.d_w_gate_up = d_w_gate_up;
+  a.d_w_down = d_w_down;
+  a.d_ws_gate_up = d_ws_gate_up;
+  a.d_ws_down = d_ws_down;
+  a.workspace = workspace;
+  a.lay = bl;
+  a.T = d.T; a.d = d.d; a.F = d.F; a.E = d.E; a.K = d.K; a.S = d.n_shared;
+  const int64_t TK = static_cast<int64_t>(d.T) * d.K;
+  const int64_t nonempty = TK < d.E ? TK : d.E;
+  a.max_tiles = static_cast<int>(TK / maskmoe::kGemmBM + nonempty +
+                                 static_cast<int64_t>(d.n_shared) * ((d.T + maskmoe::kGemmBM - 1) / maskmoe::kGemmBM));
+  return hip_status(maskmoe::launch_layer_backward(a, stream));
 }
 
 size_t maskmoe_stage1_backward_workspace_bytes(const maskmoe_layer_desc* desc) {

@@ -1,0 +1,429 @@
+// Expert-side backward of the masked MoE layer: the SwiGLU experts' weight gradients and their
+// share of dL/dx, with the routing held fixed.
+//
+// The routers and experts update at every step (Section 3.2, Stage 1; Stage 2 continues with
+// them). By Eq. 1, routed expert e receives dL/dF = g dy on the tokens that chose it and a
+// shared expert dy on every token. Through F(x) = W_down (SiLU(W_gate x) * W_up x), with
+// a = x W_gate^T, b = x W_up^T, h = SiLU(a) * b kept by the training forward:
+//   dh = dO W_down               da = dh * b * SiLU'(a),  db = dh * SiLU(a)
+//   dX = da W_gate + db W_up     dW_down = dO^T h,  dW_gate = da^T x,  dW_up = db^T x
+// per expert, over the permuted rows of the forward (one row per (token, slot), shared
+// experts' rows after them).
+//
+// Every product is run as C = A B^T with K-contiguous rows on the 256x256x64 MFMA tile of
+// gemm_tile.hpp. The operands whose contraction index is strided in storage are transposed
+// first with an LDS-tiled copy: the weights (per call, as they change between steps), and for
+// the weight gradients the rows of dO, h, [da db] and the gathered x, laid out per expert with
+// the row count padded to a multiple of 64 and zero columns in the gaps, so each expert's
+// wgrad is one GEMM over its own padded token range (an expert no token chose gets zeros).
+// Rounding (bf16 layers): dO = g dy and [da db] are rounded to bf16 before their GEMMs;
+// accumulation is fp32; dX, dW are fp32.
+
+#include "common.hpp"
+#include "gemm_tile.hpp"
+#include "kernels.hpp"
+
+namespace maskmoe {
+namespace {
+
+constexpr int kBwdThreads = 256;
+
+__device__ __forceinline__ uint32_t scale_pair(uint32_t v, float w) {
+  const float lo = bf16_to_f32(static_cast<uint16_t>(v & 0xffffu)) * w;
+  const float hi = bf16_to_f32(static_cast<uint16_t>(v >> 16)) * w;
+  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+// dO[r, :] = bf16(w_r dy[row_tok[r], :]): w_r the gate of the (token, slot) entry at routed row
+// r, 1 for shared-expert rows. One workgroup per row; d % 8 == 0.
+__global__ __launch_bounds__(kBwdThreads) void build_dout_kernel(const uint16_t* __restrict__ dy,
+                                                                 const float* __restrict__ gate,
+                                                                 const int32_t* __restrict__ perm,
+                                                                 const int32_t* __restrict__ row_tok, int TK, int d,
+                                                                 uint16_t* __restrict__ dout) {
+  const int r = blockIdx.x;
+  const float w = r < TK ? gate[perm[r]] : 1.0f;
+  const uint16_t* src = dy + static_cast<size_t>(row_tok[r]) * d;
+  uint16_t* dst = dout + static_cast<size_t>(r) * d;
+  for (int c = threadIdx.x * 8; c < d; c += kBwdThreads * 8) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(src + c);
+    u32x4 o;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) o[h] = scale_pair(v[h], w);
+    *reinterpret_cast<u32x4*>(dst + c) = o;
+  }
+}
+
+// Padded token layout of the weight gradients: group g's rows occupy padded columns
+// [poff[g], poff[g] + n_g), n_g = offsets[g+1] - offsets[g], and poff[g+1] = poff[g] +
+// roundup(n_g, 64); pmap[pc] is the permuted row at padded column pc, or -1 (zero column).
+// One workgroup.
+__global__ __launch_bounds__(kBwdThreads) void pad_layout_kernel(const int32_t* __restrict__ offsets, int G, int P,
+                                                                 int32_t* __restrict__ poff,
+                                                                 int32_t* __restrict__ pmap) {
+  __shared__ int off[kMaxGroupsBwd + 1];
+  __shared__ int po[kMaxGroupsBwd + 1];
+  for (int g = threadIdx.x; g <= G; g += kBwdThreads) off[g] = offsets[g];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    po[0] = 0;
+    for (int g = 0; g < G; ++g) po[g + 1] = po[g] + (off[g + 1] - off[g] + kTileK - 1) / kTileK * kTileK;
+  }
+  __syncthreads();
+  for (int g = threadIdx.x; g <= G; g += kBwdThreads) poff[g] = po[g];
+  for (int pc = threadIdx.x; pc < P; pc += kBwdThreads) {
+    int row = -1;
+    if (pc < po[G]) {
+      int lo = 0, hi = G;   // po[lo] <= pc < po[hi]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (po[mid] <= pc) lo = mid; else hi = mid;
+      }
+      const int k = pc - po[lo];
+      if (k < off[lo + 1] - off[lo]) row = off[lo] + k;
+    }
+    pmap[pc] = row;
+  }
+}
+
+// out[c * ldo + pc] = source row of pc at column c, for c < C (C % 64 == 0), pc < P: the
+// source row is pmap[pc] (-1: a zero column) or pc itself without a map, read at
+// src + row_tok[row] * lds (GATHER) or src + row * lds. 64x64 tiles through LDS; blockIdx.z
+// selects one matrix of a batch (src_batch / out_batch elements apart): matrix z, or with an
+// active list the z-th listed group if it is below `limit` (the others are left alone).
+template <bool GATHER>
+__global__ __launch_bounds__(kBwdThreads) void transpose_kernel(const uint16_t* __restrict__ src, int lds,
+                                                                const int32_t* __restrict__ pmap,
+                                                                const int32_t* __restrict__ row_tok, int P, int C,
+                                                                uint16_t* __restrict__ out, int ldo, size_t src_batch,
+                                                                size_t out_batch, const int32_t* __restrict__ active,
+                                                                const int32_t* __restrict__ n_active, int limit) {
+  constexpr int PITCH = 64 + 8;   // 16-byte aligned rows
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][PITCH];
+  const int pc0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  int mat = blockIdx.z;
+  if (active) {
+    if (mat >= n_active[0]) return;
+    mat = active[mat];
+    if (mat >= limit) return;
+  }
+  src += mat * src_batch;
+  out += mat * out_batch;
+  for (int u = threadIdx.x; u < 64 * 8; u += kBwdThreads) {
+    const int pr = u >> 3, cc = (u & 7) * 8;
+    const int pc = pc0 + pr;
+    int row = -1;
+    if (pc < P) row = pmap ? pmap[pc] : pc;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row >= 0) {
+      const size_t srow = GATHER ? static_cast<size_t>(row_tok[row]) : static_cast<size_t>(row);
+      v = *reinterpret_cast<const u32x4*>(src + srow * lds + c0 + cc);
+    }
+    *reinterpret_cast<u32x4*>(&tile[pr][cc]) = v;
+  }
+  __syncthreads();
+  for (int u = threadIdx.x; u < 64 * 8; u += kBwdThreads) {
+    const int cr = u >> 3, pp = (u & 7) * 8;
+    uint16_t* dst = out + static_cast<size_t>(c0 + cr) * ldo + pc0 + pp;
+    if (pc0 + pp + 8 <= P) {
+      u32x4 v;
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        v[h] = static_cast<uint32_t>(tile[pp + 2 * h][cr]) | (static_cast<uint32_t>(tile[pp + 2 * h + 1][cr]) << 16);
+      *reinterpret_cast<u32x4*>(dst) = v;
+    } else {
+      for (int q = 0; q < 8 && pc0 + pp + q < P; ++q) dst[q] = tile[pp + q][cr];
+    }
+  }
+}
+
+struct NtArgs {
+  const uint16_t* a;          // ROWS: [rows, K] (lda); KSPLIT: [M, P] (lda = P)
+  const uint16_t* b;          // ROWS: per routed expert [N, K] matrices; KSPLIT: [N, P] (ldb = P)
+  const uint16_t* bs;         // ROWS: the shared experts' [N, K] matrices
+  const int32_t* offsets;     // [G+1] rows of each group (ROWS)
+  const int32_t* tile_off;    // [G+1] row tiles of each group (ROWS)
+  const int32_t* poff;        // [G+1] padded token range of each group (KSPLIT)
+  const int32_t* active;      // KSPLIT: the non-empty groups, n_active[0] of them
+  const int32_t* n_active;
+  const uint16_t* ab;         // SWIGLU_BWD: saved pre-activations [rows, 2N]
+  void* c;                    // ROWS: [rows, ldc]; KSPLIT: routed groups' [M, N] matrices
+  void* cs;                   // KSPLIT: shared groups' [M, N] matrices
+  int G, E, M, N, K, lda, ldb, ldc, mt_max, n_tiles;
+};
+
+enum { kNtRows = 0, kNtKSplit = 1 };
+enum { kEpiSwigluBwd = 0, kEpiF32 = 1 };
+
+// ROWS (dgrad): group g's rows offsets[g]..offsets[g+1] of A times its own [N, K] matrix, row
+// tiles enumerated by tile_off as in the forward. KSPLIT (wgrad): for every non-empty group g
+// the full [M, N] product over its padded token range [poff[g], poff[g+1]); the grid is sized
+// for all groups and the live tiles (n_active x tiles per group) are spread over the XCDs.
+template <int MODE, int EPI>
+__global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
+  constexpr int TM = kTileTM, TN = kTileTN, U = kTileU, WN = 4;
+  __shared__ u32x4 lds_a[2][kTileM * 8];
+  __shared__ u32x4 lds_b[2][kTileN * 8];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  int mt, nt, g, row0, row_end, nk;
+  const uint16_t* abase;
+  const uint16_t* bbase;
+  if (MODE == kNtRows) {
+    grouped_tile_coords(xcd_tile_id(), p.mt_max, p.n_tiles, mt, nt);
+    if (mt >= p.tile_off[p.G]) return;
+    int lo = 0, hi = p.G;   // tile_off[lo] <= mt < tile_off[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (p.tile_off[mid] <= mt) lo = mid; else hi = mid;
+    }
+    g = lo;
+    row0 = p.offsets[g] + (mt - p.tile_off[g]) * kTileM;
+    row_end = p.offsets[g + 1];
+    nk = p.K / kTileK;
+    abase = p.a;
+    bbase = g < p.E ? p.b + static_cast<size_t>(g) * p.N * p.K : p.bs + static_cast<size_t>(g - p.E) * p.N * p.K;
+  } else {
+    const int per = p.mt_max * p.n_tiles;
+    const int live = p.n_active[0] * per;
+    if (static_cast<int>(blockIdx.x) >= live) return;
+    const int lid = xcd_tile_id(live);
+    g = p.active[lid / per];
+    grouped_tile_coords(lid % per, p.mt_max, p.n_tiles, mt, nt);
+    row0 = mt * kTileM;
+    row_end = p.M;
+    const int k0 = p.poff[g];
+    nk = (p.poff[g + 1] - k0) / kTileK;
+    abase = p.a + k0;
+    bbase = p.b + k0;
+  }
+  const int n0 = nt * kTileN;
+  const int r0 = tile_load_row(), chunk = tile_load_chunk();
+  int aoffs[U], boffs[U];   // element offsets (< 2^31, checked by the host)
+#pragma unroll
+  for (int i = 0; i < U; ++i) {
+    const int r = r0 + 64 * i;
+    aoffs[i] = min(row0 + r, row_end - 1) * p.lda + chunk;
+    boffs[i] = min(n0 + r, p.N - 1) * p.ldb + chunk;
+  }
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) aoff[i] = (wm * 128 + i * 32 + (lane & 31)) * 8;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) boff[j] = (wn * 64 + j * 32 + (lane & 31)) * 8;
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  gemm_tile_mainloop(abase, aoffs, bbase, boffs, aoff, boff, nk, acc, lds_a, lds_b);
+
+  // acc[i][j][4 jj + ii] is row wm*128 + i*32 + 8 jj + 4 (lane >> 5) + ii, column
+  // wn*64 + j*32 + (lane & 31) of the tile.
+  float* cf = nullptr;
+  if (MODE == kNtKSplit)
+    cf = g < p.E ? static_cast<float*>(p.c) + static_cast<size_t>(g) * p.M * p.N
+                 : static_cast<float*>(p.cs) + static_cast<size_t>(g - p.E) * p.M * p.N;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = row0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (row >= row_end) continue;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+        if (col >= p.N) continue;
+        const float v = acc[i][j][r];
+        if (EPI == kEpiSwigluBwd) {   // v = dh; write da, db (bf16) into [rows, 2N]
+          const size_t base = static_cast<size_t>(row) * 2 * p.N;
+          const float av = bf16_to_f32(p.ab[base + col]);
+          const float bv = bf16_to_f32(p.ab[base + p.N + col]);
+          const float s = 1.0f / (1.0f + __expf(-av));
+          uint16_t* o = static_cast<uint16_t*>(p.c);
+          o[base + col] = f32_to_bf16(v * bv * (s * (1.0f + av * (1.0f - s))));
+          o[base + p.N + col] = f32_to_bf16(v * av * s);
+        } else if (MODE == kNtRows) {
+          static_cast<float*>(p.c)[static_cast<size_t>(row) * p.ldc + col] = v;
+        } else {
+          cf[static_cast<size_t>(row) * p.N + col] = v;
+        }
+      }
+    }
+  }
+}
+
+// dx[t, c] = sum_k dXr[inv[t K + k], c] + sum_s dXr[T K + s T + t, c], in that order.
+__global__ __launch_bounds__(kBwdThreads) void dx_combine_kernel(const float* __restrict__ dxr,
+                                                                 const int32_t* __restrict__ inv, int T, int K, int S,
+                                                                 int d, float* __restrict__ dx) {
+  const int t = blockIdx.x;
+  for (int c = threadIdx.x * 4; c < d; c += kBwdThreads * 4) {
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k = 0; k < K + S; ++k) {
+      const size_t row = k < K ? static_cast<size_t>(inv[t * K + k]) : static_cast<size_t>(T) * K + (k - K) * T + t;
+      const float4 v = *reinterpret_cast<const float4*>(dxr + row * d + c);
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+    *reinterpret_cast<float4*>(dx + static_cast<size_t>(t) * d + c) = s;
+  }
+}
+
+hipError_t transpose(bool gather, const uint16_t* src, int lds, const int32_t* pmap, const int32_t* row_tok, int P,
+                     int C, uint16_t* out, int ldo, int batch, size_t src_batch, size_t out_batch, hipStream_t s,
+                     const int32_t* active = nullptr, const int32_t* n_active = nullptr, int limit = 0) {
+  const dim3 grid((P + 63) / 64, C / 64, batch);
+  if (gather)
+    hipLaunchKernelGGL(transpose_kernel<true>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, C, out, ldo,
+                       src_batch, out_batch, active, n_active, limit);
+  else
+    hipLaunchKernelGGL(transpose_kernel<false>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, C, out,
+                       ldo, src_batch, out_batch, active, n_active, limit);
+  return hipGetLastError();
+}
+
+// Zero the [M, N] gradient matrices of the groups that no row reached (offsets[g+1] ==
+// offsets[g]). Grid (G, chunks); float4 stores; M N % 4 == 0.
+__global__ __launch_bounds__(kBwdThreads) void zero_unused_kernel(const int32_t* __restrict__ offsets, int E,
+                                                                  size_t mn, float* __restrict__ c,
+                                                                  float* __restrict__ cs) {
+  const int g = blockIdx.x;
+  if (offsets[g + 1] > offsets[g]) return;
+  float4* dst = reinterpret_cast<float4*>(g < E ? c + g * mn : cs + (g - E) * mn);
+  const size_t n4 = mn / 4;
+  for (size_t i = static_cast<size_t>(blockIdx.y) * kBwdThreads + threadIdx.x; i < n4;
+       i += static_cast<size_t>(gridDim.y) * kBwdThreads)
+    dst[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+#define MASKMOE_TRY(x)               \
+  do {                               \
+    const hipError_t e_ = (x);       \
+    if (e_ != hipSuccess) return e_; \
+  } while (0)
+
+}  // namespace
+
+BwdLayout backward_layout(int T, int d, int F, int E, int K, int S) {
+  BwdLayout w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) / 256 * 256;
+    return o;
+  };
+  const size_t G = static_cast<size_t>(E) + S;
+  const size_t R = static_cast<size_t>(T) * (K + S);
+  w.P = static_cast<int>((R + 64 * G + 63) / 64 * 64);
+  const size_t P = static_cast<size_t>(w.P);
+  w.w_down_t = take(G * F * d * 2);
+  w.w_gate_up_t = take(G * d * 2 * F * 2);
+  w.dout = take(R * d * 2);
+  w.dab = take(R * 2 * F * 2);
+  w.dxr = take(R * d * 4);
+  w.poff = take((G + 1) * 4);
+  w.pmap = take(P * 4);
+  w.dout_t = take(static_cast<size_t>(d) * P * 2);
+  w.h_t = take(static_cast<size_t>(F) * P * 2);
+  w.dab_t = take(static_cast<size_t>(2) * F * P * 2);
+  w.x_t = take(static_cast<size_t>(d) * P * 2);
+  w.total = off;
+  return w;
+}
+
+hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
+  const int G = a.E + a.S, T = a.T, d = a.d, F = a.F, K = a.K;
+  const int R = T * (K + a.S);
+  const BwdLayout& w = a.lay;
+  char* ws = static_cast<char*>(a.workspace);
+  uint16_t* wdt = reinterpret_cast<uint16_t*>(ws + w.w_down_t);
+  uint16_t* wgut = reinterpret_cast<uint16_t*>(ws + w.w_gate_up_t);
+  uint16_t* dout = reinterpret_cast<uint16_t*>(ws + w.dout);
+  uint16_t* dab = reinterpret_cast<uint16_t*>(ws + w.dab);
+  float* dxr = reinterpret_cast<float*>(ws + w.dxr);
+  int32_t* poff = reinterpret_cast<int32_t*>(ws + w.poff);
+  int32_t* pmap = reinterpret_cast<int32_t*>(ws + w.pmap);
+  uint16_t* dout_t = reinterpret_cast<uint16_t*>(ws + w.dout_t);
+  uint16_t* h_t = reinterpret_cast<uint16_t*>(ws + w.h_t);
+  uint16_t* dab_t = reinterpret_cast<uint16_t*>(ws + w.dab_t);
+  uint16_t* x_t = reinterpret_cast<uint16_t*>(ws + w.x_t);
+  const size_t FD = static_cast<size_t>(F) * d;
+
+  // weights, transposed: W_down [d, F] -> [F, d]; W_gate_up [2F, d] -> [d, 2F]
+  // (routed experts that no token chose are skipped: their transposed matrices are never read)
+  MASKMOE_TRY(transpose(false, a.w_down, F, nullptr, nullptr, d, F, wdt, d, a.E, FD, FD, s, a.pb.active,
+                        a.pb.n_active, a.E));
+  MASKMOE_TRY(transpose(false, a.w_gate_up, d, nullptr, nullptr, 2 * F, d, wgut, 2 * F, a.E, 2 * FD, 2 * FD, s,
+                        a.pb.active, a.pb.n_active, a.E));
+  if (a.S > 0) {
+    MASKMOE_TRY(transpose(false, a.ws_down, F, nullptr, nullptr, d, F, wdt + a.E * FD, d, a.S, FD, FD, s));
+    MASKMOE_TRY(transpose(false, a.ws_gate_up, d, nullptr, nullptr, 2 * F, d, wgut + 2 * a.E * FD, 2 * F, a.S,
+                          2 * FD, 2 * FD, s));
+  }
+  // dO, then dgrad of the down projection with the SwiGLU backward: [da db] (bf16)
+  hipLaunchKernelGGL(build_dout_kernel, dim3(R), dim3(kBwdThreads), 0, s, a.dy, a.gate, a.pb.perm, a.pb.row_tok, T * K,
+                     d, dout);
+  MASKMOE_TRY(hipGetLastError());
+  NtArgs n{};
+  n.offsets = a.pb.offsets;
+  n.tile_off = a.pb.tile_off;
+  n.G = G; n.E = a.E;
+  n.mt_max = a.max_tiles;
+  n.a = dout; n.lda = d;
+  n.b = wdt; n.bs = wdt + a.E * FD; n.N = F; n.K = d; n.ldb = d;
+  n.ab = a.ab;
+  n.c = dab;
+  n.n_tiles = (F + kTileN - 1) / kTileN;
+  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiSwigluBwd>), dim3(n.mt_max * n.n_tiles), dim3(kTileThreads), 0, s,
+                     n);
+  MASKMOE_TRY(hipGetLastError());
+  // dgrad of gate/up: dX rows = [da db] W_gate_up, then the token sums
+  n.a = dab; n.lda = 2 * F;
+  n.b = wgut; n.bs = wgut + 2 * a.E * FD; n.N = d; n.K = 2 * F; n.ldb = 2 * F;
+  n.ab = nullptr;
+  n.c = dxr; n.ldc = d;
+  n.n_tiles = (d + kTileN - 1) / kTileN;
+  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiF32>), dim3(n.mt_max * n.n_tiles), dim3(kTileThreads), 0, s, n);
+  MASKMOE_TRY(hipGetLastError());
+  hipLaunchKernelGGL(dx_combine_kernel, dim3(T), dim3(kBwdThreads), 0, s, dxr, a.pb.inv, T, K, a.S, d, a.d_x);
+  MASKMOE_TRY(hipGetLastError());
+  // weight gradients over each expert's padded token range
+  hipLaunchKernelGGL(pad_layout_kernel, dim3(1), dim3(kBwdThreads), 0, s, a.pb.offsets, G, w.P, poff, pmap);
+  MASKMOE_TRY(hipGetLastError());
+  MASKMOE_TRY(transpose(false, dout, d, pmap, nullptr, w.P, d, dout_t, w.P, 1, 0, 0, s));
+  MASKMOE_TRY(transpose(false, a.h, F, pmap, nullptr, w.P, F, h_t, w.P, 1, 0, 0, s));
+  MASKMOE_TRY(transpose(false, dab, 2 * F, pmap, nullptr, w.P, 2 * F, dab_t, w.P, 1, 0, 0, s));
+  MASKMOE_TRY(transpose(true, a.x, d, pmap, a.pb.row_tok, w.P, d, x_t, w.P, 1, 0, 0, s));
+  NtArgs m{};
+  m.poff = poff;
+  m.active = a.pb.active;
+  m.n_active = a.pb.n_active;
+  m.G = G; m.E = a.E;
+  m.lda = w.P; m.ldb = w.P;
+  // dW_down [d, F] = dO^T h
+  m.a = dout_t; m.b = h_t; m.M = d; m.N = F;
+  m.c = a.d_w_down; m.cs = a.d_ws_down;
+  m.mt_max = (d + kTileM - 1) / kTileM;
+  m.n_tiles = (F + kTileN - 1) / kTileN;
+  hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
+                     m);
+  MASKMOE_TRY(hipGetLastError());
+  hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, s, a.pb.offsets, a.E, FD, a.d_w_down,
+                     a.d_ws_down);
+  MASKMOE_TRY(hipGetLastError());
+  // dW_gate_up [2F, d] = [da db]^T x
+  m.a = dab_t; m.b = x_t; m.M = 2 * F; m.N = d;
+  m.c = a.d_w_gate_up; m.cs = a.d_ws_gate_up;
+  m.mt_max = (2 * F + kTileM - 1) / kTileM;
+  m.n_tiles = (d + kTileN - 1) / kTileN;
+  hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
+                     m);
+  MASKMOE_TRY(hipGetLastError());
+  hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, s, a.pb.offsets, a.E, 2 * FD,
+                     a.d_w_gate_up, a.d_ws_gate_up);
+  return hipGetLastError();
+}
+
+}  // namespace maskmoe

@@ -28,6 +28,7 @@
 #include <cstdlib>
 
 #include "common.hpp"
+#include "gemm_tile.hpp"
 #include "kernels.hpp"
 
 namespace maskmoe {
@@ -35,8 +36,8 @@ namespace {
 
 // ------------------------------------------------------------------ bf16 grouped GEMM
 
-constexpr int BM = kGemmBM, BN = 256, BK = 64, GEMM_THREADS = 512;
-static_assert(BM == 256, "tile mapping assumes 256-row tiles");
+constexpr int BM = kGemmBM, BN = kTileN, BK = kTileK, GEMM_THREADS = kTileThreads;
+static_assert(BM == kTileM, "tile mapping assumes 256-row tiles");
 
 struct GemmArgs {
   const uint16_t* a;        // EPI 0: x [T, d] (rows via row_tok); EPI 1: H [rows, F]
@@ -46,6 +47,7 @@ struct GemmArgs {
   const int32_t* offsets;   // [G+1]
   const int32_t* tile_off;  // [G+1]
   void* out;                // EPI 0: H bf16 [rows, F]; EPI 1: O f32 [rows, d]
+  uint16_t* ab;             // EPI 0, training: gate / up pre-activations bf16 [rows, 2F], or null
   int G, E, F, d;
   int mt_max;               // grid bound on row tiles
   int n_tiles;              // column tiles
@@ -63,26 +65,13 @@ __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt
 template <int EPI>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
   constexpr int WN = 4;                 // waves: 2 along rows x 4 along columns
-  constexpr int TM = 4, TN = 2;         // 32x32 fragments per wave: 128 rows x 64 B-rows
-  constexpr int NT = GEMM_THREADS;
-  constexpr int U = BM * 8 / NT;        // 16-byte units per thread per operand and stage (= 4)
+  constexpr int TM = kTileTM, TN = kTileTN;
+  constexpr int U = kTileU;
   __shared__ u32x4 lds_a[2][BM * 8];
   __shared__ u32x4 lds_b[2][BN * 8];
 
-  // XCD-aware block order: the hardware deals block ids round-robin over the 8 XCDs, so ids
-  // are remapped to give each XCD a contiguous range of logical tiles. Logical tiles come in
-  // groups of GN column tiles; inside a group the column tile varies fastest, so the ~32
-  // workgroups an XCD runs at once cover about 8 row tiles x 4 column tiles and share both
-  // operands in its L2.
-  constexpr int GN = 4;
-  const int nwg = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, local = bid >> 3, q = nwg >> 3, rem = nwg & 7;
-  const int lid = xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
-  const int per_group = GN * p.mt_max;
-  const int first_n = (lid / per_group) * GN;
-  const int gsize = min(p.n_tiles - first_n, GN);
-  const int within = lid % per_group;
-  const int nt = first_n + within % gsize, mt = within / gsize;
+  int mt, nt;
+  grouped_tile_coords(xcd_tile_id(), p.mt_max, p.n_tiles, mt, nt);
   if (mt >= p.tile_off[p.G]) return;
   const int g = find_group(p.tile_off, p.G, mt);
   const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM;
@@ -94,12 +83,9 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
-  // Global -> LDS mapping: thread tid loads rows (tid >> 3) + 64 i (i < U) of each operand;
-  // LDS slot u = tid + NT * i (row u >> 3, physical chunk u & 7) receives the logical chunk
-  // (u & 7) ^ lds_swizzle(row), which keeps the MFMA operand reads free of bank conflicts.
-  // The swizzle term is the same for all i (64 rows apart), so one chunk offset serves all.
-  const int r0 = tid >> 3;
-  const int chunk = ((tid & 7) ^ lds_swizzle(r0)) * 8;
+  // Unit i of this thread: rows r0 + 64 i of the A and B tiles (see gemm_tile.hpp).
+  const int r0 = tile_load_row();
+  const int chunk = tile_load_chunk();
   const uint16_t* wg = g < p.E ? p.w + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * Kdim
                                : p.ws + static_cast<size_t>(g - p.E) * (EPI == 0 ? 2 * p.F : p.d) * Kdim;
   int aoffs[U], boffs[U];   // element offsets (< 2^31, checked by the host)
@@ -128,7 +114,6 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     const int br = EPI == 0 ? (j == 0 ? 0 : 128) + wn * 32 : wn * 64 + j * 32;
     boff[j] = (br + (lane & 31)) * 8;
   }
-  const int sw = lds_swizzle(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -137,66 +122,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  u32x4 ra[U], rb[U];
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < U; ++i) {
-      ra[i] = *reinterpret_cast<const u32x4*>(p.a + (aoffs[i] + kt * BK));
-      rb[i] = *reinterpret_cast<const u32x4*>(wg + (boffs[i] + kt * BK));
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < U; ++i) {
-      lds_a[buf][tid + NT * i] = ra[i];
-      lds_b[buf][tid + NT * i] = rb[i];
-    }
-  };
-  u32x4 af[2][TM], bf[2][TN];
-  auto read_frags = [&](int buf, int kk, int slot) {
-    const int ch = (kk * 2 + (lane >> 5)) ^ sw;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) af[slot][i] = lds_a[buf][aoff[i] + ch];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) bf[slot][j] = lds_b[buf][boff[j] + ch];
-  };
-
-  // Pipeline: tile kt is in LDS buffer kt & 1, tile kt + 1 in registers. Right after the
-  // first k16 step of tile kt the registers go to the other LDS buffer and are refilled with
-  // tile kt + 2, so every global load has a whole k-tile of MFMA work to arrive. Operand
-  // fragments for the next k16 step are read while the current one multiplies.
-  const int nk = Kdim / BK;
-  gload(0);
-  lstore(0);
-  if (nk > 1) gload(1);
-  __syncthreads();
-  read_frags(0, 0, 0);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < BK / 16) read_frags(buf, kk + 1, cur ^ 1);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_32x32x16(af[cur][i], bf[cur][j], acc[i][j]);
-      if (kk + 1 < BK / 16) {
-#pragma unroll
-        for (int s = 0; s < TM + TN; ++s) {   // interleave one operand read per MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        }
-      }
-      if (kk == 0) {
-        if (kt + 1 < nk) lstore(buf ^ 1);
-        if (kt + 2 < nk) gload(kt + 2);
-      }
-    }
-    __syncthreads();
-    if (kt + 1 < nk) read_frags(buf ^ 1, 0, 0);
-  }
+  gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, Kdim / BK, acc, lds_a, lds_b);
 
   // Epilogue. acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column
   // (lane & 31) of fragment j.
@@ -215,6 +141,10 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
           if (col < Ndim) {
             const float h = silu(acc[i][0][r]) * acc[i][1][r];
             static_cast<uint16_t*>(p.out)[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(h);
+            if (p.ab) {
+              p.ab[static_cast<size_t>(row) * 2 * Ndim + col] = f32_to_bf16(acc[i][0][r]);
+              p.ab[static_cast<size_t>(row) * 2 * Ndim + Ndim + col] = f32_to_bf16(acc[i][1][r]);
+            }
           }
         } else {
 #pragma unroll
@@ -577,9 +507,10 @@ __global__ __launch_bounds__(256) void f32_down_kernel(const F32Args p) {
 }  // namespace
 
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
-                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks) {
+                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks, uint16_t* ab) {
   const int G = a.E + a.n_shared;
   GemmArgs g;
+  g.ab = ab;
   g.row_tok = pb.row_tok;
   g.offsets = pb.offsets;
   g.tile_off = pb.tile_off;
@@ -597,6 +528,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
 
+  g.ab = nullptr;
   g.a = H;
   g.w = static_cast<const uint16_t*>(a.w_down);
   g.ws = static_cast<const uint16_t*>(a.ws_down);

@@ -1,0 +1,119 @@
+// The 256 x 256 x 64 bf16 MFMA tile pipeline shared by the expert GEMMs (forward, dgrad and
+// wgrad): acc += A_tile * B_tile^T for 256 rows of A and 256 rows of B, both K-contiguous.
+//
+// 512 threads in 8 waves (2 along A rows x 4 along B rows); each wave owns 4 x 2 fragments of
+// v_mfma_f32_32x32x16_bf16 (128 A rows x 64 B rows). Thread tid loads 16-byte chunks of rows
+// (tid >> 3) + 64 i (i < 4) of each operand; LDS slot u = tid + 512 i (row u >> 3, physical
+// chunk u & 7) receives the logical chunk (u & 7) ^ lds_swizzle(row), which keeps the operand
+// reads free of bank conflicts. Pipeline: k-tile kt sits in LDS buffer kt & 1 and tile kt + 1 in
+// registers; right after the first k16 step of tile kt the registers go to the other buffer and
+// are refilled with tile kt + 2, so every global load has a whole k-tile of MFMA work to
+// arrive. Operand fragments of the next k16 step are read while the current one multiplies.
+#pragma once
+
+#include "common.hpp"
+
+namespace maskmoe {
+
+constexpr int kTileM = 256, kTileN = 256, kTileK = 64, kTileThreads = 512;
+constexpr int kTileU = kTileM * 8 / kTileThreads;   // 16-byte units per thread, operand and stage
+constexpr int kTileTM = 4, kTileTN = 2;             // 32x32 fragments per wave
+
+// Row r0 = tid >> 3 of a thread's first unit and its swizzled chunk offset (elements).
+__device__ __forceinline__ int tile_load_row() { return threadIdx.x >> 3; }
+__device__ __forceinline__ int tile_load_chunk() {
+  return ((threadIdx.x & 7) ^ lds_swizzle(threadIdx.x >> 3)) * 8;
+}
+
+// aoffs / boffs: element offsets from abase / bbase of the thread's unit i rows, chunk included
+// (rows r0 + 64 i of the tile); aoff / boff: 16-byte LDS slot offsets of the wave's fragment
+// rows (row * 8). nk: k-tiles of 64; nk <= 0 leaves acc unchanged.
+__device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ abase, const int (&aoffs)[kTileU],
+                                                   const uint16_t* __restrict__ bbase, const int (&boffs)[kTileU],
+                                                   const int (&aoff)[kTileTM], const int (&boff)[kTileTN], int nk,
+                                                   f32x16 (&acc)[kTileTM][kTileTN], u32x4 (*lds_a)[kTileM * 8],
+                                                   u32x4 (*lds_b)[kTileN * 8]) {
+  constexpr int U = kTileU, TM = kTileTM, TN = kTileTN, BK = kTileK, NT = kTileThreads;
+  if (nk <= 0) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int sw = lds_swizzle(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
+  u32x4 ra[U], rb[U];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      ra[i] = *reinterpret_cast<const u32x4*>(abase + (aoffs[i] + kt * BK));
+      rb[i] = *reinterpret_cast<const u32x4*>(bbase + (boffs[i] + kt * BK));
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      lds_a[buf][tid + NT * i] = ra[i];
+      lds_b[buf][tid + NT * i] = rb[i];
+    }
+  };
+  u32x4 af[2][TM], bf[2][TN];
+  auto read_frags = [&](int buf, int kk, int slot) {
+    const int ch = (kk * 2 + (lane >> 5)) ^ sw;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[slot][i] = lds_a[buf][aoff[i] + ch];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bf[slot][j] = lds_b[buf][boff[j] + ch];
+  };
+
+  gload(0);
+  lstore(0);
+  if (nk > 1) gload(1);
+  __syncthreads();
+  read_frags(0, 0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int cur = kk & 1;
+      if (kk + 1 < BK / 16) read_frags(buf, kk + 1, cur ^ 1);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_32x32x16(af[cur][i], bf[cur][j], acc[i][j]);
+      if (kk + 1 < BK / 16) {
+#pragma unroll
+        for (int s = 0; s < TM + TN; ++s) {   // interleave one operand read per MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+      }
+      if (kk == 0) {
+        if (kt + 1 < nk) lstore(buf ^ 1);
+        if (kt + 2 < nk) gload(kt + 2);
+      }
+    }
+    __syncthreads();
+    if (kt + 1 < nk) read_frags(buf ^ 1, 0, 0);
+  }
+}
+
+// XCD-aware tile order: the hardware deals workgroup ids round-robin over the 8 XCDs, so ids
+// are remapped to give each XCD a contiguous range of logical tiles; logical tiles come in
+// groups of 4 column tiles, the column tile varying fastest, so the ~32 workgroups an XCD runs
+// at once cover about 8 row tiles x 4 column tiles and share both operands in its L2.
+// Returns the logical tile id of this workgroup when the first nwg workgroups of the grid are
+// the live ones (nwg = gridDim.x by default).
+__device__ __forceinline__ int xcd_tile_id(int nwg) {
+  const int bid = blockIdx.x;
+  const int xcd = bid & 7, local = bid >> 3, q = nwg >> 3, rem = nwg & 7;
+  return xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
+}
+__device__ __forceinline__ int xcd_tile_id() { return xcd_tile_id(static_cast<int>(gridDim.x)); }
+
+__device__ __forceinline__ void grouped_tile_coords(int lid, int mt_max, int n_tiles, int& mt, int& nt) {
+  constexpr int GN = 4;
+  const int per_group = GN * mt_max;
+  const int first_n = (lid / per_group) * GN;
+  const int gsize = min(n_tiles - first_n, GN);
+  const int within = lid % per_group;
+  nt = first_n + within % gsize;
+  mt = within / gsize;
+}
+
+}  // namespace maskmoe

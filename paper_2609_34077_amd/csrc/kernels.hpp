@@ -64,9 +64,11 @@ inline void record_mark(hipEvent_t* marks, int i, hipStream_t stream) {
   if (marks && marks[i]) (void)hipEventRecord(marks[i], stream);
 }
 
-// bf16, T > kDecodeMaxT: H = SwiGLU(X_g W_gate,up^T) per group; O = H W_down^T; y = combine.
+// bf16, T > kDecodeMaxT (any T when training): H = SwiGLU(X_g W_gate,up^T) per group;
+// O = H W_down^T; y = combine. ab (training): the gate and up pre-activations, bf16 [rows, 2F].
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
-                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks);
+                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks,
+                               uint16_t* ab = nullptr);
 // bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel (split-K into P [split_gu, rows, 2F]
 // plus a SwiGLU pass when decode_split_gate_up() > 1), split-K down projection into
 // O [split, rows, d] with split = decode_split(), then the combine.
@@ -85,6 +87,37 @@ hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float*
 hipError_t launch_cache(int policy, const int32_t* trace, int L, int S, int N, int K, int E, int B,
                         int32_t* state, int32_t* counts, int64_t* fetches, int64_t* hits,
                         uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream);
+
+// ---- expert-side backward (backward.hip)
+constexpr int kMaxGroupsBwd = 256 + 8;
+
+struct BwdLayout {          // byte offsets into the backward workspace
+  size_t w_down_t, w_gate_up_t, dout, dab, dxr, poff, pmap, dout_t, h_t, dab_t, x_t, total;
+  int P;                    // padded token columns (multiple of 64)
+};
+BwdLayout backward_layout(int T, int d, int F, int E, int K, int S);
+
+struct BwdArgs {
+  const uint16_t* x;          // [T, d]
+  const uint16_t* w_gate_up;  // [E, 2F, d]
+  const uint16_t* w_down;     // [E, d, F]
+  const uint16_t* ws_gate_up; // [S, 2F, d]
+  const uint16_t* ws_down;    // [S, d, F]
+  const float* gate;          // [T, K]
+  const uint16_t* dy;         // [T, d]
+  PermBuffers pb;             // the training forward's permutation
+  const uint16_t* h;          // [rows, F] SwiGLU activations of the forward
+  const uint16_t* ab;         // [rows, 2F] gate / up pre-activations of the forward
+  float* d_x;                 // [T, d]
+  float* d_w_gate_up;         // [E, 2F, d]
+  float* d_w_down;            // [E, d, F]
+  float* d_ws_gate_up;        // [S, 2F, d]
+  float* d_ws_down;           // [S, d, F]
+  void* workspace;
+  BwdLayout lay;
+  int T, d, F, E, K, S, max_tiles;
+};
+hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t stream);
 
 // ---- Stage 1 training: mask and router gradients (train.hip)
 constexpr int kMaxKTrain = 16;

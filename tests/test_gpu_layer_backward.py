@@ -1,0 +1,148 @@
+"""GPU parity of maskmoe_layer_backward (the experts' side of the layer backward) against the
+oracle's moe_layer_backward (Eq. 1 and the SwiGLU chain rule, routing held fixed).
+
+Both sides route on their own: tokens whose oracle margin is a near-tie get dy = 0, so they
+contribute to no gradient on either side, and every other token must be routed identically.
+Bound: max |gpu - ref| / max |ref| <= 2e-2 per output (bf16 layers: h, a, b, dO and [da db]
+are bf16-rounded on the GPU side, the oracle rounds nothing).
+
+Small layers are compared in full (ragged token counts, widths that are not multiples of the
+256-wide tile, shared experts, both gate rules). At the full Mixtral-shaped fine-tuning size
+the oracle checks sampled columns: the weight gradients of a sampled set J of FFN columns are
+exactly those of the sub-expert restricted to J (rows J of W_gate and W_up, columns J of
+W_down), and dL/dx of sampled tokens needs only those tokens' rows.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_util as U
+from oracle import routing as R
+from oracle import train as TR
+from paper_2609_34077_amd import _lib as L
+from paper_2609_34077_amd import synth
+
+pytestmark = pytest.mark.gpu
+GRAD_TOL = 2e-2
+
+
+def _run(cfg, dy_seed):
+    inp = synth.make_layer(cfg)
+    dd = {k: U.dev(inp[k]) for k in ("x", "w_router", "w_gate_up", "w_down")}
+    sgu = U.dev(inp["ws_gate_up"]) if cfg.n_shared else None
+    sdn = U.dev(inp["ws_down"]) if cfg.n_shared else None
+    xf = U.f64(inp["x"], "bf16")
+    z = R.router_logits(xf, U.f64(inp["w_router"], "bf16"))
+    idx_o, gate_o, margin_o = R.route_logits(z, cfg.K, R.HARD_MASK, cfg.gate_mode, mask=inp["mask"])
+    near = margin_o <= U.MARGIN_TOL
+    dy = np.random.default_rng(dy_seed).standard_normal((cfg.T, cfg.d)).astype(np.float32)
+    dy[near] = 0.0
+    dyb = synth.bf16_bits(dy)
+    tw = torch.empty(L.load().maskmoe_layer_train_workspace_bytes(
+        L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, cfg.n_shared, L.BF16, L.ROUTE_HARD_MASK, cfg.gate_mode)),
+        dtype=torch.uint8, device="cuda")
+    y, idx, gate, logits, eo = L.maskmoe_layer_forward_train(dd["x"], dd["w_router"], dd["w_gate_up"], dd["w_down"],
+                                                             cfg.K, L.ROUTE_HARD_MASK, cfg.gate_mode,
+                                                             mask=inp["mask"], ws_gate_up=sgu, ws_down=sdn,
+                                                             workspace=tw)
+    out = L.maskmoe_layer_backward(dd["x"], dd["w_gate_up"], dd["w_down"], cfg.K, cfg.gate_mode, gate,
+                                   U.dev(dyb), tw, ws_gate_up=sgu, ws_down=sdn)
+    torch.cuda.synchronize()
+    ig = idx.cpu().numpy()
+    clear = ~near
+    assert np.array_equal(ig[clear], idx_o[clear]), "tokens with a clear margin must route identically"
+    U.say(f"  near-tie tokens (dy = 0): {int(near.sum())} of {cfg.T}")
+    return inp, xf, idx_o, gate_o, U.f64(dyb, "bf16"), out
+
+
+def _close(got, want, what):
+    got = got.cpu().numpy().astype(np.float64) if hasattr(got, "cpu") else got
+    scale = np.abs(want).max()
+    err = np.abs(got - want).max() / max(scale, 1e-30)
+    U.say(f"  {what}: max normalised error {err:.2e}")
+    assert err <= GRAD_TOL, f"{what}: {err}"
+
+
+SMALL = [
+    synth.LayerConfig("bwd_mixtral_like", T=96, d=256, F=512, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
+                      mask_set=(0, 2, 5, 7), seed=41),
+    synth.LayerConfig("bwd_shared_gate_p", T=64, d=256, F=128, E=16, K=4, n_shared=2, route_mode=L.ROUTE_HARD_MASK,
+                      gate_mode=L.GATE_P, mask_set=tuple(range(0, 16, 2)), seed=42),
+    synth.LayerConfig("bwd_tiny", T=5, d=128, F=192, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
+                      mask_set=(1, 3, 4, 6), seed=43),
+    synth.LayerConfig("bwd_ragged", T=300, d=320, F=320, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
+                      mask_set=(0, 1, 2, 3, 4, 5), seed=44),
+]
+
+
+@pytest.mark.parametrize("cfg", SMALL, ids=lambda c: c.name)
+def test_layer_backward_matches_oracle(cfg):
+    U.say(f"layer backward {cfg.name} T={cfg.T} d={cfg.d} F={cfg.F} E={cfg.E} K={cfg.K} shared={cfg.n_shared}")
+    inp, xf, idx_o, gate_o, dyf, out = _run(cfg, dy_seed=cfg.seed)
+    w = lambda a: synth.widen(a, "bf16")
+    ref = TR.moe_layer_backward(xf, idx_o, gate_o, dyf, inp["w_gate_up"], inp["w_down"],
+                                inp["ws_gate_up"] if cfg.n_shared else None,
+                                inp["ws_down"] if cfg.n_shared else None, widen=w)
+    _close(out["d_x"], ref["dx"], "d_x")
+    _close(out["d_w_gate_up"], ref["d_w_gate_up"], "d_w_gate_up")
+    _close(out["d_w_down"], ref["d_w_down"], "d_w_down")
+    if cfg.n_shared:
+        _close(out["d_ws_gate_up"], ref["d_ws_gate_up"], "d_ws_gate_up")
+        _close(out["d_ws_down"], ref["d_ws_down"], "d_ws_down")
+    # experts that no token chose have exactly zero gradient
+    unused = np.setdiff1d(np.arange(cfg.E), np.unique(idx_o))
+    if unused.size:
+        assert torch.count_nonzero(out["d_w_gate_up"][torch.from_numpy(unused).cuda()]) == 0
+
+
+def test_layer_backward_is_deterministic():
+    cfg = SMALL[0]
+    inp = synth.make_layer(cfg)
+    dd = {k: U.dev(inp[k]) for k in ("x", "w_router", "w_gate_up", "w_down")}
+    y, idx, gate, logits, eo = L.maskmoe_layer_forward_train(dd["x"], dd["w_router"], dd["w_gate_up"], dd["w_down"],
+                                                             cfg.K, L.ROUTE_HARD_MASK, cfg.gate_mode,
+                                                             mask=inp["mask"])
+    # the binding allocated the training workspace: run the forward again with an explicit one
+    desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, 0, L.BF16, L.ROUTE_HARD_MASK, cfg.gate_mode)
+    tw = torch.empty(L.load().maskmoe_layer_train_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
+    L.maskmoe_layer_forward_train(dd["x"], dd["w_router"], dd["w_gate_up"], dd["w_down"], cfg.K, L.ROUTE_HARD_MASK,
+                                  cfg.gate_mode, mask=inp["mask"], workspace=tw)
+    dy = U.dev(synth.bf16_bits(np.random.default_rng(1).standard_normal((cfg.T, cfg.d)).astype(np.float32)))
+    a = L.maskmoe_layer_backward(dd["x"], dd["w_gate_up"], dd["w_down"], cfg.K, cfg.gate_mode, gate, dy, tw)
+    b = L.maskmoe_layer_backward(dd["x"], dd["w_gate_up"], dd["w_down"], cfg.K, cfg.gate_mode, gate, dy, tw)
+    torch.cuda.synchronize()
+    for k in ("d_x", "d_w_gate_up", "d_w_down"):
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_layer_backward_full_size_sampled():
+    """Mixtral-shaped fine-tuning layer at full size (8192 tokens, d = 4096, F = 14336)."""
+    cfg = synth.mixtral_ft_config(8192)
+    U.say("layer backward full size: generating inputs")
+    inp, xf, idx_o, gate_o, dyf, out = _run(cfg, dy_seed=7)
+    g = np.random.default_rng(5)
+    J = np.sort(g.choice(cfg.F, 32, replace=False))
+    F = cfg.F
+    w = lambda a: synth.widen(a, "bf16")
+    dwd = out["d_w_down"]
+    dwgu = out["d_w_gate_up"]
+    for e in np.unique(idx_o):
+        rows, slots = np.nonzero(idx_o == e)
+        dout = gate_o[rows, slots][:, None] * dyf[rows]
+        wgu_e = inp["w_gate_up"][e]
+        sub_gu = w(np.concatenate([wgu_e[J], wgu_e[F + J]], axis=0))
+        sub_d = w(inp["w_down"][e][:, J])
+        _, r_gu, r_d = TR.expert_backward(xf[rows], dout, sub_gu, sub_d)
+        jj = torch.from_numpy(J).cuda()
+        _close(dwd[e][:, jj], r_d, f"d_w_down[{e}][:, J]")
+        _close(dwgu[e][jj], r_gu[:len(J)], f"d_w_gate[{e}][J]")
+        _close(dwgu[e][jj + F], r_gu[len(J):], f"d_w_up[{e}][J]")
+    toks = np.sort(g.choice(cfg.T, 12, replace=False))
+    ref_dx = np.zeros((len(toks), cfg.d))
+    for e in np.unique(idx_o[toks]):
+        sel_t, sel_k = np.nonzero(idx_o[toks] == e)
+        dout = gate_o[toks[sel_t], sel_k][:, None] * dyf[toks[sel_t]]
+        gx, _, _ = TR.expert_backward(xf[toks[sel_t]], dout, w(inp["w_gate_up"][e]), w(inp["w_down"][e]))
+        np.add.at(ref_dx, sel_t, gx)
+    _close(out["d_x"][torch.from_numpy(toks).cuda()], ref_dx, "d_x (sampled tokens)")

@@ -100,3 +100,27 @@ def test_forward_train_requires_its_outputs():
         o = list(outs)
         o[miss] = None
         assert lib.maskmoe_layer_forward_train(*base, *o, FAKE, ws, None) == L.E_INVAL
+
+
+def test_layer_backward_rejects_invalid_arguments():
+    lib = L.load()
+    desc = L.make_desc(T=64, d=128, E=8, K=2, F=256, route_mode=L.ROUTE_HARD_MASK)
+    tw = lib.maskmoe_layer_train_workspace_bytes(ctypes.byref(desc))
+    bw = lib.maskmoe_layer_backward_workspace_bytes(ctypes.byref(desc))
+    assert tw > lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc)) and bw > 0
+
+    def call(desc=desc, dy=FAKE, twb=tw, bwb=bw, tws=FAKE, bws=FAKE, dwgu=FAKE):
+        return lib.maskmoe_layer_backward(ctypes.byref(desc), FAKE, FAKE, FAKE, None, None, FAKE, dy, tws, twb, FAKE,
+                                          dwgu, FAKE, None, None, bws, bwb, None)
+    assert call(desc=L.make_desc(T=64, d=128, E=8, K=2, F=256, dtype=L.F32, route_mode=L.ROUTE_HARD_MASK)) \
+        == L.E_UNSUPPORTED
+    assert call(desc=L.make_desc(T=64, d=96, E=8, K=2, F=256, route_mode=L.ROUTE_HARD_MASK)) == L.E_UNSUPPORTED
+    assert call(dy=None) == L.E_INVAL
+    assert call(dwgu=None) == L.E_INVAL
+    assert call(twb=tw - 1) == L.E_WORKSPACE
+    assert call(tws=FAKE + 64) == L.E_WORKSPACE
+    assert call(bwb=bw - 1) == L.E_WORKSPACE
+    assert call(desc=L.make_desc(T=0, d=128, E=8, K=2, F=256, route_mode=L.ROUTE_HARD_MASK)) == L.OK
+    shared = L.make_desc(T=64, d=128, E=8, K=2, F=256, n_shared=1, route_mode=L.ROUTE_HARD_MASK)
+    assert lib.maskmoe_layer_backward(ctypes.byref(shared), FAKE, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, 1 << 30,
+                                      FAKE, FAKE, FAKE, None, None, FAKE, 1 << 30, None) == L.E_INVAL
