@@ -7,12 +7,14 @@ what the masked MoE hot path computes, written from the paper:
   plain rule (Eq. 1), the hard binary mask of training (Eq. 2) and the soft
   prior of inference (Eq. 4), the two gate rules (Section 3.1);
 * ``ffn``      -- the expert FFN (SwiGLU) and the gate-weighted combine with
-  shared experts (Eq. 1 and Section 3.1);
+  shared experts (Eq. 1 and Section 3.1), and the same with the low-rank
+  adapters of Stage 2 (Section 3.2, Appendix B);
 * ``cache``    -- the per-layer expert cache of the trace simulator and the
   hit-rate / fetches-per-token metrics (Section 4.1, Eq. 5);
 * ``train``    -- Stage 1 of the fine-tuning: mask sampling without
   replacement (Eq. 2), the gradients of the gate values with respect to the
-  mask and the router, and the straight-through mask-logit gradient (Eq. 3).
+  mask and the router, the straight-through mask-logit gradient (Eq. 3), and
+  the experts' backward through their SwiGLU.
 
 It shares no code with the HIP path and imports nothing from it. Only the
 tests, the smoke check and the benchmark's CPU-baseline leg may import it;

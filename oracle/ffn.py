@@ -11,6 +11,12 @@ F..2F-1; ``w_down [E, d, F]``. Weights may be passed in their stored form
 together with a ``widen`` callable that returns exact float64 values; the
 oracle widens one expert at a time so that large layers fit in memory.
 Everything is computed in float64 with no intermediate rounding.
+
+Stage 2 (Section 3.2; Section 4 setup and Appendix B) fine-tunes the experts with low-rank
+adapters: every routed expert, and the shared experts, of rank r = 8 and alpha = 16. An
+adapted projection W (out x in) acts as W x + (alpha / r) B (A x) with A [r, in] and
+B [out, r] (``lora_expert_ffn``, ``lora_moe_layer``); the paper does not list the adapted
+projections, and the gate, up and down projections of each expert are taken.
 """
 
 from __future__ import annotations
@@ -69,3 +75,47 @@ def moe_token(x_t, idx_t, gate_t, w_gate_up, w_down, ws_gate_up=None, ws_down=No
     """Output of a single token (the same definition, evaluated one token at a time)."""
     return moe_layer(_f64(x_t)[None, :], np.asarray(idx_t)[None, :], _f64(gate_t)[None, :],
                      w_gate_up, w_down, ws_gate_up, ws_down, widen)[0]
+
+
+def lora_linear(x, w, a, b, scale: float) -> np.ndarray:
+    """x W^T + scale (x A^T) B^T: an adapted projection, rows x [n, in], W [out, in], A [r, in],
+    B [out, r]."""
+    x = _f64(x)
+    return x @ _f64(w).T + scale * ((x @ _f64(a).T) @ _f64(b).T)
+
+
+def lora_expert_ffn(x, w_gate_up, w_down, a_gate_up, b_gate_up, a_down, b_down, scale: float) -> np.ndarray:
+    """SwiGLU expert with adapted gate, up and down projections. Adapter layout: a_gate_up
+    [2r, d] (A_gate rows, then A_up rows), b_gate_up [2F, r] (B_gate rows, then B_up rows),
+    a_down [r, F], b_down [d, r]."""
+    F = w_down.shape[1]
+    r = a_down.shape[0]
+    g = lora_linear(x, w_gate_up[:F], a_gate_up[:r], b_gate_up[:F], scale)
+    u = lora_linear(x, w_gate_up[F:], a_gate_up[r:], b_gate_up[F:], scale)
+    return lora_linear(silu(g) * u, w_down, a_down, b_down, scale)
+
+
+def lora_moe_layer(x, idx, gate, w_gate_up, w_down, lora, ws_gate_up=None, ws_down=None,
+                   widen: Optional[Callable] = None) -> np.ndarray:
+    """Eq. 1 with adapted experts. ``lora`` is a dict: rank, alpha, a_gate_up [E,2r,d],
+    b_gate_up [E,2F,r], a_down [E,r,F], b_down [E,d,r] and, with shared experts,
+    as_gate_up, bs_gate_up, as_down, bs_down [S, ...]."""
+    wd = widen if widen is not None else _f64
+    scale = float(lora["alpha"]) / float(lora["rank"])
+    x = _f64(x)
+    idx = np.asarray(idx)
+    gate = _f64(gate)
+    T, d = x.shape
+    y = np.zeros((T, d), dtype=np.float64)
+    for e in range(w_gate_up.shape[0]):
+        rows, slots = np.nonzero(idx == e)
+        if rows.size == 0:
+            continue
+        out = lora_expert_ffn(x[rows], wd(w_gate_up[e]), wd(w_down[e]), wd(lora["a_gate_up"][e]),
+                              wd(lora["b_gate_up"][e]), wd(lora["a_down"][e]), wd(lora["b_down"][e]), scale)
+        np.add.at(y, rows, gate[rows, slots][:, None] * out)
+    if ws_gate_up is not None:
+        for s_ in range(ws_gate_up.shape[0]):
+            y += lora_expert_ffn(x, wd(ws_gate_up[s_]), wd(ws_down[s_]), wd(lora["as_gate_up"][s_]),
+                                 wd(lora["bs_gate_up"][s_]), wd(lora["as_down"][s_]), wd(lora["bs_down"][s_]), scale)
+    return y
