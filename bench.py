@@ -64,14 +64,20 @@ def parse():
     return ap.parse_args()
 
 
-KERNEL_SOURCES = {"decode": "paper_2609_34077_amd/csrc/experts.hip", "ft": "paper_2609_34077_amd/csrc/experts.hip",
-                  "deepseek": "paper_2609_34077_amd/csrc/experts.hip", "trace": "paper_2609_34077_amd/csrc/route.hip"}
+_EXPERT_SOURCES = ("paper_2609_34077_amd/csrc/experts.hip", "paper_2609_34077_amd/csrc/gemm_tile.hpp",
+                   "paper_2609_34077_amd/csrc/common.hpp")
+KERNEL_SOURCES = {"decode": _EXPERT_SOURCES, "ft": _EXPERT_SOURCES, "deepseek": _EXPERT_SOURCES,
+                  "trace": ("paper_2609_34077_amd/csrc/route.hip", "paper_2609_34077_amd/csrc/common.hpp")}
 
 
-def source_hash(rel: str) -> str:
+def source_hash(rels) -> str:
+    """sha256 (first 16 hex digits) of the listed source files, concatenated in order."""
     import hashlib
-    with open(os.path.join(ROOT, rel), "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for rel in rels:
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def recorded_traffic(workload: str, config_name: str):
@@ -279,7 +285,7 @@ def run_layer(args):
         achieved = gu_flops / gu_s / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": recorded_traffic(args.workload, cfg.name),
-                "kernel": "grouped_gemm_bf16<0> (gate/up + SwiGLU)",
+                "kernel": "grouped_gemm_bf16<0, false> (gate/up + SwiGLU)",
                 "algorithmic_unit": "FLOPs per launch = 2 * T*(K+shared) * 2F * d",
                 "avg_launch_us": round(1e3 * np.mean(gu_ms), 2)}
         tot_flops = sum(w["gu_flops"] + w["dn_flops"] for w in (work[i % len(work)] for i in range(steps)))
@@ -382,6 +388,56 @@ def run_layer_backward(st, args):
             "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4), "flops": flops,
             "computes": "dgrad and wgrad of every selected expert's SwiGLU FFN (dL/dx experts' share, dL/dW_gate_up, "
                         "dL/dW_down), including the weight and activation transposes it runs"}
+
+
+def run_lora_forward(st, args):
+    """Stage 2's layer forward with rank-8 (alpha 16) adapters on every expert projection
+    (maskmoe_layer_forward_lora) on the fine-tuning layer, timed on its own. FLOPs: the plain
+    forward's expert FLOPs plus the adapters' (A then B for gate, up and down)."""
+    import torch
+    from paper_2609_34077_amd import _lib as L
+    from paper_2609_34077_amd import synth
+    cfg = st["cfg"]
+    r = 8
+    lora_np = synth.make_lora(cfg, r, 16.0)
+    lora = dict(rank=r, alpha=16.0)
+    for k in L.LORA_KEYS:
+        if cfg.n_shared or not k.startswith(("as_", "bs_")):
+            lora[k] = torch.from_numpy(np.ascontiguousarray(lora_np[k])).view(torch.bfloat16).cuda()
+    desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, cfg.n_shared, L.BF16, cfg.route_mode, cfg.gate_mode)
+    ws = torch.empty(int(L.load().maskmoe_layer_lora_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
+    run = lambda i: L.maskmoe_layer_forward_lora(st["xs"][i % len(st["xs"])], st["w_router"], st["wgu"][0],
+                                                 st["wdn"][0], cfg.K, cfg.route_mode, cfg.gate_mode, lora,
+                                                 ws_gate_up=st["sgu"], ws_down=st["sdn"], workspace=ws, y=st["y"],
+                                                 topk_idx=st["idx"], topk_gate=st["gate"], **st["mp"])
+    plain = lambda i: L.maskmoe_layer_forward(st["xs"][i % len(st["xs"])], st["w_router"], st["wgu"][0],
+                                              st["wdn"][0], cfg.K, cfg.route_mode, cfg.gate_mode,
+                                              ws_gate_up=st["sgu"], ws_down=st["sdn"], workspace=st["ws"],
+                                              y=st["y"], topk_idx=st["idx"], topk_gate=st["gate"], **st["mp"])
+    steps = max(3, min(10, args.steps if args.steps is not None else 5))
+
+    def timed(fn):
+        fn(0)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for i in range(steps):
+            fn(i)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    plain_ms = timed(plain)
+    ms = timed(run)
+    rows = cfg.T * (cfg.K + cfg.n_shared)
+    flops = 2.0 * rows * (3 * cfg.F * cfg.d + 2 * r * cfg.d + 2 * cfg.F * r + r * cfg.F + cfg.d * r)
+    tf = flops / (ms / 1e3) / 1e12
+    return {"ms": round(ms, 3), "tokens_per_s": round(cfg.T / (ms / 1e3), 1), "rank": r, "alpha": 16.0,
+            "plain_forward_ms": round(plain_ms, 3),
+            "overhead_vs_plain": round(ms / plain_ms - 1.0, 4), "bound": "mfma", "achieved": round(tf, 1),
+            "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4), "flops": flops,
+            "computes": "the whole layer forward (route, permute, adapted gate/up and down GEMMs, combine) with "
+                        "low-rank adapters on every expert projection"}
 
 
 # ----------------------------------------------------------------------------- trace workload
@@ -502,6 +558,7 @@ def main():
         if args.workload == "ft":
             res["stage1_backward"] = run_stage1_backward(st, args)
             res["layer_backward"] = run_layer_backward(st, args)
+            res["lora_forward"] = run_lora_forward(st, args)
         base = None if args.no_cpu_baseline else layer_cpu_baseline(st)
     res["cpu_baseline"] = base
     pr = torch.cuda.get_device_properties(0)

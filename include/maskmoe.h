@@ -258,6 +258,54 @@ int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, c
 size_t maskmoe_layer_train_workspace_bytes(const maskmoe_layer_desc* desc);
 
 /*
+ * maskmoe_lora -- low-rank adapters of every expert (Stage 2 of the fine-tuning, Section 3.2;
+ * rank 8 and alpha 16 in Appendix B, routed and shared experts alike). An adapted projection
+ * W [out, in] computes W v + (alpha / rank) B (A v) with A [rank, in] and B [out, rank].
+ * All matrices are device bf16, row-major, owned by the caller:
+ *  a_gate_up  [E, 2 rank, d]: rows 0..rank-1 A of W_gate, rows rank..2 rank-1 A of W_up
+ *             (16-byte aligned).
+ *  b_gate_up  [E, 2F, rank]: rows 0..F-1 B of W_gate, rows F..2F-1 B of W_up.
+ *  a_down     [E, rank, F] (16-byte aligned).   b_down [E, d, rank].
+ *  as_gate_up, bs_gate_up, as_down, bs_down: the same for the n_shared shared experts
+ *             ([n_shared, ...]); NULL when n_shared == 0.
+ */
+typedef struct maskmoe_lora {
+  int32_t rank;
+  float alpha;
+  const void *a_gate_up, *b_gate_up, *a_down, *b_down;
+  const void *as_gate_up, *bs_gate_up, *as_down, *bs_down;
+} maskmoe_lora;
+
+/*
+ * maskmoe_layer_lora_workspace_bytes -- device workspace that maskmoe_layer_forward_lora needs
+ * for `desc`: that of maskmoe_layer_forward plus the adapters' rank projections of every expert
+ * row ([T (K + n_shared), 64] bf16, twice) and the scaled B matrices ([E + n_shared, 2F + d, 64]
+ * bf16). Returns 0 for an invalid desc.
+ */
+size_t maskmoe_layer_lora_workspace_bytes(const maskmoe_layer_desc* desc);
+
+/*
+ * maskmoe_layer_forward_lora -- maskmoe_layer_forward with adapted experts (Section 3.2,
+ * Stage 2): every routed and shared expert computes
+ *   F(x) = W'_down (SiLU(W'_gate x) * (W'_up x)),  W' v = W v + (alpha / rank) B (A v).
+ * Routing, gating and the combine are those of maskmoe_layer_forward (the router carries no
+ * adapter).
+ *
+ *  lora       host pointer to the adapters; 1 <= rank <= 16, alpha finite.
+ *  Other arguments as maskmoe_layer_forward; bf16 layers only, whatever T (the grouped-GEMM
+ *  path).
+ *  Rounding: A x, A h (fp32 sums) and (alpha / rank) B are rounded to bf16; each adapted
+ *  product is then accumulated with W v in one fp32 sum; the rest as maskmoe_layer_forward.
+ *  Errors: as maskmoe_layer_forward; E_INVAL for a NULL or misaligned adapter, a rank outside
+ *  1..16 or a non-finite alpha; E_UNSUPPORTED for f32 layers or T (K + n_shared) >= 2^25.
+ */
+int maskmoe_layer_forward_lora(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                               const uint8_t* mask, const float* prior, const void* w_gate_up,
+                               const void* w_down, const void* ws_gate_up, const void* ws_down,
+                               const maskmoe_lora* lora, void* y, int32_t* topk_idx, float* topk_gate,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * maskmoe_layer_backward_workspace_bytes -- device workspace of maskmoe_layer_backward for
  * `desc` (transposed weights and activations, dO, [da db], per-row dx). Returns 0 for an
  * invalid desc.

@@ -28,7 +28,8 @@ EXPORTS = ("maskmoe_route", "maskmoe_layer_workspace_bytes", "maskmoe_layer_forw
            "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string",
            "maskmoe_sample_mask", "maskmoe_layer_forward_train", "maskmoe_stage1_backward_workspace_bytes",
            "maskmoe_stage1_backward", "maskmoe_layer_train_workspace_bytes",
-           "maskmoe_layer_backward_workspace_bytes", "maskmoe_layer_backward")
+           "maskmoe_layer_backward_workspace_bytes", "maskmoe_layer_backward", "maskmoe_layer_lora_workspace_bytes",
+           "maskmoe_layer_forward_lora")
 NUM_STAGES = 5
 STAGES = ("route", "permute", "gate_up", "down", "combine")
 
@@ -38,6 +39,14 @@ class LayerDesc(ctypes.Structure):
 
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("T", "d", "E", "K", "F", "n_shared", "dtype", "route_mode", "gate_mode")]
+
+
+class Lora(ctypes.Structure):
+    """``maskmoe_lora``."""
+
+    _fields_ = [("rank", ctypes.c_int32), ("alpha", ctypes.c_float)] + [
+        (n, ctypes.c_void_p) for n in ("a_gate_up", "b_gate_up", "a_down", "b_down",
+                                       "as_gate_up", "bs_gate_up", "as_down", "bs_down")]
 
 
 class MaskMoEError(RuntimeError):
@@ -94,6 +103,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.maskmoe_layer_backward.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
                                            _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.maskmoe_layer_backward.restype = ctypes.c_int
+    lib.maskmoe_layer_lora_workspace_bytes.argtypes = [ctypes.POINTER(LayerDesc)]
+    lib.maskmoe_layer_lora_workspace_bytes.restype = _sz
+    lib.maskmoe_layer_forward_lora.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                               ctypes.POINTER(Lora), _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.maskmoe_layer_forward_lora.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -274,6 +288,47 @@ def maskmoe_layer_forward_train(x, w_router, w_gate_up, w_down, K: int, route_mo
                                            _stream()))
     del keep
     return y, idx, gate, logits, eo
+
+
+LORA_KEYS = ("a_gate_up", "b_gate_up", "a_down", "b_down", "as_gate_up", "bs_gate_up", "as_down", "bs_down")
+
+
+def maskmoe_layer_forward_lora(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int, lora: dict,
+                               mask=None, prior=None, ws_gate_up=None, ws_down=None, workspace=None, y=None,
+                               topk_idx=None, topk_gate=None):
+    """maskmoe_layer_forward with adapted experts. ``lora``: rank, alpha and bf16 device tensors
+    a_gate_up [E,2r,d], b_gate_up [E,2F,r], a_down [E,r,F], b_down [E,d,r] (and as_*/bs_* for
+    the shared experts). ``workspace`` defaults to maskmoe_layer_lora_workspace_bytes bytes."""
+    import torch
+    lib = load()
+    T, d = x.shape
+    E = w_router.shape[0]
+    F = w_gate_up.shape[1] // 2
+    ns = 0 if ws_gate_up is None else ws_gate_up.shape[0]
+    r = int(lora["rank"])
+    shapes = {"a_gate_up": (E, 2 * r, d), "b_gate_up": (E, 2 * F, r), "a_down": (E, r, F), "b_down": (E, d, r),
+              "as_gate_up": (ns, 2 * r, d), "bs_gate_up": (ns, 2 * F, r), "as_down": (ns, r, F),
+              "bs_down": (ns, d, r)}
+    for k in LORA_KEYS:
+        t = lora.get(k)
+        if k.startswith(("as_", "bs_")) and not ns:
+            continue
+        _dev(t, k)
+        if t is None or tuple(t.shape) != shapes[k] or t.dtype != x.dtype or not t.is_contiguous():
+            raise ValueError(f"lora[{k!r}] must be a contiguous {x.dtype} tensor of shape {shapes[k]}")
+    if workspace is None:
+        desc0 = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode)
+        workspace = torch.empty(max(int(lib.maskmoe_layer_lora_workspace_bytes(ctypes.byref(desc0))), 1),
+                                dtype=torch.uint8, device=x.device)
+    desc, workspace, y, keep, head = _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask,
+                                                   prior, ws_gate_up, ws_down, workspace, y, topk_idx, topk_gate)
+    la = Lora(r, float(lora["alpha"]), *[_ptr(lora.get(k)) if (ns or not k.startswith(("as_", "bs_"))) else None
+                                         for k in LORA_KEYS])
+    _check("maskmoe_layer_forward_lora",
+           lib.maskmoe_layer_forward_lora(*head[:9], ctypes.byref(la), *head[9:], _ptr(workspace), workspace.numel(),
+                                          _stream()))
+    del keep
+    return y
 
 
 def maskmoe_sample_mask(mask_logits, uniforms, e_keep: int) -> np.ndarray:

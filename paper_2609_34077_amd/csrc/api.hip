@@ -55,6 +55,8 @@ int check_mask_prior(int mode, int L, int E, int K, const uint8_t* mask, const f
 struct Layout {
   size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, H, P, O, total;
   size_t AB, train_total;   // training (bf16): gate / up pre-activations [rows, 2F] after `total`
+  // adapters (bf16), after `total`: rank projections U, V [rows, 64], scaled B [G, 2F | d, 64]
+  size_t LU, LV, LBGU, LBD, lora_total;
 };
 
 static_assert(maskmoe::kDecodeMaxT <= maskmoe::kRouteOneBlockT,
@@ -97,6 +99,12 @@ Layout layout(const maskmoe_layer_desc& d) {
   w.total = off;
   w.AB = take(d.dtype == MASKMOE_BF16 ? rows * 2 * d.F * 2 : 0);
   w.train_total = off;
+  off = w.total;
+  w.LU = take(rows * 64 * 2);
+  w.LV = take(rows * 64 * 2);
+  w.LBGU = take(G * 2 * d.F * 64 * 2);
+  w.LBD = take(G * d.d * 64 * 2);
+  w.lora_total = off;
   return w;
 }
 
@@ -155,11 +163,17 @@ size_t maskmoe_layer_train_workspace_bytes(const maskmoe_layer_desc* desc) {
   return layout(*desc).train_total;
 }
 
+size_t maskmoe_layer_lora_workspace_bytes(const maskmoe_layer_desc* desc) {
+  if (check_layer_desc(desc) != MASKMOE_OK) return 0;
+  return layout(*desc).lora_total;
+}
+
 static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                               const uint8_t* mask, const float* prior, const void* w_gate_up,
                               const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
                               int32_t* topk_idx, float* topk_gate, float* router_logits, float* expert_out,
-                              void* workspace, size_t workspace_bytes, hipStream_t stream, hipEvent_t* events) {
+                              void* workspace, size_t workspace_bytes, hipStream_t stream, hipEvent_t* events,
+                              const maskmoe_lora* lora = nullptr) {
   int st = check_layer_desc(desc);
   if (st != MASKMOE_OK) return st;
   const maskmoe_layer_desc& d = *desc;
@@ -181,9 +195,21 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   if (d.n_shared > 0 && (!aligned(ws_gate_up, 16) || !aligned(ws_down, 16))) return MASKMOE_E_INVAL;
   if ((topk_idx && !aligned(topk_idx, 4)) || (topk_gate && !aligned(topk_gate, 4))) return MASKMOE_E_INVAL;
   if ((router_logits && !aligned(router_logits, 4)) || (expert_out && !aligned(expert_out, 16))) return MASKMOE_E_INVAL;
+  if (lora) {
+    if (!bf16) return MASKMOE_E_UNSUPPORTED;
+    if (rows64 >= (int64_t{1} << 25)) return MASKMOE_E_UNSUPPORTED;   // U, V rows * 64 in 32 bits
+    if (lora->rank < 1 || lora->rank > maskmoe::kMaxLoraRank || !std::isfinite(lora->alpha)) return MASKMOE_E_INVAL;
+    const void* mats[] = {lora->a_gate_up, lora->b_gate_up, lora->a_down, lora->b_down};
+    const void* smats[] = {lora->as_gate_up, lora->bs_gate_up, lora->as_down, lora->bs_down};
+    for (int i = 0; i < 4; ++i) {
+      const size_t al = i % 2 == 0 ? 16 : 2;   // A rows are read 16 bytes at a time
+      if (!mats[i] || !aligned(mats[i], al)) return MASKMOE_E_INVAL;
+      if (d.n_shared > 0 && (!smats[i] || !aligned(smats[i], al))) return MASKMOE_E_INVAL;
+    }
+  }
   const Layout w = layout(d);
   const bool train = expert_out != nullptr;   // the training forward also keeps what the backward reads
-  const size_t need = train ? w.train_total : w.total;
+  const size_t need = lora ? w.lora_total : train ? w.train_total : w.total;
   if (!workspace || workspace_bytes < need || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
 
   char* ws = static_cast<char*>(workspace);
@@ -202,7 +228,7 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   hipError_t e;
   // Training always takes the grouped-GEMM path, whose gate/up epilogue can keep the
   // pre-activations for the backward.
-  const bool decode = uses_decode_path(d) && !train;
+  const bool decode = uses_decode_path(d) && !train && !lora;
   if (decode) {  // one workgroup routes every token and then permutes them
     e = maskmoe::launch_route_permute(x, w_router, d.T, d.d, d.E, d.K, d.route_mode, d.gate_mode, mask, prior, idx,
                                       gate, router_logits, d.n_shared, maskmoe::kGemmBM, pb, stream);
@@ -240,9 +266,27 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
     const int64_t nonempty = TK < d.E ? TK : d.E;
     const int64_t max_tiles = TK / maskmoe::kGemmBM + nonempty +
                               static_cast<int64_t>(d.n_shared) * ((d.T + maskmoe::kGemmBM - 1) / maskmoe::kGemmBM);
+    maskmoe::LoraArgs la{};
+    if (lora) {
+      la.rank = lora->rank;
+      la.scale = lora->alpha / static_cast<float>(lora->rank);
+      la.a_gate_up = static_cast<const uint16_t*>(lora->a_gate_up);
+      la.b_gate_up = static_cast<const uint16_t*>(lora->b_gate_up);
+      la.a_down = static_cast<const uint16_t*>(lora->a_down);
+      la.b_down = static_cast<const uint16_t*>(lora->b_down);
+      la.as_gate_up = static_cast<const uint16_t*>(lora->as_gate_up);
+      la.bs_gate_up = static_cast<const uint16_t*>(lora->bs_gate_up);
+      la.as_down = static_cast<const uint16_t*>(lora->as_down);
+      la.bs_down = static_cast<const uint16_t*>(lora->bs_down);
+      la.u = reinterpret_cast<uint16_t*>(ws + w.LU);
+      la.v = reinterpret_cast<uint16_t*>(ws + w.LV);
+      la.bp_gate_up = reinterpret_cast<uint16_t*>(ws + w.LBGU);
+      la.bp_down = reinterpret_cast<uint16_t*>(ws + w.LBD);
+    }
     e = maskmoe::launch_experts_bf16(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
                                      reinterpret_cast<float*>(ws + w.O), y, static_cast<int>(max_tiles), stream,
-                                     expert_marks, train ? reinterpret_cast<uint16_t*>(ws + w.AB) : nullptr);
+                                     expert_marks, train ? reinterpret_cast<uint16_t*>(ws + w.AB) : nullptr,
+                                     lora ? &la : nullptr);
   }
   return hip_status(e);
 }
@@ -265,6 +309,17 @@ int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, c
   return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
                             topk_idx, topk_gate, router_logits, expert_out, workspace, workspace_bytes, stream,
                             nullptr);
+}
+
+int maskmoe_layer_forward_lora(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                               const uint8_t* mask, const float* prior, const void* w_gate_up,
+                               const void* w_down, const void* ws_gate_up, const void* ws_down,
+                               const maskmoe_lora* lora, void* y, int32_t* topk_idx, float* topk_gate,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!lora) return MASKMOE_E_INVAL;
+  return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
+                            topk_idx, topk_gate, nullptr, nullptr, workspace, workspace_bytes, stream, nullptr,
+                            lora);
 }
 
 int maskmoe_layer_forward_profiled(const maskmoe_layer_desc* desc, const void* x, const void* w_router,

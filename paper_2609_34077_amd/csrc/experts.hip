@@ -48,6 +48,8 @@ struct GemmArgs {
   const int32_t* tile_off;  // [G+1]
   void* out;                // EPI 0: H bf16 [rows, F]; EPI 1: O f32 [rows, d]
   uint16_t* ab;             // EPI 0, training: gate / up pre-activations bf16 [rows, 2F], or null
+  const uint16_t* lora_u;   // LORA: rank-r projections of this GEMM's A rows, bf16 [rows, 64]
+  const uint16_t* lora_b;   // LORA: (alpha / r) B rows matching the B operand, bf16 [G, N rows, 64]
   int G, E, F, d;
   int mt_max;               // grid bound on row tiles
   int n_tiles;              // column tiles
@@ -62,7 +64,7 @@ __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt
   return lo;
 }
 
-template <int EPI>
+template <int EPI, bool LORA = false>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
   constexpr int WN = 4;                 // waves: 2 along rows x 4 along columns
   constexpr int TM = kTileTM, TN = kTileTN;
@@ -89,6 +91,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   const uint16_t* wg = g < p.E ? p.w + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * Kdim
                                : p.ws + static_cast<size_t>(g - p.E) * (EPI == 0 ? 2 * p.F : p.d) * Kdim;
   int aoffs[U], boffs[U];   // element offsets (< 2^31, checked by the host)
+  int brows[U];             // the units' B rows within the group
 #pragma unroll
   for (int i = 0; i < U; ++i) {
     const int r = r0 + 64 * i;
@@ -101,6 +104,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     } else {
       brow = min(n0 + r, p.d - 1);
     }
+    brows[i] = brow;
     boffs[i] = brow * Kdim + chunk;
   }
 
@@ -122,7 +126,19 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-  gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, Kdim / BK, acc, lds_a, lds_b);
+  if (LORA) {   // the adapters' term as one more k-tile: A' = [U | rows], B' = [s B | W]
+    TileExtra ex;
+    ex.xa = p.lora_u;
+    ex.xb = p.lora_b + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * 64;
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      ex.xaoffs[i] = min(row0 + r0 + 64 * i, row_end - 1) * 64 + chunk;
+      ex.xboffs[i] = brows[i] * 64 + chunk;
+    }
+    gemm_tile_mainloop<true>(p.a, aoffs, wg, boffs, aoff, boff, Kdim / BK, acc, lds_a, lds_b, &ex);
+  } else {
+    gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, Kdim / BK, acc, lds_a, lds_b);
+  }
 
   // Epilogue. acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column
   // (lane & 31) of fragment j.
@@ -507,10 +523,21 @@ __global__ __launch_bounds__(256) void f32_down_kernel(const F32Args p) {
 }  // namespace
 
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
-                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks, uint16_t* ab) {
+                               void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks, uint16_t* ab,
+                               const LoraArgs* lora) {
   const int G = a.E + a.n_shared;
-  GemmArgs g;
+  GemmArgs g{};
   g.ab = ab;
+  hipError_t err;
+  if (lora) {
+    err = launch_lora_pack(*lora, G, a.E, a.F, a.d, stream);
+    if (err != hipSuccess) return err;
+    err = launch_lora_down(static_cast<const uint16_t*>(a.x), pb.row_tok, a.d, lora->a_gate_up,
+                           lora->as_gate_up, 2 * lora->rank, G, a.E, pb, max_tiles, lora->u, stream);
+    if (err != hipSuccess) return err;
+    g.lora_u = lora->u;
+    g.lora_b = lora->bp_gate_up;
+  }
   g.row_tok = pb.row_tok;
   g.offsets = pb.offsets;
   g.tile_off = pb.tile_off;
@@ -523,10 +550,20 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   g.out = H;
   const int nt1 = (a.F + BN / 2 - 1) / (BN / 2);
   g.n_tiles = nt1;
-  hipLaunchKernelGGL(grouped_gemm_bf16<0>, dim3(max_tiles * nt1), dim3(GEMM_THREADS), 0, stream, g);
-  hipError_t err = hipGetLastError();
+  if (lora)
+    hipLaunchKernelGGL((grouped_gemm_bf16<0, true>), dim3(max_tiles * nt1), dim3(GEMM_THREADS), 0, stream, g);
+  else
+    hipLaunchKernelGGL(grouped_gemm_bf16<0>, dim3(max_tiles * nt1), dim3(GEMM_THREADS), 0, stream, g);
+  err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
+  if (lora) {
+    err = launch_lora_down(H, nullptr, a.F, lora->a_down, lora->as_down, lora->rank, G, a.E, pb, max_tiles, lora->v,
+                           stream);
+    if (err != hipSuccess) return err;
+    g.lora_u = lora->v;
+    g.lora_b = lora->bp_down;
+  }
 
   g.ab = nullptr;
   g.a = H;
@@ -535,7 +572,10 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   g.out = O;
   const int nt2 = (a.d + BN - 1) / BN;
   g.n_tiles = nt2;
-  hipLaunchKernelGGL(grouped_gemm_bf16<1>, dim3(max_tiles * nt2), dim3(GEMM_THREADS), 0, stream, g);
+  if (lora)
+    hipLaunchKernelGGL((grouped_gemm_bf16<1, true>), dim3(max_tiles * nt2), dim3(GEMM_THREADS), 0, stream, g);
+  else
+    hipLaunchKernelGGL(grouped_gemm_bf16<1>, dim3(max_tiles * nt2), dim3(GEMM_THREADS), 0, stream, g);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);

@@ -25,24 +25,39 @@ __device__ __forceinline__ int tile_load_chunk() {
   return ((threadIdx.x & 7) ^ lds_swizzle(threadIdx.x >> 3)) * 8;
 }
 
+// One more k-tile ahead of the main operands: its rows of A at xa + xaoffs[i], of B at
+// xb + xboffs[i] (64 elements each, chunk included). The low-rank adapters use it: A' = [U | X],
+// B' = [s B | W] turns W x + s B (A x) into one product. It is the first tile, so only the
+// prologue loads it and the steady-state loop is the same as without it.
+struct TileExtra {
+  const uint16_t* xa;
+  const uint16_t* xb;
+  int xaoffs[kTileU];
+  int xboffs[kTileU];
+};
+
 // aoffs / boffs: element offsets from abase / bbase of the thread's unit i rows, chunk included
 // (rows r0 + 64 i of the tile); aoff / boff: 16-byte LDS slot offsets of the wave's fragment
-// rows (row * 8). nk: k-tiles of 64; nk <= 0 leaves acc unchanged.
+// rows (row * 8). nk: k-tiles of 64 of the main operands (none and no extra tile leaves acc
+// unchanged).
+template <bool EXTRA = false>
 __device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ abase, const int (&aoffs)[kTileU],
                                                    const uint16_t* __restrict__ bbase, const int (&boffs)[kTileU],
                                                    const int (&aoff)[kTileTM], const int (&boff)[kTileTN], int nk,
                                                    f32x16 (&acc)[kTileTM][kTileTN], u32x4 (*lds_a)[kTileM * 8],
-                                                   u32x4 (*lds_b)[kTileN * 8]) {
+                                                   u32x4 (*lds_b)[kTileN * 8], const TileExtra* extra = nullptr) {
   constexpr int U = kTileU, TM = kTileTM, TN = kTileTN, BK = kTileK, NT = kTileThreads;
-  if (nk <= 0) return;
+  constexpr int X = EXTRA ? 1 : 0;   // pipeline tile kt holds main tile kt - X
+  const int ntot = nk + X;
+  if (ntot <= 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int sw = lds_swizzle(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
   u32x4 ra[U], rb[U];
-  auto gload = [&](int kt) {
+  auto gload = [&](int t) {   // main tile t
 #pragma unroll
     for (int i = 0; i < U; ++i) {
-      ra[i] = *reinterpret_cast<const u32x4*>(abase + (aoffs[i] + kt * BK));
-      rb[i] = *reinterpret_cast<const u32x4*>(bbase + (boffs[i] + kt * BK));
+      ra[i] = *reinterpret_cast<const u32x4*>(abase + (aoffs[i] + t * BK));
+      rb[i] = *reinterpret_cast<const u32x4*>(bbase + (boffs[i] + t * BK));
     }
   };
   auto lstore = [&](int buf) {
@@ -61,12 +76,20 @@ __device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ 
     for (int j = 0; j < TN; ++j) bf[slot][j] = lds_b[buf][boff[j] + ch];
   };
 
-  gload(0);
+  if (EXTRA) {
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      ra[i] = *reinterpret_cast<const u32x4*>(extra->xa + extra->xaoffs[i]);
+      rb[i] = *reinterpret_cast<const u32x4*>(extra->xb + extra->xboffs[i]);
+    }
+  } else {
+    gload(0);
+  }
   lstore(0);
-  if (nk > 1) gload(1);
+  if (ntot > 1) gload(1 - X);
   __syncthreads();
   read_frags(0, 0, 0);
-  for (int kt = 0; kt < nk; ++kt) {
+  for (int kt = 0; kt < ntot; ++kt) {
     const int buf = kt & 1;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
@@ -84,12 +107,12 @@ __device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ 
         }
       }
       if (kk == 0) {
-        if (kt + 1 < nk) lstore(buf ^ 1);
-        if (kt + 2 < nk) gload(kt + 2);
+        if (kt + 1 < ntot) lstore(buf ^ 1);
+        if (kt + 2 < ntot) gload(kt + 2 - X);
       }
     }
     __syncthreads();
-    if (kt + 1 < nk) read_frags(buf ^ 1, 0, 0);
+    if (kt + 1 < ntot) read_frags(buf ^ 1, 0, 0);
   }
 }
 

@@ -64,11 +64,31 @@ inline void record_mark(hipEvent_t* marks, int i, hipStream_t stream) {
   if (marks && marks[i]) (void)hipEventRecord(marks[i], stream);
 }
 
-// bf16, T > kDecodeMaxT (any T when training): H = SwiGLU(X_g W_gate,up^T) per group;
-// O = H W_down^T; y = combine. ab (training): the gate and up pre-activations, bf16 [rows, 2F].
+// Low-rank adapters of the experts (lora.hip). rank r <= kMaxLoraRank; adapters bf16:
+// a_gate_up [E, 2r, d], b_gate_up [E, 2F, r], a_down [E, r, F], b_down [E, d, r] and the shared
+// experts' as_* / bs_* [n_shared, ...]; u, v [rows, 64] and bp_gate_up [G, 2F, 64], bp_down
+// [G, d, 64] are workspace.
+constexpr int kMaxLoraRank = 16;
+struct LoraArgs {
+  int rank;
+  float scale;   // alpha / rank
+  const uint16_t *a_gate_up, *b_gate_up, *a_down, *b_down;
+  const uint16_t *as_gate_up, *bs_gate_up, *as_down, *bs_down;
+  uint16_t *u, *v, *bp_gate_up, *bp_down;
+};
+hipError_t launch_lora_pack(const LoraArgs& l, int G, int E, int F, int d, hipStream_t stream);
+// out [rows, 64] = src rows (gathered through row_tok when given) times the rows' group adapter
+// A [nq, K]^T, zero-padded; rows tiled as the permutation (kGemmBM rows per tile).
+hipError_t launch_lora_down(const uint16_t* src, const int32_t* row_tok, int K, const uint16_t* a, const uint16_t* as,
+                            int nq, int G, int E, const PermBuffers& pb, int max_tiles, uint16_t* out,
+                            hipStream_t stream);
+
+// bf16, T > kDecodeMaxT (any T when training or with adapters): H = SwiGLU(X_g W_gate,up^T)
+// per group; O = H W_down^T; y = combine. ab (training): the gate and up pre-activations,
+// bf16 [rows, 2F]. lora: the experts' low-rank adapters, added inside both GEMMs.
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
                                void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks,
-                               uint16_t* ab = nullptr);
+                               uint16_t* ab = nullptr, const LoraArgs* lora = nullptr);
 // bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel (split-K into P [split_gu, rows, 2F]
 // plus a SwiGLU pass when decode_split_gate_up() > 1), split-K down projection into
 // O [split, rows, d] with split = decode_split(), then the combine.

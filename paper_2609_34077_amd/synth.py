@@ -208,6 +208,30 @@ def make_layer(cfg: LayerConfig, with_x: bool = True, threads: Optional[int] = N
     return out
 
 
+def make_lora(cfg: LayerConfig, rank: int = 8, alpha: float = 16.0, b_std: float = 0.05) -> Dict[str, object]:
+    """Seeded low-rank adapters of every expert (rank 8, alpha 16 by default, as in the paper's
+    Stage-2 set-up). A ~ N(0, 1/in) (the scale of the usual uniform initialisation); B, zero at
+    initialisation, stands in for a trained adapter with std ``b_std`` (0.05 gives an adapter
+    term of about a quarter of W x for unit-variance tokens).
+
+    Returns rank, alpha and, in the storage type of ``cfg.dtype``: ``a_gate_up [E,2r,d]`` (the
+    gate adapter's A rows, then the up adapter's), ``b_gate_up [E,2F,r]``, ``a_down [E,r,F]``,
+    ``b_down [E,d,r]`` and ``as_*`` / ``bs_*`` for the ``n_shared`` shared experts.
+    """
+    E, F, d, ns, dt = cfg.E, cfg.F, cfg.d, cfg.n_shared, cfg.dtype
+    seqs = np.random.SeedSequence([cfg.seed, 104729, rank]).spawn(8)
+    out: Dict[str, object] = dict(rank=rank, alpha=alpha)
+    out["a_gate_up"] = _normal(seqs[0], (E, 2 * rank, d), 1.0 / np.sqrt(d), dt)
+    out["b_gate_up"] = _normal(seqs[1], (E, 2 * F, rank), b_std, dt)
+    out["a_down"] = _normal(seqs[2], (E, rank, F), 1.0 / np.sqrt(F), dt)
+    out["b_down"] = _normal(seqs[3], (E, d, rank), b_std, dt)
+    out["as_gate_up"] = _normal(seqs[4], (ns, 2 * rank, d), 1.0 / np.sqrt(d), dt)
+    out["bs_gate_up"] = _normal(seqs[5], (ns, 2 * F, rank), b_std, dt)
+    out["as_down"] = _normal(seqs[6], (ns, rank, F), 1.0 / np.sqrt(F), dt)
+    out["bs_down"] = _normal(seqs[7], (ns, d, rank), b_std, dt)
+    return out
+
+
 def make_tokens(cfg: LayerConfig, T: int, stream: int) -> np.ndarray:
     """Extra token batches x ~ N(0,1) [T,d] from a stream keyed by ``stream`` (>= 1)."""
     seq = np.random.SeedSequence([cfg.seed, 7919, stream])

@@ -118,6 +118,52 @@ def test_profiled_forward_needs_an_event_array():
                                               FAKE, None, None, FAKE, ws, None, None) == L.E_INVAL
 
 
+def _lora_fwd(desc, lora, ws_bytes=1 << 40, **kw):
+    lib = L.load()
+    a = dict(x=FAKE, w=FAKE, wgu=FAKE, wdn=FAKE, sgu=None, sdn=None, y=FAKE, ws=FAKE)
+    a.update(kw)
+    lp = ctypes.byref(lora) if lora is not None else None
+    return lib.maskmoe_layer_forward_lora(ctypes.byref(desc), a["x"], a["w"], None, None, a["wgu"], a["wdn"],
+                                          a["sgu"], a["sdn"], lp, a["y"], None, None, a["ws"], ws_bytes, None)
+
+
+def test_lora_forward_rejects_invalid_arguments():
+    lib = L.load()
+    good = dict(T=32, d=128, E=8, K=2, F=256, n_shared=0, dtype=L.BF16, route_mode=L.ROUTE_PLAIN,
+                gate_mode=L.GATE_RENORM)
+    desc = L.make_desc(**good)
+
+    def lora(rank=8, alpha=16.0, **ptrs):
+        p = dict(a_gate_up=FAKE, b_gate_up=FAKE, a_down=FAKE, b_down=FAKE)
+        p.update(ptrs)
+        return L.Lora(rank, alpha, *[p.get(k) for k in L.LORA_KEYS])
+
+    assert _lora_fwd(desc, None) == L.E_INVAL
+    for bad in (dict(rank=0), dict(rank=17), dict(alpha=float("inf")), dict(alpha=float("nan")),
+                dict(a_down=None), dict(b_gate_up=None), dict(a_gate_up=FAKE + 8)):
+        assert _lora_fwd(desc, lora(**bad)) == L.E_INVAL, bad
+    # shared experts need their adapters too
+    sh = L.make_desc(**{**good, "n_shared": 1})
+    assert _lora_fwd(sh, lora(), sgu=FAKE, sdn=FAKE) == L.E_INVAL
+    assert _lora_fwd(L.make_desc(**{**good, "dtype": L.F32}), lora()) == L.E_UNSUPPORTED
+    need = lib.maskmoe_layer_lora_workspace_bytes(ctypes.byref(desc))
+    assert need > lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+    assert _lora_fwd(desc, lora(), ws_bytes=need - 1) == L.E_WORKSPACE
+    # no tokens: nothing to do, whatever the adapters
+    assert _lora_fwd(L.make_desc(**{**good, "T": 0}), lora(rank=99)) == L.OK
+
+
+def test_lora_workspace_bytes_cover_the_adapter_buffers():
+    lib = L.load()
+    for (T, d, E, K, F, ns) in ((8192, 4096, 8, 2, 14336, 0), (4096, 2048, 64, 6, 1408, 2), (3, 256, 16, 4, 128, 1)):
+        desc = L.make_desc(T, d, E, K, F, ns, L.BF16)
+        base = lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+        rows, G = T * (K + ns), E + ns
+        extra = 2 * rows * 64 * 2 + G * (2 * F + d) * 64 * 2
+        got = lib.maskmoe_layer_lora_workspace_bytes(ctypes.byref(desc))
+        assert extra <= got - base <= extra + 4 * 256 and got % 256 == 0
+
+
 def test_workspace_bytes_monotone_in_tokens():
     lib = L.load()
     for (d, E, K, F, ns, dt) in ((4096, 8, 2, 14336, 0, L.BF16), (2048, 64, 6, 1408, 2, L.BF16),
