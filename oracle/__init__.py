@@ -11,6 +11,9 @@ what the masked MoE hot path computes, written from the paper:
   adapters of Stage 2 (Section 3.2, Appendix B);
 * ``cache``    -- the per-layer expert cache of the trace simulator and the
   hit-rate / fetches-per-token metrics (Section 4.1, Eq. 5);
+* ``offload``  -- a batch-1 offloaded decode of one layer: the experts each
+  step fetches and evicts, and the layer output (Section 1, Section 3.1,
+  Section 4.1);
 * ``train``    -- Stage 1 of the fine-tuning: mask sampling without
   replacement (Eq. 2), the gradients of the gate values with respect to the
   mask and the router, the straight-through mask-logit gradient (Eq. 3), and
@@ -28,4 +31,4 @@ particular prior strengths have no value printed in the paper to compare
 with; they are pinned only through the cache rules above.
 """
 
-from . import cache, ffn, routing, train  # noqa: F401
+from . import cache, ffn, offload, routing, train  # noqa: F401

@@ -49,12 +49,15 @@ def step_set(entries: Iterable[int], E: int) -> Tuple[List[int], bool]:
 
 
 def replay_stream(steps: Sequence[Sequence[int]], E: int, B: int, policy: int = LRU,
-                  state: Optional[Sequence[int]] = None, counts: Optional[Sequence[int]] = None):
+                  state: Optional[Sequence[int]] = None, counts: Optional[Sequence[int]] = None,
+                  trajectory: Optional[list] = None):
     """Replay one (layer, stream) trace through a B-slot cache under ``policy``.
 
     ``cache`` is kept as an ordered list: by last use (LRU, LFU) or by
     insertion (FIFO), oldest first. Returns ``(f, h, final_state,
-    final_counts, bad)``.
+    final_counts, bad)``. When ``trajectory`` is a list, one record per step
+    is appended to it: ``fetched`` (the misses, in insertion order),
+    ``evicted`` (in eviction order) and ``cache`` (the state after the step).
     """
     cache: List[int] = []
     for e in (state or []):
@@ -76,6 +79,7 @@ def replay_stream(steps: Sequence[Sequence[int]], E: int, B: int, policy: int = 
             for e in hits:                      # becomes most recently used
                 cache.remove(e)
                 cache.append(e)
+        evicted: List[int] = []
         for e in misses:
             if len(cache) >= B:
                 candidates = [c for c in cache if c not in A]   # oldest first
@@ -85,9 +89,12 @@ def replay_stream(steps: Sequence[Sequence[int]], E: int, B: int, policy: int = 
                 else:
                     victim = candidates[0]
                 cache.remove(victim)
+                evicted.append(victim)
             cache.append(e)
         h.append(len(hits))
         f.append(len(misses))
+        if trajectory is not None:
+            trajectory.append(dict(fetched=list(misses), evicted=evicted, cache=list(cache)))
     return f, h, cache, freq, bad_any
 
 
