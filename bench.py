@@ -17,6 +17,10 @@ Workloads (--workload):
            top-6, g = p, 4096 tokens (--mode hard|soft).
   trace    routing-and-fetch trace: 32 routers (4096 -> 8) over 256 AR(1) sequences x 512
            steps, then one LRU cache of 4 experts per (layer, sequence).
+  offload  offloaded decode, batch 1: 32 Mixtral-shaped layers whose experts live in pinned
+           host memory, a pool of --slots experts per layer in HBM (LFU by default), one AR(1)
+           token sequence; time per output token with the 4-expert prior of each layer vs the
+           zero prior, and the host-to-pool transfer rate.
 
 Prints one JSON line (rank 0). The roofline entry is for the dominant kernel, timed with
 HIP events recorded around its stage inside the timed region, on the stream the kernels run
@@ -41,6 +45,7 @@ if ROOT not in sys.path:
 
 METRIC = "masked-MoE layer tokens/s (bf16) + % MFMA/HBM roofline; fetches/token exact"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+PCIE_PEAK_GBS = 64.0           # host link, PCIe 5.0 x16, one direction (nominal)
 BF16_PEAK_TFLOPS = 2516.6      # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
 FP32_VALU_PEAK_TFLOPS = 157.3
 
@@ -54,11 +59,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--workload", choices=("decode", "ft", "deepseek", "trace"), default="decode")
+    ap.add_argument("--workload", choices=("decode", "ft", "deepseek", "trace", "offload"), default="decode")
+    ap.add_argument("--slots", type=int, default=4, help="offload: experts cached per layer")
+    ap.add_argument("--policy", choices=("lru", "lfu", "fifo"), default="lfu", help="offload: cache policy")
     ap.add_argument("--batch", type=int, default=16, help="decode tokens per step")
     ap.add_argument("--mode", choices=("hard", "soft"), default="soft", help="deepseek routing mode")
     ap.add_argument("--copies", type=int, default=3, help="decode: weight copies rotated across steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="ft: skip the backward and adapter measurements (counter runs of the forward)")
     ap.add_argument("--calibrate", action="store_true",
                     help="run one plain 512 MiB device copy before timing (reference for counter runs)")
     return ap.parse_args()
@@ -440,6 +449,119 @@ def run_lora_forward(st, args):
                         "low-rank adapters on every expert projection"}
 
 
+# ----------------------------------------------------------------------------- offload workload
+
+def run_offload(args):
+    """Batch-1 decode through 32 Mixtral-shaped layers with host-resident experts.
+
+    Every layer routes the token with its own router and prior (the trace workload's routers,
+    AR(1) hidden states and per-layer 4-expert sets), runs the cache step, copies the fetched
+    experts over PCIe into its pool and computes its output (maskmoe_offload_decode_step). The
+    layers share one pinned host copy of the 8 experts (2.8 GB; where the bytes come from does
+    not change the transfer) and each has its own pool and cache state. Caches start empty and
+    are warmed by --warmup tokens; --steps tokens are timed. The same run with every expert
+    resident in HBM (maskmoe_layer_forward) gives the compute-only time per token.
+    """
+    import torch
+    from paper_2609_34077_amd import _lib as L
+    from paper_2609_34077_amd import synth
+    policy = {"lru": 0, "lfu": 1, "fifo": 2}[args.policy]
+    n_tok = args.steps if args.steps is not None else 32
+    warm = args.warmup if args.warmup is not None else 8
+    B = args.slots
+    tcfg = synth.TraceConfig(L=32, S=1, N=warm + n_tok, d=4096, B=B)
+    lcfg = synth.mixtral_decode_config(1).with_(name="offload_mixtral_32_layers")
+    log("generating inputs (32 routers, AR(1) tokens, 8 experts)")
+    tr = synth.make_trace_inputs(tcfg)
+    inp = synth.make_layer(lcfg, with_x=False)
+    log("pinning the expert copies in host memory")
+    pin = lambda a: torch.from_numpy(np.ascontiguousarray(a)).view(torch.bfloat16).pin_memory()
+    host_gu, host_dn = pin(inp["w_gate_up"]), pin(inp["w_down"])
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).view(torch.bfloat16).cuda()
+    xs, routers = dev(tr["x"]), dev(tr["w_router"])
+    E, K, d, F, NL = lcfg.E, lcfg.K, lcfg.d, lcfg.F, tcfg.L
+    pools = [(torch.empty((B, 2 * F, d), dtype=torch.bfloat16, device="cuda"),
+              torch.empty((B, d, F), dtype=torch.bfloat16, device="cuda")) for _ in range(NL)]
+    desc = L.make_desc(1, d, E, K, F, 0, L.BF16, L.ROUTE_SOFT_PRIOR, lcfg.gate_mode)
+    ws = torch.empty(int(L.load().maskmoe_offload_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
+    y = torch.empty((1, d), dtype=torch.bfloat16, device="cuda")
+    expert_bytes = 3 * d * F * 2
+
+    def decode(priors, counters, states, n0, n1, events=None):
+        for n in range(n0, n1):
+            for l in range(NL):
+                ev = events[(n - n0) * NL + l] if events is not None else None
+                L.maskmoe_offload_decode_step(xs[n:n + 1], routers[l], host_gu, host_dn, pools[l][0], pools[l][1],
+                                              states[l], K, L.ROUTE_SOFT_PRIOR, lcfg.gate_mode, policy,
+                                              prior=priors[l], counters=counters, workspace=ws, y=y, events=ev)
+
+    results = {}
+    for name, priors in (("prior", tr["prior"]), ("zero_prior", tr["prior_zero"])):
+        states = [L.offload_empty_state(E, B) for _ in range(NL)]
+        counters = torch.zeros(2, dtype=torch.int64, device="cuda")
+        log(f"{name}: warming the caches with {warm} tokens")
+        decode(priors, counters, states, 0, warm)
+        torch.cuda.synchronize()
+        warm_fetched = int(counters[0].item())
+        counters.zero_()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n_tok * NL)]
+        for a, b in evs:
+            a.record()
+            b.record()
+        a0, b0 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        log(f"{name}: timing {n_tok} tokens")
+        a0.record()
+        decode(priors, counters, states, warm, warm + n_tok, events=evs)
+        b0.record()
+        torch.cuda.synchronize()
+        ms = a0.elapsed_time(b0)
+        fetch_ms = sum(a.elapsed_time(b) for a, b in evs)
+        fetched, hits = (int(v) for v in counters.cpu().tolist())
+        results[name] = {"tpot_ms": round(ms / n_tok, 3), "fetches_per_token": round(fetched / n_tok, 3),
+                         "hit_rate": round(hits / (n_tok * NL * K), 4), "transfer_ms_per_token": round(fetch_ms / n_tok, 3),
+                         "transfer_GBps": round(fetched * expert_bytes / (fetch_ms / 1e3) / 1e9, 2) if fetched else None,
+                         "avg_transfer_launch_us": round(1e3 * fetch_ms / (n_tok * NL), 2),
+                         "fetched_in_warmup": warm_fetched}
+        log(f"  {results[name]}")
+        del states
+    # compute only: every expert resident (one device copy shared by the layers)
+    wgu, wdn = dev(inp["w_gate_up"]), dev(inp["w_down"])
+    res_step = lambda n: [L.maskmoe_layer_forward(xs[n:n + 1], routers[l], wgu, wdn, K, L.ROUTE_SOFT_PRIOR,
+                                                  lcfg.gate_mode, prior=tr["prior"][l], y=y) for l in range(NL)]
+    for n in range(warm):
+        res_step(n)
+    a0, b0 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a0.record()
+    for n in range(warm, warm + n_tok):
+        res_step(n)
+    b0.record()
+    torch.cuda.synchronize()
+    resident_ms = a0.elapsed_time(b0) / n_tok
+    p, z = results["prior"], results["zero_prior"]
+    gbs = p["transfer_GBps"] or 0.0
+    res = {
+        "metric": "offloaded decode time per output token (32 Mixtral-shaped layers, batch 1)",
+        "value": round(1e3 / p["tpot_ms"], 3), "unit": "tokens/s", "n_gpus": 1, "steps": n_tok, "warmup": warm,
+        "ms_per_step": p["tpot_ms"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "offload_mixtral_32_layers", "layers": NL, "d": d, "F": F, "E": E, "K": K,
+                   "cache_slots": B, "policy": args.policy, "expert_bytes": expert_bytes,
+                   "prior_delta": tcfg.delta, "set_size": tcfg.set_size},
+        "roofline": {"bound": "pcie", "achieved": gbs, "peak": PCIE_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PCIE_PEAK_GBS, 4), "traffic": None, "kernel": "offload_fetch_kernel",
+                     "algorithmic_unit": "bytes per launch = fetched experts x 3 d F x 2",
+                     "avg_launch_us": p["avg_transfer_launch_us"]},
+        "with_prior": p, "zero_prior": z,
+        "tpot_reduction_vs_zero_prior": round(1.0 - p["tpot_ms"] / z["tpot_ms"], 4),
+        "fetch_reduction_vs_zero_prior": round(1.0 - p["fetches_per_token"] / z["fetches_per_token"], 4),
+        "resident_tpot_ms": round(resident_ms, 3),
+    }
+    return res
+
+
 # ----------------------------------------------------------------------------- trace workload
 
 def run_trace(args):
@@ -550,12 +672,14 @@ def main():
     L.load()
     if args.calibrate:
         calibration_copy()
-    if args.workload == "trace":
+    if args.workload == "offload":
+        res, base = run_offload(args), None
+    elif args.workload == "trace":
         res, st = run_trace(args)
         base = None if args.no_cpu_baseline else trace_cpu_baseline(st)
     else:
         res, st = run_layer(args)
-        if args.workload == "ft":
+        if args.workload == "ft" and not args.no_extras:
             res["stage1_backward"] = run_stage1_backward(st, args)
             res["layer_backward"] = run_layer_backward(st, args)
             res["lora_forward"] = run_lora_forward(st, args)

@@ -258,6 +258,56 @@ int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, c
 size_t maskmoe_layer_train_workspace_bytes(const maskmoe_layer_desc* desc);
 
 /*
+ * maskmoe_offload_workspace_bytes -- device workspace of maskmoe_offload_decode_step for `desc`
+ * (that of maskmoe_layer_forward plus the step's fetch list). Returns 0 for an invalid desc.
+ */
+size_t maskmoe_offload_workspace_bytes(const maskmoe_layer_desc* desc);
+
+/*
+ * maskmoe_offload_decode_step -- one decode step of one layer, batch 1, with the routed experts
+ * offloaded to host memory (Section 1 and Section 3.1: a layer keeps B experts in GPU memory and
+ * every selected expert that is not cached is fetched over PCIe; Section 4.1: a full cache
+ * evicts one expert per fetch under LRU, LFU or FIFO, with the rules of maskmoe_cache_fetches).
+ * In stream order and without a host round trip it routes the token (as maskmoe_layer_forward),
+ * applies the cache step to its selected experts, copies each fetched expert's weights from
+ * host memory into its slot of the device pool, and computes y from the pool (Eq. 1; shared
+ * experts stay resident).
+ *
+ *  desc          T = 1, bf16, E <= 64; d and F multiples of 64.
+ *  host_w_gate_up, host_w_down: pinned host memory (hipHostMalloc or an allocator built on it),
+ *                [E, 2F, d] and [E, d, F] bf16, 16-byte aligned; read by a kernel through its
+ *                device mapping, so it must stay allocated until the step has run.
+ *  B             slots of the pool, K <= B <= E.   policy: MASKMOE_CACHE_LRU, _LFU or _FIFO.
+ *  slots_gate_up, slots_down: device [B, 2F, d] and [B, d, F] bf16, the pool.
+ *  cache_state   device int32 [B + 2E], kept by the caller across the steps of a sequence:
+ *                [0, B) the cached experts, least recently used (LRU, LFU) or first inserted
+ *                (FIFO) first, -1 for empty slots (the state layout of maskmoe_cache_fetches);
+ *                [B, B + E) the LFU access counts; [B + E, B + 2E) the pool slot of each expert,
+ *                -1 when it is not cached. An empty cache is -1, 0, -1. A state that is not
+ *                self-consistent (an expert twice or out of range, slots that collide, are out
+ *                of range or belong to an uncached expert) sets *dev_error and is replaced by an
+ *                empty cache before the step.
+ *  y, topk_idx, topk_gate: as maskmoe_layer_forward (T = 1).
+ *  counters      device int64 [2] or NULL: the step's fetches and hits are added to [0] and [1].
+ *  dev_error     device int32 or NULL: set to 1 (never cleared) on an inconsistent state.
+ *  workspace     maskmoe_offload_workspace_bytes(desc) bytes, 256-byte aligned.
+ *  events        NULL, or 2 caller-created HIP events (entries may be NULL) recorded on `stream`
+ *                right before and right after the host-to-pool copy, to time the transfer.
+ *  Rounding: as the few-token path of maskmoe_layer_forward (y is bit-identical to a forward
+ *  with the same experts resident).
+ *  Errors: E_INVAL for NULL or misaligned required pointers, host copies that are not pinned
+ *  host memory, B outside [K, E], an unknown policy, or a bad mask / prior; E_UNSUPPORTED for
+ *  T != 1, f32, E > 64 or d, F not multiples of 64.
+ */
+int maskmoe_offload_decode_step(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                const uint8_t* mask, const float* prior, const void* host_w_gate_up,
+                                const void* host_w_down, const void* ws_gate_up, const void* ws_down, int32_t B,
+                                int32_t policy, void* slots_gate_up, void* slots_down, int32_t* cache_state,
+                                void* y, int32_t* topk_idx, float* topk_gate, int64_t* counters,
+                                int32_t* dev_error, void* workspace, size_t workspace_bytes,
+                                hipEvent_t* events, hipStream_t stream);
+
+/*
  * maskmoe_lora -- low-rank adapters of every expert (Stage 2 of the fine-tuning, Section 3.2;
  * rank 8 and alpha 16 in Appendix B, routed and shared experts alike). An adapted projection
  * W [out, in] computes W v + (alpha / rank) B (A v) with A [rank, in] and B [out, rank].

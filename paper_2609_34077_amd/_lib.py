@@ -29,7 +29,7 @@ EXPORTS = ("maskmoe_route", "maskmoe_layer_workspace_bytes", "maskmoe_layer_forw
            "maskmoe_sample_mask", "maskmoe_layer_forward_train", "maskmoe_stage1_backward_workspace_bytes",
            "maskmoe_stage1_backward", "maskmoe_layer_train_workspace_bytes",
            "maskmoe_layer_backward_workspace_bytes", "maskmoe_layer_backward", "maskmoe_layer_lora_workspace_bytes",
-           "maskmoe_layer_forward_lora")
+           "maskmoe_layer_forward_lora", "maskmoe_offload_workspace_bytes", "maskmoe_offload_decode_step")
 NUM_STAGES = 5
 STAGES = ("route", "permute", "gate_up", "down", "combine")
 
@@ -108,6 +108,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.maskmoe_layer_forward_lora.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                                ctypes.POINTER(Lora), _vp, _vp, _vp, _vp, _sz, _vp]
     lib.maskmoe_layer_forward_lora.restype = ctypes.c_int
+    lib.maskmoe_offload_workspace_bytes.argtypes = [ctypes.POINTER(LayerDesc)]
+    lib.maskmoe_offload_workspace_bytes.restype = _sz
+    lib.maskmoe_offload_decode_step.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                                _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp,
+                                                _vp]
+    lib.maskmoe_offload_decode_step.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -328,6 +334,65 @@ def maskmoe_layer_forward_lora(x, w_router, w_gate_up, w_down, K: int, route_mod
            lib.maskmoe_layer_forward_lora(*head[:9], ctypes.byref(la), *head[9:], _ptr(workspace), workspace.numel(),
                                           _stream()))
     del keep
+    return y
+
+
+def offload_empty_state(E: int, B: int, device="cuda"):
+    """A fresh cache state for maskmoe_offload_decode_step: int32 [B + 2E] = -1 | 0 | -1."""
+    import torch
+    st = torch.full((B + 2 * E,), -1, dtype=torch.int32, device=device)
+    st[B:B + E] = 0
+    return st
+
+
+def maskmoe_offload_decode_step(x, w_router, host_w_gate_up, host_w_down, slots_gate_up, slots_down, cache_state,
+                                K: int, route_mode: int, gate_mode: int, policy: int, mask=None, prior=None,
+                                ws_gate_up=None, ws_down=None, counters=None, dev_error=None, workspace=None,
+                                y=None, topk_idx=None, topk_gate=None, events=None):
+    """One batch-1 decode step of one layer with host-resident experts. x [1,d] (device),
+    host_w_gate_up [E,2F,d] / host_w_down [E,d,F] pinned host tensors, slots_* [B,...] device
+    pool, cache_state int32 [B + 2E] device (see offload_empty_state). ``events``: 2 entries,
+    each None or a torch.cuda.Event, recorded around the host-to-pool copy. Returns y [1,d]."""
+    import torch
+    lib = load()
+    for t, n in ((x, "x"), (w_router, "w_router"), (slots_gate_up, "slots_gate_up"), (slots_down, "slots_down"),
+                 (cache_state, "cache_state"), (ws_gate_up, "ws_gate_up"), (ws_down, "ws_down"),
+                 (counters, "counters"), (dev_error, "dev_error"), (workspace, "workspace"), (y, "y"),
+                 (topk_idx, "topk_idx"), (topk_gate, "topk_gate")):
+        _dev(t, n)
+    for t, n in ((host_w_gate_up, "host_w_gate_up"), (host_w_down, "host_w_down")):
+        if t.is_cuda or not t.is_pinned() or not t.is_contiguous():
+            raise ValueError(f"{n} must be a contiguous pinned host tensor")
+    T, d = x.shape
+    E, F2, d2 = host_w_gate_up.shape
+    F = F2 // 2
+    B = slots_gate_up.shape[0]
+    if (d2 != d or tuple(host_w_down.shape) != (E, d, F) or tuple(slots_gate_up.shape) != (B, 2 * F, d)
+            or tuple(slots_down.shape) != (B, d, F) or tuple(w_router.shape) != (E, d)
+            or tuple(cache_state.shape) != (B + 2 * E,) or cache_state.dtype != torch.int32):
+        raise ValueError("inconsistent offloaded-layer shapes")
+    ns = 0 if ws_gate_up is None else ws_gate_up.shape[0]
+    desc = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode)
+    if workspace is None:
+        workspace = torch.empty(max(int(lib.maskmoe_offload_workspace_bytes(ctypes.byref(desc))), 1),
+                                dtype=torch.uint8, device=x.device)
+    if y is None:
+        y = torch.empty((T, d), dtype=x.dtype, device=x.device)
+    m_arr, m_p = _host_u8(mask, E) if route_mode == ROUTE_HARD_MASK else (None, None)
+    p_arr, p_p = _host_f32(prior, E) if route_mode == ROUTE_SOFT_PRIOR else (None, None)
+    handles = None
+    if events is not None:
+        if len(events) != 2:
+            raise ValueError("events needs 2 entries")
+        handles = (ctypes.c_void_p * 2)(*[None if ev is None else ev.cuda_event for ev in events])
+    _check("maskmoe_offload_decode_step",
+           lib.maskmoe_offload_decode_step(ctypes.byref(desc), _ptr(x), _ptr(w_router), m_p, p_p,
+                                           _ptr(host_w_gate_up), _ptr(host_w_down), _ptr(ws_gate_up),
+                                           _ptr(ws_down), B, policy, _ptr(slots_gate_up), _ptr(slots_down),
+                                           _ptr(cache_state), _ptr(y), _ptr(topk_idx), _ptr(topk_gate),
+                                           _ptr(counters), _ptr(dev_error), _ptr(workspace), workspace.numel(),
+                                           handles, _stream()))
+    del m_arr, p_arr
     return y
 
 

@@ -57,6 +57,8 @@ struct Layout {
   size_t AB, train_total;   // training (bf16): gate / up pre-activations [rows, 2F] after `total`
   // adapters (bf16), after `total`: rank projections U, V [rows, 64], scaled B [G, 2F | d, 64]
   size_t LU, LV, LBGU, LBD, lora_total;
+  // offloaded decode, after `total`: the step's fetch list int32 [1 + 2K]
+  size_t FL, offload_total;
 };
 
 static_assert(maskmoe::kDecodeMaxT <= maskmoe::kRouteOneBlockT,
@@ -105,6 +107,9 @@ Layout layout(const maskmoe_layer_desc& d) {
   w.LBGU = take(G * 2 * d.F * 64 * 2);
   w.LBD = take(G * d.d * 64 * 2);
   w.lora_total = off;
+  off = w.total;
+  w.FL = take((1 + 2 * static_cast<size_t>(d.K)) * 4);
+  w.offload_total = off;
   return w;
 }
 
@@ -494,6 +499,97 @@ int maskmoe_cache_fetches(const int32_t* trace, int32_t L, int32_t S, int32_t N,
   return hip_status(maskmoe::launch_cache(policy, trace, L, S, N, K, E, B, state,
                                           policy == MASKMOE_CACHE_LFU ? counts : nullptr, fetches, hits,
                                           f_per_step, dev_error, stream));
+}
+
+size_t maskmoe_offload_workspace_bytes(const maskmoe_layer_desc* desc) {
+  if (check_layer_desc(desc) != MASKMOE_OK) return 0;
+  return layout(*desc).offload_total;
+}
+
+// Device-side address of pinned host memory; null when p is not pinned host memory.
+static const void* host_device_address(const void* p) {
+  hipPointerAttribute_t attr;
+  if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+    (void)hipGetLastError();   // clear the error this query leaves for unknown pointers
+    return nullptr;
+  }
+  if (attr.type != hipMemoryTypeHost) return nullptr;
+  return attr.devicePointer;
+}
+
+int maskmoe_offload_decode_step(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                const uint8_t* mask, const float* prior, const void* host_w_gate_up,
+                                const void* host_w_down, const void* ws_gate_up, const void* ws_down, int32_t B,
+                                int32_t policy, void* slots_gate_up, void* slots_down, int32_t* cache_state,
+                                void* y, int32_t* topk_idx, float* topk_gate, int64_t* counters,
+                                int32_t* dev_error, void* workspace, size_t workspace_bytes, hipEvent_t* events,
+                                hipStream_t stream) {
+  int st = check_layer_desc(desc);
+  if (st != MASKMOE_OK) return st;
+  const maskmoe_layer_desc& d = *desc;
+  st = check_mask_prior(d.route_mode, 1, d.E, d.K, mask, prior);
+  if (st != MASKMOE_OK) return st;
+  if (policy != MASKMOE_CACHE_LRU && policy != MASKMOE_CACHE_LFU && policy != MASKMOE_CACHE_FIFO)
+    return MASKMOE_E_INVAL;
+  if (B < d.K || B > d.E) return MASKMOE_E_INVAL;
+  if (d.T != 1 || d.dtype != MASKMOE_BF16 || d.E > maskmoe::kOffloadMaxE) return MASKMOE_E_UNSUPPORTED;
+  if (d.d % 64 != 0 || d.F % 64 != 0 || int64_t{2} * d.F * d.d >= (int64_t{1} << 31)) return MASKMOE_E_UNSUPPORTED;
+  if (!x || !w_router || !host_w_gate_up || !host_w_down || !slots_gate_up || !slots_down || !cache_state || !y)
+    return MASKMOE_E_INVAL;
+  if (d.n_shared > 0 && (!ws_gate_up || !ws_down)) return MASKMOE_E_INVAL;
+  const void* p16[] = {x, w_router, host_w_gate_up, host_w_down, slots_gate_up, slots_down, y};
+  for (const void* p : p16)
+    if (!aligned(p, 16)) return MASKMOE_E_INVAL;
+  if (d.n_shared > 0 && (!aligned(ws_gate_up, 16) || !aligned(ws_down, 16))) return MASKMOE_E_INVAL;
+  if (!aligned(cache_state, 4) || (topk_idx && !aligned(topk_idx, 4)) || (topk_gate && !aligned(topk_gate, 4)) ||
+      (counters && !aligned(counters, 8)) || (dev_error && !aligned(dev_error, 4)))
+    return MASKMOE_E_INVAL;
+  // the expert copies must be pinned host memory, which the fetch kernel reads through its
+  // device mapping
+  const void* host_gu = host_device_address(host_w_gate_up);
+  const void* host_dn = host_device_address(host_w_down);
+  if (!host_gu || !host_dn) return MASKMOE_E_INVAL;
+  const Layout w = layout(d);
+  if (!workspace || workspace_bytes < w.offload_total || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  int32_t* idx = topk_idx ? topk_idx : reinterpret_cast<int32_t*>(ws + w.idx);
+  float* gate = topk_gate ? topk_gate : reinterpret_cast<float*>(ws + w.gate);
+  PermBuffers pb;
+  pb.offsets = reinterpret_cast<int32_t*>(ws + w.offsets);
+  pb.tile_off = reinterpret_cast<int32_t*>(ws + w.tile_off);
+  pb.active = reinterpret_cast<int32_t*>(ws + w.active);
+  pb.n_active = reinterpret_cast<int32_t*>(ws + w.n_active);
+  pb.perm = reinterpret_cast<int32_t*>(ws + w.perm);
+  pb.inv = reinterpret_cast<int32_t*>(ws + w.inv);
+  pb.row_tok = reinterpret_cast<int32_t*>(ws + w.row_tok);
+  int32_t* fetch = reinterpret_cast<int32_t*>(ws + w.FL);
+
+  hipError_t e = maskmoe::launch_route_permute(x, w_router, d.T, d.d, d.E, d.K, d.route_mode, d.gate_mode, mask,
+                                               prior, idx, gate, nullptr, d.n_shared, maskmoe::kGemmBM, pb, stream);
+  if (e != hipSuccess) return MASKMOE_E_HIP;
+  e = maskmoe::launch_offload_cache(policy, idx, d.E, d.K, B, cache_state, fetch, counters, dev_error, stream);
+  if (e != hipSuccess) return MASKMOE_E_HIP;
+  maskmoe::record_mark(events, 0, stream);
+  e = maskmoe::launch_offload_fetch(fetch, d.K, d.E, B, d.d, d.F, host_gu, host_dn, slots_gate_up, slots_down,
+                                    stream);
+  if (e != hipSuccess) return MASKMOE_E_HIP;
+  maskmoe::record_mark(events, 1, stream);
+  maskmoe::ExpertArgs a;
+  a.x = x;
+  a.w_gate_up = slots_gate_up;
+  a.w_down = slots_down;
+  a.ws_gate_up = ws_gate_up;
+  a.ws_down = ws_down;
+  a.gate = gate;
+  a.expert_out = nullptr;
+  a.slot_of = cache_state + B + d.E;
+  a.n_slots = B;
+  a.T = d.T; a.d = d.d; a.F = d.F; a.E = d.E; a.K = d.K; a.n_shared = d.n_shared;
+  e = maskmoe::launch_experts_bf16_decode(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
+                                          reinterpret_cast<float*>(ws + w.P), reinterpret_cast<float*>(ws + w.O), y,
+                                          stream, nullptr);
+  return hip_status(e);
 }
 
 }  // extern "C"

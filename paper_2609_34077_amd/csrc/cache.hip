@@ -19,6 +19,7 @@
 
 #include <limits.h>
 
+#include "cache_step.hpp"
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -95,44 +96,8 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_kernel(
       // the step's set, read back as a wave-uniform (scalar) value
       const uint64_t sel = (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readlane(sel_hi, j))) << 32) |
                            static_cast<uint32_t>(__builtin_amdgcn_readlane(sel_lo, j));
-      const bool mine = (sel >> lane) & 1ull;
-      if (POLICY == 1 && mine) ++count;
-      const uint64_t cmask = __ballot(cached);
-      const uint64_t hitm = sel & cmask;
-      uint64_t missm = sel & ~cmask;
-      const int h = __popcll(hitm), f = __popcll(missm);
-      if (POLICY != 2) {  // a hit becomes the most recently used
-        if ((hitm >> lane) & 1ull) stamp = clock + __popcll(hitm & lanemask_lt(lane));
-        clock += h;
-      }
-      while (missm) {
-        const int e = __ffsll(static_cast<unsigned long long>(missm)) - 1;
-        missm &= missm - 1;
-        if (ncached >= B) {
-          const bool eligible = cached && !mine;
-          int key;
-          if (POLICY == 1) {  // lowest count first, then oldest stamp
-            const int low = wave_min_int(eligible ? count : INT_MAX);
-            key = (eligible && count == low) ? stamp : INT_MAX;
-          } else {
-            key = eligible ? stamp : INT_MAX;
-          }
-          const int mn = wave_min_int(key);
-          const uint64_t vm = __ballot(eligible && key == mn);
-          const int victim = __ffsll(static_cast<unsigned long long>(vm)) - 1;
-          if (lane == victim) {
-            cached = false;
-            stamp = INT_MAX;
-          }
-          --ncached;
-        }
-        if (lane == e) {
-          cached = true;
-          stamp = clock;
-        }
-        ++clock;
-        ++ncached;
-      }
+      const int h = cache_step<POLICY>(sel, B, lane, cached, stamp, count, ncached, clock, [](int, int) {});
+      const int f = __popcll(sel) - h;
       tot_h += h;
       tot_f += f;
       if (lane == j) my_f = f;
@@ -147,12 +112,7 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_kernel(
   }
   if (POLICY == 1 && counts && lane < E) counts[stream * E + lane] = count;
   if (state) {
-    // rank of each cached expert by stamp = its slot, oldest first
-    int rank = 0;
-    for (int o = 0; o < 64; ++o) {
-      const int so = __shfl(cached ? stamp : INT_MAX, o, kWave);
-      if (cached && so < stamp) ++rank;
-    }
+    const int rank = cache_rank(cached, stamp);   // its position, oldest first
     int32_t* st = state + stream * B;
     const int nc = __popcll(__ballot(cached));
     for (int s = lane; s < B; s += 64)

@@ -279,8 +279,15 @@ struct DecodeArgs {
   uint16_t* H;        // [rows, F] bf16
   float* P;           // [split_gu, rows, 2F] fp32 partial gate/up sums (split_gu > 1)
   float* O;           // [split, rows, d] fp32
-  int T, d, F, E, K, rows, split, split_gu;
+  const int32_t* slot_of;   // routed expert -> weight block (offloaded decode), or null
+  int T, d, F, E, K, rows, split, split_gu, n_slots;
 };
+
+// Weight block of routed expert g: g itself, or its slot in the pool of an offloaded decode
+// (clamped into the pool, which the cache step guarantees anyway).
+__device__ __forceinline__ int weight_block(const DecodeArgs& p, int g) {
+  return p.slot_of ? min(max(p.slot_of[g], 0), p.n_slots - 1) : g;
+}
 
 // Streams R = 16 * NTILE weight rows (row r starts at wrow(r)) over k in [k0, k0 + klen) and
 // accumulates tile (wave + 4q) of A(16 x k) * W^T into acc[q]. A row (lane & 15) is `arow`.
@@ -355,7 +362,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const Decod
   const int nrows = p.offsets[g + 1] - row0;   // 1..16
   const int n0 = blockIdx.x * 16 * DEC_NT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const uint16_t* wg = g < p.E ? p.w_gate_up + static_cast<size_t>(g) * 2 * p.F * p.d
+  const uint16_t* wg = g < p.E ? p.w_gate_up + static_cast<size_t>(weight_block(p, g)) * 2 * p.F * p.d
                                : p.ws_gate_up + static_cast<size_t>(g - p.E) * 2 * p.F * p.d;
   const int F = p.F, d = p.d;
   auto wrow = [=](int r) {  // rows 0..16*DEC_NT-1: W_gate, then the matching W_up rows
@@ -447,7 +454,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeAr
   const int z = blockIdx.z;
   const int klen = p.F / p.split;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint16_t* wd = g < p.E ? p.w_down + static_cast<size_t>(g) * p.d * p.F
+  const uint16_t* wd = g < p.E ? p.w_down + static_cast<size_t>(weight_block(p, g)) * p.d * p.F
                                : p.ws_down + static_cast<size_t>(g - p.E) * p.d * p.F;
   const int F = p.F;
   auto wrow = [=](int r) { return wd + static_cast<size_t>(n0 + r) * F; };
@@ -647,6 +654,8 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
   p.H = H;
   p.P = P;
   p.O = O;
+  p.slot_of = a.slot_of;
+  p.n_slots = a.n_slots;
   p.T = a.T; p.d = a.d; p.F = a.F; p.E = a.E; p.K = a.K;
   p.rows = a.T * (a.K + a.n_shared);
   p.split = decode_split(a.T, a.d, a.F, a.E, a.K, a.n_shared);

@@ -54,6 +54,8 @@ struct ExpertArgs {
   const void* ws_down;     // [n_shared, d, F]
   const float* gate;       // [T, K]
   float* expert_out;       // [T, K, d] fp32 output of each selected expert before gating, or null
+  const int32_t* slot_of = nullptr;   // few-token path: routed expert -> block of w_gate_up / w_down
+  int n_slots = 0;                    // blocks in w_gate_up / w_down when slot_of is given
   int T, d, F, E, K, n_shared;
 };
 
@@ -63,6 +65,18 @@ struct ExpertArgs {
 inline void record_mark(hipEvent_t* marks, int i, hipStream_t stream) {
   if (marks && marks[i]) (void)hipEventRecord(marks[i], stream);
 }
+
+// Offloaded decode, batch 1 (offload.hip). state: int32 [B + 2E] (cached experts oldest first,
+// LFU counts, slot of each expert); fetch: int32 [1 + 2K] workspace (count, experts, slots);
+// counters: int64 [2] (fetches, hits) accumulated, or null. E <= 64, K <= B <= E.
+constexpr int kOffloadMaxE = 64;
+constexpr int kOffloadFetchBlocks = 512;   // workgroups per fetched expert
+hipError_t launch_offload_cache(int policy, const int32_t* idx, int E, int K, int B, int32_t* state, int32_t* fetch,
+                                int64_t* counters, int32_t* dev_error, hipStream_t stream);
+// host_gu / host_dn: device-side addresses of the pinned host copies [E, 2F, d] and [E, d, F];
+// slots_gu / slots_dn: the device pool [B, 2F, d] and [B, d, F].
+hipError_t launch_offload_fetch(const int32_t* fetch, int K, int E, int B, int d, int F, const void* host_gu,
+                                const void* host_dn, void* slots_gu, void* slots_dn, hipStream_t stream);
 
 // Low-rank adapters of the experts (lora.hip). rank r <= kMaxLoraRank; adapters bf16:
 // a_gate_up [E, 2r, d], b_gate_up [E, 2F, r], a_down [E, r, F], b_down [E, d, r] and the shared

@@ -164,6 +164,35 @@ def test_lora_workspace_bytes_cover_the_adapter_buffers():
         assert extra <= got - base <= extra + 4 * 256 and got % 256 == 0
 
 
+def _offload(desc, B=4, policy=0, host=FAKE, ws_bytes=1 << 40, **kw):
+    lib = L.load()
+    a = dict(x=FAKE, w=FAKE, sgu=None, sdn=None, slots=FAKE, state=FAKE, y=FAKE, ws=FAKE)
+    a.update(kw)
+    return lib.maskmoe_offload_decode_step(ctypes.byref(desc), a["x"], a["w"], None, None, host, host, a["sgu"],
+                                           a["sdn"], B, policy, a["slots"], a["slots"], a["state"], a["y"], None,
+                                           None, None, None, a["ws"], ws_bytes, None, None)
+
+
+def test_offload_step_rejects_invalid_arguments():
+    lib = L.load()
+    good = dict(T=1, d=128, E=8, K=2, F=256, n_shared=0, dtype=L.BF16, route_mode=L.ROUTE_PLAIN,
+                gate_mode=L.GATE_RENORM)
+    desc = L.make_desc(**good)
+    assert _offload(L.make_desc(**{**good, "T": 2})) == L.E_UNSUPPORTED
+    assert _offload(L.make_desc(**{**good, "dtype": L.F32})) == L.E_UNSUPPORTED
+    assert _offload(L.make_desc(**{**good, "E": 65, "K": 2}), B=4) == L.E_UNSUPPORTED
+    assert _offload(L.make_desc(**{**good, "d": 96})) == L.E_UNSUPPORTED
+    assert _offload(desc, B=1) == L.E_INVAL           # B < K
+    assert _offload(desc, B=9) == L.E_INVAL           # B > E
+    assert _offload(desc, policy=3) == L.E_INVAL
+    assert _offload(desc, state=None) == L.E_INVAL
+    assert _offload(desc, slots=FAKE + 8) == L.E_INVAL
+    assert _offload(desc, host=FAKE) == L.E_INVAL     # not pinned host memory
+    assert _offload(L.make_desc(**{**good, "n_shared": 1})) == L.E_INVAL
+    need = lib.maskmoe_offload_workspace_bytes(ctypes.byref(desc))
+    assert need > lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc))
+
+
 def test_workspace_bytes_monotone_in_tokens():
     lib = L.load()
     for (d, E, K, F, ns, dt) in ((4096, 8, 2, 14336, 0, L.BF16), (2048, 64, 6, 1408, 2, L.BF16),
