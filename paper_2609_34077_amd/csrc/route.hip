@@ -19,6 +19,7 @@
 // both operands through LDS.
 // The selection runs one thread per (token, layer) on the fp32 logits in LDS.
 
+#include <limits.h>
 #include <math.h>
 
 #include "common.hpp"
@@ -131,6 +132,100 @@ __device__ void route_finalize(const RouteParams& p, const float* logits, int ld
   }
 }
 
+// The same selection and gates for the single-workgroup launch (one layer, tokens 0..T-1), one
+// wavefront per token: lane e holds the keys of experts e, e + 64, ...; each of the K + 1 picks
+// is a wave reduction (largest key, then lowest index), and the softmax normaliser is summed in
+// expert order (selection order for the renormalised rule), as in route_finalize, so both give
+// the same bits. The selections are also left in sel_lds [T, K] for the permutation.
+__device__ void route_finalize_wave(const RouteParams& p, const float* logits, int ld, const float* lo, int TT,
+                                    int32_t* sel_lds) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  const int E = p.E, K = p.K;
+  constexpr int Q = 4;   // experts per lane, E <= 256
+  for (int t = wave; t < TT && t < p.T; t += nwaves) {
+    const float* z = logits + t * ld;
+    float key[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int e = lane + 64 * q;
+      key[q] = e < E ? z[e] + lo[e] : -INFINITY;
+    }
+    uint32_t taken = 0;   // bit q: expert lane + 64 q is selected
+    int my_sel = 0;
+    float my_selz = 0.0f, kth = -INFINITY, nxt = -INFINITY;
+    for (int j = 0; j <= K; ++j) {
+      float bv = -INFINITY;
+      int bi = -1;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int e = lane + 64 * q;
+        if (e < E && !((taken >> q) & 1u) && key[q] > bv) {
+          bv = key[q];
+          bi = e;
+        }
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const float ov = __shfl_xor(bv, m, kWave);
+        const int oi = __shfl_xor(bi, m, kWave);
+        if (oi >= 0 && (bi < 0 || ov > bv || (ov == bv && oi < bi))) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if (j < K) {
+        if (bi < 0) {   // only reachable with non-finite logits: the lowest expert not taken
+          int lowest = INT_MAX;
+#pragma unroll
+          for (int q = 0; q < Q; ++q) {
+            const int e = lane + 64 * q;
+            if (e < E && !((taken >> q) & 1u)) lowest = min(lowest, e);
+          }
+          bi = wave_min_int(lowest);
+        }
+        if (lane == (bi & 63)) taken |= 1u << (bi >> 6);
+        const float zb = z[bi];
+        if (lane == j) {
+          my_sel = bi;
+          my_selz = zb;
+        }
+        kth = bv;
+      } else {
+        nxt = bv;
+      }
+    }
+    float zref, norm = 0.0f;
+    if (p.gate_mode == 0) {   // g = p_i: softmax over all E experts
+      float m = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        if (lane + 64 * q < E) m = fmaxf(m, z[lane + 64 * q]);
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+      zref = m;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const float ex = lane + 64 * q < E ? expf(z[lane + 64 * q] - zref) : 0.0f;
+        const int n_q = min(64, E - 64 * q);
+        for (int l = 0; l < n_q; ++l) norm += __shfl(ex, l, kWave);   // expert order
+      }
+    } else {   // g = p_i / sum_{j in A} p_j, in selection order
+      zref = __shfl(my_selz, 0, kWave);
+      for (int j = 1; j < K; ++j) zref = fmaxf(zref, __shfl(my_selz, j, kWave));
+      for (int j = 0; j < K; ++j) norm += expf(__shfl(my_selz, j, kWave) - zref);
+    }
+    const float inv = 1.0f / norm;
+    if (lane < K) {
+      p.idx[static_cast<size_t>(t) * K + lane] = my_sel;
+      p.gate[static_cast<size_t>(t) * K + lane] = expf(my_selz - zref) * inv;
+      sel_lds[t * K + lane] = my_sel;
+    }
+    if (lane == 0 && p.margin) p.margin[t] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+    if (p.logits)
+      for (int e = lane; e < E; e += 64) p.logits[static_cast<size_t>(t) * E + e] = z[e];
+  }
+}
+
 // FUSE: the grid is one workgroup holding every token of one layer; after the selection it
 // also groups the (token, slot) pairs by expert (permute_block).
 template <int MB, int NB, int WN, int WK, bool FUSE>
@@ -221,11 +316,14 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
     }
     __syncthreads();
   }
-  route_finalize(p, red, NO, lo, t0, TT, lg0, nl);
   if (FUSE) {
     __shared__ PermLds plds;
-    __syncthreads();   // the selections written above are read back by other threads
-    permute_block(p.idx, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb, plds);
+    __shared__ int32_t sel_lds[kRouteOneBlockT * kMaxK];
+    route_finalize_wave(p, red, NO, lo, TT, sel_lds);
+    __syncthreads();   // the selections written above are read by other threads
+    permute_block(sel_lds, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb, plds);
+  } else {
+    route_finalize(p, red, NO, lo, t0, TT, lg0, nl);
   }
 }
 
