@@ -626,7 +626,7 @@ def run_trace(args):
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
                      "traffic": recorded_traffic("trace", "routing_fetch_trace"),
-                     "kernel": "route_bf16_kernel<2,4,4,1>",
+                     "kernel": "route_gemm_kernel",
                      "algorithmic_unit": "FLOPs per launch = 2 * S*N * L*E * d",
                      "hbm_frac_of_x_read": round(x_bytes / (route_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                      "avg_launch_us": round(1e3 * route_ms, 2)},

@@ -53,7 +53,7 @@ int check_mask_prior(int mode, int L, int E, int K, const uint8_t* mask, const f
 }
 
 struct Layout {
-  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, H, P, O, total;
+  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, pcount, H, P, O, total;
   size_t AB, train_total;   // training (bf16): gate / up pre-activations [rows, 2F] after `total`
   // adapters (bf16), after `total`: rank projections U, V [rows, 64], scaled B [G, 2F | d, 64]
   size_t LU, LV, LBGU, LBD, lora_total;
@@ -89,6 +89,7 @@ Layout layout(const maskmoe_layer_desc& d) {
   w.perm = take(TK * 4);
   w.inv = take(TK * 4);
   w.row_tok = take(rows * 4);
+  w.pcount = take(static_cast<size_t>(maskmoe::permute_chunks(d.T, d.K)) * d.E * 4);
   w.H = take(rows * d.F * hsz);
   // O holds the expert outputs: [rows, d], or [split, rows, d] on the few-token path; P the
   // few-token partial gate/up sums [split_gu, rows, 2F]. Both are sized for the largest
@@ -244,7 +245,8 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
                               idx, gate, nullptr, router_logits, stream);
     if (e != hipSuccess) return MASKMOE_E_HIP;
     maskmoe::record_mark(events, 1, stream);
-    e = maskmoe::launch_permute(idx, d.T, d.K, d.E, d.n_shared, maskmoe::kGemmBM, pb, stream);
+    e = maskmoe::launch_permute(idx, d.T, d.K, d.E, d.n_shared, maskmoe::kGemmBM, pb,
+                                reinterpret_cast<int32_t*>(ws + w.pcount), stream);
     if (e != hipSuccess) return MASKMOE_E_HIP;
   }
   maskmoe::record_mark(events, 2, stream);

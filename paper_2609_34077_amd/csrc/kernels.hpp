@@ -38,8 +38,14 @@ hipError_t launch_route_permute(const void* x, const void* w_router, int T, int 
                                 float* gate, float* logits, int n_shared, int tile_rows, const PermBuffers& pb,
                                 hipStream_t stream);
 
+// Many tokens: the same grouping over chunks of kPermChunk entries; chunk_counts is workspace
+// int32 [permute_chunks(T, K), E].
+constexpr int kPermChunk = 1024;
+inline int permute_chunks(int T, int K) {
+  return static_cast<int>((static_cast<int64_t>(T) * K + kPermChunk - 1) / kPermChunk);
+}
 hipError_t launch_permute(const int32_t* idx, int T, int K, int E, int n_shared, int tile_rows,
-                          const PermBuffers& pb, hipStream_t stream);
+                          const PermBuffers& pb, int32_t* chunk_counts, hipStream_t stream);
 
 // Row-tile size of the bf16 grouped GEMMs (the permutation counts tiles of this many rows).
 constexpr int kGemmBM = 256;

@@ -56,12 +56,16 @@ __device__ __forceinline__ float key_offset(int mode, float v) {
 }
 
 // Selection and gates for every (token, layer) pair of the tile. logits[tt * ld + lw*E + e]
-// are the fp32 router logits, lo[lw*E + e] the key offsets.
+// are the fp32 router logits, lo[lw*E + e] the key offsets. TOKEN_FASTEST: consecutive threads
+// take consecutive tokens of one layer (conflict-free LDS reads when ld is odd, coalesced
+// stores); otherwise consecutive layers of one token.
+template <bool TOKEN_FASTEST = false>
 __device__ void route_finalize(const RouteParams& p, const float* logits, int ld, const float* lo,
                                int t0, int TT, int lg0, int nl) {
   const int E = p.E, K = p.K;
   for (int pi = threadIdx.x; pi < TT * nl; pi += blockDim.x) {
-    const int tt = pi / nl, lw = pi - tt * nl;
+    const int tt = TOKEN_FASTEST ? pi % TT : pi / nl;
+    const int lw = TOKEN_FASTEST ? pi / TT : pi - tt * nl;
     const int t = t0 + tt;
     if (t >= p.T) continue;
     const float* z = logits + tt * ld + lw * E;
@@ -343,12 +347,13 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
   constexpr int UA = BM * 8 / NT, UB = BN * 8 / NT;   // 16-byte units per thread and stage
   constexpr int SA = BM * 8, SB = BN * 8;             // 16-byte slots per stage
   constexpr int STAGING = 2 * (SA + SB) * 16;
-  constexpr int LOGITS = HALF * BN * 4;
+  constexpr int LD = BN + 1;                   // logits row stride: odd, so token rows fall on distinct banks
+  constexpr int LOGITS = HALF * LD * 4;
   __shared__ __attribute__((aligned(16))) unsigned char smem[STAGING > LOGITS ? STAGING : LOGITS];
   __shared__ float lo[BN];
   u32x4* lds_a = reinterpret_cast<u32x4*>(smem);   // [2][SA]
   u32x4* lds_b = lds_a + 2 * SA;                    // [2][SB]
-  float* logits = reinterpret_cast<float*>(smem);   // [HALF][BN], after the k-loop
+  float* logits = reinterpret_cast<float*>(smem);   // [HALF][LD], after the k-loop
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -448,11 +453,11 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int row = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            logits[row * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+            logits[row * LD + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
           }
     }
     __syncthreads();
-    route_finalize(p, logits, BN, lo, t0 + h * HALF, HALF, lg0, nl);
+    route_finalize<true>(p, logits, LD, lo, t0 + h * HALF, HALF, lg0, nl);
     __syncthreads();   // the next phase overwrites the logits
   }
 }
