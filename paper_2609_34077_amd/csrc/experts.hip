@@ -51,7 +51,7 @@ struct GemmArgs {
   const uint16_t* lora_u;   // LORA: rank-r projections of this GEMM's A rows, bf16 [rows, 64]
   const uint16_t* lora_b;   // LORA: (alpha / r) B rows matching the B operand, bf16 [G, N rows, 64]
   int G, E, F, d;
-  int mt_max;               // grid bound on row tiles
+  int mt_max;               // grid bound on row tiles (the grid is mt_max * n_tiles workgroups)
   int n_tiles;              // column tiles
 };
 
@@ -72,9 +72,14 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   __shared__ u32x4 lds_a[2][BM * 8];
   __shared__ u32x4 lds_b[2][BN * 8];
 
+  // The grid covers the most row tiles any routing can need; only the first mt_live * n_tiles
+  // workgroups (spread evenly over the XCDs by the hardware's round-robin) have a tile, and the
+  // XCD-aware order is built over those, so every XCD gets an equal share of the live tiles.
+  const int mt_live = p.tile_off[p.G];
+  const int live = mt_live * p.n_tiles;
+  if (static_cast<int>(blockIdx.x) >= live) return;
   int mt, nt;
-  grouped_tile_coords(xcd_tile_id(), p.mt_max, p.n_tiles, mt, nt);
-  if (mt >= p.tile_off[p.G]) return;
+  grouped_tile_coords(xcd_tile_id(live), mt_live, p.n_tiles, mt, nt);
   const int g = find_group(p.tile_off, p.G, mt);
   const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM;
   const int row_end = p.offsets[g + 1];
