@@ -169,9 +169,11 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
   int mt, nt, g, row0, row_end, nk;
   const uint16_t* abase;
   const uint16_t* bbase;
-  if (MODE == kNtRows) {
-    grouped_tile_coords(xcd_tile_id(), p.mt_max, p.n_tiles, mt, nt);
-    if (mt >= p.tile_off[p.G]) return;
+  if (MODE == kNtRows) {   // tile order over the live row tiles only (see grouped_gemm_bf16)
+    const int mt_live = p.tile_off[p.G];
+    const int live = mt_live * p.n_tiles;
+    if (static_cast<int>(blockIdx.x) >= live) return;
+    grouped_tile_coords(xcd_tile_id(live), mt_live, p.n_tiles, mt, nt);
     int lo = 0, hi = p.G;   // tile_off[lo] <= mt < tile_off[hi]
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
