@@ -288,7 +288,9 @@ size_t maskmoe_offload_workspace_bytes(const maskmoe_layer_desc* desc);
  *                of range or belong to an uncached expert) sets *dev_error and is replaced by an
  *                empty cache before the step.
  *  y, topk_idx, topk_gate: as maskmoe_layer_forward (T = 1).
- *  counters      device int64 [2] or NULL: the step's fetches and hits are added to [0] and [1].
+ *  counters      device int64 [2] or NULL: the step's fetches and hits are added to [0] and [1]
+ *                (a plain read-modify-write: calls that may overlap, e.g. on different streams,
+ *                must not share counters, and none may share a cache_state or a pool).
  *  dev_error     device int32 or NULL: set to 1 (never cleared) on an inconsistent state.
  *  workspace     maskmoe_offload_workspace_bytes(desc) bytes, 256-byte aligned.
  *  events        NULL, or 2 caller-created HIP events (entries may be NULL) recorded on `stream`

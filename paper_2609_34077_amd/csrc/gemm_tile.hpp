@@ -86,33 +86,31 @@ __device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ 
     gload(0);
   }
   lstore(0);
-  if (ntot > 1) gload(1 - X);
+  gload(min(1 - X, nk - 1));
   __syncthreads();
   read_frags(0, 0, 0);
+  // The loop body has no branches, so that LDS stores and global loads can be interleaved
+  // with the MFMAs (LLVM's MFMA/DS interleaving strategy 0): past the end, the last main tile is
+  // loaded again and stored into the idle buffer, which nothing reads afterwards (every LDS
+  // access of the loop has completed at its last barrier).
   for (int kt = 0; kt < ntot; ++kt) {
     const int buf = kt & 1;
+    __builtin_amdgcn_iglp_opt(0);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       const int cur = kk & 1;
       if (kk + 1 < BK / 16) read_frags(buf, kk + 1, cur ^ 1);
+      if (kk == 0) {
+        lstore(buf ^ 1);
+        gload(min(kt + 2 - X, nk - 1));
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = mfma_32x32x16(af[cur][i], bf[cur][j], acc[i][j]);
-      if (kk + 1 < BK / 16) {
-#pragma unroll
-        for (int s = 0; s < TM + TN; ++s) {   // interleave one operand read per MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        }
-      }
-      if (kk == 0) {
-        if (kt + 1 < ntot) lstore(buf ^ 1);
-        if (kt + 2 < ntot) gload(kt + 2 - X);
-      }
     }
     __syncthreads();
-    if (kt + 1 < ntot) read_frags(buf ^ 1, 0, 0);
+    read_frags(buf ^ 1, 0, 0);
   }
 }
 
