@@ -413,29 +413,32 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
 
   // k-tile kt sits in LDS buffer kt & 1 and tile kt + 1 in registers; after the first k16 step
   // of tile kt the registers go to the other buffer and are refilled with tile kt + 2.
+  // Branch-free body, interleaved by LLVM's MFMA/DS strategy as in the expert GEMM: past the end
+  // the last tile is loaded again into the idle buffer, which nothing reads.
   const int nk = p.d / BK;
   gload(0);
   lstore(0);
-  if (nk > 1) gload(1);
+  gload(min(1, nk - 1));
   __syncthreads();
   read_frags(0, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
+    __builtin_amdgcn_iglp_opt(0);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       const int cur = kk & 1;
       if (kk + 1 < BK / 16) read_frags(buf, kk + 1, cur ^ 1);
+      if (kk == 0) {
+        lstore(buf ^ 1);
+        gload(min(kt + 2, nk - 1));
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = mfma_32x32x16(af[cur][i], bf[cur][j], acc[i][j]);
-      if (kk == 0) {
-        if (kt + 1 < nk) lstore(buf ^ 1);
-        if (kt + 2 < nk) gload(kt + 2);
-      }
     }
     __syncthreads();
-    if (kt + 1 < nk) read_frags(buf ^ 1, 0, 0);
+    read_frags(buf ^ 1, 0, 0);
   }
 
   // The last barrier of the loop ends every read of the staging buffers. Phase h: the waves
