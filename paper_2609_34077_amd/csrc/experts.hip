@@ -599,21 +599,24 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   return err;
 }
 
-// Slices of the reduction dimension for the two streaming kernels. Measured on MI355X, a
-// weight stream of this shape runs best with about 1800 workgroups in flight: fewer leave
-// HBM channels idle, and a count just past one full residency wave leaves a ragged second
-// wave. The split is the power of two (dividing the chunk count) whose workgroup count is
-// closest to that target, for the number of experts a batch of T tokens is expected to
-// activate under uniform routing, E (1 - (1 - K/E)^T), plus the shared experts. The grid is
-// still sized for the most experts that can be active; the estimate only picks the split.
-constexpr int kDecodeTargetWGs = 1792;
+// Slices of the reduction dimension for the two streaming kernels. Measured on MI355X (a sweep
+// of the target at 1, 4 and 16 tokens), the gate/up stream runs best with about 1800
+// workgroups in flight and the down stream with about 2600, as long as each slice keeps at
+// least 16 chunks (shorter slices lose more to their start-up than the extra workgroups
+// gain): fewer workgroups leave HBM channels idle, and a count just past one full residency
+// wave leaves a ragged second wave. The split is the power of two (dividing the chunk count,
+// keeping >= kDecodeMinChunks per slice) whose workgroup count is closest to the target, for
+// the number of experts a batch of T tokens is expected to activate under uniform routing,
+// E (1 - (1 - K/E)^T), plus the shared experts. The grid is still sized for the most experts
+// that can be active; the estimate only picks the split.
+constexpr int kDecodeTargetWGsGateUp = 1792, kDecodeTargetWGsDown = 2560, kDecodeMinChunks = 16;
 
-static int best_split(int per_slice_wgs, int chunks, int max_split) {
+static int best_split(int per_slice_wgs, int chunks, int max_split, int target) {
   if (per_slice_wgs <= 0) return 1;  // no tokens: nothing is launched
   int best = 1, best_gap = 1 << 30;
   for (int s = 1; s <= max_split; s *= 2) {
-    if (chunks % s) break;
-    const int gap = std::abs(per_slice_wgs * s - kDecodeTargetWGs);
+    if (chunks % s || (s > 1 && chunks / s < kDecodeMinChunks)) break;
+    const int gap = std::abs(per_slice_wgs * s - target);
     if (gap < best_gap) {
       best_gap = gap;
       best = s;
@@ -636,12 +639,13 @@ static int expected_active_groups(int T, int E, int K, int n_shared) {
 }
 
 int decode_split(int T, int d, int F, int E, int K, int n_shared) {
-  return best_split(d / (16 * DEC_NT) * expected_active_groups(T, E, K, n_shared), F / DEC_CK, kDecodeMaxSplit);
+  return best_split(d / (16 * DEC_NT) * expected_active_groups(T, E, K, n_shared), F / DEC_CK, kDecodeMaxSplit,
+                    kDecodeTargetWGsDown);
 }
 
 int decode_split_gate_up(int T, int d, int F, int E, int K, int n_shared) {
   return best_split(F / (16 * DEC_NT) * expected_active_groups(T, E, K, n_shared), d / DEC_CK,
-                    kDecodeMaxSplitGateUp);
+                    kDecodeMaxSplitGateUp, kDecodeTargetWGsGateUp);
 }
 
 hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* P, float* O,
