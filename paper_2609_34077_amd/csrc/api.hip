@@ -98,7 +98,9 @@ Layout layout(const maskmoe_layer_desc& d) {
   const size_t dec_rows = dec_T * (d.K + d.n_shared);
   w.P = take(maskmoe::kDecodeMaxSplitGateUp * dec_rows * 2 * d.F * 4);
   const size_t o_rows = maskmoe::kDecodeMaxSplit * dec_rows;
-  w.O = take((rows > o_rows ? rows : o_rows) * d.d * 4);
+  // the grouped path's down GEMM may split its reduction into kGroupedMaxKSplit partials
+  const size_t g_rows = rows * maskmoe::kGroupedMaxKSplit;
+  w.O = take((g_rows > o_rows ? g_rows : o_rows) * d.d * 4);
   w.total = off;
   w.AB = take(d.dtype == MASKMOE_BF16 ? rows * 2 * d.F * 2 : 0);
   w.train_total = off;

@@ -52,7 +52,8 @@ struct GemmArgs {
   const uint16_t* lora_b;   // LORA: (alpha / r) B rows matching the B operand, bf16 [G, N rows, 64]
   int G, E, F, d;
   int mt_max;               // grid bound on row tiles (the grid is mt_max * n_tiles workgroups)
-  int n_tiles;              // column tiles
+  int n_tiles;              // column tiles times k_split
+  int k_split;              // EPI 1: slices of the reduction, slice z writes out + z * rows * d
 };
 
 __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt) {
@@ -80,12 +81,16 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   if (static_cast<int>(blockIdx.x) >= live) return;
   int mt, nt;
   grouped_tile_coords(xcd_tile_id(live), mt_live, p.n_tiles, mt, nt);
+  const int z = nt % p.k_split;   // reduction slice (adjacent slices of a tile share its B rows)
+  nt /= p.k_split;
   const int g = find_group(p.tile_off, p.G, mt);
   const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM;
   const int row_end = p.offsets[g + 1];
   const int Kdim = EPI == 0 ? p.d : p.F;
   const int Ndim = EPI == 0 ? p.F : p.d;
   const int n0 = nt * (EPI == 0 ? BN / 2 : BN);
+  const int nks = Kdim / BK / p.k_split;   // k-tiles of this slice
+  const int k0 = z * nks * BK;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -101,7 +106,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   for (int i = 0; i < U; ++i) {
     const int r = r0 + 64 * i;
     const int row = min(row0 + r, row_end - 1);
-    aoffs[i] = (EPI == 0 ? p.row_tok[row] : row) * Kdim + chunk;
+    aoffs[i] = (EPI == 0 ? p.row_tok[row] : row) * Kdim + k0 + chunk;
     int brow;
     if (EPI == 0) {  // tile rows 0..127: W_gate rows n0.., rows 128..255: the matching W_up rows
       const int n = min(n0 + (r & 127), p.F - 1);
@@ -110,7 +115,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
       brow = min(n0 + r, p.d - 1);
     }
     brows[i] = brow;
-    boffs[i] = brow * Kdim + chunk;
+    boffs[i] = brow * Kdim + k0 + chunk;
   }
 
   // Fragment rows: A rows wm*128 + i*32 + (lane & 31); B rows: EPI 0 -> gate wn*32 + ... and
@@ -131,7 +136,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-  if (LORA) {   // the adapters' term as one more k-tile: A' = [U | rows], B' = [s B | W]
+  if (LORA && z == 0) {   // the adapters' term as one more k-tile: A' = [U | rows], B' = [s B | W]
     TileExtra ex;
     ex.xa = p.lora_u;
     ex.xb = p.lora_b + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * 64;
@@ -140,10 +145,11 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
       ex.xaoffs[i] = min(row0 + r0 + 64 * i, row_end - 1) * 64 + chunk;
       ex.xboffs[i] = brows[i] * 64 + chunk;
     }
-    gemm_tile_mainloop<true>(p.a, aoffs, wg, boffs, aoff, boff, Kdim / BK, acc, lds_a, lds_b, &ex);
+    gemm_tile_mainloop<true>(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b, &ex);
   } else {
-    gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, Kdim / BK, acc, lds_a, lds_b);
+    gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b);
   }
+  float* out_f32 = EPI == 1 ? static_cast<float*>(p.out) + static_cast<size_t>(z) * p.offsets[p.G] * Ndim : nullptr;
 
   // Epilogue. acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column
   // (lane & 31) of fragment j.
@@ -171,7 +177,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int col = n0 + wn * 64 + j * 32 + col_in;
-            if (col < Ndim) static_cast<float*>(p.out)[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
+            if (col < Ndim) out_f32[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
           }
         }
       }
@@ -534,12 +540,35 @@ __global__ __launch_bounds__(256) void f32_down_kernel(const F32Args p) {
 
 }  // namespace
 
+// Reduction slices of the down GEMM. Its tiles are few compared with the CUs (the Mixtral
+// fine-tuning layer has 68 x 16 = 1088, 4.25 rounds of 256 CUs), so a last partial round can
+// idle most of the chip; two slices of half the k-tiles each (8.5 rounds) waste less, at the
+// price of one more partial [rows, d] for the combine to add. Two slices are used when that
+// raises the share of busy CU-rounds by more than 5 points and each slice keeps >= 32 k-tiles.
+int grouped_down_split(int max_tiles, int n_tiles, int k_tiles) {
+  static const int n_cu = [] {
+    int dev = 0, cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                               hipSuccess || cu <= 0)
+      cu = 256;
+    return cu;
+  }();
+  if (k_tiles % 2 || k_tiles / 2 < 32) return 1;
+  auto busy = [&](long wgs) {
+    const long rounds = (wgs + n_cu - 1) / n_cu;
+    return rounds > 0 ? static_cast<double>(wgs) / (rounds * n_cu) : 1.0;
+  };
+  const long w1 = static_cast<long>(max_tiles) * n_tiles;
+  return busy(2 * w1) > busy(w1) + 0.05 ? 2 : 1;
+}
+
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
                                void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks, uint16_t* ab,
                                const LoraArgs* lora) {
   const int G = a.E + a.n_shared;
   GemmArgs g{};
   g.ab = ab;
+  g.k_split = 1;
   hipError_t err;
   if (lora) {
     err = launch_lora_pack(*lora, G, a.E, a.F, a.d, stream);
@@ -579,21 +608,22 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
 
   g.ab = nullptr;
   g.a = H;
+  g.k_split = grouped_down_split(max_tiles, (a.d + BN - 1) / BN, a.F / BK);
   g.w = static_cast<const uint16_t*>(a.w_down);
   g.ws = static_cast<const uint16_t*>(a.ws_down);
   g.out = O;
   const int nt2 = (a.d + BN - 1) / BN;
-  g.n_tiles = nt2;
+  g.n_tiles = nt2 * g.k_split;
   if (lora)
-    hipLaunchKernelGGL((grouped_gemm_bf16<1, true>), dim3(max_tiles * nt2), dim3(GEMM_THREADS), 0, stream, g);
+    hipLaunchKernelGGL((grouped_gemm_bf16<1, true>), dim3(max_tiles * g.n_tiles), dim3(GEMM_THREADS), 0, stream, g);
   else
-    hipLaunchKernelGGL(grouped_gemm_bf16<1>, dim3(max_tiles * nt2), dim3(GEMM_THREADS), 0, stream, g);
+    hipLaunchKernelGGL(grouped_gemm_bf16<1>, dim3(max_tiles * g.n_tiles), dim3(GEMM_THREADS), 0, stream, g);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
 
   hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                     a.K, a.n_shared, a.d, y, 1, a.expert_out);
+                     a.K, a.n_shared, a.d, y, g.k_split, a.expert_out);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;

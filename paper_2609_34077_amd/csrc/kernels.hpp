@@ -103,6 +103,11 @@ hipError_t launch_lora_down(const uint16_t* src, const int32_t* row_tok, int K, 
                             int nq, int G, int E, const PermBuffers& pb, int max_tiles, uint16_t* out,
                             hipStream_t stream);
 
+// Slices of the down GEMM's reduction (1 or kGroupedMaxKSplit); O then holds that many [rows, d]
+// partials.
+constexpr int kGroupedMaxKSplit = 2;
+int grouped_down_split(int max_tiles, int n_tiles, int k_tiles);
+
 // bf16, T > kDecodeMaxT (any T when training or with adapters): H = SwiGLU(X_g W_gate,up^T)
 // per group; O = H W_down^T; y = combine. ab (training): the gate and up pre-activations,
 // bf16 [rows, 2F]. lora: the experts' low-rank adapters, added inside both GEMMs.
