@@ -576,9 +576,13 @@ def run_trace(args):
     xd = torch.from_numpy(inp["x"]).view(torch.bfloat16).cuda()
     wd = torch.from_numpy(inp["w_router"]).view(torch.bfloat16).cuda()
     T = cfg.S * cfg.N
+    desc = L.make_desc(T, cfg.d, cfg.E, cfg.K, dtype=L.BF16, route_mode=L.ROUTE_SOFT_PRIOR, gate_mode=L.GATE_RENORM)
+    nbytes = L.load().maskmoe_route_workspace_bytes(desc, cfg.L)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda") if nbytes else None
 
     def step(prior, events=None):
-        idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=prior, with_margin=False)
+        idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=prior, with_margin=False,
+                                    workspace=ws)
         if events:
             events[1].record()
         res = L.maskmoe_cache_fetches(idx.view(cfg.L, cfg.S, cfg.N, cfg.K), cfg.E, cfg.B)
@@ -626,7 +630,7 @@ def run_trace(args):
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
                      "traffic": recorded_traffic("trace", "routing_fetch_trace"),
-                     "kernel": "route_gemm_kernel",
+                     "kernel": "routing stage: route_gemm_kernel<true> + route_select_kernel",
                      "algorithmic_unit": "FLOPs per launch = 2 * S*N * L*E * d",
                      "hbm_frac_of_x_read": round(x_bytes / (route_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                      "avg_launch_us": round(1e3 * route_ms, 2)},

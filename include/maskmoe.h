@@ -95,13 +95,29 @@ typedef struct maskmoe_layer_desc {
  *  topk_margin device [L, T] float or NULL: gap in logit units between the K-th and the
  *              (K+1)-th largest log-domain key (+inf when fewer than K+1 experts are
  *              eligible). Index sets are unique wherever the margin is clearly positive.
+ *  workspace   device buffer of at least maskmoe_route_workspace_bytes(desc, L) bytes,
+ *              16-byte aligned, owned by the caller, or NULL. Given, many-token launches
+ *              write the router logits there first and select in a second kernel (faster
+ *              when the selection would otherwise run at the logit GEMM's occupancy); NULL
+ *              selects inside the logit kernel. Both give bit-identical outputs. Its
+ *              contents on entry are irrelevant; calls that may overlap must not share it.
+ *  workspace_bytes  size of workspace in bytes (ignored when workspace is NULL).
  *  Errors: E_INVAL for T < 0, L < 1, d < 1, K/E outside their ranges, an unknown mode, a
- *  NULL required pointer, a mask row with fewer than K ones, or a prior value that is not
- *  finite and > 0; E_UNSUPPORTED for bf16 with d % 32 != 0.
+ *  NULL required pointer, a mask row with fewer than K ones, a prior value that is not
+ *  finite and > 0, or a workspace that is too small or misaligned; E_UNSUPPORTED for bf16
+ *  with d % 32 != 0.
  */
 int maskmoe_route(const maskmoe_layer_desc* desc, int32_t L, const void* x, const void* w_router,
                   const uint8_t* mask, const float* prior, int32_t* topk_idx, float* topk_gate,
-                  float* topk_margin, hipStream_t stream);
+                  float* topk_margin, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * maskmoe_route_workspace_bytes -- workspace that maskmoe_route uses for `desc` and L layers
+ * (fp32 [L, T, E] router logits when the launch splits logits and selection; 0 when it never
+ * does, e.g. fp32 inputs, fewer than 512 tokens or more than 64 experts). Returns 0 for an
+ * invalid desc or L < 1.
+ */
+size_t maskmoe_route_workspace_bytes(const maskmoe_layer_desc* desc, int32_t L);
 
 /*
  * maskmoe_layer_workspace_bytes -- device workspace that maskmoe_layer_forward needs for

@@ -24,8 +24,8 @@ GATE_P, GATE_RENORM = 0, 1
 BF16, F32 = 0, 1
 CACHE_LRU, CACHE_LFU, CACHE_FIFO = 0, 1, 2
 
-EXPORTS = ("maskmoe_route", "maskmoe_layer_workspace_bytes", "maskmoe_layer_forward",
-           "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string",
+EXPORTS = ("maskmoe_route", "maskmoe_route_workspace_bytes", "maskmoe_layer_workspace_bytes",
+           "maskmoe_layer_forward", "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string",
            "maskmoe_sample_mask", "maskmoe_layer_forward_train", "maskmoe_stage1_backward_workspace_bytes",
            "maskmoe_stage1_backward", "maskmoe_layer_train_workspace_bytes",
            "maskmoe_layer_backward_workspace_bytes", "maskmoe_layer_backward", "maskmoe_layer_lora_workspace_bytes",
@@ -71,8 +71,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     # so the process holds a single HIP runtime.
     import torch  # noqa: F401
     lib = ctypes.CDLL(path)
-    lib.maskmoe_route.argtypes = [ctypes.POINTER(LayerDesc), _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    lib.maskmoe_route.argtypes = [ctypes.POINTER(LayerDesc), _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                  ctypes.c_size_t, _vp]
     lib.maskmoe_route.restype = ctypes.c_int
+    lib.maskmoe_route_workspace_bytes.argtypes = [ctypes.POINTER(LayerDesc), _i32]
+    lib.maskmoe_route_workspace_bytes.restype = ctypes.c_size_t
     lib.maskmoe_layer_workspace_bytes.argtypes = [ctypes.POINTER(LayerDesc)]
     lib.maskmoe_layer_workspace_bytes.restype = _sz
     lib.maskmoe_layer_forward.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
@@ -173,10 +176,12 @@ def make_desc(T, d, E, K, F=1, n_shared=0, dtype=BF16, route_mode=ROUTE_PLAIN, g
 
 
 def maskmoe_route(x, w_router, K: int, route_mode: int, gate_mode: int, mask=None, prior=None,
-                  with_margin: bool = True):
+                  with_margin: bool = True, workspace="auto"):
     """Route tokens x [T,d] through L routers w_router [L,E,d] (or [E,d] for L=1).
 
-    mask / prior: host arrays [L,E] (or [E]). Returns ``(idx [L,T,K] int32,
+    mask / prior: host arrays [L,E] (or [E]). workspace: a uint8 device tensor of at least
+    maskmoe_route_workspace_bytes bytes, None (selection inside the logit kernel) or "auto"
+    (allocated here when the library asks for one). Returns ``(idx [L,T,K] int32,
     gate [L,T,K] float32, margin [L,T] float32 or None)``; L is squeezed when
     ``w_router`` is 2-D.
     """
@@ -196,8 +201,16 @@ def maskmoe_route(x, w_router, K: int, route_mode: int, gate_mode: int, mask=Non
     idx = torch.empty((L, T, K), dtype=torch.int32, device=x.device)
     gate = torch.empty((L, T, K), dtype=torch.float32, device=x.device)
     margin = torch.empty((L, T), dtype=torch.float32, device=x.device) if with_margin else None
+    if isinstance(workspace, str):
+        if workspace != "auto":
+            raise ValueError("workspace: a device tensor, None or 'auto'")
+        nbytes = lib.maskmoe_route_workspace_bytes(ctypes.byref(desc), L)
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=x.device) if nbytes else None
+    if workspace is not None:
+        _dev(workspace, "workspace")
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check("maskmoe_route", lib.maskmoe_route(ctypes.byref(desc), L, _ptr(x), _ptr(w3), m_p, p_p, _ptr(idx),
-                                              _ptr(gate), _ptr(margin), _stream()))
+                                              _ptr(gate), _ptr(margin), _ptr(workspace), ws_bytes, _stream()))
     del m_arr, p_arr
     if squeeze:
         return idx[0], gate[0], (margin[0] if margin is not None else None)

@@ -53,7 +53,7 @@ int check_mask_prior(int mode, int L, int E, int K, const uint8_t* mask, const f
 }
 
 struct Layout {
-  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, pcount, H, P, O, total;
+  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, pcount, Z, H, P, O, total;
   size_t AB, train_total;   // training (bf16): gate / up pre-activations [rows, 2F] after `total`
   // adapters (bf16), after `total`: rank projections U, V [rows, 64], scaled B [G, 2F | d, 64]
   size_t LU, LV, LBGU, LBD, lora_total;
@@ -90,6 +90,8 @@ Layout layout(const maskmoe_layer_desc& d) {
   w.inv = take(TK * 4);
   w.row_tok = take(rows * 4);
   w.pcount = take(static_cast<size_t>(maskmoe::permute_chunks(d.T, d.K)) * d.E * 4);
+  // router logits of split routing (fp32 [T, E]) when no logits output is requested
+  w.Z = take(maskmoe::route_splits(d.dtype == MASKMOE_BF16, d.T, d.E) ? static_cast<size_t>(d.T) * d.E * 4 : 0);
   w.H = take(rows * d.F * hsz);
   // O holds the expert outputs: [rows, d], or [split, rows, d] on the few-token path; P the
   // few-token partial gate/up sums [split_gu, rows, 2F]. Both are sized for the largest
@@ -141,12 +143,20 @@ const char* maskmoe_status_string(int status) {
   }
 }
 
+size_t maskmoe_route_workspace_bytes(const maskmoe_layer_desc* desc, int32_t L) {
+  if (check_route_desc(desc) != MASKMOE_OK || L < 1) return 0;
+  if (!maskmoe::route_splits(desc->dtype == MASKMOE_BF16, desc->T, desc->E)) return 0;
+  return static_cast<size_t>(L) * desc->T * desc->E * 4;
+}
+
 int maskmoe_route(const maskmoe_layer_desc* desc, int32_t L, const void* x, const void* w_router,
                   const uint8_t* mask, const float* prior, int32_t* topk_idx, float* topk_gate,
-                  float* topk_margin, hipStream_t stream) {
+                  float* topk_margin, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int st = check_route_desc(desc);
   if (st != MASKMOE_OK) return st;
   if (L < 1 || static_cast<int64_t>(L) * desc->T * desc->K >= (int64_t{1} << 31)) return MASKMOE_E_INVAL;
+  if (workspace && (workspace_bytes < maskmoe_route_workspace_bytes(desc, L) || !aligned(workspace, 16)))
+    return MASKMOE_E_INVAL;
   st = check_mask_prior(desc->route_mode, L, desc->E, desc->K, mask, prior);
   if (st != MASKMOE_OK) return st;
   if (desc->T == 0) return MASKMOE_OK;
@@ -158,7 +168,8 @@ int maskmoe_route(const maskmoe_layer_desc* desc, int32_t L, const void* x, cons
     return MASKMOE_E_INVAL;
   return hip_status(maskmoe::launch_route(bf16, x, w_router, desc->T, desc->d, desc->E, desc->K, L,
                                          desc->route_mode, desc->gate_mode, mask, prior, topk_idx,
-                                         topk_gate, topk_margin, nullptr, stream));
+                                         topk_gate, topk_margin, nullptr, static_cast<float*>(workspace),
+                                         stream));
 }
 
 size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc) {
@@ -244,7 +255,7 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
     maskmoe::record_mark(events, 1, stream);
   } else {
     e = maskmoe::launch_route(bf16, x, w_router, d.T, d.d, d.E, d.K, 1, d.route_mode, d.gate_mode, mask, prior,
-                              idx, gate, nullptr, router_logits, stream);
+                              idx, gate, nullptr, router_logits, reinterpret_cast<float*>(ws + w.Z), stream);
     if (e != hipSuccess) return MASKMOE_E_HIP;
     maskmoe::record_mark(events, 1, stream);
     e = maskmoe::launch_permute(idx, d.T, d.K, d.E, d.n_shared, maskmoe::kGemmBM, pb,

@@ -24,9 +24,16 @@ struct PermBuffers {
 // ([L, E, d]); host `mask` [L, E] (HARD_MASK) or `prior` [L, E] (SOFT_PRIOR), unused for
 // PLAIN. Outputs idx/gate [L, T, K], margin [L, T].
 // logits (fp32 [L, T, E]) and margin ([L, T]) are optional outputs (null: not written).
+// When route_splits(bf16, T, E) and a logits buffer is at hand (logits, else split_ws: fp32
+// [L, T, E] workspace), the logits are written first and selected by a second kernel at full
+// occupancy; otherwise the logit kernel selects itself. Both give the same bits.
+constexpr int kRouteSplitMinT = 512;
+constexpr int kRouteSplitMaxE = 64;
+inline bool route_splits(bool bf16, int T, int E) { return bf16 && T >= kRouteSplitMinT && E <= kRouteSplitMaxE; }
 hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
                         int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
-                        int32_t* idx, float* gate, float* margin, float* logits, hipStream_t stream);
+                        int32_t* idx, float* gate, float* margin, float* logits, float* split_ws,
+                        hipStream_t stream);
 
 // Tokens at or below which one bf16 routing workgroup covers every token, so the routing
 // kernel can also perform the permutation (launch_route_permute).

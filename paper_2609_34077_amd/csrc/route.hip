@@ -55,6 +55,76 @@ __device__ __forceinline__ float key_offset(int mode, float v) {
   return 0.0f;                                          // plain
 }
 
+// Selection, gates and outputs of one (token, layer) pair: z the E fp32 logits, o the E key
+// offsets, obase the pair's index in the [L, T] outputs. write_logits: also store z in p.logits.
+// EC: the expert count when known at compile time (0: p.E); the arithmetic is the same.
+template <int EC = 0>
+__device__ __forceinline__ void select_pair(const RouteParams& p, const float* z, const float* o, size_t obase,
+                                            bool write_logits) {
+  const int E = EC ? EC : p.E, K = p.K;
+  uint64_t tk0 = 0, tk1 = 0, tk2 = 0, tk3 = 0;
+  int sel[kMaxK];
+  float selz[kMaxK];
+  float kth = -INFINITY, nxt = -INFINITY;
+#pragma unroll
+  for (int j = 0; j <= kMaxK; ++j) {
+    if (j <= K) {
+      float best = -INFINITY;
+      int bi = -1;
+      for (int e = 0; e < E; ++e) {
+        const uint64_t word = e < 64 ? tk0 : e < 128 ? tk1 : e < 192 ? tk2 : tk3;
+        if ((word >> (e & 63)) & 1ull) continue;
+        const float key = z[e] + o[e];
+        if (key > best) {
+          best = key;
+          bi = e;
+        }
+      }
+      if (j < K) {
+        if (bi < 0) {  // only reachable with non-finite logits: keep the output well formed
+          for (int e = 0; e < E && bi < 0; ++e) {
+            const uint64_t word = e < 64 ? tk0 : e < 128 ? tk1 : e < 192 ? tk2 : tk3;
+            if (!((word >> (e & 63)) & 1ull)) bi = e;
+          }
+        }
+        const uint64_t bit = 1ull << (bi & 63);
+        if (bi < 64) tk0 |= bit; else if (bi < 128) tk1 |= bit; else if (bi < 192) tk2 |= bit; else tk3 |= bit;
+        sel[j] = bi;
+        selz[j] = z[bi];
+        kth = best;
+      } else {
+        nxt = best;
+      }
+    }
+  }
+
+  float zref, norm = 0.0f;
+  if (p.gate_mode == 0) {  // g = p_i: full softmax over all E experts
+    zref = z[0];
+    for (int e = 1; e < E; ++e) zref = fmaxf(zref, z[e]);
+    for (int e = 0; e < E; ++e) norm += expf(z[e] - zref);
+  } else {  // g = p_i / sum_{j in A} p_j
+    zref = selz[0];
+#pragma unroll
+    for (int j = 1; j < kMaxK; ++j)
+      if (j < K) zref = fmaxf(zref, selz[j]);
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j)
+      if (j < K) norm += expf(selz[j] - zref);
+  }
+  const float inv = 1.0f / norm;
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    if (j < K) {
+      p.idx[obase * K + j] = sel[j];
+      p.gate[obase * K + j] = expf(selz[j] - zref) * inv;
+    }
+  }
+  if (p.margin) p.margin[obase] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+  if (write_logits && p.logits)
+    for (int e = 0; e < E; ++e) p.logits[obase * E + e] = z[e];
+}
+
 // Selection and gates for every (token, layer) pair of the tile. logits[tt * ld + lw*E + e]
 // are the fp32 router logits, lo[lw*E + e] the key offsets. TOKEN_FASTEST: consecutive threads
 // take consecutive tokens of one layer (conflict-free LDS reads when ld is odd, coalesced
@@ -62,7 +132,7 @@ __device__ __forceinline__ float key_offset(int mode, float v) {
 template <bool TOKEN_FASTEST = false>
 __device__ void route_finalize(const RouteParams& p, const float* logits, int ld, const float* lo,
                                int t0, int TT, int lg0, int nl) {
-  const int E = p.E, K = p.K;
+  const int E = p.E;
   for (int pi = threadIdx.x; pi < TT * nl; pi += blockDim.x) {
     const int tt = TOKEN_FASTEST ? pi % TT : pi / nl;
     const int lw = TOKEN_FASTEST ? pi / TT : pi - tt * nl;
@@ -72,68 +142,116 @@ __device__ void route_finalize(const RouteParams& p, const float* logits, int ld
     const float* o = lo + lw * E;
     const size_t obase = (static_cast<size_t>(lg0 + lw) * p.T + t);
 
-    uint64_t tk0 = 0, tk1 = 0, tk2 = 0, tk3 = 0;
-    int sel[kMaxK];
-    float selz[kMaxK];
-    float kth = -INFINITY, nxt = -INFINITY;
-#pragma unroll
-    for (int j = 0; j <= kMaxK; ++j) {
-      if (j <= K) {
-        float best = -INFINITY;
-        int bi = -1;
-        for (int e = 0; e < E; ++e) {
-          const uint64_t word = e < 64 ? tk0 : e < 128 ? tk1 : e < 192 ? tk2 : tk3;
-          if ((word >> (e & 63)) & 1ull) continue;
-          const float key = z[e] + o[e];
-          if (key > best) {
-            best = key;
-            bi = e;
-          }
-        }
-        if (j < K) {
-          if (bi < 0) {  // only reachable with non-finite logits: keep the output well formed
-            for (int e = 0; e < E && bi < 0; ++e) {
-              const uint64_t word = e < 64 ? tk0 : e < 128 ? tk1 : e < 192 ? tk2 : tk3;
-              if (!((word >> (e & 63)) & 1ull)) bi = e;
-            }
-          }
-          const uint64_t bit = 1ull << (bi & 63);
-          if (bi < 64) tk0 |= bit; else if (bi < 128) tk1 |= bit; else if (bi < 192) tk2 |= bit; else tk3 |= bit;
-          sel[j] = bi;
-          selz[j] = z[bi];
-          kth = best;
-        } else {
-          nxt = best;
-        }
-      }
-    }
-
-    float zref, norm = 0.0f;
-    if (p.gate_mode == 0) {  // g = p_i: full softmax over all E experts
-      zref = z[0];
-      for (int e = 1; e < E; ++e) zref = fmaxf(zref, z[e]);
-      for (int e = 0; e < E; ++e) norm += expf(z[e] - zref);
-    } else {  // g = p_i / sum_{j in A} p_j
-      zref = selz[0];
-#pragma unroll
-      for (int j = 1; j < kMaxK; ++j)
-        if (j < K) zref = fmaxf(zref, selz[j]);
-#pragma unroll
-      for (int j = 0; j < kMaxK; ++j)
-        if (j < K) norm += expf(selz[j] - zref);
-    }
-    const float inv = 1.0f / norm;
-#pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-      if (j < K) {
-        p.idx[obase * K + j] = sel[j];
-        p.gate[obase * K + j] = expf(selz[j] - zref) * inv;
-      }
-    }
-    if (p.margin) p.margin[obase] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
-    if (p.logits)
-      for (int e = 0; e < E; ++e) p.logits[obase * E + e] = z[e];
+    select_pair(p, z, o, obase, true);
   }
+}
+
+// Split routing: the logits of every (token, layer) pair are first written to p.logits
+// ([L, T, E] fp32, the caller's output or workspace) by the logit kernels, then selected here at
+// full occupancy (the selection otherwise runs after the logit GEMM at the GEMM's occupancy).
+// Pairs are taken token-fastest: pair q is (layer q / T, token q % T), its logits at q * E.
+constexpr int kSelThreads = 256;
+
+// E <= kSelThreadE: one thread per pair, the block's logits staged in LDS (odd row stride) so
+// the per-pair selection reads them without bank conflicts.
+constexpr int kSelThreadE = 16;
+template <int EC>
+__global__ __launch_bounds__(kSelThreads) void route_select_kernel(const RouteParams p) {
+  constexpr int EMAX = EC ? EC : kSelThreadE;
+  __shared__ float zs[kSelThreads * (EMAX + 1)];
+  __shared__ float lo[kMaxModeParams];
+  const int E = EC ? EC : p.E;
+  const uint32_t pairs = static_cast<uint32_t>(p.L) * p.T;   // < 2^31
+  const uint32_t q0 = blockIdx.x * kSelThreads;
+  for (int i = threadIdx.x; i < p.L * E; i += kSelThreads) lo[i] = key_offset(p.mode, p.modep[i]);
+  const int rows = pairs - q0 < kSelThreads ? static_cast<int>(pairs - q0) : kSelThreads;
+  const float* src = p.logits + static_cast<size_t>(q0) * E;
+  if ((E & 3) == 0) {   // 16-byte loads; a 4-float unit never straddles two rows
+    for (int i = threadIdx.x; i < rows * E / 4; i += kSelThreads) {
+      const f32x4 v = reinterpret_cast<const f32x4*>(src)[i];
+      const int r = (4 * i) / E, c = 4 * i - r * E;
+      float* d = zs + r * (E + 1) + c;
+      d[0] = v[0];
+      d[1] = v[1];
+      d[2] = v[2];
+      d[3] = v[3];
+    }
+  } else {
+    for (int i = threadIdx.x; i < rows * E; i += kSelThreads) {
+      const int r = i / E;
+      zs[r * (E + 1) + i - r * E] = src[i];
+    }
+  }
+  __syncthreads();
+  const uint32_t q = q0 + threadIdx.x;
+  if (q >= pairs) return;
+  const int l = static_cast<int>(q / static_cast<uint32_t>(p.T));
+  select_pair<EC>(p, zs + threadIdx.x * (E + 1), lo + l * E, q, false);
+}
+
+// kSelThreadE < E <= 64: one wavefront per pair, lane e holding expert e. Each expert's rank
+// (the number of valid keys larger, or equal with a lower index; -inf and NaN keys are not
+// valid) is its position in the successive picks of select_pair, so both give the same
+// selection, margin and gate bits (the normalisers are summed in the same order).
+__global__ __launch_bounds__(kSelThreads) void route_select_wave_kernel(const RouteParams p) {
+  const int lane = threadIdx.x & 63;
+  const int E = p.E, K = p.K, T = p.T;
+  const uint32_t q = blockIdx.x * (kSelThreads / 64) + (threadIdx.x >> 6);
+  if (q >= static_cast<uint32_t>(p.L) * T) return;   // the whole wavefront leaves (L * T < 2^31)
+  const int l = static_cast<int>(q / static_cast<uint32_t>(T));
+  const bool in = lane < E;
+  const float z = in ? p.logits[static_cast<size_t>(q) * E + lane] : 0.0f;
+  const float key = in ? z + key_offset(p.mode, p.modep[l * E + lane]) : -INFINITY;
+  const bool valid = in && key > -INFINITY;   // false for NaN too
+  int rank = 0;
+  for (int f = 0; f < E; ++f) {
+    const float kf = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key), f));
+    if (kf > -INFINITY && (kf > key || (kf == key && f < lane))) ++rank;
+  }
+  const uint64_t vmask = __ballot(valid);
+  const int n_valid = __popcll(vmask);
+  // picks in order: valid experts by rank, then (fewer than K valid keys) the lowest others
+  uint64_t taken = 0;
+  int my_sel = 0;
+  float my_selz = 0.0f, kth = -INFINITY, nxt = -INFINITY;
+  for (int j = 0; j < K; ++j) {
+    int e;
+    if (j < n_valid) {
+      e = __ffsll(static_cast<unsigned long long>(__ballot(valid && rank == j))) - 1;
+      kth = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key), e));
+    } else {
+      e = __ffsll(static_cast<unsigned long long>(~taken & (E == 64 ? ~0ull : ((1ull << E) - 1)))) - 1;
+      kth = -INFINITY;
+    }
+    taken |= 1ull << e;
+    const float ze = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(z), e));
+    if (lane == j) {
+      my_sel = e;
+      my_selz = ze;
+    }
+  }
+  if (K < n_valid) {
+    const int e = __ffsll(static_cast<unsigned long long>(__ballot(valid && rank == K))) - 1;
+    nxt = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key), e));
+  }
+  float zref, norm = 0.0f;
+  if (p.gate_mode == 0) {   // softmax over all E, normaliser in expert order
+    zref = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(z), 0));
+    for (int e = 1; e < E; ++e) zref = fmaxf(zref, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(z), e)));
+    const float ex = in ? expf(z - zref) : 0.0f;
+    for (int e = 0; e < E; ++e) norm += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), e));
+  } else {   // renormalised over the picks, in pick order
+    zref = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_selz), 0));
+    for (int j = 1; j < K; ++j) zref = fmaxf(zref, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_selz), j)));
+    for (int j = 0; j < K; ++j)
+      norm += expf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_selz), j)) - zref);
+  }
+  const float inv = 1.0f / norm;
+  if (lane < K) {
+    p.idx[static_cast<size_t>(q) * K + lane] = my_sel;
+    p.gate[static_cast<size_t>(q) * K + lane] = expf(my_selz - zref) * inv;
+  }
+  if (lane == 0 && p.margin) p.margin[q] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
 }
 
 // The same selection and gates for the single-workgroup launch (one layer, tokens 0..T-1), one
@@ -232,7 +350,8 @@ __device__ void route_finalize_wave(const RouteParams& p, const float* logits, i
 
 // FUSE: the grid is one workgroup holding every token of one layer; after the selection it
 // also groups the (token, slot) pairs by expert (permute_block).
-template <int MB, int NB, int WN, int WK, bool FUSE>
+// SPLIT (not with FUSE): the tile's logits go to p.logits and route_select_kernel selects.
+template <int MB, int NB, int WN, int WK, bool FUSE, bool SPLIT = false>
 __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RouteParams p) {
   constexpr int TT = 16 * MB, NO = 16 * NB * WN, NT = 64 * WN * WK;
   __shared__ float red[WK * TT * NO];
@@ -320,7 +439,14 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
     }
     __syncthreads();
   }
-  if (FUSE) {
+  if (SPLIT) {   // [TT, nl * E] tile -> p.logits [L, T, E], consecutive threads on consecutive floats
+    for (int i = threadIdx.x; i < TT * nout; i += NT) {
+      const int lw = i / (TT * p.E), rem = i - lw * TT * p.E;
+      const int tt = rem / p.E, e = rem - tt * p.E;
+      if (t0 + tt < p.T)
+        p.logits[(static_cast<size_t>(lg0 + lw) * p.T + t0 + tt) * p.E + e] = red[tt * NO + lw * p.E + e];
+    }
+  } else if (FUSE) {
     __shared__ PermLds plds;
     __shared__ int32_t sel_lds[kRouteOneBlockT * kMaxK];
     route_finalize_wave(p, red, NO, lo, TT, sel_lds);
@@ -339,6 +465,7 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
 // half of the tokens at a time, and the selection runs on them as in route_bf16_kernel.
 constexpr int kRgBM = 256, kRgBN = 256, kRgBK = 64, kRgThreads = 512;
 
+template <bool SPLIT>
 __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParams p) {
   constexpr int BM = kRgBM, BN = kRgBN, BK = kRgBK, NT = kRgThreads;
   constexpr int WN = 4;                        // waves: 2 along tokens x 4 along outputs
@@ -460,7 +587,24 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
           }
     }
     __syncthreads();
-    route_finalize<true>(p, logits, LD, lo, t0 + h * HALF, HALF, lg0, nl);
+    if (SPLIT) {   // this half's logits -> p.logits [L, T, E]: a thread per (token, layer), tokens fastest
+      const int E = p.E;
+      for (int i = tid; i < HALF * nl; i += NT) {
+        const int tt = i % HALF, lw = i / HALF;
+        const int t = t0 + h * HALF + tt;
+        if (t >= p.T) continue;
+        const float* src = logits + tt * LD + lw * E;   // odd LD: the lanes' reads fall on distinct banks
+        float* dst = p.logits + (static_cast<size_t>(lg0 + lw) * p.T + t) * E;
+        if ((E & 3) == 0) {   // rows are 16-byte aligned
+          for (int e = 0; e < E; e += 4)
+            *reinterpret_cast<f32x4*>(dst + e) = f32x4{src[e], src[e + 1], src[e + 2], src[e + 3]};
+        } else {
+          for (int e = 0; e < E; ++e) dst[e] = src[e];
+        }
+      }
+    } else {
+      route_finalize<true>(p, logits, LD, lo, t0 + h * HALF, HALF, lg0, nl);
+    }
     __syncthreads();   // the next phase overwrites the logits
   }
 }
@@ -490,14 +634,14 @@ __global__ __launch_bounds__(256) void route_f32_kernel(const RouteParams p) {
   route_finalize(p, logits, 256, lo, t0, kF32TT, lg0, nl);
 }
 
-template <int MB, int NB, int WN, int WK, bool FUSE = false>
+template <int MB, int NB, int WN, int WK, bool FUSE = false, bool SPLIT = false>
 hipError_t launch_bf16(RouteParams& p, hipStream_t stream) {
   constexpr int TT = 16 * MB, NO = 16 * NB * WN;
   p.lpw = NO / p.E < 1 ? 1 : NO / p.E;
   if (p.lpw > p.L) p.lpw = p.L;
   dim3 grid((p.T + TT - 1) / TT, (p.L + p.lpw - 1) / p.lpw);
   if (FUSE && (grid.x != 1 || grid.y != 1)) return hipErrorInvalidValue;  // needs one workgroup
-  hipLaunchKernelGGL((route_bf16_kernel<MB, NB, WN, WK, FUSE>), grid, dim3(64 * WN * WK), 0, stream, p);
+  hipLaunchKernelGGL((route_bf16_kernel<MB, NB, WN, WK, FUSE, SPLIT>), grid, dim3(64 * WN * WK), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -526,8 +670,12 @@ void fill_params(RouteParams& p, const void* x, const void* w_router, int T, int
 
 hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, int d, int E, int K,
                         int L, int mode, int gate_mode, const uint8_t* mask, const float* prior,
-                        int32_t* idx, float* gate, float* margin, float* logits, hipStream_t stream) {
+                        int32_t* idx, float* gate, float* margin, float* logits, float* split_ws,
+                        hipStream_t stream) {
   if (T == 0 || L == 0) return hipSuccess;
+  // Split routing needs an [L, T, E] fp32 buffer: the caller's logits output, else split_ws.
+  float* zbuf = logits ? logits : split_ws;
+  const bool split = route_splits(bf16, T, E) && zbuf;
   // Layers are processed in launches whose (layer, expert) parameters fit in the kernel
   // arguments; every launch covers whole layers.
   const int max_layers = kMaxModeParams / E;
@@ -535,7 +683,7 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
   for (int l0 = 0; l0 < L; l0 += max_layers) {
     RouteParams p;
     fill_params(p, x, w_router, T, d, E, K, L - l0 < max_layers ? L - l0 : max_layers, l0, mode, gate_mode, mask,
-                prior, idx, gate, margin, logits, esz);
+                prior, idx, gate, margin, split ? zbuf : logits, esz);
     hipError_t err;
     if (!bf16) {
       p.lpw = 256 / E < 1 ? 1 : 256 / E;
@@ -547,16 +695,40 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
       p.lpw = kRgBN / E;
       if (p.lpw > p.L) p.lpw = p.L;
       dim3 grid((T + kRgBM - 1) / kRgBM, (p.L + p.lpw - 1) / p.lpw);
-      hipLaunchKernelGGL(route_gemm_kernel, grid, dim3(kRgThreads), 0, stream, p);
+      if (split) hipLaunchKernelGGL(route_gemm_kernel<true>, grid, dim3(kRgThreads), 0, stream, p);
+      else hipLaunchKernelGGL(route_gemm_kernel<false>, grid, dim3(kRgThreads), 0, stream, p);
       err = hipGetLastError();
     } else {
       const int need = p.L * E < 256 ? p.L * E : 256;
       const bool small = T <= 128;
-      if (need <= 16) err = small ? launch_bf16<1, 1, 1, 16>(p, stream) : launch_bf16<1, 1, 1, 4>(p, stream);
-      else if (need <= 64) err = small ? launch_bf16<1, 4, 1, 8>(p, stream) : launch_bf16<2, 4, 1, 4>(p, stream);
-      else err = small ? launch_bf16<1, 4, 4, 2>(p, stream) : launch_bf16<2, 4, 4, 1>(p, stream);
+      if (split) {   // T >= kRouteSplitMinT
+        if (need <= 16) err = launch_bf16<1, 1, 1, 4, false, true>(p, stream);
+        else if (need <= 64) err = launch_bf16<2, 4, 1, 4, false, true>(p, stream);
+        else err = launch_bf16<2, 4, 4, 1, false, true>(p, stream);
+      } else if (need <= 16) {
+        err = small ? launch_bf16<1, 1, 1, 16>(p, stream) : launch_bf16<1, 1, 1, 4>(p, stream);
+      } else if (need <= 64) {
+        err = small ? launch_bf16<1, 4, 1, 8>(p, stream) : launch_bf16<2, 4, 1, 4>(p, stream);
+      } else {
+        err = small ? launch_bf16<1, 4, 4, 2>(p, stream) : launch_bf16<2, 4, 4, 1>(p, stream);
+      }
     }
     if (err != hipSuccess) return err;
+    if (split) {
+      const size_t pairs = static_cast<size_t>(p.L) * T;
+      if (E <= kSelThreadE) {
+        dim3 grid(static_cast<unsigned>((pairs + kSelThreads - 1) / kSelThreads));
+        if (E == 8) hipLaunchKernelGGL(route_select_kernel<8>, grid, dim3(kSelThreads), 0, stream, p);
+        else if (E == 16) hipLaunchKernelGGL(route_select_kernel<16>, grid, dim3(kSelThreads), 0, stream, p);
+        else hipLaunchKernelGGL(route_select_kernel<0>, grid, dim3(kSelThreads), 0, stream, p);
+      } else {
+        constexpr int per_block = kSelThreads / 64;
+        dim3 grid(static_cast<unsigned>((pairs + per_block - 1) / per_block));
+        hipLaunchKernelGGL(route_select_wave_kernel, grid, dim3(kSelThreads), 0, stream, p);
+      }
+      err = hipGetLastError();
+      if (err != hipSuccess) return err;
+    }
   }
   return hipSuccess;
 }

@@ -38,9 +38,25 @@ def test_status_strings():
     assert lib.maskmoe_status_string(99) == b"unknown status"
 
 
-def _route(desc, Lyr=1, x=FAKE, w=FAKE, mask=None, prior=None, idx=FAKE, gate=FAKE, margin=None):
+def _route(desc, Lyr=1, x=FAKE, w=FAKE, mask=None, prior=None, idx=FAKE, gate=FAKE, margin=None, ws=None,
+           ws_bytes=0):
     lib = L.load()
-    return lib.maskmoe_route(ctypes.byref(desc), Lyr, x, w, mask, prior, idx, gate, margin, None)
+    return lib.maskmoe_route(ctypes.byref(desc), Lyr, x, w, mask, prior, idx, gate, margin, ws, ws_bytes, None)
+
+
+def test_route_workspace_bytes():
+    """Split routing (bf16, T >= 512, E <= 64) asks for fp32 [L, T, E] router logits; else none."""
+    lib = L.load()
+    nb = lambda Lyr=1, **k: lib.maskmoe_route_workspace_bytes(
+        ctypes.byref(L.make_desc(**{**dict(T=1024, d=64, E=8, K=2, dtype=L.BF16), **k})), Lyr)
+    assert nb() == 1024 * 8 * 4
+    assert nb(Lyr=32) == 32 * 1024 * 8 * 4
+    assert nb(E=64, K=6) == 1024 * 64 * 4
+    assert nb(T=511) == 0 and nb(E=65) == 0 and nb(dtype=L.F32) == 0
+    assert nb(Lyr=0) == 0 and nb(K=0) == 0
+    desc = L.make_desc(T=1024, d=64, E=8, K=2, dtype=L.BF16)
+    assert _route(desc, ws=FAKE, ws_bytes=1024 * 8 * 4 - 1) == L.E_INVAL      # too small
+    assert _route(desc, ws=FAKE + 8, ws_bytes=1 << 20) == L.E_INVAL          # misaligned
 
 
 def test_route_rejects_invalid_arguments():

@@ -176,3 +176,68 @@ def test_full_trace_router_sampled():
     ia = idx.cpu().numpy()
     assert ((ia >= 0) & (ia < cfg.E)).all() and (ia[..., 0] != ia[..., 1]).all()
     np.testing.assert_allclose(gate.sum(-1).cpu().numpy(), 1.0, atol=1e-5)
+
+
+# Split routing (logits to a workspace, then a selection kernel) against the one-kernel
+# routing: the same bits in idx, gate and margin. Router GEMM path and small-tile path; one
+# thread per pair (E <= 16, E % 4 != 0 included) and one wavefront per pair (16 < E <= 64).
+SPLIT_CASES = [
+    (1100, 4096, 8, 2, 32, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM),
+    (1500, 512, 64, 6, 4, L.ROUTE_SOFT_PRIOR, L.GATE_P),
+    (1030, 192, 48, 4, 5, L.ROUTE_PLAIN, L.GATE_RENORM),
+    (1024, 256, 16, 16, 8, L.ROUTE_HARD_MASK, L.GATE_P),
+    (2000, 2048, 64, 6, 1, L.ROUTE_HARD_MASK, L.GATE_P),
+    (600, 4096, 8, 2, 1, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM),
+    (700, 256, 17, 3, 1, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM),
+    (515, 128, 5, 3, 3, L.ROUTE_HARD_MASK, L.GATE_P),
+    (512, 64, 64, 16, 1, L.ROUTE_PLAIN, L.GATE_RENORM),
+]
+
+
+def _bits(t):
+    return t.contiguous().view(torch.int32).cpu()
+
+
+@pytest.mark.parametrize("T,d,E,K,Lyr,mode,gate_mode", SPLIT_CASES, ids=lambda v: str(v))
+def test_split_routing_matches_fused_bitwise(T, d, E, K, Lyr, mode, gate_mode):
+    U.say(f"route split vs fused T={T} d={d} E={E} K={K} L={Lyr} mode={mode} gate={gate_mode}")
+    x, w = _inputs(T, d, E, "bf16", 4000 + T + E, Lyr=Lyr)
+    rng = np.random.default_rng(T * E)
+    keep = [sorted(rng.choice(E, max(K, E // 2), replace=False)) for _ in range(Lyr)]
+    mask = np.stack([synth.binary_mask(E, k) for k in keep]) if mode == L.ROUTE_HARD_MASK else None
+    prior = np.stack([synth.concentrated_prior(E, k, 1.0) for k in keep]) if mode == L.ROUTE_SOFT_PRIOR else None
+    xd, wd = U.dev(x), U.dev(w)
+    desc = L.make_desc(T, d, E, K, dtype=L.BF16, route_mode=mode, gate_mode=gate_mode)
+    nbytes = L.load().maskmoe_route_workspace_bytes(desc, Lyr)
+    assert nbytes == Lyr * T * E * 4
+    ws = torch.full((nbytes,), 0x7F, dtype=torch.uint8, device="cuda")
+    a = L.maskmoe_route(xd, wd, K, mode, gate_mode, mask=mask, prior=prior, workspace=ws)
+    b = L.maskmoe_route(xd, wd, K, mode, gate_mode, mask=mask, prior=prior, workspace=None)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0])
+    assert torch.equal(_bits(a[1]), _bits(b[1])) and torch.equal(_bits(a[2]), _bits(b[2]))
+    # the split logits are the router logits (fp32 accumulation of the bf16 products)
+    z = ws.view(torch.float32).view(Lyr, T, E).cpu().double().numpy()
+    zr = np.stack([R.router_logits(U.f64(x, "bf16")[:64], U.f64(w, "bf16").reshape(Lyr, E, d)[l]) for l in range(Lyr)])
+    np.testing.assert_allclose(z[:, :64], zr, rtol=1e-4, atol=1e-4 * np.abs(zr).max())
+
+
+def test_split_routing_non_finite_logits_match_fused():
+    """Tokens whose logits are all NaN, or +inf / -inf for some experts: the fallback picks
+    (lowest untaken index) and the NaN / inf gates of both paths carry the same bits."""
+    T, d, E, K = 640, 128, 32, 4
+    x, w = _inputs(T, d, E, "bf16", 91)
+    xt = torch.from_numpy(x).view(torch.bfloat16).clone()
+    xt[3] = float("nan")
+    xt[100, 0] = float("inf")
+    xt[101, 5] = float("-inf")
+    xd = xt.cuda()
+    wd = U.dev(w)
+    for mode, gm, kw in [(L.ROUTE_PLAIN, L.GATE_RENORM, {}), (L.ROUTE_SOFT_PRIOR, L.GATE_P,
+                                                            dict(prior=synth.concentrated_prior(E, [1, 2, 9], 1.0)))]:
+        a = L.maskmoe_route(xd, wd, K, mode, gm, workspace="auto", **kw)
+        b = L.maskmoe_route(xd, wd, K, mode, gm, workspace=None, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(a[0], b[0])
+        assert torch.equal(_bits(a[1]), _bits(b[1])) and torch.equal(_bits(a[2]), _bits(b[2]))
+        assert a[0][3].tolist() == list(range(K))   # every key NaN: the lowest indices
