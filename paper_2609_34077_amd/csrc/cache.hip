@@ -16,6 +16,17 @@
 // bitmask (and flags invalid entries), and each step then reads its mask back as one
 // wave-uniform value (readlane). Per-step miss counts are gathered in lanes and written 64
 // bytes at a time.
+//
+// Few experts (E <= 16): the same step on 64 / W streams per wavefront (cache_seg_kernel,
+// W = 8 or 16 lanes per stream, lane sl of segment g owning expert sl of stream g), so that
+// the 16-lane SIMDs do not spend 4 cycles per instruction on 56 idle lanes. Bitmasks are the
+// segment's bits of the ballots, and the stream-uniform values (selected set, clock, cache
+// fill) are kept in every lane of the segment. A step's evictions are taken at once: the
+// victims of its misses are the eligible experts of smallest key, each expert's rank among the
+// segment's keys coming from DPP lane exchanges, which keeps the step free of a chain of
+// reductions per miss. The selected sets of kSegChunk steps of every stream are first built in
+// LDS (an LDS OR per valid entry); a set of fewer than K experts flags an invalid or repeated
+// entry.
 
 #include <limits.h>
 
@@ -121,6 +132,233 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_kernel(
   }
 }
 
+constexpr int kSegChunk = 512;
+constexpr int kSegBatch = 32;
+
+// The value of lane (lane ^ x) for x = 1..W-1 within each aligned group of W lanes (W = 8 or
+// 16), by DPP: quad permutations give x = 1..3, the half-row mirror x = 7 (and with a quad
+// permutation after it x = 4..6), the row mirror x = 15 (and after it x = 8..14).
+__device__ __forceinline__ int dpp_xor_quad(int v, int x) {   // x = 1, 2, 3
+  return x == 1 ? __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false)    // quad_perm [1,0,3,2]
+       : x == 2 ? __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false)    // quad_perm [2,3,0,1]
+                : __builtin_amdgcn_update_dpp(v, v, 0x1B, 0xF, 0xF, false);   // quad_perm [3,2,1,0]
+}
+
+// Rank of each lane's key within its group of W lanes: the number of lanes of the group
+// whose key is smaller. Every lane of the wavefront must be active.
+template <int W>
+__device__ __forceinline__ int seg_rank(int key) {
+  int rank = 0;
+  auto add8 = [&](int v) {   // the 8 lanes (lane ^ x), x = 0..7, of v
+    const int m = __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false);   // row_half_mirror: x = 7
+#pragma unroll
+    for (int x = 1; x <= 3; ++x) {
+      rank += dpp_xor_quad(v, x) < key ? 1 : 0;
+      rank += dpp_xor_quad(m, x) < key ? 1 : 0;
+    }
+    rank += m < key ? 1 : 0;
+  };
+  add8(key);
+  if (W == 16) {
+    const int r = __builtin_amdgcn_update_dpp(key, key, 0x140, 0xF, 0xF, false);   // row_mirror: x = 15
+    rank += r < key ? 1 : 0;
+    add8(r);   // x = 15 ^ 1 .. 15 ^ 7 = 14 .. 8
+  }
+  return rank;
+}
+
+// The same rank for 64-bit keys given as (hi, lo), compared as (signed hi, unsigned lo).
+template <int W>
+__device__ __forceinline__ int seg_rank(int hi, int lo) {
+  int rank = 0;
+  auto less = [&](int h, int l) { return (h < hi || (h == hi && static_cast<uint32_t>(l) < static_cast<uint32_t>(lo))) ? 1 : 0; };
+  auto add8 = [&](int vh, int vl) {
+    const int mh = __builtin_amdgcn_update_dpp(vh, vh, 0x141, 0xF, 0xF, false);
+    const int ml = __builtin_amdgcn_update_dpp(vl, vl, 0x141, 0xF, 0xF, false);
+#pragma unroll
+    for (int x = 1; x <= 3; ++x) {
+      rank += less(dpp_xor_quad(vh, x), dpp_xor_quad(vl, x));
+      rank += less(dpp_xor_quad(mh, x), dpp_xor_quad(ml, x));
+    }
+    rank += less(mh, ml);
+  };
+  add8(hi, lo);
+  if (W == 16) {
+    const int rh = __builtin_amdgcn_update_dpp(hi, hi, 0x140, 0xF, 0xF, false);
+    const int rl = __builtin_amdgcn_update_dpp(lo, lo, 0x140, 0xF, 0xF, false);
+    rank += less(rh, rl);
+    add8(rh, rl);
+  }
+  return rank;
+}
+
+template <int W>
+__device__ __forceinline__ uint32_t seg_bits(uint64_t ballot, int g) {
+  return static_cast<uint32_t>(ballot >> (g * W)) & ((1u << W) - 1u);
+}
+
+template <int POLICY, int W>   // E <= W
+__global__ __launch_bounds__(64) void cache_seg_kernel(
+    const int32_t* __restrict__ trace, int L, int S, int N, int K, int E, int B,
+    int32_t* __restrict__ state, int32_t* __restrict__ counts, int64_t* __restrict__ fetches,
+    int64_t* __restrict__ hits, uint8_t* __restrict__ f_per_step, int32_t* __restrict__ dev_error) {
+  constexpr int G = 64 / W;
+  constexpr int LD = kSegChunk + 1;   // odd row stride: the segments' reads of one step fall on distinct banks
+  __shared__ uint32_t sel_lds[G * LD];
+  constexpr int FLD = kSegChunk + 4;   // f_lds rows one bank apart
+  __shared__ uint8_t f_lds[G * FLD];
+  const int lane = threadIdx.x, g = lane / W, sl = lane % W;
+  const long nstreams = static_cast<long>(L) * S;
+  const long stream0 = static_cast<long>(blockIdx.x) * G;
+  const long stream = stream0 + g;
+  const bool live = stream < nstreams;
+
+  bool cached = false;
+  int stamp = INT_MAX;
+  int count = 0;
+  int ncached = 0;
+  int clock = 0;
+  bool bad = false;
+
+  if (POLICY == 1 && counts && live && sl < E) count = counts[stream * E + sl];
+  if (state) {  // slots are listed oldest first
+    for (int s = 0; s < B; ++s) {
+      const int e = live ? state[stream * B + s] : -1;   // the same in every lane of the segment
+      const uint32_t cm = seg_bits<W>(__ballot(cached), g);
+      const bool use = e >= 0 && e < E && !((cm >> (e & (W - 1))) & 1u);
+      bad = bad || (e >= 0 && !use);
+      cached = cached || (use && sl == e);
+      stamp = (use && sl == e) ? s : stamp;
+      ncached += use ? 1 : 0;
+    }
+    clock = B;
+  }
+
+  long tot_f = 0, tot_h = 0;
+  const float rk = 1.0f / static_cast<float>(K);
+  for (int n0 = 0; n0 < N; n0 += kSegChunk) {
+    const int ns = min(kSegChunk, N - n0);
+    for (int i = lane; i < G * LD; i += 64) sel_lds[i] = 0;
+    __syncthreads();
+    // each segment ORs its stream's valid entries into the steps' sets, kSegBatch loads in
+    // flight per lane; invalid and repeated entries show up as sets of fewer than K experts
+    if (live) {
+      const int per = ns * K;
+      const int32_t* tr = trace + (stream * N + n0) * static_cast<long>(K);
+      for (int q0 = 0; q0 < per; q0 += W * kSegBatch) {
+        int v[kSegBatch];
+#pragma unroll
+        for (int u = 0; u < kSegBatch; ++u) {
+          const int q = q0 + u * W + sl;
+          v[u] = q < per ? tr[q] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kSegBatch; ++u) {
+          const int q = q0 + u * W + sl;
+          // q / K in single precision: exact, the quotient being below 2^13 and K <= 16
+          const int step = static_cast<int>((static_cast<float>(q) + 0.5f) * rk);
+          if (v[u] >= 0 && v[u] < E) atomicOr(&sel_lds[g * LD + step], 1u << v[u]);
+        }
+      }
+    }
+    __syncthreads();
+    int chunk_f = 0, chunk_h = 0;
+    uint32_t sel_next = sel_lds[g * LD];
+    for (int j = 0; j < ns; ++j) {
+      const uint32_t sel = sel_next;   // 0 for a segment without a stream
+      sel_next = sel_lds[g * LD + j + 1];   // j + 1 <= kSegChunk < LD: inside the row
+      const bool mine = (sel >> sl) & 1u;
+      if (POLICY == 1) count += mine ? 1 : 0;
+      const uint32_t cmask = seg_bits<W>(__ballot(cached), g);
+      const uint32_t hitm = sel & cmask;
+      const uint32_t missm = sel & ~cmask;
+      const int h = __popc(hitm), nmiss = __popc(missm);
+      const uint32_t below = (1u << sl) - 1u;
+      if (POLICY != 2) {  // a hit becomes the most recently used
+        stamp = ((hitm >> sl) & 1u) ? clock + __popc(hitm & below) : stamp;
+        clock += h;
+      }
+      // The first B - ncached misses fill free slots; each later one evicts the eligible expert
+      // (cached, not selected at this step) of smallest key. Inserted experts are selected, so
+      // never eligible, and the eligible keys do not change during the step: the victims are
+      // the nevict eligible experts of smallest key, found by rank (keys are distinct).
+      const int nevict = max(0, ncached + nmiss - B);
+      if (__ballot(nevict > 0)) {
+        const bool eligible = cached && !mine;
+        int rank;
+        if (POLICY == 1) {  // lowest count first, then oldest stamp
+          const long key = eligible ? static_cast<long>(count) * (1l << 32) + stamp : LONG_MAX;
+          rank = seg_rank<W>(static_cast<int>(key >> 32), static_cast<int>(key & 0xffffffffl));
+        } else {
+          rank = seg_rank<W>(eligible ? stamp : INT_MAX);
+        }
+        const bool evict = eligible && rank < nevict;
+        cached = cached && !evict;
+        stamp = evict ? INT_MAX : stamp;
+      }
+      const bool insert = (missm >> sl) & 1u;   // misses take stamps in ascending expert order
+      stamp = insert ? clock + __popc(missm & below) : stamp;
+      cached = cached || insert;
+      clock += nmiss;
+      ncached += nmiss - nevict;
+      bad = bad || (live && h + nmiss != K);
+      chunk_h += h;
+      chunk_f += nmiss;
+      if (f_per_step) f_lds[g * FLD + j] = static_cast<uint8_t>(nmiss);   // the segment's lanes store the same byte
+    }
+    tot_h += chunk_h;
+    tot_f += chunk_f;
+    __syncthreads();
+    if (f_per_step) {
+      for (int gg = 0; gg < G; ++gg) {
+        if (stream0 + gg >= nstreams) break;
+        for (int j = lane; j < ns; j += 64) f_per_step[(stream0 + gg) * N + n0 + j] = f_lds[gg * FLD + j];
+      }
+    }
+  }
+
+  if (__ballot(bad) && lane == 0 && dev_error) *dev_error = 1;
+  if (!live) return;   // after the last cross-lane operation
+  if (sl == 0) {
+    fetches[stream] = tot_f;
+    hits[stream] = tot_h;
+  }
+  if (POLICY == 1 && counts && sl < E) counts[stream * E + sl] = count;
+  if (state) {
+    int rank = 0;   // position of this cached expert, oldest first
+    int nc = 0;
+    for (int o = 0; o < W; ++o) {
+      const int so = __shfl(cached ? stamp : INT_MAX, g * W + o, kWave);
+      nc += so != INT_MAX ? 1 : 0;
+      if (cached && so < stamp) ++rank;
+    }
+    int32_t* st = state + stream * B;
+    for (int s = sl; s < B; s += W)
+      if (s >= nc) st[s] = -1;
+    if (cached) st[rank] = sl;
+  }
+}
+
+template <int POLICY>
+void launch_cache_policy(const int32_t* trace, int L, int S, int N, int K, int E, int B, int32_t* state,
+                         int32_t* counts, int64_t* fetches, int64_t* hits, uint8_t* f_per_step, int32_t* dev_error,
+                         hipStream_t stream) {
+  const long streams = static_cast<long>(L) * S;
+  if (E <= 8) {
+    const dim3 grid(static_cast<unsigned>((streams + 7) / 8));
+    hipLaunchKernelGGL((cache_seg_kernel<POLICY, 8>), grid, dim3(64), 0, stream, trace, L, S, N, K, E, B, state,
+                       counts, fetches, hits, f_per_step, dev_error);
+  } else if (E <= 16) {
+    const dim3 grid(static_cast<unsigned>((streams + 3) / 4));
+    hipLaunchKernelGGL((cache_seg_kernel<POLICY, 16>), grid, dim3(64), 0, stream, trace, L, S, N, K, E, B, state,
+                       counts, fetches, hits, f_per_step, dev_error);
+  } else {
+    const dim3 grid(static_cast<unsigned>((streams + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock));
+    hipLaunchKernelGGL(cache_kernel<POLICY>, grid, dim3(64 * kCacheWavesPerBlock), 0, stream, trace, L, S, N, K, E,
+                       B, state, counts, fetches, hits, f_per_step, dev_error);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_cache(int policy, const int32_t* trace, int L, int S, int N, int K, int E, int B,
@@ -128,17 +366,12 @@ hipError_t launch_cache(int policy, const int32_t* trace, int L, int S, int N, i
                         uint8_t* f_per_step, int32_t* dev_error, hipStream_t stream) {
   const long streams = static_cast<long>(L) * S;
   if (streams == 0) return hipSuccess;
-  const dim3 grid(static_cast<unsigned>((streams + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock));
-  const dim3 block(64 * kCacheWavesPerBlock);
   if (policy == 1)
-    hipLaunchKernelGGL(cache_kernel<1>, grid, block, 0, stream, trace, L, S, N, K, E, B, state, counts, fetches,
-                       hits, f_per_step, dev_error);
+    launch_cache_policy<1>(trace, L, S, N, K, E, B, state, counts, fetches, hits, f_per_step, dev_error, stream);
   else if (policy == 2)
-    hipLaunchKernelGGL(cache_kernel<2>, grid, block, 0, stream, trace, L, S, N, K, E, B, state, counts, fetches,
-                       hits, f_per_step, dev_error);
+    launch_cache_policy<2>(trace, L, S, N, K, E, B, state, counts, fetches, hits, f_per_step, dev_error, stream);
   else
-    hipLaunchKernelGGL(cache_kernel<0>, grid, block, 0, stream, trace, L, S, N, K, E, B, state, counts, fetches,
-                       hits, f_per_step, dev_error);
+    launch_cache_policy<0>(trace, L, S, N, K, E, B, state, counts, fetches, hits, f_per_step, dev_error, stream);
   return hipGetLastError();
 }
 

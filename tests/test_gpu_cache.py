@@ -55,7 +55,10 @@ def test_hand_trace():
 
 @pytest.mark.parametrize("E,K,B,N", [(8, 2, 4, 512), (8, 2, 2, 100), (8, 2, 7, 65), (8, 2, 8, 33),
                                      (8, 2, 20, 40), (64, 6, 12, 300), (64, 6, 6, 77), (16, 3, 5, 1),
-                                     (33, 11, 32, 50), (64, 64, 64, 10), (5, 1, 1, 200)])
+                                     (33, 11, 32, 50), (64, 64, 64, 10), (5, 1, 1, 200),
+                                     # several 512-step chunks with a ragged last one; 9..16 experts
+                                     (8, 2, 4, 1100), (12, 3, 5, 600), (9, 4, 4, 513), (16, 16, 16, 30),
+                                     (17, 2, 4, 520)])
 def test_random_traces_bit_exact(E, K, B, N):
     U.say(f"cache E={E} K={K} B={B} N={N}")
     tr = synth.random_trace(3, 7, N, K, E, seed=E * 1000 + B * 10 + K, locality=0.6)
@@ -155,7 +158,7 @@ POLICIES = [L.CACHE_LRU, L.CACHE_LFU, L.CACHE_FIFO]
 
 @pytest.mark.parametrize("policy", POLICIES)
 @pytest.mark.parametrize("E,K,B,N", [(8, 2, 4, 300), (8, 2, 3, 65), (64, 6, 12, 200), (16, 3, 16, 40),
-                                     (6, 1, 2, 130), (64, 64, 64, 5)])
+                                     (6, 1, 2, 130), (64, 64, 64, 5), (12, 2, 4, 700), (16, 4, 6, 1030)])
 def test_policies_bit_exact(policy, E, K, B, N):
     U.say(f"cache policy={policy} E={E} K={K} B={B} N={N}")
     tr = synth.random_trace(2, 9, N, K, E, seed=E * 31 + B * 7 + K + policy, locality=0.55)
@@ -191,3 +194,21 @@ def test_resume_with_state_and_counts(policy):
     np.testing.assert_array_equal(whole["fetches"], first["fetches"] + second["fetches"])
     np.testing.assert_array_equal(whole["state"], second["state"])
     np.testing.assert_array_equal(whole["counts"], second["counts"])
+
+
+@pytest.mark.parametrize("E", [8, 12, 20])
+def test_invalid_initial_state_entries_skipped_and_flagged(E):
+    """Initial states listing an expert twice or an index >= E: those entries are skipped (the
+    oracle's reading of the state) and the device error flag is raised."""
+    K, B = 2, 4
+    tr = synth.random_trace(2, 5, 90, K, E, seed=E + 5, locality=0.5)
+    st = np.full((2, 5, B), -1, np.int32)
+    st[:, :, 0], st[:, :, 1], st[:, :, 2] = 3, 3, E + 1
+    st[1, 2] = [5, -1, 1, E]
+    g = _gpu(tr, E, B, st)
+    f, h, fps, final, bad = C.cache_fetches(tr, E, B, st)[:5]
+    np.testing.assert_array_equal(g["fetches"], f)
+    np.testing.assert_array_equal(g["hits"], h)
+    np.testing.assert_array_equal(g["f_per_step"], fps)
+    np.testing.assert_array_equal(g["state"], final)
+    assert not bad and int(g["dev_error"][0]) == 1
