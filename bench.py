@@ -278,6 +278,7 @@ def run_layer(args):
     for i in range(n_stage):
         for s in range(L.NUM_STAGES):
             stage[s] += sev[i][s].elapsed_time(sev[i][s + 1])
+    layer_ms = np.array([sev[i][0].elapsed_time(sev[i][L.NUM_STAGES]) for i in range(n_stage)])
     gu_s = sum(gu_ms) / 1e3
     decode = args.workload == "decode"
     if decode:
@@ -312,6 +313,8 @@ def run_layer(args):
         "roofline": roof,
         "step_roofline_frac": round(step_frac, 4),
         "stages_ms": {L.STAGES[s]: round(stage[s] / n_stage, 4) for s in range(L.NUM_STAGES)},
+        # spread of the layer forward alone (route to combine, no cache step) over the stage pass
+        "layer_ms_percentiles": {f"p{q}": round(float(np.percentile(layer_ms, q)), 4) for q in (10, 50, 90)},
     }
     return res, st
 
@@ -590,15 +593,20 @@ def run_trace(args):
 
     # Fetches/tok (Eq. 5, summed over layers) with the prior and with the zero prior, for each
     # eviction policy and a sweep of cache budgets (outside the timed region).
-    sweep = {}
+    sweep, concat = {}, {}
     for name, pr in (("prior", inp["prior"]), ("zero_prior", inp["prior_zero"])):
-        idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=pr, with_margin=False)
+        idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=pr, with_margin=False,
+                                    workspace=ws)
         tr = idx.view(cfg.L, cfg.S, cfg.N, cfg.K)
         for pol_name, pol in (("LRU", L.CACHE_LRU), ("LFU", L.CACHE_LFU), ("FIFO", L.CACHE_FIFO)):
             for B in (2, 4, 6):
                 r = L.maskmoe_cache_fetches(tr, cfg.E, B, policy=pol)
                 sweep.setdefault(pol_name, {}).setdefault(f"B{B}", {})[name] = round(
                     float(r["fetches"].sum().item()) / (cfg.S * cfg.N), 4)
+            # caches persisting across the sequences: one stream per layer, sequences back to back
+            # (tokens are sequence-major, so [L, S*N, K] is that trace)
+            r = L.maskmoe_cache_fetches(idx.view(cfg.L, 1, cfg.S * cfg.N, cfg.K), cfg.E, cfg.B, policy=pol)
+            concat.setdefault(pol_name, {})[name] = round(float(r["fetches"].sum().item()) / (cfg.S * cfg.N), 4)
     torch.cuda.synchronize()
     fetch = {k: sweep["LRU"][f"B{cfg.B}"][k] for k in ("prior", "zero_prior")}
     steps = args.steps if args.steps is not None else 10
@@ -640,6 +648,10 @@ def run_trace(args):
         "fetches_per_token_sweep": sweep,
         "fetch_reduction_pct_sweep": {p: {b: round(100 * (v["prior"] - v["zero_prior"]) / v["zero_prior"], 2)
                                           for b, v in d.items()} for p, d in sweep.items()},
+        "fetches_per_token_persistent_caches": {
+            "note": f"one cache per layer kept across the {cfg.S} sequences (replayed back to back), B={cfg.B}",
+            **{p: dict(v, reduction_pct=round(100 * (v["prior"] - v["zero_prior"]) / v["zero_prior"], 2))
+               for p, v in concat.items()}},
     }
     return res, dict(cfg=cfg, inp=inp)
 

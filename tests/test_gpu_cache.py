@@ -212,3 +212,13 @@ def test_invalid_initial_state_entries_skipped_and_flagged(E):
     np.testing.assert_array_equal(g["f_per_step"], fps)
     np.testing.assert_array_equal(g["state"], final)
     assert not bad and int(g["dev_error"][0]) == 1
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+def test_long_persistent_streams(policy):
+    """Caches kept across sequences: 3 layers x 1 stream of 131072 steps (the trace workload's
+    sequences back to back), E = 8, K = 2, B = 4; every step against the oracle."""
+    Lyr, N, K, E, B = 3, 131072, 2, 8, 4
+    U.say(f"cache persistent streams policy={policy} N={N}")
+    tr = synth.random_trace(Lyr, 1, N, K, E, seed=77 + policy, locality=0.6)
+    _compare(tr, E, B, policy=policy)
