@@ -134,6 +134,7 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_kernel(
 
 constexpr int kSegChunk = 512;
 constexpr int kSegBatch = 32;
+constexpr int kSegMinSteps = 64;
 
 // The value of lane (lane ^ x) for x = 1..W-1 within each aligned group of W lanes (W = 8 or
 // 16), by DPP: quad permutations give x = 1..3, the half-row mirror x = 7 (and with a quad
@@ -344,7 +345,13 @@ void launch_cache_policy(const int32_t* trace, int L, int S, int N, int K, int E
                          int32_t* counts, int64_t* fetches, int64_t* hits, uint8_t* f_per_step, int32_t* dev_error,
                          hipStream_t stream) {
   const long streams = static_cast<long>(L) * S;
-  if (E <= 8) {
+  // Short replays (a decode step's single step per stream) are dominated by the segmented
+  // kernel's set-up (clearing its LDS sets); the one-wavefront kernel starts faster.
+  if (N < kSegMinSteps) {
+    const dim3 grid(static_cast<unsigned>((streams + kCacheWavesPerBlock - 1) / kCacheWavesPerBlock));
+    hipLaunchKernelGGL(cache_kernel<POLICY>, grid, dim3(64 * kCacheWavesPerBlock), 0, stream, trace, L, S, N, K, E,
+                       B, state, counts, fetches, hits, f_per_step, dev_error);
+  } else if (E <= 8) {
     const dim3 grid(static_cast<unsigned>((streams + 7) / 8));
     hipLaunchKernelGGL((cache_seg_kernel<POLICY, 8>), grid, dim3(64), 0, stream, trace, L, S, N, K, E, B, state,
                        counts, fetches, hits, f_per_step, dev_error);

@@ -222,3 +222,16 @@ def test_long_persistent_streams(policy):
     U.say(f"cache persistent streams policy={policy} N={N}")
     tr = synth.random_trace(Lyr, 1, N, K, E, seed=77 + policy, locality=0.6)
     _compare(tr, E, B, policy=policy)
+
+
+@pytest.mark.parametrize("E", [8, 12])
+def test_invalid_entries_long_trace(E):
+    """Invalid entries (negative, >= E, repeated within a step) in traces long enough for the
+    several-streams-per-wavefront kernel: skipped and flagged as the oracle does."""
+    tr = synth.random_trace(2, 9, 300, 3, E, seed=E * 7, locality=0.5)
+    tr[0, 1, 5] = [1, 1, 2]
+    tr[1, 8, 299] = [-1, 0, 3]
+    tr[1, 0, 70] = [E, E + 5, 2]
+    g = _compare(tr, E, 4)
+    assert int(g["dev_error"][0]) == 1
+    assert g["f_per_step"][0, 1, 5] <= 2 and g["f_per_step"][1, 0, 70] <= 1
