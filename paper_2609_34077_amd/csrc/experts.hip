@@ -27,6 +27,8 @@
 #include <cmath>
 #include <cstdlib>
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "gemm_tile.hpp"
 #include "kernels.hpp"
@@ -266,8 +268,8 @@ static dim3 combine_grid(int T, int d) { return dim3(T * ((d + kCombineCols - 1)
 // reduction dimension in chunks of DEC_CK values. Each chunk is loaded with 16-byte loads in
 // which a wavefront covers whole 128-byte row segments (full cache lines), stored to LDS with
 // a 16-byte row pad (conflict-free MFMA operand reads), and multiplied on MFMA 16x16x32 with
-// the token rows padded to 16. The next chunk's loads are in flight while the current one is
-// multiplied. Both projections split their reduction dimension into slices when few experts
+// the token rows padded to 16. The next two chunks' loads (weights and token operands) are in
+// flight while the current one is multiplied. Both projections split their reduction dimension into slices when few experts
 // are active, so that enough workgroups stream at once: the gate/up slices are added by a
 // small SwiGLU pass, the down slices by the combine, always in slice order. (Letting the
 // last workgroup of a column slab do the combine needs a device-scope release per
@@ -312,7 +314,8 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
   constexpr int PER = R * UPR / DEC_THREADS;
   constexpr int TPW = (NTILE + 3) / 4;
   static_assert(R * UPR % DEC_THREADS == 0, "chunk must split evenly over the threads");
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint16_t* src[PER];
   int dst[PER];
 #pragma unroll
@@ -324,37 +327,72 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
   }
   const uint16_t* ap = arow + k0 + (lane >> 4) * 8;
   const int nc = klen / DEC_CK;
-  u32x4 reg[PER];
+  // Weight chunks c + 1 and c + 2 are in flight in registers while chunk c is multiplied from
+  // LDS; the token rows' operands travel with them (a wait on a load issued after the weight
+  // loads would also wait for those).
+  constexpr int KS = DEC_CK / 32;
+  u32x4 reg[2][PER], areg[2][KS];
+  auto load_w = [&](int c, u32x4* r) {
 #pragma unroll
-  for (int i = 0; i < PER; ++i) reg[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i]));
+    for (int i = 0; i < PER; ++i) r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i] + c * DEC_CK));
+  };
+  auto load_a = [&](int c, u32x4* r) {
 #pragma unroll
-  for (int i = 0; i < PER; ++i) *reinterpret_cast<u32x4*>(&lds[0][dst[i]]) = reg[i];
+    for (int ks = 0; ks < KS; ++ks) r[ks] = *reinterpret_cast<const u32x4*>(ap + c * DEC_CK + ks * 32);
+  };
+  auto store = [&](int buf, const u32x4* r) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) *reinterpret_cast<u32x4*>(&lds[buf][dst[i]]) = r[i];
+  };
+  // The loop is straight-line in its loads and stores (the tail steps are peeled), so the
+  // compiler's wait counts stay exact: a wait for chunk c + 1 never waits for chunk c + 2.
+  load_w(0, reg[0]);
+  load_a(0, areg[0]);
+  load_w(min(1, nc - 1), reg[1]);   // nc == 1 (d or F of 64) reloads chunk 0
+  load_a(min(1, nc - 1), areg[1]);
+  store(0, reg[0]);
   __syncthreads();
-  for (int c = 0; c < nc; ++c) {
-    const int buf = c & 1;
-    if (c + 1 < nc) {
+  // one chunk; BUF = c & 1 is a compile-time index so that the staging stays in registers;
+  // LOAD: chunk c + 2 exists; STORE: chunk c + 1 exists
+  auto step = [&](int c, auto buf_c, auto load_c, auto store_c) {
+    constexpr int buf = decltype(buf_c)::value;
+    if (decltype(load_c)::value) load_w(c + 2, reg[buf]);   // reg[buf] held chunk c, already in LDS
+    __builtin_amdgcn_sched_barrier(0);   // keep the loads first and the LDS stores last
 #pragma unroll
-      for (int i = 0; i < PER; ++i)
-        reg[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i] + (c + 1) * DEC_CK));
-    }
-#pragma unroll
-    for (int ks = 0; ks < DEC_CK / 32; ++ks) {
-      const u32x4 a = *reinterpret_cast<const u32x4*>(ap + c * DEC_CK + ks * 32);
+    for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
       for (int q = 0; q < TPW; ++q) {
         const int tile = wave + 4 * q;
-        if (tile < NTILE) {
+        if (NTILE % 4 == 0 || tile < NTILE) {
           const int r = tile * 16 + (lane & 15);
           const u32x4 b = *reinterpret_cast<const u32x4*>(&lds[buf][r * PITCH + ks * 64 + (lane >> 4) * 16]);
-          acc[q] = mfma_16x16x32(a, b, acc[q]);
+          acc[q] = mfma_16x16x32(areg[buf][ks], b, acc[q]);
         }
       }
     }
-    if (c + 1 < nc) {
-#pragma unroll
-      for (int i = 0; i < PER; ++i) *reinterpret_cast<u32x4*>(&lds[buf ^ 1][dst[i]]) = reg[i];
-    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (decltype(load_c)::value) load_a(c + 2, areg[buf]);
+    if (decltype(store_c)::value) store(buf ^ 1, reg[buf ^ 1]);
     __syncthreads();
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using Y = std::true_type;
+  using N = std::false_type;
+  int c = 0;
+  for (; c + 3 < nc; c += 2) {
+    step(c, B0{}, Y{}, Y{});
+    step(c + 1, B1{}, Y{}, Y{});
+  }
+  if (nc - c == 3) {
+    step(c, B0{}, Y{}, Y{});
+    step(c + 1, B1{}, N{}, Y{});
+    step(c + 2, B0{}, N{}, N{});
+  } else if (nc - c == 2) {
+    step(c, B0{}, N{}, Y{});
+    step(c + 1, B1{}, N{}, N{});
+  } else {
+    step(c, B0{}, N{}, N{});
   }
 }
 
