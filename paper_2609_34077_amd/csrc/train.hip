@@ -73,7 +73,9 @@ __device__ __forceinline__ float wave_max(float v) {
 // products share one pass over d (four columns per lane and step when the rows allow vector
 // loads) and are summed across lanes in a fixed order; lane l holds the softmax probability of
 // experts l, l + 64, l + 128, l + 192 of the token's logits.
-template <typename TIn>
+// KC: K when known at compile time (0: the runtime K), so that the K rows' loads of a step are
+// issued together rather than behind one branch each.
+template <typename TIn, int KC>
 __global__ __launch_bounds__(kTrainThreads) void gate_grad_kernel(const TIn* __restrict__ dy,
                                                                   const float* __restrict__ eo,
                                                                   const float* __restrict__ logits,
@@ -91,13 +93,14 @@ __global__ __launch_bounds__(kTrainThreads) void gate_grad_kernel(const TIn* __r
   float acc[kMaxKTrain];
 #pragma unroll
   for (int k = 0; k < kMaxKTrain; ++k) acc[k] = 0.0f;
+  constexpr int KL = KC ? KC : kMaxKTrain;
   if (vec) {   // d % 4 == 0, rows 16-byte (fp32) / 8-byte (bf16) aligned
 #pragma unroll 4
     for (int c = lane * 4; c < d; c += kWave * 4) {
       const float4 a = load4(dyt, c);
 #pragma unroll
-      for (int k = 0; k < kMaxKTrain; ++k) {
-        if (k < K) {
+      for (int k = 0; k < KL; ++k) {
+        if (KC || k < K) {
           const float4 e = load4(eot, static_cast<size_t>(k) * d + c);
           acc[k] += a.x * e.x + a.y * e.y + a.z * e.z + a.w * e.w;
         }
@@ -402,9 +405,16 @@ int wgrad_slices(int T, int d, int E, int cols) {
 template <typename TIn>
 hipError_t launch_stage1(const Stage1Args& a, hipStream_t stream) {
   const TIn* dy = static_cast<const TIn*>(a.dy);
-  hipLaunchKernelGGL((gate_grad_kernel<TIn>), dim3((a.T + kWaves - 1) / kWaves), dim3(kTrainThreads), 0, stream,
-                     dy, a.expert_out,
-                     a.router_logits, a.idx, a.T, a.d, a.E, a.K, a.gate_mode, a.vec_rows, a.d_gate, a.dz, a.dm_tok);
+  const dim3 grid((a.T + kWaves - 1) / kWaves), block(kTrainThreads);
+#define MASKMOE_GATE_GRAD(KC)                                                                                  \
+  hipLaunchKernelGGL((gate_grad_kernel<TIn, KC>), grid, block, 0, stream, dy, a.expert_out, a.router_logits, a.idx, \
+                     a.T, a.d, a.E, a.K, a.gate_mode, a.vec_rows, a.d_gate, a.dz, a.dm_tok)
+  switch (a.K) {   // the two models' K, and a runtime-K instance for the rest
+    case 2: MASKMOE_GATE_GRAD(2); break;
+    case 6: MASKMOE_GATE_GRAD(6); break;
+    default: MASKMOE_GATE_GRAD(0); break;
+  }
+#undef MASKMOE_GATE_GRAD
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(mask_sum_kernel, dim3(a.E), dim3(kTrainThreads), 0, stream, a.dm_tok, a.T, a.E, a.dm);
