@@ -53,7 +53,7 @@ int check_mask_prior(int mode, int L, int E, int K, const uint8_t* mask, const f
 }
 
 struct Layout {
-  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, pcount, Z, H, P, O, total;
+  size_t idx, gate, offsets, tile_off, active, n_active, perm, inv, row_tok, pcount, Z, H, P, O, TP, total;
   size_t AB, train_total;   // training (bf16): gate / up pre-activations [rows, 2F] after `total`
   // adapters (bf16), after `total`: rank projections U, V [rows, 64], scaled B [G, 2F | d, 64]
   size_t LU, LV, LBGU, LBD, lora_total;
@@ -100,9 +100,9 @@ Layout layout(const maskmoe_layer_desc& d) {
   const size_t dec_rows = dec_T * (d.K + d.n_shared);
   w.P = take(maskmoe::kDecodeMaxSplitGateUp * dec_rows * 2 * d.F * 4);
   const size_t o_rows = maskmoe::kDecodeMaxSplit * dec_rows;
-  // the grouped path's down GEMM may split its reduction into kGroupedMaxKSplit partials
-  const size_t g_rows = rows * maskmoe::kGroupedMaxKSplit;
-  w.O = take((g_rows > o_rows ? g_rows : o_rows) * d.d * 4);
+  w.O = take((rows > o_rows ? rows : o_rows) * d.d * 4);
+  // partial tiles of the grouped GEMMs' split tail tiles (bf16 layers)
+  w.TP = take(d.dtype == MASKMOE_BF16 ? maskmoe::kTailPartBytes : 0);
   w.total = off;
   w.AB = take(d.dtype == MASKMOE_BF16 ? rows * 2 * d.F * 2 : 0);
   w.train_total = off;
@@ -304,7 +304,8 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
       la.bp_down = reinterpret_cast<uint16_t*>(ws + w.LBD);
     }
     e = maskmoe::launch_experts_bf16(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
-                                     reinterpret_cast<float*>(ws + w.O), y, static_cast<int>(max_tiles), stream,
+                                     reinterpret_cast<float*>(ws + w.O), reinterpret_cast<float*>(ws + w.TP), y,
+                                     static_cast<int>(max_tiles), stream,
                                      expert_marks, train ? reinterpret_cast<uint16_t*>(ws + w.AB) : nullptr,
                                      lora ? &la : nullptr);
   }

@@ -52,11 +52,76 @@ struct GemmArgs {
   uint16_t* ab;             // EPI 0, training: gate / up pre-activations bf16 [rows, 2F], or null
   const uint16_t* lora_u;   // LORA: rank-r projections of this GEMM's A rows, bf16 [rows, 64]
   const uint16_t* lora_b;   // LORA: (alpha / r) B rows matching the B operand, bf16 [G, N rows, 64]
+  float* part;              // partial tiles of split tail tiles, kTailSlots x [64 x 512 x 4] fp32
   int G, E, F, d;
-  int mt_max;               // grid bound on row tiles (the grid is mt_max * n_tiles workgroups)
-  int n_tiles;              // column tiles times k_split
-  int k_split;              // EPI 1: slices of the reduction, slice z writes out + z * rows * d
+  int mt_max;               // bound on row tiles (the grid is sized for mt_max * n_tiles tiles)
+  int n_tiles;              // column tiles
+  int cu_xcd;               // workgroups an XCD runs at once (one per CU)
 };
+
+// Tail split. The hardware deals workgroups round-robin over the 8 XCDs; XCD x takes a
+// contiguous range of the live tiles (the partition of xcd_tile_id) and runs cu_xcd of them at
+// a time. All tiles cost the same, so the r tiles of an XCD's last, partial round would leave
+// most of its CUs idle; instead each of them is split into s reduction slices (the largest
+// power of two <= kTailMaxSplit with r * s <= min(cu_xcd, kTailSlotsPerXcd), s dividing the
+// k-tiles and leaving >= kTailMinK per slice), so the last round is short and full. A slice
+// writes its partial tile to a slot; grouped_tail_fixup adds a tile's slices in slice order and
+// applies the epilogue.
+// Only the down GEMM splits (its long reductions amortise a slice's fixed costs; the gate/up
+// GEMM's epilogue needs whole sums): measured, slices shorter than 16 k-tiles and splits of
+// the gate/up tiles cost more than the idle round they save.
+constexpr int kTailSlotsPerXcd = kTailSlots / 8;
+constexpr int kTailMaxSplit = 8, kTailMinK = 16;
+__host__ __device__ constexpr bool tail_can_split(int epi, int nk) { return epi == 1 && nk % 2 == 0 && nk / 2 >= kTailMinK; }
+
+struct TileJob {
+  int lid;    // logical tile (grouped_tile_coords order)
+  int z, s;   // reduction slice z of s (s == 1: the whole tile)
+  int slot;   // partial-tile slot when s > 1
+};
+
+struct XcdShare {
+  int base, full, r, s;   // first tile, tiles run whole, tail tiles, their slices
+};
+
+__device__ __forceinline__ XcdShare xcd_share(int xcd, int live, int cu_xcd, int nk, bool split_ok) {
+  XcdShare x;
+  const int q = live >> 3, rem = live & 7;
+  const int count = q + (xcd < rem ? 1 : 0);
+  x.base = xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q;
+  x.full = count / cu_xcd * cu_xcd;
+  x.r = count - x.full;
+  const int cap = min(cu_xcd, kTailSlotsPerXcd);
+  x.s = 1;
+  if (split_ok && x.r > 0)
+    for (int s = 2; s <= kTailMaxSplit; s *= 2)
+      if (x.r * s <= cap && nk % s == 0 && nk / s >= kTailMinK) x.s = s;
+  return x;
+}
+
+// The job of workgroup bid, or false when it has none.
+__device__ __forceinline__ bool tile_job(int bid, int live, int cu_xcd, int nk, bool split_ok, TileJob& j) {
+  const int xcd = bid & 7, local = bid >> 3;
+  const XcdShare x = xcd_share(xcd, live, cu_xcd, nk, split_ok);
+  if (local < x.full || x.s == 1) {
+    if (local >= x.full + x.r) return false;
+    j.lid = x.base + local;
+    j.z = 0;
+    j.s = 1;
+    j.slot = -1;
+    return true;
+  }
+  const int t = local - x.full;   // tail unit
+  if (t >= x.r * x.s) return false;
+  j.lid = x.base + x.full + t / x.s;
+  j.z = t % x.s;
+  j.s = x.s;
+  j.slot = xcd * kTailSlotsPerXcd + t;
+  return true;
+}
+
+// Partial-tile slot layout: float4 e of thread tid at [e][tid] (coalesced for both sides).
+constexpr int kTailTileFloats = kTileM * kTileN;
 
 __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt) {
   int lo = 0, hi = G;  // tile_off[lo] <= mt < tile_off[hi]
@@ -67,6 +132,50 @@ __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt
   return lo;
 }
 
+// Epilogue of a finished tile: rows [row0, row_end) of one group, columns from n0. EPI 0:
+// SwiGLU of the gate / up column pairs into H (bf16; the pre-activations into ab when given);
+// EPI 1: O (fp32). acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column
+// (lane & 31) of fragment j.
+template <int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&acc)[kTileTM][kTileTN], int row0,
+                                              int row_end, int n0) {
+  constexpr int WN = 4, TM = kTileTM, TN = kTileTN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int Ndim = EPI == 0 ? p.F : p.d;
+  float* out_f32 = static_cast<float*>(p.out);
+  const int col_in = lane & 31;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int row = row0 + wm * 128 + i * 32 + 8 * jj + 4 * (lane >> 5) + ii;
+        if (row >= row_end) continue;
+        const int r = 4 * jj + ii;
+        if (EPI == 0) {
+          const int col = n0 + wn * 32 + col_in;
+          if (col < Ndim) {
+            const float h = silu(acc[i][0][r]) * acc[i][1][r];
+            static_cast<uint16_t*>(p.out)[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(h);
+            if (p.ab) {
+              p.ab[static_cast<size_t>(row) * 2 * Ndim + col] = f32_to_bf16(acc[i][0][r]);
+              p.ab[static_cast<size_t>(row) * 2 * Ndim + Ndim + col] = f32_to_bf16(acc[i][1][r]);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int col = n0 + wn * 64 + j * 32 + col_in;
+            if (col < Ndim) out_f32[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
+          }
+        }
+      }
+    }
+  }
+}
+
 template <int EPI, bool LORA = false>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
   constexpr int WN = 4;                 // waves: 2 along rows x 4 along columns
@@ -75,23 +184,22 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   __shared__ u32x4 lds_a[2][BM * 8];
   __shared__ u32x4 lds_b[2][BN * 8];
 
-  // The grid covers the most row tiles any routing can need; only the first mt_live * n_tiles
-  // workgroups (spread evenly over the XCDs by the hardware's round-robin) have a tile, and the
-  // XCD-aware order is built over those, so every XCD gets an equal share of the live tiles.
+  // The grid covers the most tiles any routing can need plus the tail slices; tile_job gives
+  // each XCD's workgroups that XCD's share of the live tiles (their count read on the device),
+  // so every XCD gets an equal share however many tiles are live.
   const int mt_live = p.tile_off[p.G];
   const int live = mt_live * p.n_tiles;
-  if (static_cast<int>(blockIdx.x) >= live) return;
+  const int Kdim = EPI == 0 ? p.d : p.F;
+  TileJob job;
+  if (!tile_job(static_cast<int>(blockIdx.x), live, p.cu_xcd, Kdim / BK, tail_can_split(EPI, Kdim / BK), job)) return;
   int mt, nt;
-  grouped_tile_coords(xcd_tile_id(live), mt_live, p.n_tiles, mt, nt);
-  const int z = nt % p.k_split;   // reduction slice (adjacent slices of a tile share its B rows)
-  nt /= p.k_split;
+  grouped_tile_coords(job.lid, mt_live, p.n_tiles, mt, nt);
+  const int z = job.z;
   const int g = find_group(p.tile_off, p.G, mt);
   const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM;
   const int row_end = p.offsets[g + 1];
-  const int Kdim = EPI == 0 ? p.d : p.F;
-  const int Ndim = EPI == 0 ? p.F : p.d;
   const int n0 = nt * (EPI == 0 ? BN / 2 : BN);
-  const int nks = Kdim / BK / p.k_split;   // k-tiles of this slice
+  const int nks = Kdim / BK / job.s;   // k-tiles of this slice
   const int k0 = z * nks * BK;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -151,40 +259,58 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   } else {
     gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b);
   }
-  float* out_f32 = EPI == 1 ? static_cast<float*>(p.out) + static_cast<size_t>(z) * p.offsets[p.G] * Ndim : nullptr;
-
-  // Epilogue. acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column
-  // (lane & 31) of fragment j.
-  const int col_in = lane & 31;
+  if (job.s > 1) {   // a slice of a split tail tile: its partial tile goes to the slot
+    float4* dst = reinterpret_cast<float4*>(p.part + static_cast<size_t>(job.slot) * kTailTileFloats);
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int row = row0 + wm * 128 + i * 32 + 8 * jj + 4 * (lane >> 5) + ii;
-        if (row >= row_end) continue;
-        const int r = 4 * jj + ii;
-        if (EPI == 0) {
-          const int col = n0 + wn * 32 + col_in;
-          if (col < Ndim) {
-            const float h = silu(acc[i][0][r]) * acc[i][1][r];
-            static_cast<uint16_t*>(p.out)[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(h);
-            if (p.ab) {
-              p.ab[static_cast<size_t>(row) * 2 * Ndim + col] = f32_to_bf16(acc[i][0][r]);
-              p.ab[static_cast<size_t>(row) * 2 * Ndim + Ndim + col] = f32_to_bf16(acc[i][1][r]);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wn * 64 + j * 32 + col_in;
-            if (col < Ndim) out_f32[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
-          }
-        }
-      }
-    }
+        for (int q = 0; q < 4; ++q)
+          dst[((i * TN + j) * 4 + q) * GEMM_THREADS + tid] =
+              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+    return;
   }
+  gemm_epilogue<EPI>(p, acc, row0, row_end, n0);
+}
+
+// Adds the slices of each split tail tile (grouped_gemm_bf16) in slice order and applies the
+// GEMM's epilogue; one workgroup per possible tail tile, grid 8 x kTailSlotsPerXcd.
+template <int EPI>
+__global__ __launch_bounds__(GEMM_THREADS) void grouped_tail_fixup(const GemmArgs p) {
+  const int mt_live = p.tile_off[p.G];
+  const int live = mt_live * p.n_tiles;
+  const int nk = (EPI == 0 ? p.d : p.F) / BK;
+  const int xcd = blockIdx.x & 7, t = blockIdx.x >> 3;
+  const XcdShare x = xcd_share(xcd, live, p.cu_xcd, nk, tail_can_split(EPI, nk));
+  if (x.s == 1 || t >= x.r) return;
+  const int tid = threadIdx.x;
+  constexpr int TM = kTileTM, TN = kTileTN;
+  const float4* src = reinterpret_cast<const float4*>(p.part) +
+                      static_cast<size_t>(xcd * kTailSlotsPerXcd + t * x.s) * (kTailTileFloats / 4);
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const size_t e = static_cast<size_t>((i * TN + j) * 4 + q) * GEMM_THREADS + tid;
+        float4 v = src[e];
+        for (int z = 1; z < x.s; ++z) {
+          const float4 u = src[static_cast<size_t>(z) * (kTailTileFloats / 4) + e];
+          v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+        }
+        acc[i][j][4 * q] = v.x;
+        acc[i][j][4 * q + 1] = v.y;
+        acc[i][j][4 * q + 2] = v.z;
+        acc[i][j][4 * q + 3] = v.w;
+      }
+  int mt, nt;
+  grouped_tile_coords(x.base + x.full + t, mt_live, p.n_tiles, mt, nt);
+  const int g = find_group(p.tile_off, p.G, mt);
+  gemm_epilogue<EPI>(p, acc, p.offsets[g] + (mt - p.tile_off[g]) * BM, p.offsets[g + 1],
+                     nt * (EPI == 0 ? BN / 2 : BN));
 }
 
 // y_t = sum_k gate[t,k] * O[inv[t*K+k]] + sum_s O[T*K + s*T + t]; fp32 sum in k order, one
@@ -578,35 +704,34 @@ __global__ __launch_bounds__(256) void f32_down_kernel(const F32Args p) {
 
 }  // namespace
 
-// Reduction slices of the down GEMM. Its tiles are few compared with the CUs (the Mixtral
-// fine-tuning layer has 68 x 16 = 1088, 4.25 rounds of 256 CUs), so a last partial round can
-// idle most of the chip; two slices of half the k-tiles each (8.5 rounds) waste less, at the
-// price of one more partial [rows, d] for the combine to add. Two slices are used when that
-// raises the share of busy CU-rounds by more than 5 points and each slice keeps >= 32 k-tiles.
-int grouped_down_split(int max_tiles, int n_tiles, int k_tiles) {
-  static const int n_cu = [] {
+// Workgroups an XCD runs at once: one per CU (the tile's 128 KiB of LDS), the CUs split evenly
+// over the 8 XCDs.
+static int cus_per_xcd() {
+  static const int n = [] {
     int dev = 0, cu = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                               hipSuccess || cu <= 0)
+                                               hipSuccess || cu < 8)
       cu = 256;
-    return cu;
+    return cu / 8;
   }();
-  if (k_tiles % 2 || k_tiles / 2 < 32) return 1;
-  auto busy = [&](long wgs) {
-    const long rounds = (wgs + n_cu - 1) / n_cu;
-    return rounds > 0 ? static_cast<double>(wgs) / (rounds * n_cu) : 1.0;
-  };
-  const long w1 = static_cast<long>(max_tiles) * n_tiles;
-  return busy(2 * w1) > busy(w1) + 0.05 ? 2 : 1;
+  return n;
 }
 
-hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
+// Grid of a grouped GEMM: 8 XCDs x (their largest share of tiles + tail slices).
+static dim3 grouped_grid(int max_tiles, int n_tiles) {
+  const long per_xcd = (static_cast<long>(max_tiles) * n_tiles + 7) / 8 + kTailSlotsPerXcd;
+  return dim3(static_cast<unsigned>(8 * per_xcd));
+}
+
+hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O, float* part,
                                void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks, uint16_t* ab,
                                const LoraArgs* lora) {
   const int G = a.E + a.n_shared;
   GemmArgs g{};
   g.ab = ab;
-  g.k_split = 1;
+  g.part = part;
+  g.cu_xcd = cus_per_xcd();
+  const dim3 fixup_grid(8 * kTailSlotsPerXcd);
   hipError_t err;
   if (lora) {
     err = launch_lora_pack(*lora, G, a.E, a.F, a.d, stream);
@@ -630,9 +755,9 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   const int nt1 = (a.F + BN / 2 - 1) / (BN / 2);
   g.n_tiles = nt1;
   if (lora)
-    hipLaunchKernelGGL((grouped_gemm_bf16<0, true>), dim3(max_tiles * nt1), dim3(GEMM_THREADS), 0, stream, g);
+    hipLaunchKernelGGL((grouped_gemm_bf16<0, true>), grouped_grid(max_tiles, nt1), dim3(GEMM_THREADS), 0, stream, g);
   else
-    hipLaunchKernelGGL(grouped_gemm_bf16<0>, dim3(max_tiles * nt1), dim3(GEMM_THREADS), 0, stream, g);
+    hipLaunchKernelGGL(grouped_gemm_bf16<0>, grouped_grid(max_tiles, nt1), dim3(GEMM_THREADS), 0, stream, g);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
@@ -646,22 +771,26 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
 
   g.ab = nullptr;
   g.a = H;
-  g.k_split = grouped_down_split(max_tiles, (a.d + BN - 1) / BN, a.F / BK);
   g.w = static_cast<const uint16_t*>(a.w_down);
   g.ws = static_cast<const uint16_t*>(a.ws_down);
   g.out = O;
   const int nt2 = (a.d + BN - 1) / BN;
-  g.n_tiles = nt2 * g.k_split;
+  g.n_tiles = nt2;
   if (lora)
-    hipLaunchKernelGGL((grouped_gemm_bf16<1, true>), dim3(max_tiles * g.n_tiles), dim3(GEMM_THREADS), 0, stream, g);
+    hipLaunchKernelGGL((grouped_gemm_bf16<1, true>), grouped_grid(max_tiles, nt2), dim3(GEMM_THREADS), 0, stream, g);
   else
-    hipLaunchKernelGGL(grouped_gemm_bf16<1>, dim3(max_tiles * g.n_tiles), dim3(GEMM_THREADS), 0, stream, g);
+    hipLaunchKernelGGL(grouped_gemm_bf16<1>, grouped_grid(max_tiles, nt2), dim3(GEMM_THREADS), 0, stream, g);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
+  if (tail_can_split(1, a.F / BK)) {
+    hipLaunchKernelGGL(grouped_tail_fixup<1>, fixup_grid, dim3(GEMM_THREADS), 0, stream, g);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
   record_mark(marks, 1, stream);
 
   hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                     a.K, a.n_shared, a.d, y, g.k_split, a.expert_out);
+                     a.K, a.n_shared, a.d, y, 1, a.expert_out);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;

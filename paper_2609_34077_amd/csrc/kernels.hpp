@@ -110,15 +110,15 @@ hipError_t launch_lora_down(const uint16_t* src, const int32_t* row_tok, int K, 
                             int nq, int G, int E, const PermBuffers& pb, int max_tiles, uint16_t* out,
                             hipStream_t stream);
 
-// Slices of the down GEMM's reduction (1 or kGroupedMaxKSplit); O then holds that many [rows, d]
-// partials.
-constexpr int kGroupedMaxKSplit = 2;
-int grouped_down_split(int max_tiles, int n_tiles, int k_tiles);
+// Partial-tile slots of the grouped GEMMs' split tail tiles (fp32 256 x 256 each, 64 MiB).
+constexpr int kTailSlots = 256;
+constexpr size_t kTailPartBytes = static_cast<size_t>(kTailSlots) * 256 * 256 * 4;
 
 // bf16, T > kDecodeMaxT (any T when training or with adapters): H = SwiGLU(X_g W_gate,up^T)
 // per group; O = H W_down^T; y = combine. ab (training): the gate and up pre-activations,
 // bf16 [rows, 2F]. lora: the experts' low-rank adapters, added inside both GEMMs.
-hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O,
+// part: kTailPartBytes of workspace for the split tail tiles.
+hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O, float* part,
                                void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks,
                                uint16_t* ab = nullptr, const LoraArgs* lora = nullptr);
 // bf16, T <= kDecodeMaxT: weight-streaming gate/up kernel (split-K into P [split_gu, rows, 2F]
