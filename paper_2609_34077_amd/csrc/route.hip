@@ -189,19 +189,15 @@ __global__ __launch_bounds__(kSelThreads) void route_select_kernel(const RoutePa
   select_pair<EC>(p, zs + threadIdx.x * (E + 1), lo + l * E, q, false);
 }
 
-// kSelThreadE < E <= 64: one wavefront per pair, lane e holding expert e. Each expert's rank
-// (the number of valid keys larger, or equal with a lower index; -inf and NaN keys are not
-// valid) is its position in the successive picks of select_pair, so both give the same
-// selection, margin and gate bits (the normalisers are summed in the same order).
-__global__ __launch_bounds__(kSelThreads) void route_select_wave_kernel(const RouteParams p) {
+// One (token, layer) pair on one wavefront, lane e holding expert e (E <= 64): z its logit,
+// key its log-domain key (z + offset). Each expert's rank (the number of valid keys larger, or
+// equal with a lower index; -inf and NaN keys are not valid) is its position in the successive
+// picks of select_pair, so both give the same selection, margin and gate bits (the normalisers
+// are summed in the same order). Writes the pair's outputs at obase; returns, in lanes j < K,
+// pick j.
+__device__ __forceinline__ int wave_select_pair(const RouteParams& p, float z, float key, bool in, size_t obase) {
   const int lane = threadIdx.x & 63;
-  const int E = p.E, K = p.K, T = p.T;
-  const uint32_t q = blockIdx.x * (kSelThreads / 64) + (threadIdx.x >> 6);
-  if (q >= static_cast<uint32_t>(p.L) * T) return;   // the whole wavefront leaves (L * T < 2^31)
-  const int l = static_cast<int>(q / static_cast<uint32_t>(T));
-  const bool in = lane < E;
-  const float z = in ? p.logits[static_cast<size_t>(q) * E + lane] : 0.0f;
-  const float key = in ? z + key_offset(p.mode, p.modep[l * E + lane]) : -INFINITY;
+  const int E = p.E, K = p.K;
   const bool valid = in && key > -INFINITY;   // false for NaN too
   int rank = 0;
   for (int f = 0; f < E; ++f) {
@@ -248,10 +244,24 @@ __global__ __launch_bounds__(kSelThreads) void route_select_wave_kernel(const Ro
   }
   const float inv = 1.0f / norm;
   if (lane < K) {
-    p.idx[static_cast<size_t>(q) * K + lane] = my_sel;
-    p.gate[static_cast<size_t>(q) * K + lane] = expf(my_selz - zref) * inv;
+    p.idx[obase * K + lane] = my_sel;
+    p.gate[obase * K + lane] = expf(my_selz - zref) * inv;
   }
-  if (lane == 0 && p.margin) p.margin[q] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+  if (lane == 0 && p.margin) p.margin[obase] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+  return my_sel;
+}
+
+// kSelThreadE < E <= 64: one wavefront per pair (wave_select_pair).
+__global__ __launch_bounds__(kSelThreads) void route_select_wave_kernel(const RouteParams p) {
+  const int lane = threadIdx.x & 63;
+  const int E = p.E, T = p.T;
+  const uint32_t q = blockIdx.x * (kSelThreads / 64) + (threadIdx.x >> 6);
+  if (q >= static_cast<uint32_t>(p.L) * T) return;   // the whole wavefront leaves (L * T < 2^31)
+  const int l = static_cast<int>(q / static_cast<uint32_t>(T));
+  const bool in = lane < E;
+  const float z = in ? p.logits[static_cast<size_t>(q) * E + lane] : 0.0f;
+  const float key = in ? z + key_offset(p.mode, p.modep[l * E + lane]) : -INFINITY;
+  wave_select_pair(p, z, key, in, q);
 }
 
 // The same selection and gates for the single-workgroup launch (one layer, tokens 0..T-1), one
@@ -263,6 +273,17 @@ __device__ void route_finalize_wave(const RouteParams& p, const float* logits, i
                                     int32_t* sel_lds) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
   const int E = p.E, K = p.K;
+  if (E <= 64) {   // one expert per lane: rank-based picks, no cross-lane reductions
+    for (int t = wave; t < TT && t < p.T; t += nwaves) {
+      const bool in = lane < E;
+      const float z = in ? logits[t * ld + lane] : 0.0f;
+      const float key = in ? z + lo[lane] : -INFINITY;
+      const int my_sel = wave_select_pair(p, z, key, in, t);
+      if (lane < K) sel_lds[t * K + lane] = my_sel;
+      if (p.logits && in) p.logits[static_cast<size_t>(t) * E + lane] = z;
+    }
+    return;
+  }
   constexpr int Q = 4;   // experts per lane, E <= 256
   for (int t = wave; t < TT && t < p.T; t += nwaves) {
     const float* z = logits + t * ld;
