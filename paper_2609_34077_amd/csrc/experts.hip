@@ -617,15 +617,16 @@ __global__ __launch_bounds__(256) void decode_swiglu_kernel(const float* __restr
 
 // O[z, row0 + r, n0 + j] = sum over k in slice z of H[row0 + r, k] * W_down[n0 + j, k];
 // grid (d / (16 * DEC_NT), max active experts, split).
+template <int NTILE>   // 16-row tiles of W_down per workgroup (4 or 8)
 __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeArgs p) {
-  constexpr int NTILE = DEC_NT;
+  constexpr int TPW = (NTILE + 3) / 4;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][16 * NTILE * (DEC_CK * 2 + 16)];
   const int slot = blockIdx.y;
   if (slot >= p.n_active[0]) return;
   const int g = p.active[slot];
   const int row0 = p.offsets[g];
   const int nrows = p.offsets[g + 1] - row0;
-  const int n0 = blockIdx.x * 16 * DEC_NT;
+  const int n0 = blockIdx.x * 16 * NTILE;
   const int z = blockIdx.z;
   const int klen = p.F / p.split;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -634,16 +635,19 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeAr
   const int F = p.F;
   auto wrow = [=](int r) { return wd + static_cast<size_t>(n0 + r) * F; };
   const uint16_t* arow = p.H + static_cast<size_t>(row0 + min(lane & 15, nrows - 1)) * p.F;
-  f32x4 acc[1] = {f32x4{0.f, 0.f, 0.f, 0.f}};
-  stream_rows<NTILE>(wrow, arow, z * klen, klen, lds, acc);
-  // wave w holds tile w: rows 4*(lane>>4)+i, column lane & 15
+  f32x4 acc[TPW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 4 * (lane >> 4) + i;
-    if (row < nrows)
-      p.O[(static_cast<size_t>(z) * p.rows + row0 + row) * p.d + n0 + wave * 16 + (lane & 15)] = acc[0][i];
-  }
-
+  for (int q = 0; q < TPW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  stream_rows<NTILE>(wrow, arow, z * klen, klen, lds, acc);
+  // wave w holds tiles w, w + 4: rows 4*(lane>>4)+i, column lane & 15
+#pragma unroll
+  for (int q = 0; q < TPW; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * (lane >> 4) + i;
+      if (row < nrows)
+        p.O[(static_cast<size_t>(z) * p.rows + row0 + row) * p.d + n0 + (wave + 4 * q) * 16 + (lane & 15)] = acc[q][i];
+    }
 }
 
 // ------------------------------------------------------------------ f32 kernels
@@ -807,6 +811,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
 // E (1 - (1 - K/E)^T), plus the shared experts. The grid is still sized for the most experts
 // that can be active; the estimate only picks the split.
 constexpr int kDecodeTargetWGsGateUp = 1792, kDecodeTargetWGsDown = 2560, kDecodeMinChunks = 16;
+constexpr int kDecodeDownTiles = 8;
 
 static int best_split(int per_slice_wgs, int chunks, int max_split, int target) {
   if (per_slice_wgs <= 0) return 1;  // no tokens: nothing is launched
@@ -835,9 +840,12 @@ static int expected_active_groups(int T, int E, int K, int n_shared) {
   return a + n_shared;
 }
 
+// W_down rows per decode workgroup: 16 * decode_down_tiles(d).
+static int decode_down_tiles(int d) { return d % (16 * kDecodeDownTiles) == 0 ? kDecodeDownTiles : DEC_NT; }
+
 int decode_split(int T, int d, int F, int E, int K, int n_shared) {
-  return best_split(d / (16 * DEC_NT) * expected_active_groups(T, E, K, n_shared), F / DEC_CK, kDecodeMaxSplit,
-                    kDecodeTargetWGsDown);
+  return best_split(d / (16 * decode_down_tiles(d)) * expected_active_groups(T, E, K, n_shared), F / DEC_CK,
+                    kDecodeMaxSplit, kDecodeTargetWGsDown);
 }
 
 int decode_split_gate_up(int T, int d, int F, int E, int K, int n_shared) {
@@ -879,8 +887,11 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
-  hipLaunchKernelGGL(decode_down_kernel, dim3(a.d / (16 * DEC_NT), max_active, p.split), dim3(DEC_THREADS), 0,
-                     stream, p);
+  if (decode_down_tiles(a.d) == 8)
+    hipLaunchKernelGGL(decode_down_kernel<8>, dim3(a.d / 128, max_active, p.split), dim3(DEC_THREADS), 0, stream, p);
+  else
+    hipLaunchKernelGGL(decode_down_kernel<DEC_NT>, dim3(a.d / (16 * DEC_NT), max_active, p.split), dim3(DEC_THREADS),
+                       0, stream, p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
