@@ -149,8 +149,35 @@ struct NtArgs {
   const uint16_t* ab;         // SWIGLU_BWD: saved pre-activations [rows, 2N]
   void* c;                    // ROWS: [rows, ldc]; KSPLIT: routed groups' [M, N] matrices
   void* cs;                   // KSPLIT: shared groups' [M, N] matrices
+  float* part;                // ROWS, fp32 output: partial tiles of split tail tiles (tile_job)
   int G, E, M, N, K, lda, ldb, ldc, mt_max, n_tiles;
+  int cu_xcd;                 // workgroups an XCD runs at once
 };
+
+// ROWS with fp32 output may split each XCD's last-round tiles (see tile_job).
+__host__ __device__ constexpr bool nt_tail_split(int mode, int epi, int nk) {
+  return mode == 0 && epi == 1 && tail_splittable(nk);
+}
+
+// Stores a finished ROWS tile of fp32 output: rows [row0, row_end), columns from n0.
+__device__ __forceinline__ void nt_store_rows(const NtArgs& p, const f32x16 (&acc)[kTileTM][kTileTN], int row0,
+                                              int row_end, int n0) {
+  constexpr int WN = 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+#pragma unroll
+  for (int i = 0; i < kTileTM; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = row0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (row >= row_end) continue;
+#pragma unroll
+      for (int j = 0; j < kTileTN; ++j) {
+        const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+        if (col < p.N) static_cast<float*>(p.c)[static_cast<size_t>(row) * p.ldc + col] = acc[i][j][r];
+      }
+    }
+}
 
 enum { kNtRows = 0, kNtKSplit = 1 };
 enum { kEpiSwigluBwd = 0, kEpiF32 = 1 };
@@ -169,11 +196,13 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
   int mt, nt, g, row0, row_end, nk;
   const uint16_t* abase;
   const uint16_t* bbase;
-  if (MODE == kNtRows) {   // tile order over the live row tiles only (see grouped_gemm_bf16)
+  TileJob job{0, 0, 1, -1};
+  if (MODE == kNtRows) {   // each XCD's share of the live row tiles (tile_job)
     const int mt_live = p.tile_off[p.G];
     const int live = mt_live * p.n_tiles;
-    if (static_cast<int>(blockIdx.x) >= live) return;
-    grouped_tile_coords(xcd_tile_id(live), mt_live, p.n_tiles, mt, nt);
+    const int nkf = p.K / kTileK;
+    if (!tile_job(static_cast<int>(blockIdx.x), live, p.cu_xcd, nkf, nt_tail_split(MODE, EPI, nkf), job)) return;
+    grouped_tile_coords(job.lid, mt_live, p.n_tiles, mt, nt);
     int lo = 0, hi = p.G;   // tile_off[lo] <= mt < tile_off[hi]
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
@@ -182,9 +211,10 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
     g = lo;
     row0 = p.offsets[g] + (mt - p.tile_off[g]) * kTileM;
     row_end = p.offsets[g + 1];
-    nk = p.K / kTileK;
-    abase = p.a;
-    bbase = g < p.E ? p.b + static_cast<size_t>(g) * p.N * p.K : p.bs + static_cast<size_t>(g - p.E) * p.N * p.K;
+    nk = nkf / job.s;
+    const int k0 = job.z * nk * kTileK;
+    abase = p.a + k0;
+    bbase = (g < p.E ? p.b + static_cast<size_t>(g) * p.N * p.K : p.bs + static_cast<size_t>(g - p.E) * p.N * p.K) + k0;
   } else {
     const int per = p.mt_max * p.n_tiles;
     const int live = p.n_active[0] * per;
@@ -221,6 +251,11 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
   gemm_tile_mainloop(abase, aoffs, bbase, boffs, aoff, boff, nk, acc, lds_a, lds_b);
+  if (MODE == kNtRows && EPI == kEpiF32) {
+    if (job.s > 1) tail_store_partial(p.part, job.slot, acc);   // a slice of a split tail tile
+    else nt_store_rows(p, acc, row0, row_end, nt * kTileN);
+    return;
+  }
 
   // acc[i][j][4 jj + ii] is row wm*128 + i*32 + 8 jj + 4 (lane >> 5) + ii, column
   // wn*64 + j*32 + (lane & 31) of the tile.
@@ -255,6 +290,27 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
       }
     }
   }
+}
+
+// Adds the slices of each split tail tile of the ROWS fp32 product in slice order and stores
+// it; one workgroup per possible tail tile, grid 8 x kTailSlotsPerXcd.
+__global__ __launch_bounds__(kTileThreads) void nt_tail_fixup(const NtArgs p) {
+  const int mt_live = p.tile_off[p.G];
+  const int live = mt_live * p.n_tiles;
+  const int nk = p.K / kTileK;
+  const int xcd = blockIdx.x & 7, t = blockIdx.x >> 3;
+  const XcdShare x = xcd_share(xcd, live, p.cu_xcd, nk, nt_tail_split(kNtRows, kEpiF32, nk));
+  if (x.s == 1 || t >= x.r) return;
+  f32x16 acc[kTileTM][kTileTN];
+  tail_sum_partials(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, acc);
+  int mt, nt;
+  grouped_tile_coords(x.base + x.full + t, mt_live, p.n_tiles, mt, nt);
+  int lo = 0, hi = p.G;   // tile_off[lo] <= mt < tile_off[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (p.tile_off[mid] <= mt) lo = mid; else hi = mid;
+  }
+  nt_store_rows(p, acc, p.offsets[lo] + (mt - p.tile_off[lo]) * kTileM, p.offsets[lo + 1], nt * kTileN);
 }
 
 // dx[t, c] = sum_k dXr[inv[t K + k], c] + sum_s dXr[T K + s T + t, c], in that order.
@@ -331,8 +387,25 @@ BwdLayout backward_layout(int T, int d, int F, int E, int K, int S) {
   w.h_t = take(static_cast<size_t>(F) * P * 2);
   w.dab_t = take(static_cast<size_t>(2) * F * P * 2);
   w.x_t = take(static_cast<size_t>(d) * P * 2);
+  w.part = take(kTailPartBytes);
   w.total = off;
   return w;
+}
+
+// Workgroups an XCD runs at once (one 256 x 256 tile per CU) and the ROWS grid: 8 XCDs x
+// (their largest share of the tiles + tail slices).
+static int cus_per_xcd() {
+  static const int n = [] {
+    int dev = 0, cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                               hipSuccess || cu < 8)
+      cu = 256;
+    return cu / 8;
+  }();
+  return n;
+}
+static dim3 rows_grid(int mt_max, int n_tiles) {
+  return dim3(static_cast<unsigned>(8 * ((static_cast<long>(mt_max) * n_tiles + 7) / 8 + kTailSlotsPerXcd)));
 }
 
 hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
@@ -378,8 +451,10 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   n.ab = a.ab;
   n.c = dab;
   n.n_tiles = (F + kTileN - 1) / kTileN;
-  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiSwigluBwd>), dim3(n.mt_max * n.n_tiles), dim3(kTileThreads), 0, s,
-                     n);
+  n.cu_xcd = cus_per_xcd();
+  n.part = reinterpret_cast<float*>(ws + w.part);
+  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiSwigluBwd>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads), 0,
+                     s, n);
   MASKMOE_TRY(hipGetLastError());
   // dgrad of gate/up: dX rows = [da db] W_gate_up, then the token sums
   n.a = dab; n.lda = 2 * F;
@@ -387,8 +462,12 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   n.ab = nullptr;
   n.c = dxr; n.ldc = d;
   n.n_tiles = (d + kTileN - 1) / kTileN;
-  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiF32>), dim3(n.mt_max * n.n_tiles), dim3(kTileThreads), 0, s, n);
+  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiF32>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads), 0, s, n);
   MASKMOE_TRY(hipGetLastError());
+  if (nt_tail_split(kNtRows, kEpiF32, n.K / kTileK)) {
+    hipLaunchKernelGGL(nt_tail_fixup, dim3(8 * kTailSlotsPerXcd), dim3(kTileThreads), 0, s, n);
+    MASKMOE_TRY(hipGetLastError());
+  }
   hipLaunchKernelGGL(dx_combine_kernel, dim3(T), dim3(kBwdThreads), 0, s, dxr, a.pb.inv, T, K, a.S, d, a.d_x);
   MASKMOE_TRY(hipGetLastError());
   // weight gradients over each expert's padded token range

@@ -59,69 +59,11 @@ struct GemmArgs {
   int cu_xcd;               // workgroups an XCD runs at once (one per CU)
 };
 
-// Tail split. The hardware deals workgroups round-robin over the 8 XCDs; XCD x takes a
-// contiguous range of the live tiles (the partition of xcd_tile_id) and runs cu_xcd of them at
-// a time. All tiles cost the same, so the r tiles of an XCD's last, partial round would leave
-// most of its CUs idle; instead each of them is split into s reduction slices (the largest
-// power of two <= kTailMaxSplit with r * s <= min(cu_xcd, kTailSlotsPerXcd), s dividing the
-// k-tiles and leaving >= kTailMinK per slice), so the last round is short and full. A slice
-// writes its partial tile to a slot; grouped_tail_fixup adds a tile's slices in slice order and
-// applies the epilogue.
-// Only the down GEMM splits (its long reductions amortise a slice's fixed costs; the gate/up
-// GEMM's epilogue needs whole sums): measured, slices shorter than 16 k-tiles and splits of
-// the gate/up tiles cost more than the idle round they save.
-constexpr int kTailSlotsPerXcd = kTailSlots / 8;
-constexpr int kTailMaxSplit = 8, kTailMinK = 16;
-__host__ __device__ constexpr bool tail_can_split(int epi, int nk) { return epi == 1 && nk % 2 == 0 && nk / 2 >= kTailMinK; }
-
-struct TileJob {
-  int lid;    // logical tile (grouped_tile_coords order)
-  int z, s;   // reduction slice z of s (s == 1: the whole tile)
-  int slot;   // partial-tile slot when s > 1
-};
-
-struct XcdShare {
-  int base, full, r, s;   // first tile, tiles run whole, tail tiles, their slices
-};
-
-__device__ __forceinline__ XcdShare xcd_share(int xcd, int live, int cu_xcd, int nk, bool split_ok) {
-  XcdShare x;
-  const int q = live >> 3, rem = live & 7;
-  const int count = q + (xcd < rem ? 1 : 0);
-  x.base = xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q;
-  x.full = count / cu_xcd * cu_xcd;
-  x.r = count - x.full;
-  const int cap = min(cu_xcd, kTailSlotsPerXcd);
-  x.s = 1;
-  if (split_ok && x.r > 0)
-    for (int s = 2; s <= kTailMaxSplit; s *= 2)
-      if (x.r * s <= cap && nk % s == 0 && nk / s >= kTailMinK) x.s = s;
-  return x;
-}
-
-// The job of workgroup bid, or false when it has none.
-__device__ __forceinline__ bool tile_job(int bid, int live, int cu_xcd, int nk, bool split_ok, TileJob& j) {
-  const int xcd = bid & 7, local = bid >> 3;
-  const XcdShare x = xcd_share(xcd, live, cu_xcd, nk, split_ok);
-  if (local < x.full || x.s == 1) {
-    if (local >= x.full + x.r) return false;
-    j.lid = x.base + local;
-    j.z = 0;
-    j.s = 1;
-    j.slot = -1;
-    return true;
-  }
-  const int t = local - x.full;   // tail unit
-  if (t >= x.r * x.s) return false;
-  j.lid = x.base + x.full + t / x.s;
-  j.z = t % x.s;
-  j.s = x.s;
-  j.slot = xcd * kTailSlotsPerXcd + t;
-  return true;
-}
-
-// Partial-tile slot layout: float4 e of thread tid at [e][tid] (coalesced for both sides).
-constexpr int kTailTileFloats = kTileM * kTileN;
+// Only the down GEMM splits its tail tiles (tile_job in gemm_tile.hpp): its long reductions
+// amortise a slice's fixed costs, and the gate/up GEMM's epilogue needs whole sums. Measured,
+// slices shorter than 16 k-tiles and splits of the gate/up tiles cost more than the idle round
+// they save.
+__host__ __device__ constexpr bool tail_can_split(int epi, int nk) { return epi == 1 && tail_splittable(nk); }
 
 __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt) {
   int lo = 0, hi = G;  // tile_off[lo] <= mt < tile_off[hi]
@@ -260,15 +202,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b);
   }
   if (job.s > 1) {   // a slice of a split tail tile: its partial tile goes to the slot
-    float4* dst = reinterpret_cast<float4*>(p.part + static_cast<size_t>(job.slot) * kTailTileFloats);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          dst[((i * TN + j) * 4 + q) * GEMM_THREADS + tid] =
-              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+    tail_store_partial(p.part, job.slot, acc);
     return;
   }
   gemm_epilogue<EPI>(p, acc, row0, row_end, n0);
@@ -284,28 +218,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_tail_fixup(const GemmArg
   const int xcd = blockIdx.x & 7, t = blockIdx.x >> 3;
   const XcdShare x = xcd_share(xcd, live, p.cu_xcd, nk, tail_can_split(EPI, nk));
   if (x.s == 1 || t >= x.r) return;
-  const int tid = threadIdx.x;
-  constexpr int TM = kTileTM, TN = kTileTN;
-  const float4* src = reinterpret_cast<const float4*>(p.part) +
-                      static_cast<size_t>(xcd * kTailSlotsPerXcd + t * x.s) * (kTailTileFloats / 4);
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const size_t e = static_cast<size_t>((i * TN + j) * 4 + q) * GEMM_THREADS + tid;
-        float4 v = src[e];
-        for (int z = 1; z < x.s; ++z) {
-          const float4 u = src[static_cast<size_t>(z) * (kTailTileFloats / 4) + e];
-          v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
-        }
-        acc[i][j][4 * q] = v.x;
-        acc[i][j][4 * q + 1] = v.y;
-        acc[i][j][4 * q + 2] = v.z;
-        acc[i][j][4 * q + 3] = v.w;
-      }
+  f32x16 acc[kTileTM][kTileTN];
+  tail_sum_partials(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, acc);
   int mt, nt;
   grouped_tile_coords(x.base + x.full + t, mt_live, p.n_tiles, mt, nt);
   const int g = find_group(p.tile_off, p.G, mt);

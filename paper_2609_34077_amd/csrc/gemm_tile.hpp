@@ -12,6 +12,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "kernels.hpp"
 
 namespace maskmoe {
 
@@ -135,6 +136,106 @@ __device__ __forceinline__ void grouped_tile_coords(int lid, int mt_max, int n_t
   const int within = lid % per_group;
   nt = first_n + within % gsize;
   mt = within / gsize;
+}
+
+// Tail split. The hardware deals workgroups round-robin over the 8 XCDs; XCD x takes a
+// contiguous range of the live tiles (the partition of xcd_tile_id) and runs cu_xcd of them at
+// a time. All tiles cost the same, so the r tiles of an XCD's last, partial round would leave
+// most of its CUs idle; instead each of them is split into s reduction slices (the largest
+// power of two <= kTailMaxSplit with r * s <= min(cu_xcd, kTailSlotsPerXcd), s dividing the
+// k-tiles and leaving >= kTailMinK per slice), so the last round is short and full. A slice
+// writes its partial tile to a slot (tail_store_partial); a fix-up kernel adds a tile's slices
+// in slice order (tail_sum_partials) and applies the GEMM's epilogue, so results stay
+// deterministic.
+constexpr int kTailSlotsPerXcd = kTailSlots / 8;
+constexpr int kTailMaxSplit = 8, kTailMinK = 16;
+// a split into two slices is possible: nk even, >= kTailMinK k-tiles each
+__host__ __device__ constexpr bool tail_splittable(int nk) { return nk % 2 == 0 && nk / 2 >= kTailMinK; }
+
+struct TileJob {
+  int lid;    // logical tile (grouped_tile_coords order)
+  int z, s;   // reduction slice z of s (s == 1: the whole tile)
+  int slot;   // partial-tile slot when s > 1
+};
+
+struct XcdShare {
+  int base, full, r, s;   // first tile, tiles run whole, tail tiles, their slices
+};
+
+__device__ __forceinline__ XcdShare xcd_share(int xcd, int live, int cu_xcd, int nk, bool split_ok) {
+  XcdShare x;
+  const int q = live >> 3, rem = live & 7;
+  const int count = q + (xcd < rem ? 1 : 0);
+  x.base = xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q;
+  x.full = count / cu_xcd * cu_xcd;
+  x.r = count - x.full;
+  const int cap = min(cu_xcd, kTailSlotsPerXcd);
+  x.s = 1;
+  if (split_ok && x.r > 0)
+    for (int s = 2; s <= kTailMaxSplit; s *= 2)
+      if (x.r * s <= cap && nk % s == 0 && nk / s >= kTailMinK) x.s = s;
+  return x;
+}
+
+// The job of workgroup bid, or false when it has none.
+__device__ __forceinline__ bool tile_job(int bid, int live, int cu_xcd, int nk, bool split_ok, TileJob& j) {
+  const int xcd = bid & 7, local = bid >> 3;
+  const XcdShare x = xcd_share(xcd, live, cu_xcd, nk, split_ok);
+  if (local < x.full || x.s == 1) {
+    if (local >= x.full + x.r) return false;
+    j.lid = x.base + local;
+    j.z = 0;
+    j.s = 1;
+    j.slot = -1;
+    return true;
+  }
+  const int t = local - x.full;   // tail unit
+  if (t >= x.r * x.s) return false;
+  j.lid = x.base + x.full + t / x.s;
+  j.z = t % x.s;
+  j.s = x.s;
+  j.slot = xcd * kTailSlotsPerXcd + t;
+  return true;
+}
+
+// Partial-tile slot layout: float4 e of thread tid at [e][tid] (coalesced for both sides).
+constexpr int kTailTileFloats = kTileM * kTileN;
+
+__device__ __forceinline__ void tail_store_partial(float* part, int slot, const f32x16 (&acc)[kTileTM][kTileTN]) {
+  float4* dst = reinterpret_cast<float4*>(part + static_cast<size_t>(slot) * kTailTileFloats);
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < kTileTM; ++i)
+#pragma unroll
+    for (int j = 0; j < kTileTN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        dst[((i * kTileTN + j) * 4 + q) * kTileThreads + tid] =
+            make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+}
+
+// acc = the sum, in slice order, of the s partial tiles in slots slot0 .. slot0 + s - 1.
+__device__ __forceinline__ void tail_sum_partials(const float* part, int slot0, int s,
+                                                  f32x16 (&acc)[kTileTM][kTileTN]) {
+  const float4* src = reinterpret_cast<const float4*>(part) + static_cast<size_t>(slot0) * (kTailTileFloats / 4);
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < kTileTM; ++i)
+#pragma unroll
+    for (int j = 0; j < kTileTN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const size_t e = static_cast<size_t>((i * kTileTN + j) * 4 + q) * kTileThreads + tid;
+        float4 v = src[e];
+        for (int z = 1; z < s; ++z) {
+          const float4 u = src[static_cast<size_t>(z) * (kTailTileFloats / 4) + e];
+          v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+        }
+        acc[i][j][4 * q] = v.x;
+        acc[i][j][4 * q + 1] = v.y;
+        acc[i][j][4 * q + 2] = v.z;
+        acc[i][j][4 * q + 3] = v.w;
+      }
 }
 
 }  // namespace maskmoe
