@@ -111,6 +111,10 @@ SMALL_BF16 = [
     synth.LayerConfig("bf16_shared_soft", T=300, d=256, F=192, E=64, K=6, n_shared=2,
                       route_mode=L.ROUTE_SOFT_PRIOR, gate_mode=L.GATE_P, mask_set=tuple(synth.deepseek_mask_set()), seed=4),
     synth.LayerConfig("bf16_one_expert", T=40, d=64, F=64, E=1, K=1, route_mode=L.ROUTE_PLAIN, seed=5),
+    # F = 2048: the down GEMM's 32 k-tiles per tile let each XCD split its (here: only) round of
+    # tiles into two reduction slices, added by the fix-up kernel
+    synth.LayerConfig("bf16_long_reduction_tail_split", T=1200, d=256, F=2048, E=8, K=2,
+                      route_mode=L.ROUTE_HARD_MASK, mask_set=(0, 2, 5, 7), seed=6),
 ]
 
 

@@ -73,6 +73,10 @@ SMALL = [
                       mask_set=(1, 3, 4, 6), seed=43),
     synth.LayerConfig("bwd_ragged", T=300, d=320, F=320, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
                       mask_set=(0, 1, 2, 3, 4, 5), seed=44),
+    # 2F = 2048: the gate/up dgrad's 32 k-tiles per tile are split into two slices (and F = 1024
+    # gives the forward's down GEMM 16 k-tiles: no split there)
+    synth.LayerConfig("bwd_long_k_tail_split", T=200, d=256, F=1024, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
+                      mask_set=(0, 2, 5, 7), seed=45),
 ]
 
 
