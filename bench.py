@@ -676,8 +676,8 @@ def trace_cpu_baseline(st):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build has no multi-GPU path; "
-              "the sharding design is described in the design notes", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the library has no multi-GPU path",
+              file=sys.stderr)
         sys.exit(2)
     import torch
     if not torch.cuda.is_available():
