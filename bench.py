@@ -188,6 +188,7 @@ def layer_work(st):
         layer_step(st, i)
         torch.cuda.synchronize()
         sel = st["idx"].cpu().numpy()
+        st.setdefault("n_e", np.bincount(sel.ravel(), minlength=cfg.E).tolist())   # first batch's histogram
         D = len(np.unique(sel)) + cfg.n_shared
         rows = cfg.T * (cfg.K + cfg.n_shared)
         gu_bytes = D * 2 * cfg.F * cfg.d * 2 + cfg.T * cfg.d * 2 + rows * cfg.F * 2
@@ -309,7 +310,8 @@ def run_layer(args):
                    "route": {1: "hard_mask", 2: "soft_prior", 0: "plain"}[cfg.route_mode],
                    "gate": "renorm" if cfg.gate_mode == 1 else "p", "mask_set": list(cfg.mask_set),
                    "prior_delta": cfg.delta, "cache_slots": st["B"], "weight_copies": len(st["wgu"]),
-                   "distinct_experts_per_step": round(float(np.mean([w["D"] for w in work])), 2)},
+                   "distinct_experts_per_step": round(float(np.mean([w["D"] for w in work])), 2),
+                   "tokens_per_expert": st["n_e"]},
         "roofline": roof,
         "step_roofline_frac": round(step_frac, 4),
         "stages_ms": {L.STAGES[s]: round(stage[s] / n_stage, 4) for s in range(L.NUM_STAGES)},
