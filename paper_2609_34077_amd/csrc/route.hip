@@ -723,13 +723,13 @@ hipError_t launch_route(bool bf16, const void* x, const void* w_router, int T, i
       const int need = p.L * E < 256 ? p.L * E : 256;
       const bool small = T <= 128;
       if (split) {   // T >= kRouteSplitMinT
-        if (need <= 16) err = launch_bf16<1, 1, 1, 4, false, true>(p, stream);
-        else if (need <= 64) err = launch_bf16<2, 4, 1, 4, false, true>(p, stream);
+        if (need <= 16) err = launch_bf16<1, 1, 1, 8, false, true>(p, stream);
+        else if (need <= 64) err = launch_bf16<1, 4, 1, 8, false, true>(p, stream);
         else err = launch_bf16<2, 4, 4, 1, false, true>(p, stream);
-      } else if (need <= 16) {
-        err = small ? launch_bf16<1, 1, 1, 16>(p, stream) : launch_bf16<1, 1, 1, 4>(p, stream);
+      } else if (need <= 16) {   // the split launch's logit tiles for many tokens: the same bits
+        err = small ? launch_bf16<1, 1, 1, 16>(p, stream) : launch_bf16<1, 1, 1, 8>(p, stream);
       } else if (need <= 64) {
-        err = small ? launch_bf16<1, 4, 1, 8>(p, stream) : launch_bf16<2, 4, 1, 4>(p, stream);
+        err = launch_bf16<1, 4, 1, 8>(p, stream);
       } else {
         err = small ? launch_bf16<1, 4, 4, 2>(p, stream) : launch_bf16<2, 4, 4, 1>(p, stream);
       }
