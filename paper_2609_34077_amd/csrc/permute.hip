@@ -36,13 +36,18 @@ __global__ __launch_bounds__(kPermThreads) void permute_scan_kernel(int32_t* __r
   __shared__ int total[kPermMaxGroups];
   const int tid = threadIdx.x;
   const int G = E + n_shared;
+  constexpr int U = 16;   // chunk counts loaded together: a few memory round trips, not one per chunk
   for (int g = tid; g < E; g += kPermThreads) {   // counts -> first row of each chunk within group g
     int run = 0;
-    for (int c = 0; c < n_chunks; ++c) {
-      int32_t* q = counts + static_cast<size_t>(c) * E + g;
-      const int v = *q;
-      *q = run;
-      run += v;
+    for (int c0 = 0; c0 < n_chunks; c0 += U) {
+      int v[U];
+#pragma unroll
+      for (int i = 0; i < U; ++i) v[i] = c0 + i < n_chunks ? counts[static_cast<size_t>(c0 + i) * E + g] : 0;
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        if (c0 + i < n_chunks) counts[static_cast<size_t>(c0 + i) * E + g] = run;
+        run += v[i];
+      }
     }
     total[g] = run;
   }
