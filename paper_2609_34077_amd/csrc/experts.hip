@@ -256,8 +256,11 @@ __device__ __forceinline__ float4 sum_slices(const float* O, int split, size_t s
 // inv[t K + k] (the selected expert's output before gating). One workgroup of 256 threads
 // per (token, block of kCombineCols columns), token-major in a 1-D grid.
 constexpr int kCombineCols = 1024;
+constexpr int kMaxSharedCombine = 8;   // the API's limit on shared experts
 
-template <bool BF16>
+// KC: K known at compile time with one slice (the grouped path): every row's index, gate and
+// O values are loaded before any is added (same additions, same order).
+template <bool BF16, int KC = 0>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
                                                        const int32_t* __restrict__ inv,
                                                        const float* __restrict__ gate, int T, int K,
@@ -265,7 +268,40 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
                                                        float* __restrict__ eo) {
   const int nb = (d + kCombineCols - 1) / kCombineCols;
   const int t = blockIdx.x / nb, cb = blockIdx.x % nb;
-  if (BF16) {  // d % 4 == 0
+  if (BF16 && KC > 0) {  // d % 4 == 0, split == 1, K == KC, n_shared <= kMaxSharedCombine
+    const int c = cb * kCombineCols + threadIdx.x * 4;
+    if (c >= d) return;
+    constexpr int KA = KC > 0 ? KC : 1;   // array extent of the generic instance (branch not taken)
+    int row[KA];
+    float gk[KA];
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      row[k] = inv[t * KC + k];
+      gk[k] = gate[t * KC + k];
+    }
+    float4 v[KA], vs[kMaxSharedCombine];
+#pragma unroll
+    for (int k = 0; k < KC; ++k) v[k] = *reinterpret_cast<const float4*>(O + static_cast<size_t>(row[k]) * d + c);
+#pragma unroll
+    for (int sh = 0; sh < kMaxSharedCombine; ++sh)
+      if (sh < n_shared)
+        vs[sh] = *reinterpret_cast<const float4*>(O + (static_cast<size_t>(T) * KC + static_cast<size_t>(sh) * T + t) * d + c);
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      s.x += gk[k] * v[k].x; s.y += gk[k] * v[k].y; s.z += gk[k] * v[k].z; s.w += gk[k] * v[k].w;
+      if (eo) *reinterpret_cast<float4*>(eo + (static_cast<size_t>(t) * KC + k) * d + c) = v[k];
+    }
+#pragma unroll
+    for (int sh = 0; sh < kMaxSharedCombine; ++sh)
+      if (sh < n_shared) {
+        s.x += vs[sh].x; s.y += vs[sh].y; s.z += vs[sh].z; s.w += vs[sh].w;
+      }
+    uint2 packed;
+    packed.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
+    packed.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d + c) = packed;
+  } else if (BF16) {  // d % 4 == 0
     const size_t slice = static_cast<size_t>(T) * (K + n_shared) * d;
     const int c = cb * kCombineCols + threadIdx.x * 4;
     if (c >= d) return;
@@ -707,8 +743,15 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   }
   record_mark(marks, 1, stream);
 
-  hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                     a.K, a.n_shared, a.d, y, 1, a.expert_out);
+  if (a.K == 2)
+    hipLaunchKernelGGL((combine_kernel<true, 2>), combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate,
+                       a.T, a.K, a.n_shared, a.d, y, 1, a.expert_out);
+  else if (a.K == 6)
+    hipLaunchKernelGGL((combine_kernel<true, 6>), combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate,
+                       a.T, a.K, a.n_shared, a.d, y, 1, a.expert_out);
+  else
+    hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
+                       a.K, a.n_shared, a.d, y, 1, a.expert_out);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
