@@ -65,6 +65,9 @@ def parse():
     ap.add_argument("--batch", type=int, default=16, help="decode tokens per step")
     ap.add_argument("--mode", choices=("hard", "soft"), default="soft", help="deepseek routing mode")
     ap.add_argument("--copies", type=int, default=3, help="decode: weight copies rotated across steps")
+    ap.add_argument("--layout", choices=("packed", "rows"), default="packed",
+                    help="layer workloads: expert weights packed once at set-up (maskmoe_pack_expert_weights) "
+                         "or row-major")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="ft: skip the backward and adapter measurements (counter runs of the forward)")
@@ -89,9 +92,10 @@ def source_hash(rels) -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(workload: str, config_name: str):
+def recorded_traffic(workload: str, config_name: str, layout: str = "rows"):
     """HBM bytes per launch of the dominant kernel from the committed counter summary, if the
-    summary was taken on the current kernel source (matching hash); else None."""
+    summary was taken on the current kernel source (matching hash) with the same expert-weight
+    layout; else None."""
     path = os.path.join(ROOT, "profiles", f"{config_name}_traffic.md")
     if not os.path.exists(path):
         return None
@@ -102,6 +106,8 @@ def recorded_traffic(workload: str, config_name: str):
                 k, v = line[2:].split(": ", 1)
                 vals[k.strip().strip("`")] = v.strip().strip("`")
     if vals.get("kernel source hash") != source_hash(KERNEL_SOURCES[workload]):
+        return None
+    if vals.get("weight layout", "rows") != layout:
         return None
     try:
         return float(vals["traffic bytes per launch"])
@@ -153,9 +159,20 @@ def layer_setup(args):
     wgu0, wdn0 = dev(inp["w_gate_up"]), dev(inp["w_down"])
     wgu = [wgu0] + [wgu0.clone() for _ in range(copies - 1)]
     wdn = [wdn0] + [wdn0.clone() for _ in range(copies - 1)]
-    st = dict(cfg=cfg, inp=inp, xs_host=xs, xs=[dev(x) for x in xs], w_router=dev(inp["w_router"]), wgu=wgu, wdn=wdn,
-              sgu=dev(inp["ws_gate_up"]) if cfg.n_shared else None,
-              sdn=dev(inp["ws_down"]) if cfg.n_shared else None)
+    sgu = dev(inp["ws_gate_up"]) if cfg.n_shared else None
+    sdn = dev(inp["ws_down"]) if cfg.n_shared else None
+    # Row-major weights (the training, backward and adapter extras take these) and, with
+    # --layout packed, packed copies for the timed layer steps: packing is a one-time
+    # conversion of the static weights, done here, outside the timed region.
+    rows = dict(wgu=wgu, wdn=wdn, sgu=sgu, sdn=sdn, layout=L.LAYOUT_ROWS)
+    if args.layout == "packed":
+        pk = [L.maskmoe_pack_expert_weights(a, b) for a, b in zip(wgu, wdn)]
+        spk = L.maskmoe_pack_expert_weights(sgu, sdn) if cfg.n_shared else (None, None)
+        lay = dict(wgu=[p[0] for p in pk], wdn=[p[1] for p in pk], sgu=spk[0], sdn=spk[1], layout=L.LAYOUT_PACKED)
+    else:
+        lay = rows
+    st = dict(cfg=cfg, inp=inp, xs_host=xs, xs=[dev(x) for x in xs], w_router=dev(inp["w_router"]), rows=rows,
+              **lay)
     desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, cfg.n_shared, L.BF16, cfg.route_mode, cfg.gate_mode)
     st["ws"] = torch.empty(L.maskmoe_layer_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
     st["y"] = torch.empty((cfg.T, cfg.d), dtype=torch.bfloat16, device="cuda")
@@ -174,7 +191,7 @@ def layer_step(st, i, events=None):
     L.maskmoe_layer_forward(st["xs"][i % len(st["xs"])], st["w_router"], st["wgu"][c], st["wdn"][c], cfg.K,
                             cfg.route_mode, cfg.gate_mode, ws_gate_up=st["sgu"], ws_down=st["sdn"],
                             workspace=st["ws"], y=st["y"], topk_idx=st["idx"], topk_gate=st["gate"],
-                            events=events, **st["mp"])
+                            events=events, weight_layout=st["layout"], **st["mp"])
     # fetch accounting of this step: every token is one sequence (stream) at one decode step
     return L.maskmoe_cache_fetches(st["idx"].view(1, cfg.T, 1, cfg.K), cfg.E, st["B"], state=st["state"])
 
@@ -281,12 +298,34 @@ def run_layer(args):
             stage[s] += sev[i][s].elapsed_time(sev[i][s + 1])
     layer_ms = np.array([sev[i][0].elapsed_time(sev[i][L.NUM_STAGES]) for i in range(n_stage)])
     gu_s = sum(gu_ms) / 1e3
+    packed = st["layout"] == L.LAYOUT_PACKED
+    # The same timed loop with the row-major weights, for comparison (not the reported value).
+    rows_cmp = None
+    if packed and not args.no_extras:
+        saved = {k: st[k] for k in ("wgu", "wdn", "sgu", "sdn", "layout")}
+        st.update(st["rows"])
+        for i in range(warmup):
+            layer_step(st, i)
+        rev = make_events(steps, (GU, GU + 1))
+        torch.cuda.synchronize()
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        r0.record()
+        for i in range(steps):
+            layer_step(st, i, events=rev[i])
+        r1.record()
+        torch.cuda.synchronize()
+        rms = r0.elapsed_time(r1) / steps
+        rows_cmp = {"ms_per_step": round(rms, 4), "value": round(cfg.T / (rms / 1e3), 1),
+                    "gate_up_avg_launch_us": round(1e3 * float(np.mean([rev[i][GU].elapsed_time(rev[i][GU + 1])
+                                                                        for i in range(steps)])), 2)}
+        st.update(saved)
     decode = args.workload == "decode"
     if decode:
         achieved = gu_bytes / gu_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(args.workload, cfg.name),
-                "kernel": "decode_gate_up_kernel",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": recorded_traffic(args.workload, cfg.name, "packed" if packed else "rows"),
+                "kernel": "decode_gate_up_kernel<%s>" % ("true" if packed else "false"),
                 "algorithmic_unit": "bytes per launch = D x 2*F*d*2 (W_gate, W_up of each distinct selected "
                                     "expert) + x rows + H writes",
                 "avg_launch_us": round(1e3 * np.mean(gu_ms), 2)}
@@ -295,8 +334,9 @@ def run_layer(args):
     else:
         achieved = gu_flops / gu_s / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": recorded_traffic(args.workload, cfg.name),
-                "kernel": "grouped_gemm_bf16<0, false> (gate/up + SwiGLU)",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                "traffic": recorded_traffic(args.workload, cfg.name, "packed" if packed else "rows"),
+                "kernel": "grouped_gemm_bf16<0, false%s> (gate/up + SwiGLU)" % (", true" if packed else ""),
                 "algorithmic_unit": "FLOPs per launch = 2 * T*(K+shared) * 2F * d",
                 "avg_launch_us": round(1e3 * np.mean(gu_ms), 2)}
         tot_flops = sum(w["gu_flops"] + w["dn_flops"] for w in (work[i % len(work)] for i in range(steps)))
@@ -310,6 +350,7 @@ def run_layer(args):
                    "route": {1: "hard_mask", 2: "soft_prior", 0: "plain"}[cfg.route_mode],
                    "gate": "renorm" if cfg.gate_mode == 1 else "p", "mask_set": list(cfg.mask_set),
                    "prior_delta": cfg.delta, "cache_slots": st["B"], "weight_copies": len(st["wgu"]),
+                   "weight_layout": "packed" if st["layout"] == L.LAYOUT_PACKED else "rows",
                    "distinct_experts_per_step": round(float(np.mean([w["D"] for w in work])), 2),
                    "tokens_per_expert": st["n_e"]},
         "roofline": roof,
@@ -318,6 +359,8 @@ def run_layer(args):
         # spread of the layer forward alone (route to combine, no cache step) over the stage pass
         "layer_ms_percentiles": {f"p{q}": round(float(np.percentile(layer_ms, q)), 4) for q in (10, 50, 90)},
     }
+    if rows_cmp is not None:
+        res["row_major_layout"] = rows_cmp
     return res, st
 
 
@@ -332,7 +375,8 @@ def run_stage1_backward(st, args):
     from paper_2609_34077_amd import synth
     cfg, inp = st["cfg"], st["inp"]
     x = st["xs"][0]
-    y, idx, gate, logits, eo = L.maskmoe_layer_forward_train(x, st["w_router"], st["wgu"][0], st["wdn"][0], cfg.K,
+    y, idx, gate, logits, eo = L.maskmoe_layer_forward_train(x, st["w_router"], st["rows"]["wgu"][0],
+                                                             st["rows"]["wdn"][0], cfg.K,
                                                              cfg.route_mode, cfg.gate_mode, mask=inp["mask"])
     g = np.random.default_rng(123)
     dy = torch.from_numpy(synth.bf16_bits(g.standard_normal((cfg.T, cfg.d)).astype(np.float32))).view(
@@ -378,12 +422,13 @@ def run_layer_backward(st, args):
     lib = L.load()
     tw = torch.empty(int(lib.maskmoe_layer_train_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
     bw = torch.empty(int(lib.maskmoe_layer_backward_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
-    _, idx, gate, _, _ = L.maskmoe_layer_forward_train(x, st["w_router"], st["wgu"][0], st["wdn"][0], cfg.K,
+    _, idx, gate, _, _ = L.maskmoe_layer_forward_train(x, st["w_router"], st["rows"]["wgu"][0], st["rows"]["wdn"][0],
+                                                       cfg.K,
                                                        cfg.route_mode, cfg.gate_mode, mask=inp["mask"], workspace=tw)
     g = np.random.default_rng(321)
     dy = torch.from_numpy(synth.bf16_bits(g.standard_normal((cfg.T, cfg.d)).astype(np.float32))).view(
         torch.bfloat16).cuda()
-    run = lambda: L.maskmoe_layer_backward(x, st["wgu"][0], st["wdn"][0], cfg.K, cfg.gate_mode, gate, dy, tw,
+    run = lambda: L.maskmoe_layer_backward(x, st["rows"]["wgu"][0], st["rows"]["wdn"][0], cfg.K, cfg.gate_mode, gate, dy, tw,
                                            workspace=bw)
     run()
     steps = max(3, min(10, args.steps if args.steps is not None else 5))
@@ -420,13 +465,14 @@ def run_lora_forward(st, args):
             lora[k] = torch.from_numpy(np.ascontiguousarray(lora_np[k])).view(torch.bfloat16).cuda()
     desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, cfg.n_shared, L.BF16, cfg.route_mode, cfg.gate_mode)
     ws = torch.empty(int(L.load().maskmoe_layer_lora_workspace_bytes(desc)), dtype=torch.uint8, device="cuda")
-    run = lambda i: L.maskmoe_layer_forward_lora(st["xs"][i % len(st["xs"])], st["w_router"], st["wgu"][0],
-                                                 st["wdn"][0], cfg.K, cfg.route_mode, cfg.gate_mode, lora,
-                                                 ws_gate_up=st["sgu"], ws_down=st["sdn"], workspace=ws, y=st["y"],
+    rw = st["rows"]
+    run = lambda i: L.maskmoe_layer_forward_lora(st["xs"][i % len(st["xs"])], st["w_router"], rw["wgu"][0],
+                                                 rw["wdn"][0], cfg.K, cfg.route_mode, cfg.gate_mode, lora,
+                                                 ws_gate_up=rw["sgu"], ws_down=rw["sdn"], workspace=ws, y=st["y"],
                                                  topk_idx=st["idx"], topk_gate=st["gate"], **st["mp"])
-    plain = lambda i: L.maskmoe_layer_forward(st["xs"][i % len(st["xs"])], st["w_router"], st["wgu"][0],
-                                              st["wdn"][0], cfg.K, cfg.route_mode, cfg.gate_mode,
-                                              ws_gate_up=st["sgu"], ws_down=st["sdn"], workspace=st["ws"],
+    plain = lambda i: L.maskmoe_layer_forward(st["xs"][i % len(st["xs"])], st["w_router"], rw["wgu"][0],
+                                              rw["wdn"][0], cfg.K, cfg.route_mode, cfg.gate_mode,
+                                              ws_gate_up=rw["sgu"], ws_down=rw["sdn"], workspace=st["ws"],
                                               y=st["y"], topk_idx=st["idx"], topk_gate=st["gate"], **st["mp"])
     steps = max(3, min(10, args.steps if args.steps is not None else 5))
 

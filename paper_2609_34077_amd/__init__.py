@@ -6,6 +6,7 @@ input generator. Importing the package does not load the library; the first
 call into ``_lib`` does, and fails loudly if it has not been built.
 """
 
-from ._lib import (BF16, CACHE_FIFO, CACHE_LFU, CACHE_LRU, F32, GATE_P, GATE_RENORM, ROUTE_HARD_MASK, ROUTE_PLAIN,  # noqa: F401
+from ._lib import (BF16, CACHE_FIFO, CACHE_LFU, CACHE_LRU, F32, GATE_P, GATE_RENORM, LAYOUT_PACKED,  # noqa: F401
+                   LAYOUT_ROWS, ROUTE_HARD_MASK, ROUTE_PLAIN,
                    ROUTE_SOFT_PRIOR, LayerDesc, MaskMoEError, load, make_desc, maskmoe_cache_fetches,
-                   maskmoe_layer_forward, maskmoe_layer_workspace_bytes, maskmoe_route)
+                   maskmoe_layer_forward, maskmoe_layer_workspace_bytes, maskmoe_pack_expert_weights, maskmoe_route)

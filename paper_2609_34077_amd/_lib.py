@@ -23,13 +23,15 @@ ROUTE_PLAIN, ROUTE_HARD_MASK, ROUTE_SOFT_PRIOR = 0, 1, 2
 GATE_P, GATE_RENORM = 0, 1
 BF16, F32 = 0, 1
 CACHE_LRU, CACHE_LFU, CACHE_FIFO = 0, 1, 2
+LAYOUT_ROWS, LAYOUT_PACKED = 0, 1
 
 EXPORTS = ("maskmoe_route", "maskmoe_route_workspace_bytes", "maskmoe_layer_workspace_bytes",
            "maskmoe_layer_forward", "maskmoe_layer_forward_profiled", "maskmoe_cache_fetches", "maskmoe_status_string",
            "maskmoe_sample_mask", "maskmoe_layer_forward_train", "maskmoe_stage1_backward_workspace_bytes",
            "maskmoe_stage1_backward", "maskmoe_layer_train_workspace_bytes",
            "maskmoe_layer_backward_workspace_bytes", "maskmoe_layer_backward", "maskmoe_layer_lora_workspace_bytes",
-           "maskmoe_layer_forward_lora", "maskmoe_offload_workspace_bytes", "maskmoe_offload_decode_step")
+           "maskmoe_layer_forward_lora", "maskmoe_offload_workspace_bytes", "maskmoe_offload_decode_step",
+           "maskmoe_pack_expert_weights")
 NUM_STAGES = 5
 STAGES = ("route", "permute", "gate_up", "down", "combine")
 
@@ -38,7 +40,7 @@ class LayerDesc(ctypes.Structure):
     """``maskmoe_layer_desc``."""
 
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("T", "d", "E", "K", "F", "n_shared", "dtype", "route_mode", "gate_mode")]
+                ("T", "d", "E", "K", "F", "n_shared", "dtype", "route_mode", "gate_mode", "weight_layout")]
 
 
 class Lora(ctypes.Structure):
@@ -117,6 +119,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                 _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp,
                                                 _vp]
     lib.maskmoe_offload_decode_step.restype = ctypes.c_int
+    lib.maskmoe_pack_expert_weights.argtypes = [ctypes.POINTER(LayerDesc), _i32, _vp, _vp, _vp, _vp, _vp]
+    lib.maskmoe_pack_expert_weights.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -171,8 +175,37 @@ def _host_f32(a, n: int):
     return arr, arr.ctypes.data_as(ctypes.c_void_p)
 
 
-def make_desc(T, d, E, K, F=1, n_shared=0, dtype=BF16, route_mode=ROUTE_PLAIN, gate_mode=GATE_RENORM) -> LayerDesc:
-    return LayerDesc(T, d, E, K, F, n_shared, dtype, route_mode, gate_mode)
+def make_desc(T, d, E, K, F=1, n_shared=0, dtype=BF16, route_mode=ROUTE_PLAIN, gate_mode=GATE_RENORM,
+              weight_layout=LAYOUT_ROWS) -> LayerDesc:
+    return LayerDesc(T, d, E, K, F, n_shared, dtype, route_mode, gate_mode, weight_layout)
+
+
+def maskmoe_pack_expert_weights(w_gate_up=None, w_down=None):
+    """Packed copies (LAYOUT_PACKED) of bf16 expert weights w_gate_up [n,2F,d] and/or
+    w_down [n,d,F]; each result has its source's shape and size but the packed storage
+    order, and is only meaningful to the library's entry points with weight_layout=LAYOUT_PACKED.
+    Returns (packed_gate_up, packed_down), None where no source was given."""
+    import torch
+    if w_gate_up is None and w_down is None:
+        raise ValueError("nothing to pack")
+    for t, n in ((w_gate_up, "w_gate_up"), (w_down, "w_down")):
+        _dev(t, n)
+        if t is not None and (t.dim() != 3 or t.dtype != torch.bfloat16):
+            raise ValueError(f"{n} must be a 3-d bf16 tensor")
+    if w_gate_up is not None:
+        n, F2, d = w_gate_up.shape
+        F = F2 // 2
+    else:
+        n, d, F = w_down.shape
+    if w_down is not None and tuple(w_down.shape) != (n, d, F):
+        raise ValueError("w_down does not match w_gate_up")
+    pg = torch.empty_like(w_gate_up) if w_gate_up is not None else None
+    pd = torch.empty_like(w_down) if w_down is not None else None
+    desc = make_desc(0, d, 1, 1, F, 0, BF16)
+    _check("maskmoe_pack_expert_weights",
+           load().maskmoe_pack_expert_weights(ctypes.byref(desc), n, _ptr(w_gate_up), _ptr(w_down), _ptr(pg),
+                                              _ptr(pd), _stream()))
+    return pg, pd
 
 
 def maskmoe_route(x, w_router, K: int, route_mode: int, gate_mode: int, mask=None, prior=None,
@@ -222,7 +255,7 @@ def maskmoe_layer_workspace_bytes(desc: LayerDesc) -> int:
 
 
 def _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask, prior, ws_gate_up, ws_down,
-                  workspace, y, topk_idx, topk_gate):
+                  workspace, y, topk_idx, topk_gate, weight_layout=LAYOUT_ROWS):
     """Checks shapes and dtypes of a layer call and marshals its leading arguments."""
     import torch
     for t, n in ((x, "x"), (w_router, "w_router"), (w_gate_up, "w_gate_up"), (w_down, "w_down"),
@@ -240,7 +273,7 @@ def _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask
     for t in (w_router, w_gate_up, w_down, ws_gate_up, ws_down):
         if t is not None and t.dtype != x.dtype:
             raise ValueError("all weights must have the dtype of x")
-    desc = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode)
+    desc = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode, weight_layout)
     need = maskmoe_layer_workspace_bytes(desc)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
@@ -255,9 +288,11 @@ def _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask
 
 def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int,
                           mask=None, prior=None, ws_gate_up=None, ws_down=None, workspace=None, y=None,
-                          topk_idx=None, topk_gate=None, events=None):
+                          topk_idx=None, topk_gate=None, events=None, weight_layout=LAYOUT_ROWS):
     """One masked MoE layer. Shapes: x [T,d], w_router [E,d], w_gate_up [E,2F,d],
     w_down [E,d,F], ws_gate_up [S,2F,d], ws_down [S,d,F]; mask/prior host [E].
+    ``weight_layout``: LAYOUT_PACKED when the four expert tensors come from
+    maskmoe_pack_expert_weights.
 
     Returns y [T,d] (dtype of x). ``workspace`` (uint8 device tensor) is
     allocated when not given; ``topk_idx``/``topk_gate`` [T,K] receive the
@@ -267,7 +302,8 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
     """
     lib = load()
     desc, workspace, y, keep, head = _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask,
-                                                   prior, ws_gate_up, ws_down, workspace, y, topk_idx, topk_gate)
+                                                   prior, ws_gate_up, ws_down, workspace, y, topk_idx, topk_gate,
+                                                   weight_layout)
     args = head + (_ptr(workspace), workspace.numel())
     if events is None:
         _check("maskmoe_layer_forward", lib.maskmoe_layer_forward(*args, _stream()))
@@ -314,7 +350,7 @@ LORA_KEYS = ("a_gate_up", "b_gate_up", "a_down", "b_down", "as_gate_up", "bs_gat
 
 def maskmoe_layer_forward_lora(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int, lora: dict,
                                mask=None, prior=None, ws_gate_up=None, ws_down=None, workspace=None, y=None,
-                               topk_idx=None, topk_gate=None):
+                               topk_idx=None, topk_gate=None, weight_layout=LAYOUT_ROWS):
     """maskmoe_layer_forward with adapted experts. ``lora``: rank, alpha and bf16 device tensors
     a_gate_up [E,2r,d], b_gate_up [E,2F,r], a_down [E,r,F], b_down [E,d,r] (and as_*/bs_* for
     the shared experts). ``workspace`` defaults to maskmoe_layer_lora_workspace_bytes bytes."""
@@ -336,11 +372,12 @@ def maskmoe_layer_forward_lora(x, w_router, w_gate_up, w_down, K: int, route_mod
         if t is None or tuple(t.shape) != shapes[k] or t.dtype != x.dtype or not t.is_contiguous():
             raise ValueError(f"lora[{k!r}] must be a contiguous {x.dtype} tensor of shape {shapes[k]}")
     if workspace is None:
-        desc0 = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode)
+        desc0 = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode, weight_layout)
         workspace = torch.empty(max(int(lib.maskmoe_layer_lora_workspace_bytes(ctypes.byref(desc0))), 1),
                                 dtype=torch.uint8, device=x.device)
     desc, workspace, y, keep, head = _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask,
-                                                   prior, ws_gate_up, ws_down, workspace, y, topk_idx, topk_gate)
+                                                   prior, ws_gate_up, ws_down, workspace, y, topk_idx, topk_gate,
+                                                   weight_layout)
     la = Lora(r, float(lora["alpha"]), *[_ptr(lora.get(k)) if (ns or not k.startswith(("as_", "bs_"))) else None
                                          for k in LORA_KEYS])
     _check("maskmoe_layer_forward_lora",

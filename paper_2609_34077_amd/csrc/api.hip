@@ -118,11 +118,18 @@ Layout layout(const maskmoe_layer_desc& d) {
   return w;
 }
 
+// The packed weight layout: bf16, groups of 128 rows of W_down (d) and 64-column chunks.
+bool packable(int dtype, int d, int F) {
+  return dtype == MASKMOE_BF16 && d % maskmoe::kPackRows == 0 && F % maskmoe::kPackCols == 0;
+}
+
 int check_layer_desc(const maskmoe_layer_desc* d) {
   int st = check_route_desc(d);
   if (st != MASKMOE_OK) return st;
   if (d->F < 1 || d->n_shared < 0 || d->n_shared > kMaxShared) return MASKMOE_E_INVAL;
   if (static_cast<int64_t>(d->T) * (d->K + d->n_shared) >= (int64_t{1} << 31)) return MASKMOE_E_INVAL;
+  if (d->weight_layout != MASKMOE_LAYOUT_ROWS && d->weight_layout != MASKMOE_LAYOUT_PACKED) return MASKMOE_E_INVAL;
+  if (d->weight_layout == MASKMOE_LAYOUT_PACKED && !packable(d->dtype, d->d, d->F)) return MASKMOE_E_UNSUPPORTED;
   return MASKMOE_OK;
 }
 
@@ -131,6 +138,25 @@ int hip_status(hipError_t e) { return e == hipSuccess ? MASKMOE_OK : MASKMOE_E_H
 }  // namespace
 
 extern "C" {
+
+int maskmoe_pack_expert_weights(const maskmoe_layer_desc* desc, int32_t n, const void* w_gate_up,
+                                const void* w_down, void* packed_gate_up, void* packed_down,
+                                hipStream_t stream) {
+  if (!desc || desc->d < 1 || desc->F < 1 || n < 0) return MASKMOE_E_INVAL;
+  if ((w_gate_up == nullptr) != (packed_gate_up == nullptr) || (w_down == nullptr) != (packed_down == nullptr))
+    return MASKMOE_E_INVAL;
+  if ((w_gate_up && w_gate_up == packed_gate_up) || (w_down && w_down == packed_down)) return MASKMOE_E_INVAL;
+  const void* ptrs[] = {w_gate_up, w_down, packed_gate_up, packed_down};
+  for (const void* p : ptrs)
+    if (p && !aligned(p, 16)) return MASKMOE_E_INVAL;
+  if (desc->dtype != MASKMOE_BF16 && desc->dtype != MASKMOE_F32) return MASKMOE_E_INVAL;
+  if (!packable(desc->dtype, desc->d, desc->F)) return MASKMOE_E_UNSUPPORTED;
+  if (n == 0) return MASKMOE_OK;
+  return hip_status(maskmoe::launch_pack_weights(static_cast<const uint16_t*>(w_gate_up),
+                                                 static_cast<const uint16_t*>(w_down),
+                                                 static_cast<uint16_t*>(packed_gate_up),
+                                                 static_cast<uint16_t*>(packed_down), n, desc->d, desc->F, stream));
+}
 
 const char* maskmoe_status_string(int status) {
   switch (status) {
@@ -226,8 +252,10 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
       if (d.n_shared > 0 && (!smats[i] || !aligned(smats[i], al))) return MASKMOE_E_INVAL;
     }
   }
-  const Layout w = layout(d);
   const bool train = expert_out != nullptr;   // the training forward also keeps what the backward reads
+  const bool packed = d.weight_layout == MASKMOE_LAYOUT_PACKED;
+  if (packed && train) return MASKMOE_E_UNSUPPORTED;
+  const Layout w = layout(d);
   const size_t need = lora ? w.lora_total : train ? w.train_total : w.total;
   if (!workspace || workspace_bytes < need || !aligned(workspace, 256)) return MASKMOE_E_WORKSPACE;
 
@@ -274,6 +302,7 @@ static int layer_forward_impl(const maskmoe_layer_desc* desc, const void* x, con
   a.gate = gate;
   a.expert_out = expert_out;
   a.T = d.T; a.d = d.d; a.F = d.F; a.E = d.E; a.K = d.K; a.n_shared = d.n_shared;
+  a.packed = packed;
   if (!bf16) {
     e = maskmoe::launch_experts_f32(a, pb, reinterpret_cast<float*>(ws + w.H), reinterpret_cast<float*>(ws + w.O),
                                     y, stream, expert_marks);
@@ -367,7 +396,7 @@ int maskmoe_layer_backward(const maskmoe_layer_desc* desc, const void* x, const 
   int st = check_layer_desc(desc);
   if (st != MASKMOE_OK) return st;
   const maskmoe_layer_desc& d = *desc;
-  if (d.dtype != MASKMOE_BF16) return MASKMOE_E_UNSUPPORTED;
+  if (d.dtype != MASKMOE_BF16 || d.weight_layout != MASKMOE_LAYOUT_ROWS) return MASKMOE_E_UNSUPPORTED;
   if (d.d % 64 != 0 || d.F % 64 != 0) return MASKMOE_E_UNSUPPORTED;
   if (d.T == 0) return MASKMOE_OK;
   if (!x || !w_gate_up || !w_down || !topk_gate || !dy || !d_x || !d_w_gate_up || !d_w_down) return MASKMOE_E_INVAL;
@@ -543,6 +572,7 @@ int maskmoe_offload_decode_step(const maskmoe_layer_desc* desc, const void* x, c
   int st = check_layer_desc(desc);
   if (st != MASKMOE_OK) return st;
   const maskmoe_layer_desc& d = *desc;
+  if (d.weight_layout != MASKMOE_LAYOUT_ROWS) return MASKMOE_E_UNSUPPORTED;
   st = check_mask_prior(d.route_mode, 1, d.E, d.K, mask, prior);
   if (st != MASKMOE_OK) return st;
   if (policy != MASKMOE_CACHE_LRU && policy != MASKMOE_CACHE_LFU && policy != MASKMOE_CACHE_FIFO)

@@ -118,7 +118,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&
   }
 }
 
-template <int EPI, bool LORA = false>
+// PACKED: the expert matrices are in the packed layout (kPackRows x kPackCols blocks).
+template <int EPI, bool LORA = false, bool PACKED = false>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
   constexpr int WN = 4;                 // waves: 2 along rows x 4 along columns
   constexpr int TM = kTileTM, TN = kTileTN;
@@ -159,15 +160,20 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     const int r = r0 + 64 * i;
     const int row = min(row0 + r, row_end - 1);
     aoffs[i] = (EPI == 0 ? p.row_tok[row] : row) * Kdim + k0 + chunk;
-    int brow;
+    int brow, grp, rig;   // row in the matrix; its packed group and row within the group
     if (EPI == 0) {  // tile rows 0..127: W_gate rows n0.., rows 128..255: the matching W_up rows
       const int n = min(n0 + (r & 127), p.F - 1);
       brow = r < 128 ? n : p.F + n;
+      grp = n / 64;
+      rig = n % 64 + (r < 128 ? 0 : 64);
     } else {
       brow = min(n0 + r, p.d - 1);
+      grp = brow / kPackRows;
+      rig = brow % kPackRows;
     }
     brows[i] = brow;
-    boffs[i] = brow * Kdim + k0 + chunk;
+    boffs[i] = PACKED ? grp * kPackRows * Kdim + (k0 / kPackCols) * kPackBlock + rig * kPackCols + chunk
+                      : brow * Kdim + k0 + chunk;
   }
 
   // Fragment rows: A rows wm*128 + i*32 + (lane & 31); B rows: EPI 0 -> gate wn*32 + ... and
@@ -197,9 +203,10 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
       ex.xaoffs[i] = min(row0 + r0 + 64 * i, row_end - 1) * 64 + chunk;
       ex.xboffs[i] = brows[i] * 64 + chunk;
     }
-    gemm_tile_mainloop<true>(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b, &ex);
+    gemm_tile_mainloop<true, PACKED ? kPackBlock : BK>(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b,
+                                                       &ex);
   } else {
-    gemm_tile_mainloop(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b);
+    gemm_tile_mainloop<false, PACKED ? kPackBlock : BK>(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b);
   }
   if (job.s > 1) {   // a slice of a split tail tile: its partial tile goes to the slot
     tail_store_partial(p.part, job.slot, acc);
@@ -378,9 +385,12 @@ __device__ __forceinline__ int weight_block(const DecodeArgs& p, int g) {
   return p.slot_of ? min(max(p.slot_of[g], 0), p.n_slots - 1) : g;
 }
 
-// Streams R = 16 * NTILE weight rows (row r starts at wrow(r)) over k in [k0, k0 + klen) and
-// accumulates tile (wave + 4q) of A(16 x k) * W^T into acc[q]. A row (lane & 15) is `arow`.
-template <int NTILE, class RowPtr>
+// Streams R = 16 * NTILE weight rows over k in [k0, k0 + klen) and accumulates tile
+// (wave + 4q) of A(16 x k) * W^T into acc[q]. A row (lane & 15) is `arow`. Row r's values
+// k .. k + 63 of chunk k / 64 start at wrow(r) + (k / 64) * CSTRIDE: CSTRIDE = DEC_CK for
+// row-major weights, kPackBlock for packed ones (where the R rows of a chunk are one
+// contiguous block).
+template <int NTILE, int CSTRIDE, class RowPtr>
 __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* arow, int k0, int klen,
                                             unsigned char (*lds)[16 * NTILE * (DEC_CK * 2 + 16)],
                                             f32x4* acc) {
@@ -398,7 +408,7 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
   for (int i = 0; i < PER; ++i) {
     const int u = tid + DEC_THREADS * i;
     const int r = u / UPR, piece = u % UPR;
-    src[i] = wrow(r) + k0 + piece * 8;
+    src[i] = wrow(r) + (CSTRIDE == DEC_CK ? k0 : (k0 / DEC_CK) * CSTRIDE) + piece * 8;
     dst[i] = r * PITCH + piece * 16;
   }
   const uint16_t* ap = arow + k0 + (lane >> 4) * 8;
@@ -410,7 +420,7 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
   u32x4 reg[2][PER], areg[2][KS];
   auto load_w = [&](int c, u32x4* r) {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i] + c * DEC_CK));
+    for (int i = 0; i < PER; ++i) r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i] + c * CSTRIDE));
   };
   auto load_a = [&](int c, u32x4* r) {
 #pragma unroll
@@ -476,6 +486,7 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
 // active expert; grid (F / (16 * DEC_NT), max active experts, split_gu). With split_gu > 1
 // each workgroup covers one slice of d and writes its partial dot products to P instead;
 // decode_swiglu_kernel then adds the slices and applies SwiGLU.
+template <bool PACKED>
 __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const DecodeArgs p) {
   constexpr int NTILE = 2 * DEC_NT;
   constexpr int TPW = (NTILE + 3) / 4;
@@ -490,7 +501,9 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const Decod
   const uint16_t* wg = g < p.E ? p.w_gate_up + static_cast<size_t>(weight_block(p, g)) * 2 * p.F * p.d
                                : p.ws_gate_up + static_cast<size_t>(g - p.E) * 2 * p.F * p.d;
   const int F = p.F, d = p.d;
+  static_assert(16 * DEC_NT * 2 == kPackRows, "a workgroup's rows are one packed group");
   auto wrow = [=](int r) {  // rows 0..16*DEC_NT-1: W_gate, then the matching W_up rows
+    if (PACKED) return wg + static_cast<size_t>(blockIdx.x) * kPackRows * d + r * kPackCols;
     const int n = n0 + (r % (16 * DEC_NT));
     return wg + static_cast<size_t>(r < 16 * DEC_NT ? n : F + n) * d;
   };
@@ -499,7 +512,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const Decod
 #pragma unroll
   for (int q = 0; q < TPW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int klen = p.d / p.split_gu, z = blockIdx.z;
-  stream_rows<NTILE>(wrow, arow, z * klen, klen, lds, acc);
+  stream_rows<NTILE, PACKED ? kPackBlock : DEC_CK>(wrow, arow, z * klen, klen, lds, acc);
   if (p.split_gu > 1) {  // partial sums: wave w holds tiles w and w + 4 (gate tile j, up tile j)
 #pragma unroll
     for (int q = 0; q < TPW; ++q) {
@@ -567,8 +580,9 @@ __global__ __launch_bounds__(256) void decode_swiglu_kernel(const float* __restr
 
 // O[z, row0 + r, n0 + j] = sum over k in slice z of H[row0 + r, k] * W_down[n0 + j, k];
 // grid (d / (16 * DEC_NT), max active experts, split).
-template <int NTILE>   // 16-row tiles of W_down per workgroup (4 or 8)
+template <int NTILE, bool PACKED>   // 16-row tiles of W_down per workgroup (4 or 8; 8 when packed)
 __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeArgs p) {
+  static_assert(!PACKED || 16 * NTILE == kPackRows, "a workgroup's rows are one packed group");
   constexpr int TPW = (NTILE + 3) / 4;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][16 * NTILE * (DEC_CK * 2 + 16)];
   const int slot = blockIdx.y;
@@ -583,12 +597,14 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeAr
   const uint16_t* wd = g < p.E ? p.w_down + static_cast<size_t>(weight_block(p, g)) * p.d * p.F
                                : p.ws_down + static_cast<size_t>(g - p.E) * p.d * p.F;
   const int F = p.F;
-  auto wrow = [=](int r) { return wd + static_cast<size_t>(n0 + r) * F; };
+  auto wrow = [=](int r) {
+    return PACKED ? wd + static_cast<size_t>(n0) * F + r * kPackCols : wd + static_cast<size_t>(n0 + r) * F;
+  };
   const uint16_t* arow = p.H + static_cast<size_t>(row0 + min(lane & 15, nrows - 1)) * p.F;
   f32x4 acc[TPW];
 #pragma unroll
   for (int q = 0; q < TPW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  stream_rows<NTILE>(wrow, arow, z * klen, klen, lds, acc);
+  stream_rows<NTILE, PACKED ? kPackBlock : DEC_CK>(wrow, arow, z * klen, klen, lds, acc);
   // wave w holds tiles w, w + 4: rows 4*(lane>>4)+i, column lane & 15
 #pragma unroll
   for (int q = 0; q < TPW; ++q)
@@ -677,6 +693,18 @@ static dim3 grouped_grid(int max_tiles, int n_tiles) {
   return dim3(static_cast<unsigned>(8 * per_xcd));
 }
 
+template <int EPI>
+static void launch_grouped(bool lora, bool packed, dim3 grid, const GemmArgs& g, hipStream_t stream) {
+  if (lora && packed)
+    hipLaunchKernelGGL((grouped_gemm_bf16<EPI, true, true>), grid, dim3(GEMM_THREADS), 0, stream, g);
+  else if (lora)
+    hipLaunchKernelGGL((grouped_gemm_bf16<EPI, true>), grid, dim3(GEMM_THREADS), 0, stream, g);
+  else if (packed)
+    hipLaunchKernelGGL((grouped_gemm_bf16<EPI, false, true>), grid, dim3(GEMM_THREADS), 0, stream, g);
+  else
+    hipLaunchKernelGGL((grouped_gemm_bf16<EPI>), grid, dim3(GEMM_THREADS), 0, stream, g);
+}
+
 hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint16_t* H, float* O, float* part,
                                void* y, int max_tiles, hipStream_t stream, hipEvent_t* marks, uint16_t* ab,
                                const LoraArgs* lora) {
@@ -708,10 +736,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   g.out = H;
   const int nt1 = (a.F + BN / 2 - 1) / (BN / 2);
   g.n_tiles = nt1;
-  if (lora)
-    hipLaunchKernelGGL((grouped_gemm_bf16<0, true>), grouped_grid(max_tiles, nt1), dim3(GEMM_THREADS), 0, stream, g);
-  else
-    hipLaunchKernelGGL(grouped_gemm_bf16<0>, grouped_grid(max_tiles, nt1), dim3(GEMM_THREADS), 0, stream, g);
+  launch_grouped<0>(lora != nullptr, a.packed, grouped_grid(max_tiles, nt1), g, stream);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
@@ -730,10 +755,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   g.out = O;
   const int nt2 = (a.d + BN - 1) / BN;
   g.n_tiles = nt2;
-  if (lora)
-    hipLaunchKernelGGL((grouped_gemm_bf16<1, true>), grouped_grid(max_tiles, nt2), dim3(GEMM_THREADS), 0, stream, g);
-  else
-    hipLaunchKernelGGL(grouped_gemm_bf16<1>, grouped_grid(max_tiles, nt2), dim3(GEMM_THREADS), 0, stream, g);
+  launch_grouped<1>(lora != nullptr, a.packed, grouped_grid(max_tiles, nt2), g, stream);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (tail_can_split(1, a.F / BK)) {
@@ -832,8 +854,11 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
   p.split = decode_split(a.T, a.d, a.F, a.E, a.K, a.n_shared);
   p.split_gu = decode_split_gate_up(a.T, a.d, a.F, a.E, a.K, a.n_shared);
   const int max_active = max_active_groups(a.T, a.E, a.K, a.n_shared);
-  hipLaunchKernelGGL(decode_gate_up_kernel, dim3(a.F / (16 * DEC_NT), max_active, p.split_gu), dim3(DEC_THREADS),
-                     0, stream, p);
+  const dim3 gu_grid(a.F / (16 * DEC_NT), max_active, p.split_gu);
+  if (a.packed)
+    hipLaunchKernelGGL(decode_gate_up_kernel<true>, gu_grid, dim3(DEC_THREADS), 0, stream, p);
+  else
+    hipLaunchKernelGGL(decode_gate_up_kernel<false>, gu_grid, dim3(DEC_THREADS), 0, stream, p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
@@ -844,11 +869,15 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
-  if (decode_down_tiles(a.d) == 8)
-    hipLaunchKernelGGL(decode_down_kernel<8>, dim3(a.d / 128, max_active, p.split), dim3(DEC_THREADS), 0, stream, p);
+  if (a.packed)   // d % kPackRows == 0, so decode_down_tiles(d) == 8
+    hipLaunchKernelGGL((decode_down_kernel<8, true>), dim3(a.d / 128, max_active, p.split), dim3(DEC_THREADS), 0,
+                       stream, p);
+  else if (decode_down_tiles(a.d) == 8)
+    hipLaunchKernelGGL((decode_down_kernel<8, false>), dim3(a.d / 128, max_active, p.split), dim3(DEC_THREADS), 0,
+                       stream, p);
   else
-    hipLaunchKernelGGL(decode_down_kernel<DEC_NT>, dim3(a.d / (16 * DEC_NT), max_active, p.split), dim3(DEC_THREADS),
-                       0, stream, p);
+    hipLaunchKernelGGL((decode_down_kernel<DEC_NT, false>), dim3(a.d / (16 * DEC_NT), max_active, p.split),
+                       dim3(DEC_THREADS), 0, stream, p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);
@@ -857,6 +886,49 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
+}
+
+// ------------------------------------------------------------------ packed weight layout
+//
+// One thread per 16-byte piece of the packed output, in output order: piece u of block
+// ((e * groups + q) * chunks + c) is row i = (u % 1024) / 8 of the block, columns
+// 8 * (u % 8) .. + 7 of chunk c. gate_up: block row i < 64 is W_gate row 64 q + i, the rest
+// the matching W_up rows F + 64 q + i - 64; otherwise block row i is row kPackRows q + i.
+// Reads are 128-byte row pieces, writes are contiguous.
+__global__ __launch_bounds__(256) void pack_weights_kernel(const uint16_t* __restrict__ src,
+                                                           uint16_t* __restrict__ dst, int n, int rows, int cols,
+                                                           bool gate_up, int F) {
+  const size_t pieces = static_cast<size_t>(n) * rows * cols / 8;
+  const int chunks = cols / kPackCols, groups = rows / kPackRows;
+  for (size_t u = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; u < pieces;
+       u += static_cast<size_t>(gridDim.x) * 256) {
+    const size_t blk = u / (kPackBlock / 8);
+    const int within = static_cast<int>(u % (kPackBlock / 8));
+    const int i = within / 8, j = (within % 8) * 8;
+    const int c = static_cast<int>(blk % chunks);
+    const size_t eq = blk / chunks;
+    const int q = static_cast<int>(eq % groups);
+    const size_t e = eq / groups;
+    const int row = gate_up ? (i < 64 ? q * 64 + i : F + q * 64 + (i - 64)) : q * kPackRows + i;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(src + (e * rows + row) * cols + static_cast<size_t>(c) * kPackCols + j);
+    *reinterpret_cast<u32x4*>(dst + u * 8) = v;
+  }
+}
+
+hipError_t launch_pack_weights(const uint16_t* w_gate_up, const uint16_t* w_down, uint16_t* p_gate_up,
+                               uint16_t* p_down, int n, int d, int F, hipStream_t stream) {
+  const size_t pieces = static_cast<size_t>(n) * 2 * F * d / 8;   // gate/up; down has half
+  const dim3 grid(static_cast<unsigned>(std::min<size_t>((pieces + 255) / 256, 16384)));
+  if (w_gate_up) {
+    hipLaunchKernelGGL(pack_weights_kernel, grid, dim3(256), 0, stream, w_gate_up, p_gate_up, n, 2 * F, d, true, F);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  if (w_down) {
+    hipLaunchKernelGGL(pack_weights_kernel, grid, dim3(256), 0, stream, w_down, p_down, n, d, F, false, F);
+    return hipGetLastError();
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_experts_f32(const ExpertArgs& a, const PermBuffers& pb, float* H, float* O,

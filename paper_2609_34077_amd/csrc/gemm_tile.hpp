@@ -40,8 +40,9 @@ struct TileExtra {
 // aoffs / boffs: element offsets from abase / bbase of the thread's unit i rows, chunk included
 // (rows r0 + 64 i of the tile); aoff / boff: 16-byte LDS slot offsets of the wave's fragment
 // rows (row * 8). nk: k-tiles of 64 of the main operands (none and no extra tile leaves acc
-// unchanged).
-template <bool EXTRA = false>
+// unchanged). BSTEP: elements between consecutive k-tiles of a B row (kTileK row-major,
+// kPackBlock in the packed weight layout).
+template <bool EXTRA = false, int BSTEP = kTileK>
 __device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ abase, const int (&aoffs)[kTileU],
                                                    const uint16_t* __restrict__ bbase, const int (&boffs)[kTileU],
                                                    const int (&aoff)[kTileTM], const int (&boff)[kTileTN], int nk,
@@ -58,7 +59,7 @@ __device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ 
 #pragma unroll
     for (int i = 0; i < U; ++i) {
       ra[i] = *reinterpret_cast<const u32x4*>(abase + (aoffs[i] + t * BK));
-      rb[i] = *reinterpret_cast<const u32x4*>(bbase + (boffs[i] + t * BK));
+      rb[i] = *reinterpret_cast<const u32x4*>(bbase + (boffs[i] + t * BSTEP));
     }
   };
   auto lstore = [&](int buf) {

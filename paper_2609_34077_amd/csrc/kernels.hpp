@@ -70,7 +70,15 @@ struct ExpertArgs {
   const int32_t* slot_of = nullptr;   // few-token path: routed expert -> block of w_gate_up / w_down
   int n_slots = 0;                    // blocks in w_gate_up / w_down when slot_of is given
   int T, d, F, E, K, n_shared;
+  bool packed = false;                // weights in the packed layout (pack_weights_kernel)
 };
+
+// Packed expert weights (bf16): each matrix is cut into groups of kPackRows rows (gate/up:
+// 64 W_gate rows and their 64 W_up rows) and kPackCols-column chunks; block (group q,
+// chunk c) is [kPackRows][kPackCols] contiguous at (q * cols / kPackCols + c) * kPackBlock.
+constexpr int kPackRows = 128, kPackCols = 64, kPackBlock = kPackRows * kPackCols;
+hipError_t launch_pack_weights(const uint16_t* w_gate_up, const uint16_t* w_down, uint16_t* p_gate_up,
+                               uint16_t* p_down, int n, int d, int F, hipStream_t stream);
 
 // Optional stage markers: when `marks` is non-null, marks[i] is recorded on the stream after
 // the i-th of the three expert stages (gate/up, down, combine); a stage that a path fuses

@@ -239,3 +239,42 @@ def test_cache_rejects_invalid_arguments():
     assert _cache(fetches=None) == L.E_INVAL
     assert _cache(trace=None) == L.E_INVAL
     assert _cache(L_=0, trace=None, fetches=None, hits=None) == L.OK   # nothing to do
+
+
+def test_packed_layout_validation():
+    """The packed weight layout: an unknown layout value is invalid; packed needs bf16,
+    d % 128 == 0 and F % 64 == 0; the training, backward and offload entry points refuse it."""
+    lib = L.load()
+    good = dict(T=32, d=128, E=8, K=2, F=256, n_shared=0, dtype=L.BF16, route_mode=L.ROUTE_PLAIN,
+                gate_mode=L.GATE_RENORM, weight_layout=L.LAYOUT_PACKED)
+    desc = L.make_desc(**good)
+    assert lib.maskmoe_layer_workspace_bytes(ctypes.byref(desc)) > 0
+    assert lib.maskmoe_layer_workspace_bytes(ctypes.byref(L.make_desc(**{**good, "weight_layout": 2}))) == 0
+    assert _fwd(L.make_desc(**{**good, "weight_layout": 2}), ws_bytes=1 << 30) == L.E_INVAL
+    assert _fwd(L.make_desc(**{**good, "weight_layout": -1}), ws_bytes=1 << 30) == L.E_INVAL
+    assert _fwd(L.make_desc(**{**good, "dtype": L.F32}), ws_bytes=1 << 30) == L.E_UNSUPPORTED
+    assert _fwd(L.make_desc(**{**good, "d": 192}), ws_bytes=1 << 30) == L.E_UNSUPPORTED
+    assert _fwd(L.make_desc(**{**good, "F": 96}), ws_bytes=1 << 30) == L.E_UNSUPPORTED
+    assert _fwd(L.make_desc(**{**good, "weight_layout": L.LAYOUT_ROWS, "d": 192}), ws_bytes=0) == L.E_WORKSPACE
+    assert lib.maskmoe_layer_forward_train(ctypes.byref(desc), FAKE, FAKE, None, None, FAKE, FAKE, None, None, FAKE,
+                                           FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == L.E_UNSUPPORTED
+    assert lib.maskmoe_layer_backward(ctypes.byref(desc), FAKE, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, 1 << 40,
+                                      FAKE, FAKE, FAKE, None, None, FAKE, 1 << 40, None) == L.E_UNSUPPORTED
+    assert _offload(L.make_desc(**{**good, "T": 1})) == L.E_UNSUPPORTED
+
+
+def test_pack_rejects_invalid_arguments():
+    lib = L.load()
+    pack = lambda desc, n=2, gu=FAKE, dn=FAKE, pgu=FAKE + 0x1000, pdn=FAKE + 0x2000: lib.maskmoe_pack_expert_weights(
+        ctypes.byref(desc), n, gu, dn, pgu, pdn, None)
+    desc = L.make_desc(T=0, d=256, E=1, K=1, F=128)
+    assert pack(desc, n=0) == L.OK                                    # nothing to do, nothing launched
+    assert pack(desc, n=-1) == L.E_INVAL
+    assert pack(desc, pgu=None) == L.E_INVAL                          # source without destination
+    assert pack(desc, gu=None) == L.E_INVAL                           # destination without source
+    assert pack(desc, pdn=FAKE) == L.E_INVAL                          # in place
+    assert pack(desc, gu=FAKE + 8) == L.E_INVAL                       # misaligned
+    assert pack(L.make_desc(T=0, d=256, E=1, K=1, F=128, dtype=L.F32)) == L.E_UNSUPPORTED
+    assert pack(L.make_desc(T=0, d=192, E=1, K=1, F=128)) == L.E_UNSUPPORTED
+    assert pack(L.make_desc(T=0, d=256, E=1, K=1, F=96)) == L.E_UNSUPPORTED
+    assert pack(L.make_desc(T=0, d=0, E=1, K=1, F=128)) == L.E_INVAL

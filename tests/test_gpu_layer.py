@@ -44,24 +44,35 @@ def _mp(cfg, inp):
     return {}
 
 
-def run_gpu(cfg, inp, dd=None, workspace=None, events=None):
+def pack_uploaded(dd):
+    """dd with its expert weights in the packed layout (maskmoe_pack_expert_weights)."""
+    out = dict(dd)
+    out["w_gate_up"], out["w_down"] = L.maskmoe_pack_expert_weights(dd["w_gate_up"], dd["w_down"])
+    if dd.get("ws_gate_up") is not None:
+        out["ws_gate_up"], out["ws_down"] = L.maskmoe_pack_expert_weights(dd["ws_gate_up"], dd["ws_down"])
+    return out
+
+
+def run_gpu(cfg, inp, dd=None, workspace=None, events=None, packed=False):
     dd = dd or _upload(inp, cfg)
+    if packed:
+        dd = pack_uploaded(dd)
     T, K = cfg.T, cfg.K
     idx = torch.empty((T, K), dtype=torch.int32, device="cuda")
     gate = torch.empty((T, K), dtype=torch.float32, device="cuda")
     y = L.maskmoe_layer_forward(dd["x"], dd["w_router"], dd["w_gate_up"], dd["w_down"], K, cfg.route_mode,
                                 cfg.gate_mode, ws_gate_up=dd.get("ws_gate_up"), ws_down=dd.get("ws_down"),
                                 topk_idx=idx, topk_gate=gate, workspace=workspace, events=events,
-                                **_mp(cfg, inp))
+                                weight_layout=L.LAYOUT_PACKED if packed else L.LAYOUT_ROWS, **_mp(cfg, inp))
     torch.cuda.synchronize()
     return y, idx, gate
 
 
-def check_layer(cfg, n_sample=None, seed=0):
+def check_layer(cfg, n_sample=None, seed=0, packed=False):
     U.say(f"layer {cfg.name} T={cfg.T} d={cfg.d} F={cfg.F} E={cfg.E} K={cfg.K} shared={cfg.n_shared} "
-          f"mode={cfg.route_mode} gate={cfg.gate_mode} {cfg.dtype}")
+          f"mode={cfg.route_mode} gate={cfg.gate_mode} {cfg.dtype}{' packed' if packed else ''}")
     inp = _inputs(cfg)
-    y, idx, gate = run_gpu(cfg, inp)
+    y, idx, gate = run_gpu(cfg, inp, packed=packed)
     dt = cfg.dtype
     xf = U.f64(inp["x"], dt)
     mp = _mp(cfg, inp)

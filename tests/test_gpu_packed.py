@@ -1,0 +1,134 @@
+"""The packed expert-weight layout (maskmoe_pack_expert_weights, weight_layout = LAYOUT_PACKED).
+
+The packing is checked as a bit-exact permutation against the layout the header documents
+(index work, written here with reshapes and permutes of the row-major tensor). The layer
+paths that take packed weights (few-token decode kernels, grouped GEMMs, the adapted
+grouped GEMMs) read the same values in the same order, so their outputs must equal those
+with row-major weights bit for bit; one decode and one grouped case are also compared with
+the oracle directly.
+"""
+
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_util as U
+from paper_2609_34077_amd import _lib as L
+from paper_2609_34077_amd import synth
+from test_gpu_layer import _inputs, _upload, check_layer, pack_uploaded, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def packed_gate_up_reference(w):
+    """[n, 2F, d] -> blocks (group q, chunk c) of [64 W_gate rows + their 64 W_up rows][64]."""
+    n, F2, d = w.shape
+    F = F2 // 2
+    g = w[:, :F].reshape(n, F // 64, 64, d // 64, 64)
+    u = w[:, F:].reshape(n, F // 64, 64, d // 64, 64)
+    return torch.cat([g, u], dim=2).permute(0, 1, 3, 2, 4).contiguous().reshape(n, F2, d)
+
+
+def packed_down_reference(w):
+    """[n, d, F] -> blocks (group q, chunk c) of [128 rows][64]."""
+    n, d, F = w.shape
+    return w.reshape(n, d // 128, 128, F // 64, 64).permute(0, 1, 3, 2, 4).contiguous().reshape(n, d, F)
+
+
+def _bits(n, rows, cols, seed):
+    g = torch.Generator().manual_seed(seed)
+    return torch.randint(-32768, 32768, (n, rows, cols), dtype=torch.int32, generator=g).to(torch.int16)
+
+
+@pytest.mark.parametrize("n,d,F", [(3, 256, 192), (1, 128, 64), (2, 512, 1408), (8, 384, 320)])
+def test_pack_is_the_documented_permutation(n, d, F):
+    U.say(f"pack n={n} d={d} F={F}")
+    gu, dn = _bits(n, 2 * F, d, n + d + F), _bits(n, d, F, 7 * n + d + F)
+    pg, pd = L.maskmoe_pack_expert_weights(gu.cuda().view(torch.bfloat16), dn.cuda().view(torch.bfloat16))
+    torch.cuda.synchronize()
+    assert torch.equal(pg.view(torch.int16).cpu(), packed_gate_up_reference(gu))
+    assert torch.equal(pd.view(torch.int16).cpu(), packed_down_reference(dn))
+    only_gu, none = L.maskmoe_pack_expert_weights(w_gate_up=gu.cuda().view(torch.bfloat16))
+    torch.cuda.synchronize()
+    assert none is None and torch.equal(only_gu.view(torch.int16).cpu(), packed_gate_up_reference(gu))
+
+
+CASES = [
+    # few-token path (decode kernels), with and without shared experts and split reductions
+    synth.LayerConfig("pk_dec_t1", T=1, d=512, F=1024, E=8, K=2, route_mode=L.ROUTE_SOFT_PRIOR,
+                      mask_set=(0, 2, 5, 7), seed=31),
+    synth.LayerConfig("pk_dec_t7", T=7, d=256, F=640, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
+                      mask_set=(0, 2, 5, 7), seed=32),
+    synth.LayerConfig("pk_dec_shared_t16", T=16, d=384, F=192, E=16, K=4, n_shared=2, route_mode=L.ROUTE_HARD_MASK,
+                      gate_mode=L.GATE_P, mask_set=tuple(range(0, 16, 2)), seed=33),
+    # grouped-GEMM path: ragged row tiles, ragged last column tile (F % 128 = 64), shared experts,
+    # the down GEMM's split tail tiles (F = 2048)
+    synth.LayerConfig("pk_grp_hard", T=600, d=256, F=320, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
+                      mask_set=(0, 2, 5, 7), seed=34),
+    synth.LayerConfig("pk_grp_shared_soft", T=300, d=256, F=192, E=64, K=6, n_shared=2,
+                      route_mode=L.ROUTE_SOFT_PRIOR, gate_mode=L.GATE_P, mask_set=tuple(synth.deepseek_mask_set()),
+                      seed=35),
+    synth.LayerConfig("pk_grp_tail_split", T=1200, d=128, F=2048, E=8, K=2, route_mode=L.ROUTE_HARD_MASK,
+                      mask_set=(0, 2, 5, 7), seed=36),
+]
+
+
+@pytest.mark.parametrize("cfg", CASES, ids=lambda c: c.name)
+def test_packed_forward_equals_row_major_bitwise(cfg):
+    U.say(f"packed vs row-major {cfg.name}")
+    inp = _inputs(cfg)
+    dd = _upload(inp, cfg)
+    y0, i0, g0 = run_gpu(cfg, inp, dd)
+    y1, i1, g1 = run_gpu(cfg, inp, dd, packed=True)
+    assert torch.equal(i0, i1) and torch.equal(g0, g1)
+    assert torch.equal(y0.view(torch.int16), y1.view(torch.int16))
+
+
+@pytest.mark.parametrize("cfg", [CASES[1], CASES[4]], ids=lambda c: c.name)
+def test_packed_forward_oracle_parity(cfg):
+    check_layer(cfg, packed=True)
+
+
+def test_packed_mixtral_decode_full_shape():
+    """The Mixtral decode layer (16 tokens, d = 4096, F = 14336): bitwise equal to row-major."""
+    cfg = synth.mixtral_decode_config(16)
+    inp = _inputs(cfg)
+    dd = _upload(inp, cfg)
+    y0, _, _ = run_gpu(cfg, inp, dd)
+    y1, _, _ = run_gpu(cfg, inp, dd, packed=True)
+    assert torch.equal(y0.view(torch.int16), y1.view(torch.int16))
+
+
+def test_packed_lora_forward_equals_row_major_bitwise():
+    from test_gpu_lora import _mp, _upload_lora
+    cfg = CASES[4]
+    U.say(f"packed vs row-major, adapters, {cfg.name}")
+    inp = _inputs(cfg)
+    dd = _upload(inp, cfg)
+    lora = _upload_lora(synth.make_lora(cfg, 8, 16.0), cfg.n_shared)
+    ys = []
+    for packed in (False, True):
+        w = pack_uploaded(dd) if packed else dd
+        ys.append(L.maskmoe_layer_forward_lora(
+            w["x"], w["w_router"], w["w_gate_up"], w["w_down"], cfg.K, cfg.route_mode, cfg.gate_mode, lora,
+            ws_gate_up=w.get("ws_gate_up"), ws_down=w.get("ws_down"),
+            weight_layout=L.LAYOUT_PACKED if packed else L.LAYOUT_ROWS, **_mp(cfg, inp)))
+    torch.cuda.synchronize()
+    assert torch.equal(ys[0].view(torch.int16), ys[1].view(torch.int16))
+
+
+def test_packed_training_forward_is_refused():
+    cfg = CASES[3]
+    inp = _inputs(cfg)
+    pk = pack_uploaded(_upload(inp, cfg))
+    desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, 0, L.BF16, cfg.route_mode, cfg.gate_mode, L.LAYOUT_PACKED)
+    ws = torch.empty(L.maskmoe_layer_workspace_bytes(desc) * 2, dtype=torch.uint8, device="cuda")
+    lib = L.load()
+    f = lambda t: t.data_ptr()
+    mask = np.ascontiguousarray(inp["mask"], dtype=np.uint8)
+    st = lib.maskmoe_layer_forward_train(
+        ctypes.byref(desc), f(pk["x"]), f(pk["w_router"]), mask.ctypes.data, None, f(pk["w_gate_up"]), f(pk["w_down"]), None,
+        None, f(ws), f(ws), f(ws), f(ws), f(ws), f(ws), ws.numel(), None)
+    assert st == L.E_UNSUPPORTED
