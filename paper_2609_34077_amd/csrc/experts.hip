@@ -781,7 +781,8 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
 
 // Slices of the reduction dimension for the two streaming kernels. Measured on MI355X (a sweep
 // of the target at 1, 4 and 16 tokens), the gate/up stream runs best with about 1800
-// workgroups in flight and the down stream with about 2600, as long as each slice keeps at
+// workgroups in flight and the down stream with about 1300 (fewer slices also shorten the
+// combine, which adds them), as long as each slice keeps at
 // least 16 chunks (shorter slices lose more to their start-up than the extra workgroups
 // gain): fewer workgroups leave HBM channels idle, and a count just past one full residency
 // wave leaves a ragged second wave. The split is the power of two (dividing the chunk count,
@@ -789,7 +790,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
 // the number of experts a batch of T tokens is expected to activate under uniform routing,
 // E (1 - (1 - K/E)^T), plus the shared experts. The grid is still sized for the most experts
 // that can be active; the estimate only picks the split.
-constexpr int kDecodeTargetWGsGateUp = 1792, kDecodeTargetWGsDown = 2560, kDecodeMinChunks = 16;
+constexpr int kDecodeTargetWGsGateUp = 1792, kDecodeTargetWGsDown = 1280, kDecodeMinChunks = 16;
 constexpr int kDecodeDownTiles = 8;
 
 static int best_split(int per_slice_wgs, int chunks, int max_split, int target) {
