@@ -186,7 +186,8 @@ size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc);
  *  Errors: as maskmoe_route, plus E_INVAL for F < 1 or n_shared outside 0..8 or a NULL
  *  shared-weight pointer with n_shared > 0; E_WORKSPACE when the workspace is too small;
  *  E_UNSUPPORTED for bf16 with d % 64 != 0 or F % 64 != 0, or with T*d, T*(K+n_shared)*F or
- *  2*F*d at or above 2^31 elements.
+ *  2*F*d at or above 2^31 elements. weight_layout: E_INVAL for a value other than
+ *  MASKMOE_LAYOUT_*, E_UNSUPPORTED for LAYOUT_PACKED with f32, d % 128 != 0 or F % 64 != 0.
  */
 int maskmoe_layer_forward(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                           const uint8_t* mask, const float* prior, const void* w_gate_up,
@@ -294,7 +295,8 @@ int maskmoe_sample_mask(const float* mask_logits, const double* uniforms, int32_
  *                keeps what maskmoe_layer_backward reads (the permutation, the SwiGLU
  *                activations and the gate / up pre-activations, bf16).
  *  Other arguments, rounding and errors as maskmoe_layer_forward (whatever T, bf16 layers take
- *  the grouped-GEMM path), plus E_INVAL for a NULL output above when T > 0.
+ *  the grouped-GEMM path), plus E_INVAL for a NULL output above when T > 0 and E_UNSUPPORTED for
+ *  packed weights (LAYOUT_PACKED).
  */
 int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                                 const uint8_t* mask, const float* prior, const void* w_gate_up,
@@ -352,7 +354,7 @@ size_t maskmoe_offload_workspace_bytes(const maskmoe_layer_desc* desc);
  *  with the same experts resident).
  *  Errors: E_INVAL for NULL or misaligned required pointers, host copies that are not pinned
  *  host memory, B outside [K, E], an unknown policy, or a bad mask / prior; E_UNSUPPORTED for
- *  T != 1, f32, E > 64 or d, F not multiples of 64.
+ *  T != 1, f32, E > 64, d, F not multiples of 64, or packed weights (LAYOUT_PACKED).
  */
 int maskmoe_offload_decode_step(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                                 const uint8_t* mask, const float* prior, const void* host_w_gate_up,
@@ -443,8 +445,9 @@ size_t maskmoe_layer_backward_workspace_bytes(const maskmoe_layer_desc* desc);
  *  workspace       device, maskmoe_layer_backward_workspace_bytes(desc) bytes, 256-byte aligned.
  *  Rounding: dO = g dy and [da db] are rounded to bf16 before their products, a and b are the
  *  forward's bf16-rounded pre-activations; accumulation and all outputs are fp32.
- *  Errors: as maskmoe_layer_forward; E_UNSUPPORTED for f32 layers or index ranges at or above
- *  2^31 elements; E_WORKSPACE for a missing, small or misaligned workspace of either kind.
+ *  Errors: as maskmoe_layer_forward; E_UNSUPPORTED for f32 layers, packed weights
+ *  (LAYOUT_PACKED) or index ranges at or above 2^31 elements; E_WORKSPACE for a missing, small
+ *  or misaligned workspace of either kind.
  *  T = 0 writes nothing.
  */
 int maskmoe_layer_backward(const maskmoe_layer_desc* desc, const void* x, const void* w_gate_up,
