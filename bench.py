@@ -22,6 +22,11 @@ Workloads (--workload):
            token sequence; time per output token with the 4-expert prior of each layer vs the
            zero prior, and the host-to-pool transfer rate.
 
+The layer workloads (decode, ft, deepseek) run on expert weights packed once at set-up,
+outside the timed region (maskmoe_pack_expert_weights; --layout rows keeps them row-major).
+Unless --no-extras is given, the same timed loop is repeated with the row-major weights and
+reported under `row_major_layout` (comparison only; `value` is the first loop).
+
 Prints one JSON line (rank 0). The roofline entry is for the dominant kernel, timed with
 HIP events recorded around its stage inside the timed region, on the stream the kernels run
 on (`stages_ms` comes from a separate untimed pass with every stage bracketed); `traffic` comes from
