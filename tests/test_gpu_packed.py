@@ -91,13 +91,20 @@ def test_packed_forward_oracle_parity(cfg):
     check_layer(cfg, packed=True)
 
 
-def test_packed_mixtral_decode_full_shape():
-    """The Mixtral decode layer (16 tokens, d = 4096, F = 14336): bitwise equal to row-major."""
-    cfg = synth.mixtral_decode_config(16)
+FULL = [synth.mixtral_decode_config(16), synth.mixtral_decode_config(1), synth.mixtral_ft_config(8192),
+        synth.deepseek_config(L.ROUTE_SOFT_PRIOR), synth.deepseek_config(L.ROUTE_HARD_MASK)]
+
+
+@pytest.mark.parametrize("cfg", FULL, ids=lambda c: f"{c.name}_{c.route_mode}")
+def test_packed_full_shapes_equal_row_major_bitwise(cfg):
+    """The bench's layer workloads at full size, in the bench's launch configuration (packed
+    weights): bitwise equal to the row-major path, which the layer tests compare with the oracle."""
+    U.say(f"packed vs row-major, full shape {cfg.name} T={cfg.T}")
     inp = _inputs(cfg)
     dd = _upload(inp, cfg)
-    y0, _, _ = run_gpu(cfg, inp, dd)
-    y1, _, _ = run_gpu(cfg, inp, dd, packed=True)
+    y0, i0, g0 = run_gpu(cfg, inp, dd)
+    y1, i1, g1 = run_gpu(cfg, inp, dd, packed=True)
+    assert torch.equal(i0, i1) and torch.equal(g0, g1)
     assert torch.equal(y0.view(torch.int16), y1.view(torch.int16))
 
 
