@@ -86,7 +86,8 @@ __global__ __launch_bounds__(kBwdThreads) void pad_layout_kernel(const int32_t* 
   }
 }
 
-// out[c * ldo + pc] = source row of pc at column c, for c < C (C % 64 == 0), pc < P: the
+// out[c * ldo + pc] = source row of pc at column c, for c < 64 gridDim.y (transpose() sizes the
+// grid from the column count C, C % 64 == 0) and pc < P: the
 // source row is pmap[pc] (-1: a zero column) or pc itself without a map, read at
 // src + row_tok[row] * lds (GATHER) or src + row * lds. 64x64 tiles through LDS; blockIdx.z
 // selects one matrix of a batch (src_batch / out_batch elements apart): matrix z, or with an
@@ -94,7 +95,7 @@ __global__ __launch_bounds__(kBwdThreads) void pad_layout_kernel(const int32_t* 
 template <bool GATHER>
 __global__ __launch_bounds__(kBwdThreads) void transpose_kernel(const uint16_t* __restrict__ src, int lds,
                                                                 const int32_t* __restrict__ pmap,
-                                                                const int32_t* __restrict__ row_tok, int P, int C,
+                                                                const int32_t* __restrict__ row_tok, int P,
                                                                 uint16_t* __restrict__ out, int ldo, size_t src_batch,
                                                                 size_t out_batch, const int32_t* __restrict__ active,
                                                                 const int32_t* __restrict__ n_active, int limit) {
@@ -332,13 +333,13 @@ __global__ __launch_bounds__(kBwdThreads) void dx_combine_kernel(const float* __
 hipError_t transpose(bool gather, const uint16_t* src, int lds, const int32_t* pmap, const int32_t* row_tok, int P,
                      int C, uint16_t* out, int ldo, int batch, size_t src_batch, size_t out_batch, hipStream_t s,
                      const int32_t* active = nullptr, const int32_t* n_active = nullptr, int limit = 0) {
-  const dim3 grid((P + 63) / 64, C / 64, batch);
+  const dim3 grid((P + 63) / 64, C / 64, batch);   // C: a multiple of 64 (d and F are, for bf16 layers)
   if (gather)
-    hipLaunchKernelGGL(transpose_kernel<true>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, C, out, ldo,
+    hipLaunchKernelGGL(transpose_kernel<true>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, out, ldo,
                        src_batch, out_batch, active, n_active, limit);
   else
-    hipLaunchKernelGGL(transpose_kernel<false>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, C, out,
-                       ldo, src_batch, out_batch, active, n_active, limit);
+    hipLaunchKernelGGL(transpose_kernel<false>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, out, ldo,
+                       src_batch, out_batch, active, n_active, limit);
   return hipGetLastError();
 }
 
