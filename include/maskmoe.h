@@ -84,8 +84,9 @@ enum { MASKMOE_CACHE_LRU = 0, MASKMOE_CACHE_LFU = 1, MASKMOE_CACHE_FIFO = 2 };
  *  route_mode MASKMOE_ROUTE_*; gate_mode MASKMOE_GATE_*
  *  weight_layout MASKMOE_LAYOUT_*: order of the expert weights. LAYOUT_PACKED needs bf16,
  *             d % 128 == 0 and F % 64 == 0 (else E_UNSUPPORTED) and is taken by the inference
- *             entry points (maskmoe_layer_forward, _profiled, _lora); the training, backward
- *             and offload entry points return E_UNSUPPORTED for it. maskmoe_route ignores it. */
+ *             entry points (maskmoe_layer_forward, _profiled, _lora, maskmoe_offload_decode_step);
+ *             the training and backward entry points return E_UNSUPPORTED for it.
+ *             maskmoe_route ignores it. */
 typedef struct maskmoe_layer_desc {
   int32_t T, d, E, K, F, n_shared, dtype, route_mode, gate_mode, weight_layout;
 } maskmoe_layer_desc;
@@ -354,7 +355,8 @@ size_t maskmoe_offload_workspace_bytes(const maskmoe_layer_desc* desc);
  *  with the same experts resident).
  *  Errors: E_INVAL for NULL or misaligned required pointers, host copies that are not pinned
  *  host memory, B outside [K, E], an unknown policy, or a bad mask / prior; E_UNSUPPORTED for
- *  T != 1, f32, E > 64, d, F not multiples of 64, or packed weights (LAYOUT_PACKED).
+ *  T != 1, f32, E > 64 or d, F not multiples of 64. Packed weights (desc->weight_layout):
+ *  the host copies, the shared experts and hence the pool are all in the packed layout.
  */
 int maskmoe_offload_decode_step(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
                                 const uint8_t* mask, const float* prior, const void* host_w_gate_up,

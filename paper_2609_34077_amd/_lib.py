@@ -398,7 +398,7 @@ def offload_empty_state(E: int, B: int, device="cuda"):
 def maskmoe_offload_decode_step(x, w_router, host_w_gate_up, host_w_down, slots_gate_up, slots_down, cache_state,
                                 K: int, route_mode: int, gate_mode: int, policy: int, mask=None, prior=None,
                                 ws_gate_up=None, ws_down=None, counters=None, dev_error=None, workspace=None,
-                                y=None, topk_idx=None, topk_gate=None, events=None):
+                                y=None, topk_idx=None, topk_gate=None, events=None, weight_layout=LAYOUT_ROWS):
     """One batch-1 decode step of one layer with host-resident experts. x [1,d] (device),
     host_w_gate_up [E,2F,d] / host_w_down [E,d,F] pinned host tensors, slots_* [B,...] device
     pool, cache_state int32 [B + 2E] device (see offload_empty_state). ``events``: 2 entries,
@@ -422,7 +422,7 @@ def maskmoe_offload_decode_step(x, w_router, host_w_gate_up, host_w_down, slots_
             or tuple(cache_state.shape) != (B + 2 * E,) or cache_state.dtype != torch.int32):
         raise ValueError("inconsistent offloaded-layer shapes")
     ns = 0 if ws_gate_up is None else ws_gate_up.shape[0]
-    desc = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode)
+    desc = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode, weight_layout)
     if workspace is None:
         workspace = torch.empty(max(int(lib.maskmoe_offload_workspace_bytes(ctypes.byref(desc))), 1),
                                 dtype=torch.uint8, device=x.device)

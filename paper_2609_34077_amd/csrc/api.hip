@@ -572,7 +572,6 @@ int maskmoe_offload_decode_step(const maskmoe_layer_desc* desc, const void* x, c
   int st = check_layer_desc(desc);
   if (st != MASKMOE_OK) return st;
   const maskmoe_layer_desc& d = *desc;
-  if (d.weight_layout != MASKMOE_LAYOUT_ROWS) return MASKMOE_E_UNSUPPORTED;
   st = check_mask_prior(d.route_mode, 1, d.E, d.K, mask, prior);
   if (st != MASKMOE_OK) return st;
   if (policy != MASKMOE_CACHE_LRU && policy != MASKMOE_CACHE_LFU && policy != MASKMOE_CACHE_FIFO)
@@ -631,6 +630,7 @@ int maskmoe_offload_decode_step(const maskmoe_layer_desc* desc, const void* x, c
   a.expert_out = nullptr;
   a.slot_of = cache_state + B + d.E;
   a.n_slots = B;
+  a.packed = d.weight_layout == MASKMOE_LAYOUT_PACKED;   // the pool holds copies of the host experts
   a.T = d.T; a.d = d.d; a.F = d.F; a.E = d.E; a.K = d.K; a.n_shared = d.n_shared;
   e = maskmoe::launch_experts_bf16_decode(a, pb, reinterpret_cast<uint16_t*>(ws + w.H),
                                           reinterpret_cast<float*>(ws + w.P), reinterpret_cast<float*>(ws + w.O), y,

@@ -243,7 +243,7 @@ def test_cache_rejects_invalid_arguments():
 
 def test_packed_layout_validation():
     """The packed weight layout: an unknown layout value is invalid; packed needs bf16,
-    d % 128 == 0 and F % 64 == 0; the training, backward and offload entry points refuse it."""
+    d % 128 == 0 and F % 64 == 0; the training and backward entry points refuse it."""
     lib = L.load()
     good = dict(T=32, d=128, E=8, K=2, F=256, n_shared=0, dtype=L.BF16, route_mode=L.ROUTE_PLAIN,
                 gate_mode=L.GATE_RENORM, weight_layout=L.LAYOUT_PACKED)
@@ -260,7 +260,8 @@ def test_packed_layout_validation():
                                            FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == L.E_UNSUPPORTED
     assert lib.maskmoe_layer_backward(ctypes.byref(desc), FAKE, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, 1 << 40,
                                       FAKE, FAKE, FAKE, None, None, FAKE, 1 << 40, None) == L.E_UNSUPPORTED
-    assert _offload(L.make_desc(**{**good, "T": 1})) == L.E_UNSUPPORTED
+    assert _offload(L.make_desc(**{**good, "T": 1, "d": 192})) == L.E_UNSUPPORTED
+    assert _offload(L.make_desc(**{**good, "T": 1})) == L.E_INVAL     # accepted; FAKE is not pinned host memory
 
 
 def test_pack_rejects_invalid_arguments():

@@ -28,10 +28,14 @@ def _pinned(a):
     return torch.from_numpy(np.ascontiguousarray(a)).view(torch.bfloat16).pin_memory()
 
 
-def _decode(cfg, inp, B, policy, state=None):
-    """Runs the cfg.T tokens of inp one step at a time; returns per-step results."""
+def _decode(cfg, inp, B, policy, state=None, packed=False):
+    """Runs the cfg.T tokens of inp one step at a time; returns per-step results. packed: the
+    host copies (and the shared experts) in the packed layout, packed on the device."""
     E, K, d = cfg.E, cfg.K, cfg.d
     host_gu, host_dn = _pinned(inp["w_gate_up"]), _pinned(inp["w_down"])
+    if packed:
+        pg, pd = L.maskmoe_pack_expert_weights(U.dev(inp["w_gate_up"]), U.dev(inp["w_down"]))
+        host_gu, host_dn = pg.cpu().pin_memory(), pd.cpu().pin_memory()
     slots_gu = torch.zeros((B, 2 * cfg.F, d), dtype=torch.bfloat16, device="cuda")
     slots_dn = torch.zeros((B, d, cfg.F), dtype=torch.bfloat16, device="cuda")
     st = L.offload_empty_state(E, B) if state is None else state
@@ -39,6 +43,8 @@ def _decode(cfg, inp, B, policy, state=None):
     wr = U.dev(inp["w_router"])
     sgu = U.dev(inp["ws_gate_up"]) if cfg.n_shared else None
     sdn = U.dev(inp["ws_down"]) if cfg.n_shared else None
+    if packed and cfg.n_shared:
+        sgu, sdn = L.maskmoe_pack_expert_weights(sgu, sdn)
     counters = torch.zeros(2, dtype=torch.int64, device="cuda")
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     mp = dict(prior=inp["prior"]) if cfg.route_mode == L.ROUTE_SOFT_PRIOR else dict(mask=inp["mask"])
@@ -49,7 +55,8 @@ def _decode(cfg, inp, B, policy, state=None):
         before = counters[0].item()
         y = L.maskmoe_offload_decode_step(xs[n:n + 1], wr, host_gu, host_dn, slots_gu, slots_dn, st, K,
                                           cfg.route_mode, cfg.gate_mode, policy, ws_gate_up=sgu, ws_down=sdn,
-                                          counters=counters, dev_error=err, topk_idx=idx, topk_gate=gate, **mp)
+                                          counters=counters, dev_error=err, topk_idx=idx, topk_gate=gate,
+                                          weight_layout=L.LAYOUT_PACKED if packed else L.LAYOUT_ROWS, **mp)
         torch.cuda.synchronize()
         out["f"].append(counters[0].item() - before)
         out["y"].append(y.clone())
@@ -155,3 +162,17 @@ def test_offload_mixtral_full_size():
     """Mixtral-shaped layer (d = 4096, F = 14336, 8 experts of 352 MB in pinned host memory), 8 steps, B = 4."""
     cfg = synth.mixtral_decode_config(8).with_(name="offload_mixtral", delta=0.2, seed=2)
     _check(cfg, 4, C.LRU)
+
+
+@pytest.mark.parametrize("cfg", [SMALL, SHARED], ids=lambda c: c.name)
+def test_offload_packed_weights_match_row_major_bitwise(cfg):
+    """Packed host copies (and shared experts): the same selections, fetches, cache states and
+    output bits as the row-major offloaded decode."""
+    U.say(f"offload packed vs row-major {cfg.name}")
+    inp = synth.make_layer(cfg)
+    a = _decode(cfg, inp, 4, C.LFU)
+    b = _decode(cfg, inp, 4, C.LFU, packed=True)
+    assert a["f"] == b["f"] and a["err"] == b["err"] == 0
+    for n in range(cfg.T):
+        assert np.array_equal(a["idx"][n], b["idx"][n]) and np.array_equal(a["state"][n], b["state"][n]), n
+        assert torch.equal(a["y"][n].view(torch.int16), b["y"][n].view(torch.int16)), n
