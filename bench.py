@@ -8,11 +8,16 @@ selections (maskmoe_cache_fetches, LRU, one cache per sequence, state carried fr
 step to step). Inputs are resident in HBM before timing starts.
 
 Workloads (--workload):
-  decode   (default) Mixtral-shaped decode layer: d=4096, F=14336, 8 experts, top-2,
+  ft       (default) Mixtral-shaped fine-tuning forward: 8192 tokens (4 x 2048), hard mask
+           keeping 4 experts; the largest single-GPU configuration and the headline line. Unless
+           --no-extras is given the same run also reports, as nested keys, the decode layer at
+           1, 4 and 16 tokens (`decode`), the routing-and-fetch trace with Fetches/tok under the
+           prior and the zero prior (`trace`, with the oracle's fetch counts compared in its
+           CPU-baseline leg), the training backward and the adapted forward.
+  decode   Mixtral-shaped decode layer: d=4096, F=14336, 8 experts, top-2,
            soft prior from a 4-expert set; --batch tokens per step (1, 4 or 16; default 16).
            Expert weights are rotated over --copies device copies so that no step re-reads
            weights from the 256 MB Infinity Cache left by the previous one.
-  ft       Mixtral-shaped fine-tuning forward: 8192 tokens, hard mask keeping 4 experts.
   deepseek DeepSeek-V2-Lite-shaped layer: d=2048, 64 routed (F=1408) + 2 shared experts,
            top-6, g = p, 4096 tokens (--mode hard|soft).
   trace    routing-and-fetch trace: 32 routers (4096 -> 8) over 256 AR(1) sequences x 512
@@ -64,7 +69,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--workload", choices=("decode", "ft", "deepseek", "trace", "offload"), default="decode")
+    ap.add_argument("--workload", choices=("decode", "ft", "deepseek", "trace", "offload"), default="ft")
     ap.add_argument("--slots", type=int, default=4, help="offload: experts cached per layer")
     ap.add_argument("--policy", choices=("lru", "lfu", "fifo"), default="lfu", help="offload: cache policy")
     ap.add_argument("--batch", type=int, default=16, help="decode tokens per step")
@@ -142,7 +147,9 @@ def blas_threads() -> int:
 
 # ----------------------------------------------------------------------------- layer workloads
 
-def layer_setup(args):
+def layer_setup(args, base=None):
+    """Inputs of a layer workload. ``base``: the state of a layer workload with the same weights
+    (the decode and fine-tuning layers share them), whose host and device weights are reused."""
     import torch
     from paper_2609_34077_amd import _lib as L
     from paper_2609_34077_amd import synth
@@ -155,13 +162,20 @@ def layer_setup(args):
         cfg = synth.deepseek_config(L.ROUTE_HARD_MASK if args.mode == "hard" else L.ROUTE_SOFT_PRIOR)
     log(f"generating {cfg.name} inputs")
     t0 = time.time()
-    inp = synth.make_layer(cfg)
+    if base is not None:
+        inp = dict(base["inp"], x=synth.layer_tokens(cfg), mask=synth.binary_mask(cfg.E, cfg.mask_set),
+                   prior=synth.concentrated_prior(cfg.E, cfg.mask_set, cfg.delta))
+    else:
+        inp = synth.make_layer(cfg)
     log(f"  inputs ready in {time.time() - t0:.1f}s")
     n_batches = 8 if args.workload == "decode" else 2
     xs = [inp["x"]] + [synth.make_tokens(cfg, cfg.T, s) for s in range(1, n_batches)]
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).view(torch.bfloat16).cuda()
     copies = max(1, args.copies) if args.workload == "decode" else 1
-    wgu0, wdn0 = dev(inp["w_gate_up"]), dev(inp["w_down"])
+    if base is not None:
+        wgu0, wdn0 = base["rows"]["wgu"][0], base["rows"]["wdn"][0]
+    else:
+        wgu0, wdn0 = dev(inp["w_gate_up"]), dev(inp["w_down"])
     wgu = [wgu0] + [wgu0.clone() for _ in range(copies - 1)]
     wdn = [wdn0] + [wdn0.clone() for _ in range(copies - 1)]
     sgu = dev(inp["ws_gate_up"]) if cfg.n_shared else None
@@ -176,8 +190,8 @@ def layer_setup(args):
         lay = dict(wgu=[p[0] for p in pk], wdn=[p[1] for p in pk], sgu=spk[0], sdn=spk[1], layout=L.LAYOUT_PACKED)
     else:
         lay = rows
-    st = dict(cfg=cfg, inp=inp, xs_host=xs, xs=[dev(x) for x in xs], w_router=dev(inp["w_router"]), rows=rows,
-              **lay)
+    st = dict(cfg=cfg, inp=inp, xs_host=xs, xs=[dev(x) for x in xs],
+              w_router=base["w_router"] if base is not None else dev(inp["w_router"]), rows=rows, **lay)
     desc = L.make_desc(cfg.T, cfg.d, cfg.E, cfg.K, cfg.F, cfg.n_shared, L.BF16, cfg.route_mode, cfg.gate_mode)
     st["ws"] = torch.empty(L.maskmoe_layer_workspace_bytes(desc), dtype=torch.uint8, device="cuda")
     st["y"] = torch.empty((cfg.T, cfg.d), dtype=torch.bfloat16, device="cuda")
@@ -250,10 +264,10 @@ def layer_cpu_baseline(st, budget_s: float = 10.0):
                       f"SwiGLU FFN of every selected expert, weights widened to fp64 per call"}
 
 
-def run_layer(args):
+def run_layer(args, base=None):
     import torch
     from paper_2609_34077_amd import _lib as L
-    st = layer_setup(args)
+    st = layer_setup(args, base)
     cfg = st["cfg"]
     work = layer_work(st)
     steps = args.steps if args.steps is not None else (200 if args.workload == "decode" else 20)
@@ -706,24 +720,100 @@ def run_trace(args):
             **{p: dict(v, reduction_pct=round(100 * (v["prior"] - v["zero_prior"]) / v["zero_prior"], 2))
                for p, v in concat.items()}},
     }
-    return res, dict(cfg=cfg, inp=inp)
+    # per-(layer, sequence) GPU counts and routing, for the oracle's comparison in the
+    # CPU-baseline leg (every sequence)
+    S_CMP = cfg.S
+    gpu_counts = {}
+    for name, pr in (("prior", inp["prior"]), ("zero_prior", inp["prior_zero"])):
+        idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=pr, with_margin=False,
+                                    workspace=ws)
+        r = L.maskmoe_cache_fetches(idx.view(cfg.L, cfg.S, cfg.N, cfg.K), cfg.E, cfg.B)
+        torch.cuda.synchronize()
+        gpu_counts[name] = dict(idx=idx.view(cfg.L, cfg.S, cfg.N, cfg.K)[:, :S_CMP].cpu().numpy(),
+                                fetches=r["fetches"][:, :S_CMP].cpu().numpy(), hits=r["hits"][:, :S_CMP].cpu().numpy())
+    return res, dict(cfg=cfg, inp=inp, gpu_counts=gpu_counts, S_cmp=S_CMP)
 
 
 def trace_cpu_baseline(st):
-    """The oracle on 32 of the 256 sequences (all layers and steps)."""
+    """The oracle on the whole trace (256 sequences, all 32 layers and 512 steps); its fetch and
+    hit counts are compared with the GPU's, per (layer, sequence), for the prior and the zero
+    prior (`fetch_parity`). Where the oracle's top-2 margin is <= 1e-3
+    several sets are correct: the GPU's set is checked to be a valid Top-K and the oracle's
+    replay adopts it (the near-tie reading of the routing rule); everywhere else the oracle
+    replays its own routing. Only the prior run is timed."""
     from oracle import cache as C
     from oracle import routing as R
     from paper_2609_34077_amd import synth
-    cfg, inp = st["cfg"], st["inp"]
-    S = 32
-    t0 = time.perf_counter()
-    x = synth.widen(inp["x"][: S * cfg.N], "bf16")
+    cfg, inp, S = st["cfg"], st["inp"], st["S_cmp"]
     w = synth.widen(inp["w_router"], "bf16")
-    idx, _, _ = R.route_layers(x, w, cfg.K, R.SOFT_PRIOR, R.GATE_RENORM, priors=inp["prior"])
-    C.cache_fetches(idx.reshape(cfg.L, S, cfg.N, cfg.K), cfg.E, cfg.B)
-    dt = time.perf_counter() - t0
-    return {"value": S * cfg.N / dt, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
-            "sample": f"{S} of {cfg.S} sequences x {cfg.N} steps, 32 layers: fp64 routing + Python LRU ({dt:.1f} s)"}
+    parity = {}
+    value = dt = None
+    for name, pr in (("prior", inp["prior"]), ("zero_prior", inp["prior_zero"])):
+        g = st["gpu_counts"][name]
+        t0 = time.perf_counter()
+        x = synth.widen(inp["x"][: S * cfg.N], "bf16")
+        idx, _, margin = R.route_layers(x, w, cfg.K, R.SOFT_PRIOR, R.GATE_RENORM, priors=pr)
+        idx = idx.reshape(cfg.L, S, cfg.N, cfg.K)
+        f_own, h_own, _, _, _ = C.cache_fetches(idx, cfg.E, cfg.B)
+        if name == "prior":
+            dt = time.perf_counter() - t0
+            value = S * cfg.N / dt
+        near = (margin <= 1e-3).reshape(cfg.L, S, cfg.N)
+        gi = g["idx"].astype(np.int64)
+        valid = all(R.valid_selection(R.router_logits(x[s_ * cfg.N + n][None], w[l])[0], gi[l, s_, n], cfg.K,
+                                      R.SOFT_PRIOR, prior=pr[l]) for l, s_, n in zip(*np.nonzero(near)))
+        eff = np.where(near[..., None], gi, idx)
+        f_o, h_o, _, _, _ = C.cache_fetches(eff, cfg.E, cfg.B)
+        clear = ~near.any(axis=2)
+        parity[name] = {
+            "streams": int(cfg.L * S),
+            "fetches_exact": bool(np.array_equal(f_o, g["fetches"])),
+            "hits_exact": bool(np.array_equal(h_o, g["hits"])),
+            "near_tie_pairs": int(near.sum()),
+            "near_tie_sets_valid": bool(valid),
+            "streams_without_near_tie": int(clear.sum()),
+            "clear_streams_exact_on_oracle_routing": bool(np.array_equal(f_own[clear], g["fetches"][clear])
+                                                          and np.array_equal(h_own[clear], g["hits"][clear])),
+            "fetches_per_token_oracle": round(float(f_o.sum()) / (S * cfg.N), 4),
+            "fetches_per_token_gpu": round(float(g["fetches"].sum()) / (S * cfg.N), 4),
+        }
+    return {"value": round(value, 1), "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{S} of {cfg.S} sequences x {cfg.N} steps, 32 layers, with the prior: fp64 routing + "
+                      f"Python LRU ({dt:.1f} s)",
+            "fetch_parity": parity}
+
+
+def run_nested_decode(args, ft_state):
+    """The decode layer at 1, 4 and 16 tokens on the fine-tuning layer's weights (the decode and
+    fine-tuning configurations share them), reported under the headline line's `decode` key."""
+    import copy
+    import torch
+    out = {}
+    for T in (1, 4, 16):
+        a = copy.copy(args)
+        a.workload, a.batch, a.steps, a.warmup, a.no_extras = "decode", T, 200, 20, True
+        r, st = run_layer(a, base=ft_state)
+        out[f"t{T}"] = {k: r[k] for k in ("value", "unit", "ms_per_step", "roofline", "step_roofline_frac",
+                                          "stages_ms")}
+        out[f"t{T}"]["distinct_experts_per_step"] = r["config"]["distinct_experts_per_step"]
+        del st
+        torch.cuda.empty_cache()
+    return out
+
+
+def run_nested_trace(args):
+    """The routing-and-fetch trace (Fetches/tok under the prior and the zero prior), reported
+    under the headline line's `trace` key, with the oracle's comparison of fetch counts."""
+    import copy
+    a = copy.copy(args)
+    a.steps, a.warmup = 10, 2
+    r, st = run_trace(a)
+    keep = ("value", "unit", "ms_per_step", "roofline", "stages_ms", "fetches_per_token", "fetch_reduction_pct",
+            "fetches_per_token_sweep", "fetches_per_token_persistent_caches")
+    out = {k: r[k] for k in keep}
+    out["config"] = r["config"]
+    out["cpu_baseline"] = None if args.no_cpu_baseline else trace_cpu_baseline(st)
+    return out
 
 
 def main():
@@ -753,6 +843,9 @@ def main():
             res["layer_backward"] = run_layer_backward(st, args)
             res["lora_forward"] = run_lora_forward(st, args)
         base = None if args.no_cpu_baseline else layer_cpu_baseline(st)
+        if args.workload == "ft" and not args.no_extras:
+            res["decode"] = run_nested_decode(args, st)
+            res["trace"] = run_nested_trace(args)
     res["cpu_baseline"] = base
     pr = torch.cuda.get_device_properties(0)
     res["device"] = f"{pr.name} ({pr.gcnArchName}, {pr.multi_processor_count} CUs, {pr.total_memory / 2**30:.0f} GiB)"

@@ -393,18 +393,7 @@ BwdLayout backward_layout(int T, int d, int F, int E, int K, int S) {
   return w;
 }
 
-// Workgroups an XCD runs at once (one 256 x 256 tile per CU) and the ROWS grid: 8 XCDs x
-// (their largest share of the tiles + tail slices).
-static int cus_per_xcd() {
-  static const int n = [] {
-    int dev = 0, cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                               hipSuccess || cu < 8)
-      cu = 256;
-    return cu / 8;
-  }();
-  return n;
-}
+// The ROWS grid: 8 XCDs x (their largest share of the tiles + tail slices).
 static dim3 rows_grid(int mt_max, int n_tiles) {
   return dim3(static_cast<unsigned>(8 * ((static_cast<long>(mt_max) * n_tiles + 7) / 8 + kTailSlotsPerXcd)));
 }
@@ -452,7 +441,7 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   n.ab = a.ab;
   n.c = dab;
   n.n_tiles = (F + kTileN - 1) / kTileN;
-  n.cu_xcd = cus_per_xcd();
+  n.cu_xcd = device_cus_per_xcd();
   n.part = reinterpret_cast<float*>(ws + w.part);
   hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiSwigluBwd>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads), 0,
                      s, n);

@@ -674,17 +674,12 @@ __global__ __launch_bounds__(256) void f32_down_kernel(const F32Args p) {
 
 }  // namespace
 
-// Workgroups an XCD runs at once: one per CU (the tile's 128 KiB of LDS), the CUs split evenly
-// over the 8 XCDs.
-static int cus_per_xcd() {
-  static const int n = [] {
-    int dev = 0, cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                               hipSuccess || cu < 8)
-      cu = 256;
-    return cu / 8;
-  }();
-  return n;
+int device_cus_per_xcd() {
+  int dev = 0, cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu < 8)
+    cu = 256;
+  return cu / 8;
 }
 
 // Grid of a grouped GEMM: 8 XCDs x (their largest share of tiles + tail slices).
@@ -712,7 +707,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   GemmArgs g{};
   g.ab = ab;
   g.part = part;
-  g.cu_xcd = cus_per_xcd();
+  g.cu_xcd = device_cus_per_xcd();
   const dim3 fixup_grid(8 * kTailSlotsPerXcd);
   hipError_t err;
   if (lora) {

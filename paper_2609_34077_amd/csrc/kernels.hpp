@@ -119,6 +119,11 @@ hipError_t launch_lora_down(const uint16_t* src, const int32_t* row_tok, int K, 
                             hipStream_t stream);
 
 // Partial-tile slots of the grouped GEMMs' split tail tiles (fp32 256 x 256 each, 64 MiB).
+// Workgroups one XCD of the current device runs at once (one 256 x 256 tile per CU, the CUs
+// split evenly over the 8 XCDs): queried for the current device on every call, so devices with
+// different CU counts each get their own figure.
+int device_cus_per_xcd();
+
 constexpr int kTailSlots = 256;
 constexpr size_t kTailPartBytes = static_cast<size_t>(kTailSlots) * 256 * 256 * 4;
 

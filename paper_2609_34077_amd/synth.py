@@ -232,6 +232,12 @@ def make_lora(cfg: LayerConfig, rank: int = 8, alpha: float = 16.0, b_std: float
     return out
 
 
+def layer_tokens(cfg: LayerConfig) -> np.ndarray:
+    """The tokens ``x [T,d]`` that ``make_layer(cfg)`` returns, drawn alone (same stream)."""
+    s_x = np.random.SeedSequence(cfg.seed).spawn(4)[3]
+    return _normal(s_x, (cfg.T, cfg.d), 1.0, cfg.dtype)
+
+
 def make_tokens(cfg: LayerConfig, T: int, stream: int) -> np.ndarray:
     """Extra token batches x ~ N(0,1) [T,d] from a stream keyed by ``stream`` (>= 1)."""
     seq = np.random.SeedSequence([cfg.seed, 7919, stream])

@@ -153,6 +153,72 @@ def test_route_then_replay_end_to_end(delta):
     np.testing.assert_array_equal(g2["hits"], h_o)
 
 
+def _trace_inputs_full():
+    if "full" not in _TRACE_CACHE:
+        U.say("trace full size: generating AR(1) inputs (256 sequences x 512 steps, d = 4096)")
+        cfg = synth.TraceConfig()
+        _TRACE_CACHE["full"] = (cfg, synth.make_trace_inputs(cfg))
+    return _TRACE_CACHE["full"]
+
+
+_TRACE_CACHE = {}
+
+
+@pytest.mark.parametrize("delta", [1.0, 0.0])
+def test_trace_full_size_fetch_parity(delta):
+    """The routing-and-fetch trace at full size (32 layers, 256 sequences x 512 AR(1) steps,
+    K = 2, LRU with B = 4, each (layer, sequence) its own cache starting empty), with the
+    per-layer prior and with the zero prior (Eq. 4; Eq. 5's counts).
+
+    The GPU routes all 131072 tokens through the 32 routers (maskmoe_route, split routing) and
+    replays the whole trace (maskmoe_cache_fetches). The oracle routes every token in float64;
+    where its margin is <= 1e-3 it adopts the GPU's set after checking it is a valid Top-K
+    (gpu_util.effective_routing), and replays every stream in Python. Fetches and hits must be
+    bit-exact for all 8192 (layer, sequence) streams, and so must Fetches/tok (Eq. 5).
+    """
+    cfg, inp = _trace_inputs_full()
+    prior = inp["prior"] if delta else inp["prior_zero"]
+    U.say(f"trace full size, delta={delta}: GPU routing + cache replay")
+    xd, wd = U.dev(inp["x"]), U.dev(inp["w_router"])
+    idx, _, _ = L.maskmoe_route(xd, wd, cfg.K, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, prior=prior, with_margin=False)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    res = L.maskmoe_cache_fetches(idx.view(cfg.L, cfg.S, cfg.N, cfg.K), cfg.E, cfg.B, dev_error=err)
+    torch.cuda.synchronize()
+    ig = idx.cpu().numpy()                       # [L, S*N, K]
+    fg, hg = res["fetches"].cpu().numpy(), res["hits"].cpu().numpy()
+    assert int(err.item()) == 0
+    del xd, wd, idx
+    T = cfg.S * cfg.N
+    if "z" not in _TRACE_CACHE:   # the logits do not depend on the prior
+        U.say("  oracle router logits (float64) of every token through the 32 routers")
+        wf = U.f64(inp["w_router"], "bf16").reshape(cfg.L * cfg.E, cfg.d)
+        z = np.empty((cfg.L, T, cfg.E))
+        step = 16384
+        for t0 in range(0, T, step):
+            zc = R.router_logits(U.f64(inp["x"][t0:t0 + step], "bf16"), wf)   # [t, L*E]
+            z[:, t0:t0 + step] = zc.reshape(-1, cfg.L, cfg.E).transpose(1, 0, 2)
+        _TRACE_CACHE["z"] = z
+    z = _TRACE_CACHE["z"]
+    trace_o = np.empty((cfg.L, T, cfg.K), np.int32)
+    near_total = clear_streams = 0
+    for l in range(cfg.L):
+        io, _, near = U.effective_routing(z[l], ig[l], cfg.K, R.SOFT_PRIOR, R.GATE_RENORM, prior=prior[l])
+        trace_o[l] = io
+        near_total += int(near.sum())
+        clear_streams += int((~near.reshape(cfg.S, cfg.N).any(axis=1)).sum())
+    U.say(f"  near-tie (layer, token) pairs {near_total} of {cfg.L * T} (GPU set adopted after validation); "
+          f"{clear_streams} of {cfg.L * cfg.S} streams have no near-tie")
+    assert clear_streams >= 32
+    U.say("  oracle cache replay of all 8192 streams")
+    f_o, h_o, _, _, bad = C.cache_fetches(trace_o.reshape(cfg.L, cfg.S, cfg.N, cfg.K), cfg.E, cfg.B)
+    assert not bad
+    np.testing.assert_array_equal(fg, f_o)
+    np.testing.assert_array_equal(hg, h_o)
+    fpt = C.fetches_per_token(int(f_o.sum()), T)
+    U.say(f"  Fetches/tok {fpt:.4f} (delta={delta}), bit-exact on every (layer, sequence)")
+    assert 0 < fpt <= cfg.L * cfg.K
+
+
 POLICIES = [L.CACHE_LRU, L.CACHE_LFU, L.CACHE_FIFO]
 
 

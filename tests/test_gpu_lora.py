@@ -1,8 +1,10 @@
 """GPU parity of maskmoe_layer_forward_lora (Stage 2: every routed and shared expert carries
 low-rank adapters on its gate, up and down projections) against the oracle's lora_moe_layer.
 
-Both sides route on their own; near-tie tokens (oracle margin <= 1e-3) are validated by the
-routing checks of the plain layer tests and left out here. Bound: max-normalised error
+Both sides route on their own. Near-tie tokens (oracle margin <= 1e-3) are evaluated by the
+oracle on the GPU's validated set with gates from its own p (gpu_util.effective_routing), so
+no token is left out. At the full shape the compared tokens cover every 256-row tile of every
+expert group. Bound: max-normalised error
 <= 1e-2 (bf16 storage; the GPU rounds A x, A h and (alpha / r) B to bf16, the oracle rounds
 nothing).
 """
@@ -51,7 +53,7 @@ def _run(cfg, inp, lora_np, workspace=None):
     return y, idx, gate
 
 
-def check_lora(cfg, rank=8, alpha=16.0, n_sample=None, seed=0):
+def check_lora(cfg, rank=8, alpha=16.0, sample=False, seed=0):
     U.say(f"lora layer {cfg.name} T={cfg.T} d={cfg.d} F={cfg.F} E={cfg.E} K={cfg.K} shared={cfg.n_shared} "
           f"rank={rank} alpha={alpha}")
     inp = synth.make_layer(cfg)
@@ -60,13 +62,14 @@ def check_lora(cfg, rank=8, alpha=16.0, n_sample=None, seed=0):
     xf = U.f64(inp["x"], "bf16")
     mp = _mp(cfg, inp)
     z = R.router_logits(xf, U.f64(inp["w_router"], "bf16"))
-    io, go, mo = R.route_logits(z, cfg.K, cfg.route_mode, cfg.gate_mode, mp.get("mask"), mp.get("prior"))
-    toks = np.arange(cfg.T)
-    if n_sample is not None and n_sample < cfg.T:
-        toks = np.sort(np.random.default_rng(seed).choice(cfg.T, n_sample, replace=False))
-    toks = toks[mo[toks] > U.MARGIN_TOL]
     ig = idx.cpu().numpy()
-    assert np.array_equal(ig[toks], io[toks]), "tokens with a clear margin must route identically"
+    U.check_routing(z, ig, gate.cpu().numpy(), None, cfg.K, cfg.route_mode, cfg.gate_mode, mp.get("mask"),
+                    mp.get("prior"))
+    io, go, near = U.effective_routing(z, ig, cfg.K, cfg.route_mode, cfg.gate_mode, mp.get("mask"),
+                                       mp.get("prior"))
+    toks = np.arange(cfg.T)
+    if sample:
+        toks = U.tile_sample_tokens(ig, cfg.E, cfg.n_shared, seed=seed)
     widen = functools.partial(synth.widen, dtype="bf16")
     ref = O.lora_moe_layer(xf[toks], io[toks], go[toks], inp["w_gate_up"], inp["w_down"], lora,
                            inp["ws_gate_up"] if cfg.n_shared else None, inp["ws_down"] if cfg.n_shared else None,
@@ -78,7 +81,8 @@ def check_lora(cfg, rank=8, alpha=16.0, n_sample=None, seed=0):
                        inp["ws_gate_up"] if cfg.n_shared else None, inp["ws_down"] if cfg.n_shared else None,
                        widen=widen)
     gap = U.normalized_max_error(base, ref)
-    U.say(f"  normalised max error {err:.3e} over {len(toks)} tokens (adapter term {gap:.2e})")
+    U.say(f"  normalised max error {err:.3e} over {len(toks)} tokens, {int(near[toks].sum())} near-ties "
+          f"(adapter term {gap:.2e})")
     assert err <= U.BF16_TOL
     assert gap > 3 * U.BF16_TOL
     rel = np.linalg.norm(yg - ref, axis=1) / np.maximum(np.linalg.norm(ref, axis=1), 1e-30)
@@ -160,4 +164,4 @@ def test_lora_rejects_bad_rank():
 
 def test_lora_mixtral_ft_full_sampled():
     """Mixtral-shaped fine-tuning layer (8192 tokens, d = 4096, F = 14336) with rank-8 adapters."""
-    check_lora(synth.mixtral_ft_config(8192), n_sample=40)
+    check_lora(synth.mixtral_ft_config(8192), sample=True)

@@ -227,3 +227,53 @@ def test_valid_selection_accepts_near_ties_only():
     assert not R.valid_selection(z2, [0, 3], 2, R.PLAIN)
     assert not R.valid_selection(z2, [0, 0], 2, R.PLAIN)
     assert not R.valid_selection(z2, [0, 1], 2, R.HARD_MASK, mask=np.array([1, 0, 1, 1]))
+
+
+@pytest.mark.parametrize("mode", [R.HARD_MASK, R.SOFT_PRIOR, R.PLAIN])
+def test_route_layers_brute_force_per_layer(mode):
+    """route_layers routes the same tokens through L independent routers, each with its own
+    mask or prior (Section 3.1: every MoE layer has its own router; Section 3.2: one mask and
+    prior per layer). Every (layer, token) is checked by brute force over K-subsets with that
+    layer's own logits x W_l^T (written out here as explicit dot products) and its own
+    mask / prior, and the gates against scipy's softmax of those logits. The layers' masks,
+    priors and routers differ, so applying layer 0's mask or prior to every layer, or
+    swapping the layer and token axes, fails."""
+    g = np.random.default_rng(4242 + mode)
+    Lyr, T, d, E, K = 4, 24, 12, 6, 2
+    x = g.normal(0, 1.0, size=(T, d))
+    w = g.normal(0, 0.6, size=(Lyr, E, d))
+    masks = np.zeros((Lyr, E), np.uint8)
+    for l, keep in enumerate([(0, 1, 2), (3, 4, 5), (0, 2, 4), (1, 3, 5)]):
+        masks[l, list(keep)] = 1
+    priors = np.stack([sp_softmax(np.where(masks[l] == 1, 3.0, 0.0)) for l in range(Lyr)])
+    idx, gate, margin = R.route_layers(x, w, K, mode, R.GATE_RENORM,
+                                       masks=masks if mode == R.HARD_MASK else None,
+                                       priors=priors if mode == R.SOFT_PRIOR else None)
+    assert idx.shape == (Lyr, T, K) and gate.shape == (Lyr, T, K) and margin.shape == (Lyr, T)
+    sets_differ = 0
+    for l in range(Lyr):
+        for t in range(T):
+            z = np.array([sum(x[t, j] * w[l, e, j] for j in range(d)) for e in range(E)])
+            p = sp_softmax(z)
+            if mode == R.PLAIN:
+                keys, elig = p, np.ones(E, bool)
+            elif mode == R.HARD_MASK:
+                keys, elig = p * masks[l], masks[l].astype(bool)
+            else:
+                keys, elig = p * priors[l], np.ones(E, bool)
+            want = _brute_force_set(keys, K, elig)
+            assert set(idx[l, t].tolist()) == want, (l, t)
+            sel = [int(e) for e in idx[l, t]]
+            np.testing.assert_allclose(gate[l, t], p[sel] / p[sel].sum(), rtol=1e-12)
+            if mode == R.HARD_MASK:
+                assert all(masks[l, e] for e in sel)
+            if set(idx[l, t].tolist()) != set(idx[0, t].tolist()):
+                sets_differ += 1
+    # the layers really route differently, so a layer mix-up cannot pass unnoticed
+    assert sets_differ >= T
+    # layer by layer, the result is the single-router routing of that layer
+    for l in range(Lyr):
+        i1, g1, m1 = R.route(x, w[l], K, mode, R.GATE_RENORM,
+                             mask=masks[l] if mode == R.HARD_MASK else None,
+                             prior=priors[l] if mode == R.SOFT_PRIOR else None)
+        assert np.array_equal(i1, idx[l]) and np.array_equal(g1, gate[l]) and np.array_equal(m1, margin[l])
