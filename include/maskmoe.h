@@ -14,8 +14,10 @@
  *  - Every pointer marked "device" must point to device memory of the current HIP device;
  *    pointers marked "host" are read synchronously during the call and not kept.
  *  - The caller owns every buffer. The library allocates nothing, keeps no global state and
- *    is reentrant. All work is enqueued asynchronously on `stream` (0 = the null stream);
- *    nothing is synchronised. Outputs are valid once the stream reaches that point.
+ *    is reentrant, with one exception: maskmoe_layer_forward_noalloc uses a device array of
+ *    the library (one per device) and remembers its address per device. All work is enqueued
+ *    asynchronously on `stream` (0 = the null stream); nothing is synchronised. Outputs are
+ *    valid once the stream reaches that point.
  *  - Every argument is validated before anything is enqueued: a non-zero status means that
  *    nothing was written. MASKMOE_E_HIP reports a failed launch (work enqueued before the
  *    failing launch may still run).
@@ -205,6 +207,35 @@ enum {
   MASKMOE_STAGE_COMBINE = 4,     /* y = sum_k g O + shared experts                      */
   MASKMOE_NUM_STAGES = 5
 };
+
+/*
+ * maskmoe_layer_forward_noalloc -- maskmoe_layer_forward without a caller workspace, for
+ * callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation). The workspace is a file-scope device array of the
+ * library, MASKMOE_NOALLOC_SCRATCH_BYTES (128 MiB) per device, created when the library's code
+ * is loaded onto a device and held until the process ends; its device address is looked up
+ * once per device, on the first call made with that device current. The call allocates
+ * nothing (no hipMalloc / hipFree, no allocating library routine).
+ *
+ *  Arguments, outputs, rounding and determinism are those of maskmoe_layer_forward, whose
+ *  kernels it runs; the results are bit-identical to it. 128 MiB covers every desc with
+ *  maskmoe_layer_workspace_bytes(desc) <= MASKMOE_NOALLOC_SCRATCH_BYTES, e.g. the bf16
+ *  Mixtral-shaped layer (d = 4096, F = 14336, E = 8, K = 2) up to 400 tokens, which includes
+ *  the decode batches.
+ *  Shared state: every call on one GPU uses that GPU's single array and leaves its last
+ *  contents there (nothing in it needs to start at zero). Calls that overlap on one GPU (on
+ *  different streams, or from different threads without ordering) race on it and give
+ *  undefined results; calls on different GPUs do not interact.
+ *  Errors: those of maskmoe_layer_forward, except that E_WORKSPACE means that
+ *  maskmoe_layer_workspace_bytes(desc) exceeds MASKMOE_NOALLOC_SCRATCH_BYTES; E_HIP when the
+ *  array's device address cannot be obtained (nothing is enqueued then); E_UNSUPPORTED for a
+ *  device ordinal >= 64.
+ */
+#define MASKMOE_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int maskmoe_layer_forward_noalloc(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                  const uint8_t* mask, const float* prior, const void* w_gate_up,
+                                  const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
+                                  int32_t* topk_idx, float* topk_gate, hipStream_t stream);
 
 /*
  * maskmoe_layer_forward_profiled -- maskmoe_layer_forward that also records caller-owned

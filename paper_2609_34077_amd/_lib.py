@@ -31,7 +31,7 @@ EXPORTS = ("maskmoe_route", "maskmoe_route_workspace_bytes", "maskmoe_layer_work
            "maskmoe_stage1_backward", "maskmoe_layer_train_workspace_bytes",
            "maskmoe_layer_backward_workspace_bytes", "maskmoe_layer_backward", "maskmoe_layer_lora_workspace_bytes",
            "maskmoe_layer_forward_lora", "maskmoe_offload_workspace_bytes", "maskmoe_offload_decode_step",
-           "maskmoe_pack_expert_weights")
+           "maskmoe_pack_expert_weights", "maskmoe_layer_forward_noalloc")
 NUM_STAGES = 5
 STAGES = ("route", "permute", "gate_up", "down", "combine")
 
@@ -83,6 +83,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.maskmoe_layer_forward.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                           _vp, _vp, _vp, _vp, _sz, _vp]
     lib.maskmoe_layer_forward.restype = ctypes.c_int
+    lib.maskmoe_layer_forward_noalloc.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                                  _vp, _vp, _vp, _vp, _vp]
+    lib.maskmoe_layer_forward_noalloc.restype = ctypes.c_int
     lib.maskmoe_layer_forward_profiled.argtypes = [ctypes.POINTER(LayerDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                                    _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp]
     lib.maskmoe_layer_forward_profiled.restype = ctypes.c_int
@@ -255,7 +258,7 @@ def maskmoe_layer_workspace_bytes(desc: LayerDesc) -> int:
 
 
 def _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask, prior, ws_gate_up, ws_down,
-                  workspace, y, topk_idx, topk_gate, weight_layout=LAYOUT_ROWS):
+                  workspace, y, topk_idx, topk_gate, weight_layout=LAYOUT_ROWS, with_workspace=True):
     """Checks shapes and dtypes of a layer call and marshals its leading arguments."""
     import torch
     for t, n in ((x, "x"), (w_router, "w_router"), (w_gate_up, "w_gate_up"), (w_down, "w_down"),
@@ -274,9 +277,8 @@ def _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask
         if t is not None and t.dtype != x.dtype:
             raise ValueError("all weights must have the dtype of x")
     desc = make_desc(T, d, E, K, F, ns, _dtype_code(x), route_mode, gate_mode, weight_layout)
-    need = maskmoe_layer_workspace_bytes(desc)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    if workspace is None and with_workspace:
+        workspace = torch.empty(max(maskmoe_layer_workspace_bytes(desc), 1), dtype=torch.uint8, device=x.device)
     if y is None:
         y = torch.empty((T, d), dtype=x.dtype, device=x.device)
     m_arr, m_p = _host_u8(mask, E) if route_mode == ROUTE_HARD_MASK else (None, None)
@@ -312,6 +314,26 @@ def maskmoe_layer_forward(x, w_router, w_gate_up, w_down, K: int, route_mode: in
             raise ValueError(f"need {NUM_STAGES + 1} events")
         handles = (ctypes.c_void_p * len(events))(*[None if ev is None else ev.cuda_event for ev in events])
         _check("maskmoe_layer_forward_profiled", lib.maskmoe_layer_forward_profiled(*args, handles, _stream()))
+    del keep
+    return y
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def maskmoe_layer_forward_noalloc(x, w_router, w_gate_up, w_down, K: int, route_mode: int, gate_mode: int,
+                                  y, mask=None, prior=None, ws_gate_up=None, ws_down=None, topk_idx=None,
+                                  topk_gate=None, weight_layout=LAYOUT_ROWS):
+    """maskmoe_layer_forward with the library's own per-device scratch array as its workspace
+    (the entry point for callers that cannot allocate). ``y`` [T,d] is the caller's output
+    tensor; nothing is allocated here or in the library. Returns y."""
+    if y is None:
+        raise ValueError("maskmoe_layer_forward_noalloc writes into a caller-owned y")
+    lib = load()
+    _, _, y, keep, head = _forward_args(x, w_router, w_gate_up, w_down, K, route_mode, gate_mode, mask, prior,
+                                        ws_gate_up, ws_down, None, y, topk_idx, topk_gate, weight_layout,
+                                        with_workspace=False)
+    _check("maskmoe_layer_forward_noalloc", lib.maskmoe_layer_forward_noalloc(*head, _stream()))
     del keep
     return y
 

@@ -5,8 +5,15 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "kernels.hpp"
 #include "maskmoe.h"
+
+// Workspace of maskmoe_layer_forward_noalloc: one copy per device, held while the process
+// runs. Host code reaches it only through the device address that hipGetSymbolAddress returns
+// for the current device (noalloc_scratch below), never through this name.
+static __device__ __align__(256) unsigned char scratch[MASKMOE_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -134,6 +141,24 @@ int check_layer_desc(const maskmoe_layer_desc* d) {
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? MASKMOE_OK : MASKMOE_E_HIP; }
+
+// Device address of `scratch` on the current device, looked up once per device (with that
+// device current) and kept; concurrent first calls store the same address.
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MASKMOE_E_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return MASKMOE_E_UNSUPPORTED;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MASKMOE_E_HIP;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return MASKMOE_OK;
+}
 
 }  // namespace
 
@@ -348,6 +373,20 @@ int maskmoe_layer_forward(const maskmoe_layer_desc* desc, const void* x, const v
                           size_t workspace_bytes, hipStream_t stream) {
   return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y,
                             topk_idx, topk_gate, nullptr, nullptr, workspace, workspace_bytes, stream, nullptr);
+}
+
+int maskmoe_layer_forward_noalloc(const maskmoe_layer_desc* desc, const void* x, const void* w_router,
+                                  const uint8_t* mask, const float* prior, const void* w_gate_up,
+                                  const void* w_down, const void* ws_gate_up, const void* ws_down, void* y,
+                                  int32_t* topk_idx, float* topk_gate, hipStream_t stream) {
+  int st = check_layer_desc(desc);
+  if (st != MASKMOE_OK) return st;
+  if (layout(*desc).total > MASKMOE_NOALLOC_SCRATCH_BYTES) return MASKMOE_E_WORKSPACE;
+  void* ws = nullptr;
+  st = noalloc_scratch(&ws);
+  if (st != MASKMOE_OK) return st;
+  return layer_forward_impl(desc, x, w_router, mask, prior, w_gate_up, w_down, ws_gate_up, ws_down, y, topk_idx,
+                            topk_gate, nullptr, nullptr, ws, MASKMOE_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 int maskmoe_layer_forward_train(const maskmoe_layer_desc* desc, const void* x, const void* w_router,

@@ -134,6 +134,23 @@ def test_profiled_forward_needs_an_event_array():
                                               FAKE, None, None, FAKE, ws, None, None) == L.E_INVAL
 
 
+def test_noalloc_forward_checks_its_limit_before_touching_the_device():
+    """The no-allocation entry point rejects a layer whose workspace exceeds its fixed scratch
+    array (E_WORKSPACE) and an invalid desc (E_INVAL) before any HIP call."""
+    lib = L.load()
+    call = lambda desc: lib.maskmoe_layer_forward_noalloc(ctypes.byref(desc), FAKE, FAKE, None, None, FAKE, FAKE,
+                                                          None, None, FAKE, None, None, None)
+    big = L.make_desc(T=8192, d=4096, E=8, K=2, F=14336, dtype=L.BF16, route_mode=L.ROUTE_PLAIN)
+    assert lib.maskmoe_layer_workspace_bytes(ctypes.byref(big)) > L.NOALLOC_SCRATCH_BYTES
+    assert call(big) == L.E_WORKSPACE
+    assert call(L.make_desc(T=16, d=4096, E=8, K=0, F=14336)) == L.E_INVAL
+    # the decode batches of the Mixtral-shaped layer fit the array
+    for T in (1, 4, 16):
+        dec = L.make_desc(T=T, d=4096, E=8, K=2, F=14336, dtype=L.BF16, route_mode=L.ROUTE_SOFT_PRIOR,
+                          weight_layout=L.LAYOUT_PACKED)
+        assert lib.maskmoe_layer_workspace_bytes(ctypes.byref(dec)) <= L.NOALLOC_SCRATCH_BYTES
+
+
 def _lora_fwd(desc, lora, ws_bytes=1 << 40, **kw):
     lib = L.load()
     a = dict(x=FAKE, w=FAKE, wgu=FAKE, wdn=FAKE, sgu=None, sdn=None, y=FAKE, ws=FAKE)
