@@ -189,9 +189,8 @@ enum { kEpiSwigluBwd = 0, kEpiF32 = 1 };
 // for all groups and the live tiles (n_active x tiles per group) are spread over the XCDs.
 template <int MODE, int EPI>
 __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
-  constexpr int TM = kTileTM, TN = kTileTN, U = kTileU, WN = 4;
-  __shared__ u32x4 lds_a[2][kTileM * 8];
-  __shared__ u32x4 lds_b[2][kTileN * 8];
+  constexpr int TM = kTileTM, TN = kTileTN, WN = 4;
+  __shared__ TileLds lds;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   int mt, nt, g, row0, row_end, nk;
@@ -231,19 +230,19 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
     bbase = p.b + k0;
   }
   const int n0 = nt * kTileN;
-  const int r0 = tile_load_row(), chunk = tile_load_chunk();
-  int aoffs[U], boffs[U];   // element offsets (< 2^31, checked by the host)
+  TileOps ops;   // this lane's four rows of each operand (tile_dma_row in gemm_tile.hpp)
+  ops.a = reinterpret_cast<const char*>(abase);
+  ops.b = reinterpret_cast<const char*>(bbase);
+  ops.b_step = kTileK * 2;
 #pragma unroll
-  for (int i = 0; i < U; ++i) {
-    const int r = r0 + 64 * i;
-    aoffs[i] = min(row0 + r, row_end - 1) * p.lda + chunk;
-    boffs[i] = min(n0 + r, p.N - 1) * p.ldb + chunk;
+  for (int i = 0; i < 4; ++i) {   // element offsets < 2^31 (checked by the host)
+    const int r = tile_dma_row(i), chunk = tile_dma_chunk(i) * 8;
+    ops.aoff[i] = static_cast<uint32_t>(min(row0 + r, row_end - 1) * p.lda + chunk) * 2u;
+    ops.boff[i] = static_cast<uint32_t>(min(n0 + r, p.N - 1) * p.ldb + chunk) * 2u;
   }
-  int aoff[TM], boff[TN];
+  int bfrag[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) aoff[i] = (wm * 128 + i * 32 + (lane & 31)) * 8;
-#pragma unroll
-  for (int j = 0; j < TN; ++j) boff[j] = (wn * 64 + j * 32 + (lane & 31)) * 8;
+  for (int j = 0; j < TN; ++j) bfrag[j] = wn * 64 + j * 32 + (lane & 31);
   f32x16 acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -251,7 +250,7 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-  gemm_tile_mainloop(abase, aoffs, bbase, boffs, aoff, boff, nk, acc, lds_a, lds_b);
+  gemm_tile_mainloop(ops, nk, bfrag, acc, lds);
   if (MODE == kNtRows && EPI == kEpiF32) {
     if (job.s > 1) tail_store_partial(p.part, job.slot, acc);   // a slice of a split tail tile
     else nt_store_rows(p, acc, row0, row_end, nt * kTileN);

@@ -123,9 +123,7 @@ template <int EPI, bool LORA = false, bool PACKED = false>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs p) {
   constexpr int WN = 4;                 // waves: 2 along rows x 4 along columns
   constexpr int TM = kTileTM, TN = kTileTN;
-  constexpr int U = kTileU;
-  __shared__ u32x4 lds_a[2][BM * 8];
-  __shared__ u32x4 lds_b[2][BN * 8];
+  __shared__ TileLds lds;
 
   // The grid covers the most tiles any routing can need plus the tail slices; tile_job gives
   // each XCD's workgroups that XCD's share of the live tiles (their count read on the device),
@@ -145,23 +143,26 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   const int nks = Kdim / BK / job.s;   // k-tiles of this slice
   const int k0 = z * nks * BK;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wn = wave % WN;
 
-  // Unit i of this thread: rows r0 + 64 i of the A and B tiles (see gemm_tile.hpp).
-  const int r0 = tile_load_row();
-  const int chunk = tile_load_chunk();
+  // This lane's four rows of the A and B tiles (tile_dma_row in gemm_tile.hpp). B tile rows
+  // 0..127 of the gate/up GEMM are W_gate rows n0.., rows 128..255 the matching W_up rows.
   const uint16_t* wg = g < p.E ? p.w + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * Kdim
                                : p.ws + static_cast<size_t>(g - p.E) * (EPI == 0 ? 2 * p.F : p.d) * Kdim;
-  int aoffs[U], boffs[U];   // element offsets (< 2^31, checked by the host)
-  int brows[U];             // the units' B rows within the group
+  TileOps ops;
+  ops.a = reinterpret_cast<const char*>(p.a + k0);
+  ops.b = reinterpret_cast<const char*>(wg + (PACKED ? static_cast<size_t>(k0 / kPackCols) * kPackBlock : k0));
+  ops.b_step = PACKED ? kPackBlock * 2 : BK * 2;
+  int brows[4];   // the pieces' B rows within the matrix
 #pragma unroll
-  for (int i = 0; i < U; ++i) {
-    const int r = r0 + 64 * i;
+  for (int i = 0; i < 4; ++i) {
+    const int r = tile_dma_row(i);
+    const int chunk = tile_dma_chunk(i) * 8;
     const int row = min(row0 + r, row_end - 1);
-    aoffs[i] = (EPI == 0 ? p.row_tok[row] : row) * Kdim + k0 + chunk;
+    ops.aoff[i] = static_cast<uint32_t>((EPI == 0 ? p.row_tok[row] : row) * Kdim + chunk) * 2u;
     int brow, grp, rig;   // row in the matrix; its packed group and row within the group
-    if (EPI == 0) {  // tile rows 0..127: W_gate rows n0.., rows 128..255: the matching W_up rows
+    if (EPI == 0) {
       const int n = min(n0 + (r & 127), p.F - 1);
       brow = r < 128 ? n : p.F + n;
       grp = n / 64;
@@ -172,20 +173,14 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
       rig = brow % kPackRows;
     }
     brows[i] = brow;
-    boffs[i] = PACKED ? grp * kPackRows * Kdim + (k0 / kPackCols) * kPackBlock + rig * kPackCols + chunk
-                      : brow * Kdim + k0 + chunk;
+    ops.boff[i] = static_cast<uint32_t>(PACKED ? grp * kPackRows * Kdim + rig * kPackCols + chunk : brow * Kdim + chunk) * 2u;
   }
 
-  // Fragment rows: A rows wm*128 + i*32 + (lane & 31); B rows: EPI 0 -> gate wn*32 + ... and
-  // the matching up row 128 + wn*32 + ...; EPI 1 -> wn*64 + j*32 + ...
-  int aoff[TM], boff[TN];
+  // B fragment rows: EPI 0 -> gate wn*32 + ... and the matching up row 128 + wn*32 + ...;
+  // EPI 1 -> wn*64 + j*32 + ...
+  int bfrag[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) aoff[i] = (wm * 128 + i * 32 + (lane & 31)) * 8;
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int br = EPI == 0 ? (j == 0 ? 0 : 128) + wn * 32 : wn * 64 + j * 32;
-    boff[j] = (br + (lane & 31)) * 8;
-  }
+  for (int j = 0; j < TN; ++j) bfrag[j] = (EPI == 0 ? (j == 0 ? 0 : 128) + wn * 32 : wn * 64 + j * 32) + (lane & 31);
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -195,18 +190,19 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
   if (LORA && z == 0) {   // the adapters' term as one more k-tile: A' = [U | rows], B' = [s B | W]
-    TileExtra ex;
-    ex.xa = p.lora_u;
-    ex.xb = p.lora_b + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * 64;
+    TileOps ex;
+    ex.a = reinterpret_cast<const char*>(p.lora_u);
+    ex.b = reinterpret_cast<const char*>(p.lora_b + static_cast<size_t>(g) * (EPI == 0 ? 2 * p.F : p.d) * 64);
+    ex.b_step = 0;
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-      ex.xaoffs[i] = min(row0 + r0 + 64 * i, row_end - 1) * 64 + chunk;
-      ex.xboffs[i] = brows[i] * 64 + chunk;
+    for (int i = 0; i < 4; ++i) {
+      const int chunk = tile_dma_chunk(i) * 8;
+      ex.aoff[i] = static_cast<uint32_t>(min(row0 + tile_dma_row(i), row_end - 1) * 64 + chunk) * 2u;
+      ex.boff[i] = static_cast<uint32_t>(brows[i] * 64 + chunk) * 2u;
     }
-    gemm_tile_mainloop<true, PACKED ? kPackBlock : BK>(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b,
-                                                       &ex);
+    gemm_tile_mainloop<true>(ops, nks, bfrag, acc, lds, &ex);
   } else {
-    gemm_tile_mainloop<false, PACKED ? kPackBlock : BK>(p.a, aoffs, wg, boffs, aoff, boff, nks, acc, lds_a, lds_b);
+    gemm_tile_mainloop<false>(ops, nks, bfrag, acc, lds);
   }
   if (job.s > 1) {   // a slice of a split tail tile: its partial tile goes to the slot
     tail_store_partial(p.part, job.slot, acc);

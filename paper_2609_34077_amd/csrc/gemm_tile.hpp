@@ -1,14 +1,20 @@
 // The 256 x 256 x 64 bf16 MFMA tile pipeline shared by the expert GEMMs (forward, dgrad and
 // wgrad): acc += A_tile * B_tile^T for 256 rows of A and 256 rows of B, both K-contiguous.
 //
-// 512 threads in 8 waves (2 along A rows x 4 along B rows); each wave owns 4 x 2 fragments of
-// v_mfma_f32_32x32x16_bf16 (128 A rows x 64 B rows). Thread tid loads 16-byte chunks of rows
-// (tid >> 3) + 64 i (i < 4) of each operand; LDS slot u = tid + 512 i (row u >> 3, physical
-// chunk u & 7) receives the logical chunk (u & 7) ^ lds_swizzle(row), which keeps the operand
-// reads free of bank conflicts. Pipeline: k-tile kt sits in LDS buffer kt & 1 and tile kt + 1 in
-// registers; right after the first k16 step of tile kt the registers go to the other buffer and
-// are refilled with tile kt + 2, so every global load has a whole k-tile of MFMA work to
-// arrive. Operand fragments of the next k16 step are read while the current one multiplies.
+// 512 threads in 8 waves; wave w belongs to group g = w / 4 (A rows 128 g .. 128 g + 127) and
+// owns 4 x 2 fragments of v_mfma_f32_32x32x16_bf16 (128 A rows x 64 B rows). The two waves that
+// share a SIMD (w and w + 4) alternate roles in phases of one 32-wide k step, separated by one
+// workgroup barrier: while one multiplies on operands it already holds in registers, the other
+// issues its share of the global loads of a later k-tile and reads its next operands from LDS.
+// The matrix unit therefore never waits for a load or an LDS read, and a load has at least two
+// phases to arrive. Global loads go straight to LDS (global_load_lds_dwordx4, 1 KB per
+// instruction: 8 rows x one 128-byte line), spread over the phases so that the texture unit is
+// never flooded. LDS (160 KB): each group's 128-row A half double-buffered (16 KB each), the
+// 256-row B tile triple-buffered (32 KB each), rows of 128 bytes with a 16-byte XOR swizzle
+// (bank-conflict free for the fragment reads). Group 0 issues its A half of tile m + 1 in its
+// first phase of tile m and its B half of tile m + 2 in its second; group 1 the same one phase
+// later. Each wave waits for its own loads (vmcnt) before the barrier that precedes their first
+// reader; a barrier never waits on the other group's loads.
 #pragma once
 
 #include "common.hpp"
@@ -17,103 +23,145 @@
 namespace maskmoe {
 
 constexpr int kTileM = 256, kTileN = 256, kTileK = 64, kTileThreads = 512;
-constexpr int kTileU = kTileM * 8 / kTileThreads;   // 16-byte units per thread, operand and stage
-constexpr int kTileTM = 4, kTileTN = 2;             // 32x32 fragments per wave
+constexpr int kTileTM = 4, kTileTN = 2;   // 32x32 fragments per wave
 
-// Row r0 = tid >> 3 of a thread's first unit and its swizzled chunk offset (elements).
-__device__ __forceinline__ int tile_load_row() { return threadIdx.x >> 3; }
-__device__ __forceinline__ int tile_load_chunk() {
-  return ((threadIdx.x & 7) ^ lds_swizzle(threadIdx.x >> 3)) * 8;
-}
-
-// One more k-tile ahead of the main operands: its rows of A at xa + xaoffs[i], of B at
-// xb + xboffs[i] (64 elements each, chunk included). The low-rank adapters use it: A' = [U | X],
-// B' = [s B | W] turns W x + s B (A x) into one product. It is the first tile, so only the
-// prologue loads it and the steady-state loop is the same as without it.
-struct TileExtra {
-  const uint16_t* xa;
-  const uint16_t* xb;
-  int xaoffs[kTileU];
-  int xboffs[kTileU];
+struct TileLds {
+  u32x4 a[2][2][128 * 8];   // [group][buffer][row * 8 + chunk]
+  u32x4 b[3][256 * 8];      // [buffer][row * 8 + chunk]
 };
 
-// aoffs / boffs: element offsets from abase / bbase of the thread's unit i rows, chunk included
-// (rows r0 + 64 i of the tile); aoff / boff: 16-byte LDS slot offsets of the wave's fragment
-// rows (row * 8). nk: k-tiles of 64 of the main operands (none and no extra tile leaves acc
-// unchanged). BSTEP: elements between consecutive k-tiles of a B row (kTileK row-major,
-// kPackBlock in the packed weight layout).
-template <bool EXTRA = false, int BSTEP = kTileK>
-__device__ __forceinline__ void gemm_tile_mainloop(const uint16_t* __restrict__ abase, const int (&aoffs)[kTileU],
-                                                   const uint16_t* __restrict__ bbase, const int (&boffs)[kTileU],
-                                                   const int (&aoff)[kTileTM], const int (&boff)[kTileTN], int nk,
-                                                   f32x16 (&acc)[kTileTM][kTileTN], u32x4 (*lds_a)[kTileM * 8],
-                                                   u32x4 (*lds_b)[kTileN * 8], const TileExtra* extra = nullptr) {
-  constexpr int U = kTileU, TM = kTileTM, TN = kTileTN, BK = kTileK, NT = kTileThreads;
-  constexpr int X = EXTRA ? 1 : 0;   // pipeline tile kt holds main tile kt - X
+// Tile row (0..255) of this lane's i-th 16-byte piece of each operand per k-tile (i < 4), and
+// the piece's logical chunk (its physical LDS chunk is lane & 7).
+__device__ __forceinline__ int tile_dma_row(int i) {
+  const int wave = threadIdx.x >> 6;
+  return (wave >> 2) * 128 + 8 * (4 * (wave & 3) + i) + ((threadIdx.x & 63) >> 3);
+}
+__device__ __forceinline__ int tile_dma_chunk(int i) { return (threadIdx.x & 7) ^ lds_swizzle(tile_dma_row(i)); }
+
+// Operands of one tile: byte bases at the first k-tile (wave-uniform) and this lane's byte
+// offsets of its four rows (tile_dma_row(i), chunk included) of each; A k-tiles are 128 bytes
+// apart, B k-tiles b_step bytes apart (128 row-major, the block size in the packed layout).
+struct TileOps {
+  const char* a;
+  const char* b;
+  uint32_t aoff[4];
+  uint32_t boff[4];
+  uint32_t b_step;
+};
+
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+__device__ __forceinline__ uint32_t lds_offset(const u32x4* p) {
+  return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<size_t>((lds_u32x4*)p)));
+}
+// 16 bytes per lane from gbase + voff straight into LDS at m0v + 16 * lane. The M0 write needs
+// one wait state before the load.
+__device__ __forceinline__ void dma16(uint32_t m0v, const void* gbase, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0v), "v"(voff), "s"(gbase)
+               : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+__device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// A workgroup barrier without the memory fence of __syncthreads (which would also wait for
+// every load still in flight); LDS ordering is made explicit with the waits above.
+__device__ __forceinline__ void tile_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// acc += A B^T over nk k-tiles (nk >= 1). EXTRA: one more k-tile first, from the operands in
+// *x (its b_step is unused); the low-rank adapters use it: [U | X] [s B | W]^T turns
+// W x + s B (A x) into one product. bfrag[j]: tile row of B fragment j for this lane (a multiple
+// of 32 plus lane & 31); A fragment i is tile row 128 g + 32 i + (lane & 31).
+template <bool EXTRA = false>
+__device__ __forceinline__ void gemm_tile_mainloop(const TileOps& o, int nk, const int (&bfrag)[kTileTN],
+                                                   f32x16 (&acc)[kTileTM][kTileTN], TileLds& L,
+                                                   const TileOps* x = nullptr) {
+  constexpr int X = EXTRA ? 1 : 0;
+  if (nk <= 0) return;
   const int ntot = nk + X;
-  if (ntot <= 0) return;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int sw = lds_swizzle(lane);   // fragment rows are a multiple of 32 plus (lane & 31)
-  u32x4 ra[U], rb[U];
-  auto gload = [&](int t) {   // main tile t
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int g = wave >> 2, q = wave & 3;
+  const uint32_t la0 = lds_offset(&L.a[g][0][0]) + q * 4 * 1024;
+  const uint32_t lb0 = lds_offset(&L.b[0][0]) + (g * 16 + q * 4) * 1024;
+  // Loads of pipeline tile t (main k-tile t - X), clamped to the last one: past the end they
+  // refill a buffer that nothing reads again, which keeps every wait count the same.
+  auto dma_a = [&](int t) {
+    const int tt = min(t, ntot - 1) - X;
+    const char* ga = o.a + static_cast<size_t>(tt) * 128;
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-      ra[i] = *reinterpret_cast<const u32x4*>(abase + (aoffs[i] + t * BK));
-      rb[i] = *reinterpret_cast<const u32x4*>(bbase + (boffs[i] + t * BSTEP));
+    for (int i = 0; i < 4; ++i) dma16(la0 + static_cast<uint32_t>((t & 1) * 16384 + i * 1024), ga, o.aoff[i]);
+  };
+  auto dma_b = [&](int t) {
+    const int tt = min(t, ntot - 1) - X;
+    const char* gb = o.b + static_cast<size_t>(tt) * o.b_step;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(lb0 + static_cast<uint32_t>((t % 3) * 32768 + i * 1024), gb, o.boff[i]);
+  };
+  const int sw = lds_swizzle(lane & 31);
+  u32x4 af[2][kTileTM], bf[2][kTileTN];
+  auto read_half = [&](int t, int h) {   // operands of k steps 2h, 2h + 1 of pipeline tile t
+    const u32x4* pa = &L.a[g][t & 1][0];
+    const u32x4* pb = &L.b[t % 3][0];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int ch = (4 * h + 2 * kk + (lane >> 5)) ^ sw;
+#pragma unroll
+      for (int i = 0; i < kTileTM; ++i) af[kk][i] = pa[(i * 32 + (lane & 31)) * 8 + ch];
+#pragma unroll
+      for (int j = 0; j < kTileTN; ++j) bf[kk][j] = pb[bfrag[j] * 8 + ch];
     }
   };
-  auto lstore = [&](int buf) {
+  auto compute = [&]() {
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-      lds_a[buf][tid + NT * i] = ra[i];
-      lds_b[buf][tid + NT * i] = rb[i];
-    }
-  };
-  u32x4 af[2][TM], bf[2][TN];
-  auto read_frags = [&](int buf, int kk, int slot) {
-    const int ch = (kk * 2 + (lane >> 5)) ^ sw;
+    for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-    for (int i = 0; i < TM; ++i) af[slot][i] = lds_a[buf][aoff[i] + ch];
+      for (int i = 0; i < kTileTM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) bf[slot][j] = lds_b[buf][boff[j] + ch];
+        for (int j = 0; j < kTileTN; ++j) acc[i][j] = mfma_32x32x16(af[kk][i], bf[kk][j], acc[i][j]);
+    __builtin_amdgcn_s_setprio(0);
   };
 
+  // prologue: this wave's A piece of tile 0 and B pieces of tiles 0 and 1
   if (EXTRA) {
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-      ra[i] = *reinterpret_cast<const u32x4*>(extra->xa + extra->xaoffs[i]);
-      rb[i] = *reinterpret_cast<const u32x4*>(extra->xb + extra->xboffs[i]);
-    }
+    for (int i = 0; i < 4; ++i) dma16(la0 + static_cast<uint32_t>(i * 1024), x->a, x->aoff[i]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(lb0 + static_cast<uint32_t>(i * 1024), x->b, x->boff[i]);
   } else {
-    gload(0);
+    dma_a(0);
+    dma_b(0);
   }
-  lstore(0);
-  gload(min(1 - X, nk - 1));
-  __syncthreads();
-  read_frags(0, 0, 0);
-  // The loop body has no branches, so that LDS stores and global loads can be interleaved
-  // with the MFMAs (LLVM's MFMA/DS interleaving strategy 0): past the end, the last main tile is
-  // loaded again and stored into the idle buffer, which nothing reads afterwards (every LDS
-  // access of the loop has completed at its last barrier).
-  for (int kt = 0; kt < ntot; ++kt) {
-    const int buf = kt & 1;
-    __builtin_amdgcn_iglp_opt(0);
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < BK / 16) read_frags(buf, kk + 1, cur ^ 1);
-      if (kk == 0) {
-        lstore(buf ^ 1);
-        gload(min(kt + 2 - X, nk - 1));
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_32x32x16(af[cur][i], bf[cur][j], acc[i][j]);
-    }
-    __syncthreads();
-    read_frags(buf ^ 1, 0, 0);
+  dma_b(1);
+  wait_vmcnt<0>();
+  tile_barrier();
+  // group 1 runs one phase behind group 0: one extra barrier first (group 0 adds it at the end)
+  if (g == 1) tile_barrier();
+  for (int m = 0; m < ntot; ++m) {
+    __builtin_amdgcn_sched_barrier(0);
+    dma_a(m + 1);
+    read_half(m, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_lgkmcnt0();
+    tile_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compute();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<4>();
+    tile_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    dma_b(m + 2);
+    read_half(m, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_lgkmcnt0();
+    tile_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compute();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<4>();
+    tile_barrier();
   }
+  if (g == 0) tile_barrier();
+  wait_vmcnt<0>();
 }
 
 // XCD-aware tile order: the hardware deals workgroup ids round-robin over the 8 XCDs, so ids
