@@ -293,16 +293,14 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
 }
 
 // Adds the slices of each split tail tile of the ROWS fp32 product in slice order and stores
-// it; one workgroup per possible tail tile, grid 8 x kTailSlotsPerXcd.
+// it; kTailFixParts workgroups per possible tail tile, grid 8 x kTailSlotsPerXcd x kTailFixParts.
 __global__ __launch_bounds__(kTileThreads) void nt_tail_fixup(const NtArgs p) {
   const int mt_live = p.tile_off[p.G];
   const int live = mt_live * p.n_tiles;
   const int nk = p.K / kTileK;
-  const int xcd = blockIdx.x & 7, t = blockIdx.x >> 3;
+  const int b = blockIdx.x, xcd = b & 7, t = (b >> 3) % kTailSlotsPerXcd, part = b / (8 * kTailSlotsPerXcd);
   const XcdShare x = xcd_share(xcd, live, p.cu_xcd, nk, nt_tail_split(kNtRows, kEpiF32, nk));
   if (x.s == 1 || t >= x.r) return;
-  f32x16 acc[kTileTM][kTileTN];
-  tail_sum_partials(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, acc);
   int mt, nt;
   grouped_tile_coords(x.base + x.full + t, mt_live, p.n_tiles, mt, nt);
   int lo = 0, hi = p.G;   // tile_off[lo] <= mt < tile_off[hi]
@@ -310,7 +308,11 @@ __global__ __launch_bounds__(kTileThreads) void nt_tail_fixup(const NtArgs p) {
     const int mid = (lo + hi) >> 1;
     if (p.tile_off[mid] <= mt) lo = mid; else hi = mid;
   }
-  nt_store_rows(p, acc, p.offsets[lo] + (mt - p.tile_off[lo]) * kTileM, p.offsets[lo + 1], nt * kTileN);
+  const int row0 = p.offsets[lo] + (mt - p.tile_off[lo]) * kTileM, row_end = p.offsets[lo + 1], n0 = nt * kTileN;
+  float* out = static_cast<float*>(p.c);
+  tail_fixup_part(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, part, [&](int r, int c, float v) {
+    if (row0 + r < row_end && n0 + c < p.N) out[static_cast<size_t>(row0 + r) * p.ldc + n0 + c] = v;
+  });
 }
 
 // dx[t, c] = sum_k dXr[inv[t K + k], c] + sum_s dXr[T K + s T + t, c], in that order.
@@ -454,7 +456,7 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiF32>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads), 0, s, n);
   MASKMOE_TRY(hipGetLastError());
   if (nt_tail_split(kNtRows, kEpiF32, n.K / kTileK)) {
-    hipLaunchKernelGGL(nt_tail_fixup, dim3(8 * kTailSlotsPerXcd), dim3(kTileThreads), 0, s, n);
+    hipLaunchKernelGGL(nt_tail_fixup, dim3(8 * kTailSlotsPerXcd * kTailFixParts), dim3(kTileThreads), 0, s, n);
     MASKMOE_TRY(hipGetLastError());
   }
   hipLaunchKernelGGL(dx_combine_kernel, dim3(T), dim3(kBwdThreads), 0, s, dxr, a.pb.inv, T, K, a.S, d, a.d_x);

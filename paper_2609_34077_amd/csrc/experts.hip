@@ -211,23 +211,24 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
   gemm_epilogue<EPI>(p, acc, row0, row_end, n0);
 }
 
-// Adds the slices of each split tail tile (grouped_gemm_bf16) in slice order and applies the
-// GEMM's epilogue; one workgroup per possible tail tile, grid 8 x kTailSlotsPerXcd.
-template <int EPI>
+// Adds the slices of each split tail tile of the down GEMM (grouped_gemm_bf16<1>) in slice order
+// and stores its rows of O; kTailFixParts workgroups per possible tail tile, grid
+// 8 x kTailSlotsPerXcd x kTailFixParts.
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_tail_fixup(const GemmArgs p) {
   const int mt_live = p.tile_off[p.G];
   const int live = mt_live * p.n_tiles;
-  const int nk = (EPI == 0 ? p.d : p.F) / BK;
-  const int xcd = blockIdx.x & 7, t = blockIdx.x >> 3;
-  const XcdShare x = xcd_share(xcd, live, p.cu_xcd, nk, tail_can_split(EPI, nk));
+  const int nk = p.F / BK;
+  const int b = blockIdx.x, xcd = b & 7, t = (b >> 3) % kTailSlotsPerXcd, part = b / (8 * kTailSlotsPerXcd);
+  const XcdShare x = xcd_share(xcd, live, p.cu_xcd, nk, tail_can_split(1, nk));
   if (x.s == 1 || t >= x.r) return;
-  f32x16 acc[kTileTM][kTileTN];
-  tail_sum_partials(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, acc);
   int mt, nt;
   grouped_tile_coords(x.base + x.full + t, mt_live, p.n_tiles, mt, nt);
   const int g = find_group(p.tile_off, p.G, mt);
-  gemm_epilogue<EPI>(p, acc, p.offsets[g] + (mt - p.tile_off[g]) * BM, p.offsets[g + 1],
-                     nt * (EPI == 0 ? BN / 2 : BN));
+  const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM, row_end = p.offsets[g + 1], n0 = nt * BN;
+  float* out = static_cast<float*>(p.out);
+  tail_fixup_part(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, part, [&](int r, int c, float v) {
+    if (row0 + r < row_end && n0 + c < p.d) out[static_cast<size_t>(row0 + r) * p.d + n0 + c] = v;
+  });
 }
 
 // y_t = sum_k gate[t,k] * O[inv[t*K+k]] + sum_s O[T*K + s*T + t]; fp32 sum in k order, one
@@ -704,7 +705,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   g.ab = ab;
   g.part = part;
   g.cu_xcd = device_cus_per_xcd();
-  const dim3 fixup_grid(8 * kTailSlotsPerXcd);
+  const dim3 fixup_grid(8 * kTailSlotsPerXcd * kTailFixParts);
   hipError_t err;
   if (lora) {
     err = launch_lora_pack(*lora, G, a.E, a.F, a.d, stream);
@@ -750,7 +751,7 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (tail_can_split(1, a.F / BK)) {
-    hipLaunchKernelGGL(grouped_tail_fixup<1>, fixup_grid, dim3(GEMM_THREADS), 0, stream, g);
+    hipLaunchKernelGGL(grouped_tail_fixup, fixup_grid, dim3(GEMM_THREADS), 0, stream, g);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }

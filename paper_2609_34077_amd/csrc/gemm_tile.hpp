@@ -194,7 +194,7 @@ __device__ __forceinline__ void grouped_tile_coords(int lid, int mt_max, int n_t
 // power of two <= kTailMaxSplit with r * s <= min(cu_xcd, kTailSlotsPerXcd), s dividing the
 // k-tiles and leaving >= kTailMinK per slice), so the last round is short and full. A slice
 // writes its partial tile to a slot (tail_store_partial); a fix-up kernel adds a tile's slices
-// in slice order (tail_sum_partials) and applies the GEMM's epilogue, so results stay
+// in slice order (tail_fixup_part) and applies the GEMM's epilogue, so results stay
 // deterministic.
 constexpr int kTailSlotsPerXcd = kTailSlots / 8;
 constexpr int kTailMaxSplit = 8, kTailMinK = 16;
@@ -263,28 +263,41 @@ __device__ __forceinline__ void tail_store_partial(float* part, int slot, const 
             make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
 }
 
-// acc = the sum, in slice order, of the s partial tiles in slots slot0 .. slot0 + s - 1.
-__device__ __forceinline__ void tail_sum_partials(const float* part, int slot0, int s,
-                                                  f32x16 (&acc)[kTileTM][kTileTN]) {
+// Fix-up of split tail tiles, spread over kTailFixParts workgroups per tile: part p adds, in
+// slice order, the partial-tile units e = kTailUnitsPerPart p .. (4 units of each thread; unit
+// e of thread tid holds acc[i][j][4 q .. 4 q + 3] with e = (i * kTileTN + j) * 4 + q, i.e. tile
+// rows wm*128 + i*32 + 8q + 4 (lane >> 5) + (0..3) of tile column wn*64 + j*32 + (lane & 31))
+// and hands each sum to st(tile_row, tile_col, value). All slices of a unit are loaded before
+// any is added.
+constexpr int kTailFixParts = 8, kTailUnitsPerPart = kTileTM * kTileTN * 4 / kTailFixParts;
+
+template <class Store>
+__device__ __forceinline__ void tail_fixup_part(const float* part, int slot0, int s, int p, Store st) {
+  constexpr int WN = 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
   const float4* src = reinterpret_cast<const float4*>(part) + static_cast<size_t>(slot0) * (kTailTileFloats / 4);
-  const int tid = threadIdx.x;
 #pragma unroll
-  for (int i = 0; i < kTileTM; ++i)
+  for (int u = 0; u < kTailUnitsPerPart; ++u) {
+    const int e = p * kTailUnitsPerPart + u;
+    float4 v[kTailMaxSplit];
 #pragma unroll
-    for (int j = 0; j < kTileTN; ++j)
+    for (int z = 0; z < kTailMaxSplit; ++z)
+      if (z < s) v[z] = src[static_cast<size_t>(z) * (kTailTileFloats / 4) + static_cast<size_t>(e) * kTileThreads + tid];
+    float4 a = v[0];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const size_t e = static_cast<size_t>((i * kTileTN + j) * 4 + q) * kTileThreads + tid;
-        float4 v = src[e];
-        for (int z = 1; z < s; ++z) {
-          const float4 u = src[static_cast<size_t>(z) * (kTailTileFloats / 4) + e];
-          v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
-        }
-        acc[i][j][4 * q] = v.x;
-        acc[i][j][4 * q + 1] = v.y;
-        acc[i][j][4 * q + 2] = v.z;
-        acc[i][j][4 * q + 3] = v.w;
+    for (int z = 1; z < kTailMaxSplit; ++z)
+      if (z < s) {
+        a.x += v[z].x; a.y += v[z].y; a.z += v[z].z; a.w += v[z].w;
       }
+    const int q = e & 3, j = (e >> 2) % kTileTN, i = (e >> 2) / kTileTN;
+    const int row = wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5);
+    const int col = wn * 64 + j * 32 + (lane & 31);
+    st(row, col, a.x);
+    st(row + 1, col, a.y);
+    st(row + 2, col, a.z);
+    st(row + 3, col, a.w);
+  }
 }
 
 }  // namespace maskmoe
