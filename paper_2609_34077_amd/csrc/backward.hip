@@ -310,8 +310,17 @@ __global__ __launch_bounds__(kTileThreads) void nt_tail_fixup(const NtArgs p) {
   }
   const int row0 = p.offsets[lo] + (mt - p.tile_off[lo]) * kTileM, row_end = p.offsets[lo + 1], n0 = nt * kTileN;
   float* out = static_cast<float*>(p.c);
-  tail_fixup_part(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, part, [&](int r, int c, float v) {
-    if (row0 + r < row_end && n0 + c < p.N) out[static_cast<size_t>(row0 + r) * p.ldc + n0 + c] = v;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave / 4, wn = wave % 4;
+  tail_fixup_part(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, part, [&](int i, int q, float4 a0, float4 a1) {
+    const float v0[4] = {a0.x, a0.y, a0.z, a0.w}, v1[4] = {a1.x, a1.y, a1.z, a1.w};
+    const int c0 = n0 + wn * 64 + (lane & 31);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int row = row0 + wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5) + u;
+      if (row >= row_end) continue;
+      if (c0 < p.N) out[static_cast<size_t>(row) * p.ldc + c0] = v0[u];
+      if (c0 + 32 < p.N) out[static_cast<size_t>(row) * p.ldc + c0 + 32] = v1[u];
+    }
   });
 }
 

@@ -61,8 +61,8 @@ struct GemmArgs {
 
 // Only the down GEMM splits its tail tiles (tile_job in gemm_tile.hpp): its long reductions
 // amortise a slice's fixed costs, and the gate/up GEMM's epilogue needs whole sums. Measured,
-// slices shorter than 16 k-tiles and splits of the gate/up tiles cost more than the idle round
-// they save.
+// slices shorter than 16 k-tiles and splits of the gate/up tiles (with SwiGLU applied in the
+// fix-up) gained nothing over the partial round they save.
 __host__ __device__ constexpr bool tail_can_split(int epi, int nk) { return epi == 1 && tail_splittable(nk); }
 
 __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt) {
@@ -224,10 +224,19 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_tail_fixup(const GemmArg
   int mt, nt;
   grouped_tile_coords(x.base + x.full + t, mt_live, p.n_tiles, mt, nt);
   const int g = find_group(p.tile_off, p.G, mt);
-  const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM, row_end = p.offsets[g + 1], n0 = nt * BN;
+  const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM, row_end = p.offsets[g + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave / 4, wn = wave % 4;
+  const int c0 = nt * BN + wn * 64 + (lane & 31);
   float* out = static_cast<float*>(p.out);
-  tail_fixup_part(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, part, [&](int r, int c, float v) {
-    if (row0 + r < row_end && n0 + c < p.d) out[static_cast<size_t>(row0 + r) * p.d + n0 + c] = v;
+  tail_fixup_part(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, part, [&](int i, int q, float4 a0, float4 a1) {
+    const float v0[4] = {a0.x, a0.y, a0.z, a0.w}, v1[4] = {a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int row = row0 + wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5) + u;
+      if (row >= row_end) continue;
+      if (c0 < p.d) out[static_cast<size_t>(row) * p.d + c0] = v0[u];
+      if (c0 + 32 < p.d) out[static_cast<size_t>(row) * p.d + c0 + 32] = v1[u];
+    }
   });
 }
 

@@ -264,39 +264,40 @@ __device__ __forceinline__ void tail_store_partial(float* part, int slot, const 
 }
 
 // Fix-up of split tail tiles, spread over kTailFixParts workgroups per tile: part p adds, in
-// slice order, the partial-tile units e = kTailUnitsPerPart p .. (4 units of each thread; unit
-// e of thread tid holds acc[i][j][4 q .. 4 q + 3] with e = (i * kTileTN + j) * 4 + q, i.e. tile
-// rows wm*128 + i*32 + 8q + 4 (lane >> 5) + (0..3) of tile column wn*64 + j*32 + (lane & 31))
-// and hands each sum to st(tile_row, tile_col, value). All slices of a unit are loaded before
-// any is added.
-constexpr int kTailFixParts = 8, kTailUnitsPerPart = kTileTM * kTileTN * 4 / kTailFixParts;
+// slice order, the partial-tile units of the fragment rows (i, q) = (iq / 4, iq % 4) for
+// iq = kTailPairsPerPart p .., both column fragments j (unit e = (i * kTileTN + j) * 4 + q of
+// thread tid holds acc[i][j][4 q .. 4 q + 3]: tile rows wm*128 + i*32 + 8q + 4 (lane >> 5) + (0..3)
+// of fragment column j), and hands the sums to st(i, q, sum_j0, sum_j1). All slices of a unit
+// are loaded before any is added.
+constexpr int kTailFixParts = 8, kTailPairsPerPart = kTileTM * 4 / kTailFixParts;
+static_assert(kTileTN == 2, "the fix-up hands over two column fragments");
 
 template <class Store>
 __device__ __forceinline__ void tail_fixup_part(const float* part, int slot0, int s, int p, Store st) {
-  constexpr int WN = 4;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
   const float4* src = reinterpret_cast<const float4*>(part) + static_cast<size_t>(slot0) * (kTailTileFloats / 4);
+  const int tid = threadIdx.x;
 #pragma unroll
-  for (int u = 0; u < kTailUnitsPerPart; ++u) {
-    const int e = p * kTailUnitsPerPart + u;
-    float4 v[kTailMaxSplit];
+  for (int u = 0; u < kTailPairsPerPart; ++u) {
+    const int iq = p * kTailPairsPerPart + u, i = iq >> 2, q = iq & 3;
+    float4 v[kTileTN][kTailMaxSplit];
 #pragma unroll
-    for (int z = 0; z < kTailMaxSplit; ++z)
-      if (z < s) v[z] = src[static_cast<size_t>(z) * (kTailTileFloats / 4) + static_cast<size_t>(e) * kTileThreads + tid];
-    float4 a = v[0];
+    for (int j = 0; j < kTileTN; ++j)
 #pragma unroll
-    for (int z = 1; z < kTailMaxSplit; ++z)
-      if (z < s) {
-        a.x += v[z].x; a.y += v[z].y; a.z += v[z].z; a.w += v[z].w;
-      }
-    const int q = e & 3, j = (e >> 2) % kTileTN, i = (e >> 2) / kTileTN;
-    const int row = wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5);
-    const int col = wn * 64 + j * 32 + (lane & 31);
-    st(row, col, a.x);
-    st(row + 1, col, a.y);
-    st(row + 2, col, a.z);
-    st(row + 3, col, a.w);
+      for (int z = 0; z < kTailMaxSplit; ++z)
+        if (z < s)
+          v[j][z] = src[static_cast<size_t>(z) * (kTailTileFloats / 4) +
+                        static_cast<size_t>((i * kTileTN + j) * 4 + q) * kTileThreads + tid];
+    float4 a[kTileTN];
+#pragma unroll
+    for (int j = 0; j < kTileTN; ++j) {
+      a[j] = v[j][0];
+#pragma unroll
+      for (int z = 1; z < kTailMaxSplit; ++z)
+        if (z < s) {
+          a[j].x += v[j][z].x; a[j].y += v[j][z].y; a[j].z += v[j][z].z; a[j].w += v[j][z].w;
+        }
+    }
+    st(i, q, a[0], a[1]);
   }
 }
 
