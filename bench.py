@@ -431,7 +431,7 @@ def run_layer_backward(st, args):
     """The experts' side of the layer backward (dgrad and wgrad of every selected expert,
     maskmoe_layer_backward) on the fine-tuning layer, timed on its own after one training forward.
     MFMA-bound: FLOPs = 2 x the forward's expert FLOPs (dgrad and wgrad of both projections,
-    4 x 2 rows F d x 2 in all); the transposes and row sums it also runs are not counted."""
+    4 x 2 rows F d x 2 in all); the gathers and row sums it also runs are not counted."""
     import torch
     from paper_2609_34077_amd import _lib as L
     from paper_2609_34077_amd import synth
@@ -465,7 +465,7 @@ def run_layer_backward(st, args):
     return {"ms": round(ms, 3), "tokens_per_s": round(cfg.T / (ms / 1e3), 1), "bound": "mfma", "achieved": round(tf, 1),
             "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4), "flops": flops,
             "computes": "dgrad and wgrad of every selected expert's SwiGLU FFN (dL/dx experts' share, dL/dW_gate_up, "
-                        "dL/dW_down), including the weight and activation transposes it runs"}
+                        "dL/dW_down), including the token gather and the zero gradients of unchosen experts"}
 
 
 def run_lora_forward(st, args):

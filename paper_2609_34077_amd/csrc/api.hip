@@ -450,10 +450,8 @@ int maskmoe_layer_backward(const maskmoe_layer_desc* desc, const void* x, const 
   const maskmoe::BwdLayout bl = maskmoe::backward_layout(d.T, d.d, d.F, d.E, d.K, d.n_shared);
   // the GEMMs address rows with 32-bit element offsets
   const int64_t rows = static_cast<int64_t>(d.T) * (d.K + d.n_shared);
-  const int64_t widest = 2 * static_cast<int64_t>(d.F) > d.d ? 2 * static_cast<int64_t>(d.F) : d.d;
   if (rows * 2 * d.F >= (int64_t{1} << 31) || rows * d.d >= (int64_t{1} << 31) ||
-      widest * bl.P >= (int64_t{1} << 31) || static_cast<int64_t>(d.T) * d.d >= (int64_t{1} << 31) ||
-      int64_t{2} * d.F * d.d >= (int64_t{1} << 31))
+      static_cast<int64_t>(d.T) * d.d >= (int64_t{1} << 31) || int64_t{2} * d.F * d.d >= (int64_t{1} << 31))
     return MASKMOE_E_UNSUPPORTED;
   const Layout w = layout(d);
   if (!train_workspace || train_workspace_bytes < w.train_total || !aligned(train_workspace, 256))

@@ -10,12 +10,12 @@
 // per expert, over the permuted rows of the forward (one row per (token, slot), shared
 // experts' rows after them).
 //
-// Every product is run as C = A B^T with K-contiguous rows on the 256x256x64 MFMA tile of
-// gemm_tile.hpp. The operands whose contraction index is strided in storage are transposed
-// first with an LDS-tiled copy: the weights (per call, as they change between steps), and for
-// the weight gradients the rows of dO, h, [da db] and the gathered x, laid out per expert with
-// the row count padded to a multiple of 64 and zero columns in the gaps, so each expert's
-// wgrad is one GEMM over its own padded token range (an expert no token chose gets zeros).
+// Every product is run as C = A B^T on the 256x256x64 MFMA tile of gemm_tile.hpp. Operands whose
+// contraction index is strided in storage are read in place as K-major operands (loaded by rows
+// of the contraction index, turned into MFMA operands by transposing LDS reads): the weights
+// of the dgrads, and both operands of the weight gradients, whose contraction runs over each
+// expert's own rows of dO, h, [da db] and the gathered x (rows past the group's end read as
+// zeros; an expert no token chose gets zeros).
 // Rounding (bf16 layers): dO = g dy and [da db] are rounded to bf16 before their GEMMs;
 // accumulation is fp32; dX, dW are fp32.
 
@@ -54,97 +54,24 @@ __global__ __launch_bounds__(kBwdThreads) void build_dout_kernel(const uint16_t*
   }
 }
 
-// Padded token layout of the weight gradients: group g's rows occupy padded columns
-// [poff[g], poff[g] + n_g), n_g = offsets[g+1] - offsets[g], and poff[g+1] = poff[g] +
-// roundup(n_g, 64); pmap[pc] is the permuted row at padded column pc, or -1 (zero column).
-// One workgroup.
-__global__ __launch_bounds__(kBwdThreads) void pad_layout_kernel(const int32_t* __restrict__ offsets, int G, int P,
-                                                                 int32_t* __restrict__ poff,
-                                                                 int32_t* __restrict__ pmap) {
-  __shared__ int off[kMaxGroupsBwd + 1];
-  __shared__ int po[kMaxGroupsBwd + 1];
-  for (int g = threadIdx.x; g <= G; g += kBwdThreads) off[g] = offsets[g];
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    po[0] = 0;
-    for (int g = 0; g < G; ++g) po[g + 1] = po[g] + (off[g + 1] - off[g] + kTileK - 1) / kTileK * kTileK;
-  }
-  __syncthreads();
-  for (int g = threadIdx.x; g <= G; g += kBwdThreads) poff[g] = po[g];
-  for (int pc = threadIdx.x; pc < P; pc += kBwdThreads) {
-    int row = -1;
-    if (pc < po[G]) {
-      int lo = 0, hi = G;   // po[lo] <= pc < po[hi]
-      while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (po[mid] <= pc) lo = mid; else hi = mid;
-      }
-      const int k = pc - po[lo];
-      if (k < off[lo + 1] - off[lo]) row = off[lo] + k;
-    }
-    pmap[pc] = row;
-  }
-}
-
-// out[c * ldo + pc] = source row of pc at column c, for c < 64 gridDim.y (transpose() sizes the
-// grid from the column count C, C % 64 == 0) and pc < P: the
-// source row is pmap[pc] (-1: a zero column) or pc itself without a map, read at
-// src + row_tok[row] * lds (GATHER) or src + row * lds. 64x64 tiles through LDS; blockIdx.z
-// selects one matrix of a batch (src_batch / out_batch elements apart): matrix z, or with an
-// active list the z-th listed group if it is below `limit` (the others are left alone).
-template <bool GATHER>
-__global__ __launch_bounds__(kBwdThreads) void transpose_kernel(const uint16_t* __restrict__ src, int lds,
-                                                                const int32_t* __restrict__ pmap,
-                                                                const int32_t* __restrict__ row_tok, int P,
-                                                                uint16_t* __restrict__ out, int ldo, size_t src_batch,
-                                                                size_t out_batch, const int32_t* __restrict__ active,
-                                                                const int32_t* __restrict__ n_active, int limit) {
-  constexpr int PITCH = 64 + 8;   // 16-byte aligned rows
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][PITCH];
-  const int pc0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-  int mat = blockIdx.z;
-  if (active) {
-    if (mat >= n_active[0]) return;
-    mat = active[mat];
-    if (mat >= limit) return;
-  }
-  src += mat * src_batch;
-  out += mat * out_batch;
-  for (int u = threadIdx.x; u < 64 * 8; u += kBwdThreads) {
-    const int pr = u >> 3, cc = (u & 7) * 8;
-    const int pc = pc0 + pr;
-    int row = -1;
-    if (pc < P) row = pmap ? pmap[pc] : pc;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (row >= 0) {
-      const size_t srow = GATHER ? static_cast<size_t>(row_tok[row]) : static_cast<size_t>(row);
-      v = *reinterpret_cast<const u32x4*>(src + srow * lds + c0 + cc);
-    }
-    *reinterpret_cast<u32x4*>(&tile[pr][cc]) = v;
-  }
-  __syncthreads();
-  for (int u = threadIdx.x; u < 64 * 8; u += kBwdThreads) {
-    const int cr = u >> 3, pp = (u & 7) * 8;
-    uint16_t* dst = out + static_cast<size_t>(c0 + cr) * ldo + pc0 + pp;
-    if (pc0 + pp + 8 <= P) {
-      u32x4 v;
-#pragma unroll
-      for (int h = 0; h < 4; ++h)
-        v[h] = static_cast<uint32_t>(tile[pp + 2 * h][cr]) | (static_cast<uint32_t>(tile[pp + 2 * h + 1][cr]) << 16);
-      *reinterpret_cast<u32x4*>(dst) = v;
-    } else {
-      for (int q = 0; q < 8 && pc0 + pp + q < P; ++q) dst[q] = tile[pp + q][cr];
-    }
-  }
+// xg[r, :] = x[row_tok[r], :] (the gathered tokens of the weight gradient of gate/up, read in
+// place as a K-major operand). One workgroup per row; d % 8 == 0.
+__global__ __launch_bounds__(kBwdThreads) void gather_rows_kernel(const uint16_t* __restrict__ x,
+                                                                  const int32_t* __restrict__ row_tok, int d,
+                                                                  uint16_t* __restrict__ xg) {
+  const int r = blockIdx.x;
+  const uint16_t* src = x + static_cast<size_t>(row_tok[r]) * d;
+  uint16_t* dst = xg + static_cast<size_t>(r) * d;
+  for (int c = threadIdx.x * 8; c < d; c += kBwdThreads * 8)
+    *reinterpret_cast<u32x4*>(dst + c) = *reinterpret_cast<const u32x4*>(src + c);
 }
 
 struct NtArgs {
-  const uint16_t* a;          // ROWS: [rows, K] (lda); KSPLIT: [M, P] (lda = P)
-  const uint16_t* b;          // ROWS: per routed expert [N, K] matrices; KSPLIT: [N, P] (ldb = P)
-  const uint16_t* bs;         // ROWS: the shared experts' [N, K] matrices
-  const int32_t* offsets;     // [G+1] rows of each group (ROWS)
+  const uint16_t* a;          // ROWS: [rows, K] (lda), K-contiguous; KSPLIT: K-major [rows, M] (lda)
+  const uint16_t* b;          // ROWS: per routed expert K-major [K, N] matrices (ldb = N); KSPLIT: K-major [rows, N]
+  const uint16_t* bs;         // ROWS: the shared experts' [K, N] matrices
+  const int32_t* offsets;     // [G+1] rows of each group
   const int32_t* tile_off;    // [G+1] row tiles of each group (ROWS)
-  const int32_t* poff;        // [G+1] padded token range of each group (KSPLIT)
   const int32_t* active;      // KSPLIT: the non-empty groups, n_active[0] of them
   const int32_t* n_active;
   const uint16_t* ab;         // SWIGLU_BWD: saved pre-activations [rows, 2N]
@@ -183,10 +110,11 @@ __device__ __forceinline__ void nt_store_rows(const NtArgs& p, const f32x16 (&ac
 enum { kNtRows = 0, kNtKSplit = 1 };
 enum { kEpiSwigluBwd = 0, kEpiF32 = 1 };
 
-// ROWS (dgrad): group g's rows offsets[g]..offsets[g+1] of A times its own [N, K] matrix, row
-// tiles enumerated by tile_off as in the forward. KSPLIT (wgrad): for every non-empty group g
-// the full [M, N] product over its padded token range [poff[g], poff[g+1]); the grid is sized
-// for all groups and the live tiles (n_active x tiles per group) are spread over the XCDs.
+// ROWS (dgrad): group g's rows offsets[g]..offsets[g+1] of A (K-contiguous) times its own
+// K-major [K, N] matrix, row tiles enumerated by tile_off as in the forward. KSPLIT (wgrad): for
+// every non-empty group g the full [M, N] product over its rows offsets[g]..offsets[g+1] of the
+// K-major A [rows, M] and B [rows, N]; the grid is sized for all groups and the live tiles
+// (n_active x tiles per group) are spread over the XCDs.
 template <int MODE, int EPI>
 __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
   constexpr int TM = kTileTM, TN = kTileTN, WN = 4;
@@ -194,9 +122,9 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   int mt, nt, g, row0, row_end, nk;
-  const uint16_t* abase;
-  const uint16_t* bbase;
   TileJob job{0, 0, 1, -1};
+  TileOps ops{};
+  TileKm akm{}, bkm{};
   if (MODE == kNtRows) {   // each XCD's share of the live row tiles (tile_job)
     const int mt_live = p.tile_off[p.G];
     const int live = mt_live * p.n_tiles;
@@ -213,8 +141,16 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
     row_end = p.offsets[g + 1];
     nk = nkf / job.s;
     const int k0 = job.z * nk * kTileK;
-    abase = p.a + k0;
-    bbase = (g < p.E ? p.b + static_cast<size_t>(g) * p.N * p.K : p.bs + static_cast<size_t>(g - p.E) * p.N * p.K) + k0;
+    const int n0 = nt * kTileN;
+    ops.a = reinterpret_cast<const char*>(p.a + k0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)   // element offsets < 2^31 (checked by the host)
+      ops.aoff[i] = static_cast<uint32_t>(min(row0 + tile_dma_row(i), row_end - 1) * p.lda + tile_dma_chunk(i) * 8) * 2u;
+    const uint16_t* bm = g < p.E ? p.b + static_cast<size_t>(g) * p.N * p.K : p.bs + static_cast<size_t>(g - p.E) * p.N * p.K;
+    bkm.base = reinterpret_cast<const char*>(bm + static_cast<size_t>(k0) * p.ldb + n0);
+    bkm.ld = p.ldb * 2;
+    bkm.krows = nk * kTileK;
+    bkm.mcols = p.N - n0;
   } else {
     const int per = p.mt_max * p.n_tiles;
     const int live = p.n_active[0] * per;
@@ -224,22 +160,18 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
     grouped_tile_coords(lid % per, p.mt_max, p.n_tiles, mt, nt);
     row0 = mt * kTileM;
     row_end = p.M;
-    const int k0 = p.poff[g];
-    nk = (p.poff[g + 1] - k0) / kTileK;
-    abase = p.a + k0;
-    bbase = p.b + k0;
+    const int r0 = p.offsets[g], nrows = p.offsets[g + 1] - r0;
+    nk = (nrows + kTileK - 1) / kTileK;
+    akm.base = reinterpret_cast<const char*>(p.a + static_cast<size_t>(r0) * p.lda + row0);
+    akm.ld = p.lda * 2;
+    akm.krows = nrows;
+    akm.mcols = p.M - row0;
+    bkm.base = reinterpret_cast<const char*>(p.b + static_cast<size_t>(r0) * p.ldb + nt * kTileN);
+    bkm.ld = p.ldb * 2;
+    bkm.krows = nrows;
+    bkm.mcols = p.N - nt * kTileN;
   }
   const int n0 = nt * kTileN;
-  TileOps ops;   // this lane's four rows of each operand (tile_dma_row in gemm_tile.hpp)
-  ops.a = reinterpret_cast<const char*>(abase);
-  ops.b = reinterpret_cast<const char*>(bbase);
-  ops.b_step = kTileK * 2;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {   // element offsets < 2^31 (checked by the host)
-    const int r = tile_dma_row(i), chunk = tile_dma_chunk(i) * 8;
-    ops.aoff[i] = static_cast<uint32_t>(min(row0 + r, row_end - 1) * p.lda + chunk) * 2u;
-    ops.boff[i] = static_cast<uint32_t>(min(n0 + r, p.N - 1) * p.ldb + chunk) * 2u;
-  }
   int bfrag[TN];
 #pragma unroll
   for (int j = 0; j < TN; ++j) bfrag[j] = wn * 64 + j * 32 + (lane & 31);
@@ -250,7 +182,7 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-  gemm_tile_mainloop(ops, nk, bfrag, acc, lds);
+  gemm_tile_mainloop<false, MODE == kNtKSplit, true>(ops, nk, bfrag, acc, lds, nullptr, &akm, &bkm);
   if (MODE == kNtRows && EPI == kEpiF32) {
     if (job.s > 1) tail_store_partial(p.part, job.slot, acc);   // a slice of a split tail tile
     else nt_store_rows(p, acc, row0, row_end, nt * kTileN);
@@ -340,19 +272,6 @@ __global__ __launch_bounds__(kBwdThreads) void dx_combine_kernel(const float* __
   }
 }
 
-hipError_t transpose(bool gather, const uint16_t* src, int lds, const int32_t* pmap, const int32_t* row_tok, int P,
-                     int C, uint16_t* out, int ldo, int batch, size_t src_batch, size_t out_batch, hipStream_t s,
-                     const int32_t* active = nullptr, const int32_t* n_active = nullptr, int limit = 0) {
-  const dim3 grid((P + 63) / 64, C / 64, batch);   // C: a multiple of 64 (d and F are, for bf16 layers)
-  if (gather)
-    hipLaunchKernelGGL(transpose_kernel<true>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, out, ldo,
-                       src_batch, out_batch, active, n_active, limit);
-  else
-    hipLaunchKernelGGL(transpose_kernel<false>, grid, dim3(kBwdThreads), 0, s, src, lds, pmap, row_tok, P, out, ldo,
-                       src_batch, out_batch, active, n_active, limit);
-  return hipGetLastError();
-}
-
 // Zero the [M, N] gradient matrices of the groups that no row reached (offsets[g+1] ==
 // offsets[g]). Grid (G, chunks); float4 stores; M N % 4 == 0.
 __global__ __launch_bounds__(kBwdThreads) void zero_unused_kernel(const int32_t* __restrict__ offsets, int E,
@@ -383,21 +302,12 @@ BwdLayout backward_layout(int T, int d, int F, int E, int K, int S) {
     off += (bytes + 255) / 256 * 256;
     return o;
   };
-  const size_t G = static_cast<size_t>(E) + S;
+  (void)E;
   const size_t R = static_cast<size_t>(T) * (K + S);
-  w.P = static_cast<int>((R + 64 * G + 63) / 64 * 64);
-  const size_t P = static_cast<size_t>(w.P);
-  w.w_down_t = take(G * F * d * 2);
-  w.w_gate_up_t = take(G * d * 2 * F * 2);
   w.dout = take(R * d * 2);
   w.dab = take(R * 2 * F * 2);
   w.dxr = take(R * d * 4);
-  w.poff = take((G + 1) * 4);
-  w.pmap = take(P * 4);
-  w.dout_t = take(static_cast<size_t>(d) * P * 2);
-  w.h_t = take(static_cast<size_t>(F) * P * 2);
-  w.dab_t = take(static_cast<size_t>(2) * F * P * 2);
-  w.x_t = take(static_cast<size_t>(d) * P * 2);
+  w.xg = take(R * d * 2);
   w.part = take(kTailPartBytes);
   w.total = off;
   return w;
@@ -413,33 +323,18 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   const int R = T * (K + a.S);
   const BwdLayout& w = a.lay;
   char* ws = static_cast<char*>(a.workspace);
-  uint16_t* wdt = reinterpret_cast<uint16_t*>(ws + w.w_down_t);
-  uint16_t* wgut = reinterpret_cast<uint16_t*>(ws + w.w_gate_up_t);
   uint16_t* dout = reinterpret_cast<uint16_t*>(ws + w.dout);
   uint16_t* dab = reinterpret_cast<uint16_t*>(ws + w.dab);
   float* dxr = reinterpret_cast<float*>(ws + w.dxr);
-  int32_t* poff = reinterpret_cast<int32_t*>(ws + w.poff);
-  int32_t* pmap = reinterpret_cast<int32_t*>(ws + w.pmap);
-  uint16_t* dout_t = reinterpret_cast<uint16_t*>(ws + w.dout_t);
-  uint16_t* h_t = reinterpret_cast<uint16_t*>(ws + w.h_t);
-  uint16_t* dab_t = reinterpret_cast<uint16_t*>(ws + w.dab_t);
-  uint16_t* x_t = reinterpret_cast<uint16_t*>(ws + w.x_t);
+  uint16_t* xg = reinterpret_cast<uint16_t*>(ws + w.xg);
   const size_t FD = static_cast<size_t>(F) * d;
 
-  // weights, transposed: W_down [d, F] -> [F, d]; W_gate_up [2F, d] -> [d, 2F]
-  // (routed experts that no token chose are skipped: their transposed matrices are never read)
-  MASKMOE_TRY(transpose(false, a.w_down, F, nullptr, nullptr, d, F, wdt, d, a.E, FD, FD, s, a.pb.active,
-                        a.pb.n_active, a.E));
-  MASKMOE_TRY(transpose(false, a.w_gate_up, d, nullptr, nullptr, 2 * F, d, wgut, 2 * F, a.E, 2 * FD, 2 * FD, s,
-                        a.pb.active, a.pb.n_active, a.E));
-  if (a.S > 0) {
-    MASKMOE_TRY(transpose(false, a.ws_down, F, nullptr, nullptr, d, F, wdt + a.E * FD, d, a.S, FD, FD, s));
-    MASKMOE_TRY(transpose(false, a.ws_gate_up, d, nullptr, nullptr, 2 * F, d, wgut + 2 * a.E * FD, 2 * F, a.S,
-                          2 * FD, 2 * FD, s));
-  }
-  // dO, then dgrad of the down projection with the SwiGLU backward: [da db] (bf16)
+  // dO and the gathered tokens, then dgrad of the down projection with the SwiGLU backward:
+  // [da db] (bf16)
   hipLaunchKernelGGL(build_dout_kernel, dim3(R), dim3(kBwdThreads), 0, s, a.dy, a.gate, a.pb.perm, a.pb.row_tok, T * K,
                      d, dout);
+  MASKMOE_TRY(hipGetLastError());
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(R), dim3(kBwdThreads), 0, s, a.x, a.pb.row_tok, d, xg);
   MASKMOE_TRY(hipGetLastError());
   NtArgs n{};
   n.offsets = a.pb.offsets;
@@ -447,7 +342,7 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   n.G = G; n.E = a.E;
   n.mt_max = a.max_tiles;
   n.a = dout; n.lda = d;
-  n.b = wdt; n.bs = wdt + a.E * FD; n.N = F; n.K = d; n.ldb = d;
+  n.b = a.w_down; n.bs = a.ws_down; n.N = F; n.K = d; n.ldb = F;   // W_down [d, F]: K-major
   n.ab = a.ab;
   n.c = dab;
   n.n_tiles = (F + kTileN - 1) / kTileN;
@@ -458,7 +353,7 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   MASKMOE_TRY(hipGetLastError());
   // dgrad of gate/up: dX rows = [da db] W_gate_up, then the token sums
   n.a = dab; n.lda = 2 * F;
-  n.b = wgut; n.bs = wgut + 2 * a.E * FD; n.N = d; n.K = 2 * F; n.ldb = 2 * F;
+  n.b = a.w_gate_up; n.bs = a.ws_gate_up; n.N = d; n.K = 2 * F; n.ldb = d;   // W_gate_up [2F, d]: K-major
   n.ab = nullptr;
   n.c = dxr; n.ldc = d;
   n.n_tiles = (d + kTileN - 1) / kTileN;
@@ -470,21 +365,14 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   }
   hipLaunchKernelGGL(dx_combine_kernel, dim3(T), dim3(kBwdThreads), 0, s, dxr, a.pb.inv, T, K, a.S, d, a.d_x);
   MASKMOE_TRY(hipGetLastError());
-  // weight gradients over each expert's padded token range
-  hipLaunchKernelGGL(pad_layout_kernel, dim3(1), dim3(kBwdThreads), 0, s, a.pb.offsets, G, w.P, poff, pmap);
-  MASKMOE_TRY(hipGetLastError());
-  MASKMOE_TRY(transpose(false, dout, d, pmap, nullptr, w.P, d, dout_t, w.P, 1, 0, 0, s));
-  MASKMOE_TRY(transpose(false, a.h, F, pmap, nullptr, w.P, F, h_t, w.P, 1, 0, 0, s));
-  MASKMOE_TRY(transpose(false, dab, 2 * F, pmap, nullptr, w.P, 2 * F, dab_t, w.P, 1, 0, 0, s));
-  MASKMOE_TRY(transpose(true, a.x, d, pmap, a.pb.row_tok, w.P, d, x_t, w.P, 1, 0, 0, s));
+  // weight gradients over each expert's own rows
   NtArgs m{};
-  m.poff = poff;
+  m.offsets = a.pb.offsets;
   m.active = a.pb.active;
   m.n_active = a.pb.n_active;
   m.G = G; m.E = a.E;
-  m.lda = w.P; m.ldb = w.P;
   // dW_down [d, F] = dO^T h
-  m.a = dout_t; m.b = h_t; m.M = d; m.N = F;
+  m.a = dout; m.lda = d; m.b = a.h; m.ldb = F; m.M = d; m.N = F;
   m.c = a.d_w_down; m.cs = a.d_ws_down;
   m.mt_max = (d + kTileM - 1) / kTileM;
   m.n_tiles = (F + kTileN - 1) / kTileN;
@@ -495,7 +383,7 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
                      a.d_ws_down);
   MASKMOE_TRY(hipGetLastError());
   // dW_gate_up [2F, d] = [da db]^T x
-  m.a = dab_t; m.b = x_t; m.M = 2 * F; m.N = d;
+  m.a = dab; m.lda = 2 * F; m.b = xg; m.ldb = d; m.M = 2 * F; m.N = d;
   m.c = a.d_w_gate_up; m.cs = a.d_ws_gate_up;
   m.mt_max = (2 * F + kTileM - 1) / kTileM;
   m.n_tiles = (d + kTileN - 1) / kTileN;

@@ -49,6 +49,25 @@ struct TileOps {
   uint32_t b_step;
 };
 
+// A K-major operand (the contraction index strided in storage): element (k, m) of the tile's
+// k-range at base + k * ld + 2 m bytes. k-rows at or beyond krows read as zeros; columns at or
+// beyond mcols (a multiple of 8) are clamped to the last valid 8-column piece, whose products
+// land in columns that are never stored. Loaded with buffer loads whose range is the krows
+// valid rows (out-of-range lanes return zeros), ld >= 512 and krows * ld < 2^32.
+struct TileKm {
+  const char* base;
+  int ld;
+  int krows;
+  int mcols;
+};
+
+// K-major operands sit in LDS as [128-row half][64 k][128 m] with 256-byte k-rows of 16
+// 16-byte units; unit u of k-row kr is stored at unit u ^ 4 (kr & 3). A transposing read
+// (ds_read_b64_tr_b16) has each 32 lanes touch 4 consecutive k-rows x 4 adjacent units; the
+// swizzle puts those 16 units in distinct banks (with u ^ 2 (kr & 3) they pair up: 2-way
+// conflicts on every read, measured).
+__device__ __forceinline__ int km_unit(int u, int kr) { return u ^ (4 * (kr & 3)); }
+
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 __device__ __forceinline__ uint32_t lds_offset(const u32x4* p) {
   return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<size_t>((lds_u32x4*)p)));
@@ -59,6 +78,43 @@ __device__ __forceinline__ void dma16(uint32_t m0v, const void* gbase, uint32_t 
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0v), "v"(voff), "s"(gbase)
                : "memory", "m0");
 }
+// The same through a buffer resource (K-major operands): 16 bytes at offset voff of the buffer
+// described by rsrc, zeros where voff is past its size. (Full 64-bit per-lane addresses halve the
+// texture unit's load rate.)
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void dma16b(uint32_t m0v, i32x4 rsrc, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m0v), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+// A raw buffer resource over [p, p + bytes): base, stride 0, size, and the gfx9 data format word.
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  i32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(a)));
+  r.y = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(a >> 32) & 0xffffu));
+  r.z = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
+  r.w = 0x00020000;
+  return r;
+}
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+// One MFMA operand (8 consecutive k of one row) from a K-major half buffer: two transposing
+// reads of 4 k-rows each. ds_read_b64_tr_b16 hands lane i of each 16-lane group element i % 4 of
+// the 8 bytes read by lane 4 c + i / 4 of the group as its element c; lane j therefore reads 4
+// adjacent columns (rbase + 16 (G & 1) + 4 (j & 3)) of k-row kk*16 + 8 (G >> 1) + j / 4, and
+// lane i ends up with column rbase + 16 (G & 1) + i of 4 consecutive k-rows: row rbase + (lane
+// & 31) of the operand, k-values 8 (lane >> 5) .. + 7 of k step kk, as the MFMA expects.
+__device__ __forceinline__ u32x4 read_km_operand(const u32x4* half, int rbase, int kk) {
+  const int lane = threadIdx.x & 63, G = lane >> 4, j = lane & 15;
+  const int m = rbase + 16 * (G & 1) + 4 * (j & 3);
+  const int kr = kk * 16 + 8 * (G >> 1) + (j >> 2);
+  const char* p = reinterpret_cast<const char*>(half) + kr * 256 + km_unit(m >> 3, kr) * 16 + (m & 7) * 2;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * 256));
+  const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+  return u32x4{a.x, a.y, b.x, b.y};
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 __device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
@@ -68,12 +124,15 @@ __device__ __forceinline__ void tile_barrier() { asm volatile("s_barrier" ::: "m
 
 // acc += A B^T over nk k-tiles (nk >= 1). EXTRA: one more k-tile first, from the operands in
 // *x (its b_step is unused); the low-rank adapters use it: [U | X] [s B | W]^T turns
-// W x + s B (A x) into one product. bfrag[j]: tile row of B fragment j for this lane (a multiple
-// of 32 plus lane & 31); A fragment i is tile row 128 g + 32 i + (lane & 31).
-template <bool EXTRA = false>
+// W x + s B (A x) into one product. AKM / BKM: operand A / B is K-major (*akm / *bkm; the
+// matching TileOps fields are unused). bfrag[j]: tile row of B fragment j for this lane (a
+// multiple of 32 plus lane & 31); A fragment i is tile row 128 g + 32 i + (lane & 31).
+template <bool EXTRA = false, bool AKM = false, bool BKM = false>
 __device__ __forceinline__ void gemm_tile_mainloop(const TileOps& o, int nk, const int (&bfrag)[kTileTN],
                                                    f32x16 (&acc)[kTileTM][kTileTN], TileLds& L,
-                                                   const TileOps* x = nullptr) {
+                                                   const TileOps* x = nullptr, const TileKm* akm = nullptr,
+                                                   const TileKm* bkm = nullptr) {
+  static_assert(!(EXTRA && (AKM || BKM)), "the extra k-tile is K-contiguous");
   constexpr int X = EXTRA ? 1 : 0;
   if (nk <= 0) return;
   const int ntot = nk + X;
@@ -82,19 +141,45 @@ __device__ __forceinline__ void gemm_tile_mainloop(const TileOps& o, int nk, con
   const int g = wave >> 2, q = wave & 3;
   const uint32_t la0 = lds_offset(&L.a[g][0][0]) + q * 4 * 1024;
   const uint32_t lb0 = lds_offset(&L.b[0][0]) + (g * 16 + q * 4) * 1024;
+  // K-major pieces of this lane: k-row 4 (4 q + i) + lane / 16 of the group's half, the
+  // 8 columns of its physical slot lane & 15; byte offsets at k-tile 0
+  uint32_t akoff[4], bkoff[4];
+  i32x4 arsrc{}, brsrc{};
+  if (AKM) arsrc = buffer_rsrc(akm->base, static_cast<uint32_t>(akm->krows) * static_cast<uint32_t>(akm->ld));
+  if (BKM) brsrc = buffer_rsrc(bkm->base, static_cast<uint32_t>(bkm->krows) * static_cast<uint32_t>(bkm->ld));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int kr = 4 * (4 * q + i) + (lane >> 4);
+    const int col = g * 128 + 8 * km_unit(lane & 15, kr);
+    if (AKM) akoff[i] = static_cast<uint32_t>(kr * akm->ld + min(col, akm->mcols - 8) * 2);
+    if (BKM) bkoff[i] = static_cast<uint32_t>(kr * bkm->ld + min(col, bkm->mcols - 8) * 2);
+  }
+  auto dma_km = [&](i32x4 rsrc, const uint32_t (&off)[4], int ld, uint32_t lbase, int tt) {
+    const uint32_t step = static_cast<uint32_t>(tt) * 64u * static_cast<uint32_t>(ld);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16b(lbase + static_cast<uint32_t>(i * 1024), rsrc, off[i] + step);
+  };
   // Loads of pipeline tile t (main k-tile t - X), clamped to the last one: past the end they
   // refill a buffer that nothing reads again, which keeps every wait count the same.
   auto dma_a = [&](int t) {
     const int tt = min(t, ntot - 1) - X;
-    const char* ga = o.a + static_cast<size_t>(tt) * 128;
+    if (AKM) {
+      dma_km(arsrc, akoff, akm->ld, la0 + static_cast<uint32_t>((t & 1) * 16384), tt);
+    } else {
+      const char* ga = o.a + static_cast<size_t>(tt) * 128;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(la0 + static_cast<uint32_t>((t & 1) * 16384 + i * 1024), ga, o.aoff[i]);
+      for (int i = 0; i < 4; ++i) dma16(la0 + static_cast<uint32_t>((t & 1) * 16384 + i * 1024), ga, o.aoff[i]);
+    }
   };
   auto dma_b = [&](int t) {
     const int tt = min(t, ntot - 1) - X;
-    const char* gb = o.b + static_cast<size_t>(tt) * o.b_step;
+    if (BKM) {
+      dma_km(brsrc, bkoff, bkm->ld, lb0 + static_cast<uint32_t>((t % 3) * 32768), tt);
+    } else {
+      const char* gb = o.b + static_cast<size_t>(tt) * o.b_step;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(lb0 + static_cast<uint32_t>((t % 3) * 32768 + i * 1024), gb, o.boff[i]);
+      for (int i = 0; i < 4; ++i) dma16(lb0 + static_cast<uint32_t>((t % 3) * 32768 + i * 1024), gb, o.boff[i]);
+    }
   };
   const int sw = lds_swizzle(lane & 31);
   u32x4 af[2][kTileTM], bf[2][kTileTN];
@@ -105,9 +190,13 @@ __device__ __forceinline__ void gemm_tile_mainloop(const TileOps& o, int nk, con
     for (int kk = 0; kk < 2; ++kk) {
       const int ch = (4 * h + 2 * kk + (lane >> 5)) ^ sw;
 #pragma unroll
-      for (int i = 0; i < kTileTM; ++i) af[kk][i] = pa[(i * 32 + (lane & 31)) * 8 + ch];
+      for (int i = 0; i < kTileTM; ++i)
+        af[kk][i] = AKM ? read_km_operand(pa, i * 32, 2 * h + kk) : pa[(i * 32 + (lane & 31)) * 8 + ch];
 #pragma unroll
-      for (int j = 0; j < kTileTN; ++j) bf[kk][j] = pb[bfrag[j] * 8 + ch];
+      for (int j = 0; j < kTileTN; ++j) {
+        const int r0 = bfrag[j] & ~31;   // the fragment's first tile row
+        bf[kk][j] = BKM ? read_km_operand(pb + (r0 >> 7) * 1024, r0 & 127, 2 * h + kk) : pb[bfrag[j] * 8 + ch];
+      }
     }
   };
   auto compute = [&]() {

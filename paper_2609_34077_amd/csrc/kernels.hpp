@@ -157,8 +157,7 @@ hipError_t launch_cache(int policy, const int32_t* trace, int L, int S, int N, i
 constexpr int kMaxGroupsBwd = 256 + 8;
 
 struct BwdLayout {          // byte offsets into the backward workspace
-  size_t w_down_t, w_gate_up_t, dout, dab, dxr, poff, pmap, dout_t, h_t, dab_t, x_t, part, total;
-  int P;                    // padded token columns (multiple of 64)
+  size_t dout, dab, dxr, xg, part, total;
 };
 BwdLayout backward_layout(int T, int d, int F, int E, int K, int S);
 
