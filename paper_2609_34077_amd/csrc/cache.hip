@@ -240,7 +240,7 @@ __global__ __launch_bounds__(64) void cache_seg_kernel(
   for (int n0 = 0; n0 < N; n0 += kSegChunk) {
     const int ns = min(kSegChunk, N - n0);
     for (int i = lane; i < G * LD; i += 64) sel_lds[i] = 0;
-    __syncthreads();
+    lds_sync();
     // each segment ORs its stream's valid entries into the steps' sets, kSegBatch loads in
     // flight per lane; invalid and repeated entries show up as sets of fewer than K experts
     if (live) {
@@ -262,7 +262,7 @@ __global__ __launch_bounds__(64) void cache_seg_kernel(
         }
       }
     }
-    __syncthreads();
+    lds_sync();
     int chunk_f = 0, chunk_h = 0;
     uint32_t sel_next = sel_lds[g * LD];
     for (int j = 0; j < ns; ++j) {
@@ -309,7 +309,7 @@ __global__ __launch_bounds__(64) void cache_seg_kernel(
     }
     tot_h += chunk_h;
     tot_f += chunk_f;
-    __syncthreads();
+    lds_sync();
     if (f_per_step) {
       for (int gg = 0; gg < G; ++gg) {
         if (stream0 + gg >= nstreams) break;

@@ -61,6 +61,15 @@ __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
+// Workgroup barrier ordering LDS accesses only. __syncthreads() also waits until every global
+// store the thread has issued is acknowledged, which costs a memory round trip after a kernel
+// writes outputs; where threads exchange data through LDS alone, this one waits for LDS only.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // XOR swizzle of the eight 16-byte chunks of a 128-byte LDS operand row: row bits 0..2, with
 // row bit 3 flipping chunk bit 0. A 16-byte operand read whose lanes walk 16 consecutive rows
 // at one logical chunk then touches 16 distinct bank groups, for 32 or 64 four-byte banks; rows

@@ -51,7 +51,7 @@ __global__ __launch_bounds__(kPermThreads) void permute_scan_kernel(int32_t* __r
     }
     total[g] = run;
   }
-  __syncthreads();
+  lds_sync();
   if (tid == 0) {
     int off = 0, toff = 0, na = 0;
     for (int g = 0; g < G; ++g) {
@@ -87,7 +87,7 @@ __global__ __launch_bounds__(kPermThreads) void permute_scatter_kernel(const int
     same &= ((e >> b) & 1) ? bb : ~bb;
   }
   for (int g = lane; g < E; g += kWave) wcnt[wave][g] = 0;
-  __syncthreads();
+  lds_sync();
   const uint64_t lower = same & lanemask_lt(lane);
   if (valid && lower == 0) wcnt[wave][e] = __popcll(same);
   __syncthreads();

@@ -1,4 +1,5 @@
-// Token permutation by expert, run by one workgroup (any multiple of 64 threads, <= 1024).
+// Token permutation by expert, run by one workgroup of `nthreads` threads (the launch's block
+// size, a multiple of 64, <= 1024).
 //
 // The combine of Eq. 1 (Section 3.1) sums, for every token, the outputs of the experts it
 // selected. To run each expert as one dense GEMM over the tokens that chose it, the T*K
@@ -13,7 +14,8 @@
 // LDS histogram, scan, then a chunked stable scatter where the rank of an entry among equal
 // experts inside a wavefront comes from ballots on the expert id bits. Integer only,
 // deterministic. `idx` may have been written by this workgroup just before the call, after
-// a __syncthreads().
+// a barrier that orders it (lds_sync for LDS, __syncthreads for global memory). The threads
+// exchange data through LDS only; the outputs are written, never read back.
 #pragma once
 
 #include "common.hpp"
@@ -31,19 +33,19 @@ struct PermLds {
 };
 
 __device__ inline void permute_block(const int32_t* idx, int T, int K, int E, int n_shared, int tile_rows,
-                                     const PermBuffers& pb, PermLds& s) {
-  const int nthreads = blockDim.x, nwaves = nthreads / kWave;
+                                     const PermBuffers& pb, PermLds& s, int nthreads) {
+  const int nwaves = nthreads / kWave;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = T * K;
   const int G = E + n_shared;
 
   for (int g = tid; g < G; g += nthreads) s.hist[g] = 0;
-  __syncthreads();
+  lds_sync();
   for (int j = tid; j < n; j += nthreads) {
     const int e = idx[j];
     if (e >= 0 && e < E) atomicAdd(&s.hist[e], 1);  // LDS integer counts: order-independent
   }
-  __syncthreads();
+  lds_sync();
   if (tid == 0) {
     int off = 0, toff = 0, na = 0;
     for (int g = 0; g < G; ++g) {
@@ -61,7 +63,7 @@ __device__ inline void permute_block(const int32_t* idx, int T, int K, int E, in
   }
   // shared-expert rows: token t of shared expert s sits at row n + s*T + t
   for (int r = tid; r < n_shared * T; r += nthreads) pb.row_tok[n + r] = r % T;
-  __syncthreads();
+  lds_sync();
 
   for (int base = 0; base < n; base += nthreads) {
     const int j = base + tid;
@@ -75,10 +77,10 @@ __device__ inline void permute_block(const int32_t* idx, int T, int K, int E, in
       same &= ((e >> b) & 1) ? bb : ~bb;
     }
     for (int g = lane; g < G; g += kWave) s.wcnt[wave][g] = 0;
-    __syncthreads();
+    lds_sync();
     const uint64_t lower = same & lanemask_lt(lane);
     if (valid && lower == 0) s.wcnt[wave][e] = __popcll(same);
-    __syncthreads();
+    lds_sync();
     if (valid) {
       int pos = s.running[e] + __popcll(lower);
       for (int w = 0; w < wave; ++w) pos += s.wcnt[w][e];
@@ -86,13 +88,13 @@ __device__ inline void permute_block(const int32_t* idx, int T, int K, int E, in
       pb.inv[j] = pos;
       pb.row_tok[pos] = j / K;
     }
-    __syncthreads();
+    lds_sync();
     for (int g = tid; g < E; g += nthreads) {
       int sum = 0;
       for (int w = 0; w < nwaves; ++w) sum += s.wcnt[w][g];
       s.running[g] += sum;
     }
-    __syncthreads();
+    lds_sync();
   }
 }
 

@@ -131,9 +131,9 @@ __device__ __forceinline__ void select_pair(const RouteParams& p, const float* z
 // stores); otherwise consecutive layers of one token.
 template <bool TOKEN_FASTEST = false>
 __device__ void route_finalize(const RouteParams& p, const float* logits, int ld, const float* lo,
-                               int t0, int TT, int lg0, int nl) {
+                               int t0, int TT, int lg0, int nl, int nthreads) {
   const int E = p.E;
-  for (int pi = threadIdx.x; pi < TT * nl; pi += blockDim.x) {
+  for (int pi = threadIdx.x; pi < TT * nl; pi += nthreads) {
     const int tt = TOKEN_FASTEST ? pi % TT : pi / nl;
     const int lw = TOKEN_FASTEST ? pi / TT : pi - tt * nl;
     const int t = t0 + tt;
@@ -270,8 +270,8 @@ __global__ __launch_bounds__(kSelThreads) void route_select_wave_kernel(const Ro
 // expert order (selection order for the renormalised rule), as in route_finalize, so both give
 // the same bits. The selections are also left in sel_lds [T, K] for the permutation.
 __device__ void route_finalize_wave(const RouteParams& p, const float* logits, int ld, const float* lo, int TT,
-                                    int32_t* sel_lds) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+                                    int32_t* sel_lds, int nwaves) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int E = p.E, K = p.K;
   if (E <= 64) {   // one expert per lane: rank-based picks, no cross-lane reductions
     for (int t = wave; t < TT && t < p.T; t += nwaves) {
@@ -372,9 +372,20 @@ __device__ void route_finalize_wave(const RouteParams& p, const float* logits, i
 // FUSE: the grid is one workgroup holding every token of one layer; after the selection it
 // also groups the (token, slot) pairs by expert (permute_block).
 // SPLIT (not with FUSE): the tile's logits go to p.logits and route_select_kernel selects.
+// Kernel parameters not needed before the epilogue, read at the start so that their loads
+// share the first memory round trip: the argument block is fetched from memory at each
+// launch, and a parameter first read after the k-loop would cost a round trip of its own.
+template <typename V>
+__device__ __forceinline__ void load_now(V v) {
+  asm volatile("" ::"s"(v));
+}
+
 template <int MB, int NB, int WN, int WK, bool FUSE, bool SPLIT = false>
 __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RouteParams p) {
   constexpr int TT = 16 * MB, NO = 16 * NB * WN, NT = 64 * WN * WK;
+  // FUSE with one 16-wide output tile: the E <= 16 key parameters of the single layer are
+  // loaded as scalars with the others.
+  constexpr bool kScalarModep = FUSE && NO <= 16;
   __shared__ float red[WK * TT * NO];
   __shared__ float lo[NO];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -387,21 +398,39 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
   const uint16_t* w = static_cast<const uint16_t*>(p.w) + static_cast<size_t>(lg0) * p.E * p.d;
   const int ksteps = p.d >> 5;
   const int kg = (lane >> 4) * 8;
+  float mp[16];
+  if (FUSE) {
+    load_now(p.idx); load_now(p.gate); load_now(p.logits);
+    load_now(p.K); load_now(p.mode); load_now(p.gate_mode); load_now(p.n_shared); load_now(p.tile_rows);
+    load_now(p.pb.offsets); load_now(p.pb.tile_off); load_now(p.pb.active); load_now(p.pb.n_active);
+    load_now(p.pb.perm); load_now(p.pb.inv); load_now(p.pb.row_tok);
+  }
+  if (kScalarModep) {   // lg0 == 0; 16 <= kMaxModeParams
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      mp[i] = p.modep[i];
+      load_now(mp[i]);
+    }
+  }
 
-  // Rows past the last token / output are clamped onto valid rows; their results are
-  // never written, and MFMA rows and columns do not mix.
+  // Rows past the last token / output are clamped onto valid rows and not loaded (zeros):
+  // their results are never written, and MFMA rows and columns do not mix.
   const uint16_t* ap[MB];
   const uint16_t* bp[NB];
+  bool arow[MB], brow[NB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int t = min(t0 + mb * 16 + (lane & 15), p.T - 1);
     ap[mb] = x + static_cast<size_t>(t) * p.d + kg;
+    arow[mb] = t0 + mb * 16 + (lane & 15) < p.T;
   }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int o = min((wn * NB + nb) * 16 + (lane & 15), nout - 1);
     bp[nb] = w + static_cast<size_t>(o) * p.d + kg;
+    brow[nb] = (wn * NB + nb) * 16 + (lane & 15) < nout;
   }
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
   f32x4 acc[MB][NB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -417,9 +446,9 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
     for (int u = 0; u < U; ++u) {
       const int k = (s + u * WK) << 5;
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) av[u][mb] = *reinterpret_cast<const u32x4*>(ap[mb] + k);
+      for (int mb = 0; mb < MB; ++mb) av[u][mb] = arow[mb] ? *reinterpret_cast<const u32x4*>(ap[mb] + k) : zero4;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) bv[u][nb] = *reinterpret_cast<const u32x4*>(bp[nb] + k);
+      for (int nb = 0; nb < NB; ++nb) bv[u][nb] = brow[nb] ? *reinterpret_cast<const u32x4*>(bp[nb] + k) : zero4;
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -432,9 +461,9 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
     const int k = s << 5;
     u32x4 av[MB], bv[NB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) av[mb] = *reinterpret_cast<const u32x4*>(ap[mb] + k);
+    for (int mb = 0; mb < MB; ++mb) av[mb] = arow[mb] ? *reinterpret_cast<const u32x4*>(ap[mb] + k) : zero4;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) bv[nb] = *reinterpret_cast<const u32x4*>(bp[nb] + k);
+    for (int nb = 0; nb < NB; ++nb) bv[nb] = brow[nb] ? *reinterpret_cast<const u32x4*>(bp[nb] + k) : zero4;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -449,8 +478,17 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         r[(mb * 16 + (lane >> 4) * 4 + i) * NO + (wn * NB + nb) * 16 + (lane & 15)] = acc[mb][nb][i];
-  for (int i = threadIdx.x; i < nout; i += NT) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
-  __syncthreads();
+  if (kScalarModep) {
+    if (wave == 0) {   // lane i: expert i
+      float v = mp[0];
+#pragma unroll
+      for (int i = 1; i < 16; ++i) v = lane == i ? mp[i] : v;
+      if (lane < nout) lo[lane] = key_offset(p.mode, v);
+    }
+  } else {
+    for (int i = threadIdx.x; i < nout; i += NT) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
+  }
+  lds_sync();
   if (WK > 1) {
     for (int i = threadIdx.x; i < TT * NO; i += NT) {
       float s = red[i];
@@ -458,7 +496,7 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
       for (int q = 1; q < WK; ++q) s += red[q * TT * NO + i];
       red[i] = s;
     }
-    __syncthreads();
+    lds_sync();
   }
   if (SPLIT) {   // [TT, nl * E] tile -> p.logits [L, T, E], consecutive threads on consecutive floats
     for (int i = threadIdx.x; i < TT * nout; i += NT) {
@@ -470,11 +508,11 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
   } else if (FUSE) {
     __shared__ PermLds plds;
     __shared__ int32_t sel_lds[kRouteOneBlockT * kMaxK];
-    route_finalize_wave(p, red, NO, lo, TT, sel_lds);
-    __syncthreads();   // the selections written above are read by other threads
-    permute_block(sel_lds, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb, plds);
+    route_finalize_wave(p, red, NO, lo, TT, sel_lds, NT / 64);
+    lds_sync();   // the selections left in sel_lds are read by other threads
+    permute_block(sel_lds, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb, plds, NT);
   } else {
-    route_finalize(p, red, NO, lo, t0, TT, lg0, nl);
+    route_finalize(p, red, NO, lo, t0, TT, lg0, nl, NT);
   }
 }
 
@@ -607,7 +645,7 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
             logits[row * LD + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
           }
     }
-    __syncthreads();
+    lds_sync();
     if (SPLIT) {   // this half's logits -> p.logits [L, T, E]: a thread per (token, layer), tokens fastest
       const int E = p.E;
       for (int i = tid; i < HALF * nl; i += NT) {
@@ -624,9 +662,9 @@ __global__ __launch_bounds__(kRgThreads) void route_gemm_kernel(const RouteParam
         }
       }
     } else {
-      route_finalize<true>(p, logits, LD, lo, t0 + h * HALF, HALF, lg0, nl);
+      route_finalize<true>(p, logits, LD, lo, t0 + h * HALF, HALF, lg0, nl, NT);
     }
-    __syncthreads();   // the next phase overwrites the logits
+    lds_sync();   // the next phase overwrites the logits
   }
 }
 
@@ -641,7 +679,7 @@ __global__ __launch_bounds__(256) void route_f32_kernel(const RouteParams p) {
   const int nout = nl * p.E;
   const float* x = static_cast<const float*>(p.x);
   const float* w = static_cast<const float*>(p.w) + static_cast<size_t>(lg0) * p.E * p.d;
-  for (int i = threadIdx.x; i < kF32TT * nout; i += blockDim.x) {
+  for (int i = threadIdx.x; i < kF32TT * nout; i += 256) {
     const int tt = i / nout, o = i - tt * nout;
     const int t = min(t0 + tt, p.T - 1);
     const float* xr = x + static_cast<size_t>(t) * p.d;
@@ -650,9 +688,9 @@ __global__ __launch_bounds__(256) void route_f32_kernel(const RouteParams p) {
     for (int k = 0; k < p.d; ++k) s = fmaf(xr[k], wr[k], s);
     logits[tt * 256 + o] = s;
   }
-  for (int i = threadIdx.x; i < nout; i += blockDim.x) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
+  for (int i = threadIdx.x; i < nout; i += 256) lo[i] = key_offset(p.mode, p.modep[lg0 * p.E + i]);
   __syncthreads();
-  route_finalize(p, logits, 256, lo, t0, kF32TT, lg0, nl);
+  route_finalize(p, logits, 256, lo, t0, kF32TT, lg0, nl, 256);
 }
 
 template <int MB, int NB, int WN, int WK, bool FUSE = false, bool SPLIT = false>
