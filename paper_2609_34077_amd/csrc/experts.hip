@@ -367,6 +367,10 @@ static dim3 combine_grid(int T, int d) { return dim3(T * ((d + kCombineCols - 1)
 constexpr int DEC_NT = 4;        // 16-row weight tiles per operand per workgroup
 constexpr int DEC_CK = 64;       // reduction values per chunk (128 bytes per row)
 constexpr int DEC_THREADS = 256;
+// Down workgroups that build their H rows from the gate/up partial sums (decode_down_kernel
+// SWIGLU): LDS bytes for the rows, four-column groups per thread (their loads issued together).
+constexpr int kFusedSwigluLds = 8192;
+constexpr int kFusedItems = 2;
 
 struct DecodeArgs {
   const uint16_t* x;
@@ -391,15 +395,29 @@ __device__ __forceinline__ int weight_block(const DecodeArgs& p, int g) {
   return p.slot_of ? min(max(p.slot_of[g], 0), p.n_slots - 1) : g;
 }
 
+// Token-row operand of stream_rows: the 8 bf16 values of row (lane & 15) at k = base +
+// c * DEC_CK + ks * 32 + (lane >> 4) * 8 for chunk c of the stream, `ap` pointing at base +
+// (lane >> 4) * 8 of the row. IN_LDS: the rows sit in LDS (written before the stream's first
+// barrier) and are read where they are used; otherwise they are global and are loaded two
+// chunks ahead, with the weights.
+template <bool IN_LDS>
+struct RowOperand {
+  const uint16_t* ap;
+  __device__ __forceinline__ u32x4 operator()(int c, int ks) const {
+    return *reinterpret_cast<const u32x4*>(ap + c * DEC_CK + ks * 32);
+  }
+};
+
 // Streams R = 16 * NTILE weight rows over k in [k0, k0 + klen) and accumulates tile
-// (wave + 4q) of A(16 x k) * W^T into acc[q]. A row (lane & 15) is `arow`. Row r's values
-// k .. k + 63 of chunk k / 64 start at wrow(r) + (k / 64) * CSTRIDE: CSTRIDE = DEC_CK for
-// row-major weights, kPackBlock for packed ones (where the R rows of a chunk are one
-// contiguous block).
-template <int NTILE, int CSTRIDE, class RowPtr>
-__device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* arow, int k0, int klen,
+// (wave + 4q) of A(16 x k) * W^T into acc[q]; `arow` gives the A operand (RowOperand, its
+// chunks counted from k0). Row r's values k .. k + 63 of chunk k / 64 start at wrow(r) +
+// (k / 64) * CSTRIDE: CSTRIDE = DEC_CK for row-major weights, kPackBlock for packed ones
+// (where the R rows of a chunk are one contiguous block). `prologue` runs once the first two
+// weight chunks are in flight, before the first barrier.
+template <int NTILE, int CSTRIDE, bool A_LDS, class RowPtr, class Prologue>
+__device__ __forceinline__ void stream_rows(const RowPtr& wrow, const RowOperand<A_LDS>& arow, int k0, int klen,
                                             unsigned char (*lds)[16 * NTILE * (DEC_CK * 2 + 16)],
-                                            f32x4* acc) {
+                                            f32x4* acc, const Prologue& prologue) {
   constexpr int R = 16 * NTILE;
   constexpr int PITCH = DEC_CK * 2 + 16;
   constexpr int UPR = DEC_CK * 2 / 16;
@@ -417,7 +435,6 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
     src[i] = wrow(r) + (CSTRIDE == DEC_CK ? k0 : (k0 / DEC_CK) * CSTRIDE) + piece * 8;
     dst[i] = r * PITCH + piece * 16;
   }
-  const uint16_t* ap = arow + k0 + (lane >> 4) * 8;
   const int nc = klen / DEC_CK;
   // Weight chunks c + 1 and c + 2 are in flight in registers while chunk c is multiplied from
   // LDS; the token rows' operands travel with them (a wait on a load issued after the weight
@@ -429,8 +446,10 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
     for (int i = 0; i < PER; ++i) r[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src[i] + c * CSTRIDE));
   };
   auto load_a = [&](int c, u32x4* r) {
+    if (!A_LDS) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) r[ks] = *reinterpret_cast<const u32x4*>(ap + c * DEC_CK + ks * 32);
+      for (int ks = 0; ks < KS; ++ks) r[ks] = arow(c, ks);
+    }
   };
   auto store = [&](int buf, const u32x4* r) {
 #pragma unroll
@@ -442,6 +461,7 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
   load_a(0, areg[0]);
   load_w(min(1, nc - 1), reg[1]);   // nc == 1 (d or F of 64) reloads chunk 0
   load_a(min(1, nc - 1), areg[1]);
+  prologue();
   store(0, reg[0]);
   __syncthreads();
   // one chunk; BUF = c & 1 is a compile-time index so that the staging stays in registers;
@@ -452,13 +472,14 @@ __device__ __forceinline__ void stream_rows(const RowPtr& wrow, const uint16_t* 
     __builtin_amdgcn_sched_barrier(0);   // keep the loads first and the LDS stores last
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 a = A_LDS ? arow(c, ks) : areg[buf][ks];
 #pragma unroll
       for (int q = 0; q < TPW; ++q) {
         const int tile = wave + 4 * q;
         if (NTILE % 4 == 0 || tile < NTILE) {
           const int r = tile * 16 + (lane & 15);
           const u32x4 b = *reinterpret_cast<const u32x4*>(&lds[buf][r * PITCH + ks * 64 + (lane >> 4) * 16]);
-          acc[q] = mfma_16x16x32(areg[buf][ks], b, acc[q]);
+          acc[q] = mfma_16x16x32(a, b, acc[q]);
         }
       }
     }
@@ -518,7 +539,8 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const Decod
 #pragma unroll
   for (int q = 0; q < TPW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int klen = p.d / p.split_gu, z = blockIdx.z;
-  stream_rows<NTILE, PACKED ? kPackBlock : DEC_CK>(wrow, arow, z * klen, klen, lds, acc);
+  const RowOperand<false> aop{arow + z * klen + (lane >> 4) * 8};
+  stream_rows<NTILE, PACKED ? kPackBlock : DEC_CK>(wrow, aop, z * klen, klen, lds, acc, [] {});
   if (p.split_gu > 1) {  // partial sums: wave w holds tiles w and w + 4 (gate tile j, up tile j)
 #pragma unroll
     for (int q = 0; q < TPW; ++q) {
@@ -550,16 +572,10 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_gate_up_kernel(const Decod
   }
 }
 
-// H[r, c] = SiLU(sum_z P[z, r, c]) * (sum_z P[z, r, F + c]), slices added in order. One
-// thread per four columns (F % 64 == 0); the loads of all slices are issued together.
-__global__ __launch_bounds__(256) void decode_swiglu_kernel(const float* __restrict__ P, uint16_t* __restrict__ H,
-                                                            int rows, int F, int split) {
-  const int i = blockIdx.x * 256 + threadIdx.x;   // index of a group of four columns
-  const int per_row = F / 4;
-  if (i >= rows * per_row) return;
-  const int r = i / per_row, c = (i - r * per_row) * 4;
-  const size_t slice = static_cast<size_t>(rows) * 2 * F;
-  const float* src = P + static_cast<size_t>(r) * 2 * F + c;
+// Four H values from the gate/up partial sums: SiLU(sum_z P[z, r, c]) * (sum_z P[z, r, F + c])
+// for c = c0 .. c0 + 3, the slices added in order; `src` is &P[0, r, c0], `slice` the stride
+// of z. The loads of all slices are issued together. Packed bf16, columns in order.
+__device__ __forceinline__ uint2 swiglu_from_partials(const float* src, size_t slice, int F, int split) {
   float4 g[kDecodeMaxSplitGateUp], u[kDecodeMaxSplitGateUp];
 #pragma unroll
   for (int z = 0; z < kDecodeMaxSplitGateUp; ++z) {
@@ -581,12 +597,29 @@ __global__ __launch_bounds__(256) void decode_swiglu_kernel(const float* __restr
              (static_cast<uint32_t>(f32_to_bf16(silu(gs.y) * us.y)) << 16);
   packed.y = static_cast<uint32_t>(f32_to_bf16(silu(gs.z) * us.z)) |
              (static_cast<uint32_t>(f32_to_bf16(silu(gs.w) * us.w)) << 16);
-  *reinterpret_cast<uint2*>(H + static_cast<size_t>(r) * F + c) = packed;
+  return packed;
+}
+
+// H[r, c] = SiLU(sum_z P[z, r, c]) * (sum_z P[z, r, F + c]), slices added in order. One
+// thread per four columns (F % 64 == 0).
+__global__ __launch_bounds__(256) void decode_swiglu_kernel(const float* __restrict__ P, uint16_t* __restrict__ H,
+                                                            int rows, int F, int split) {
+  const int i = blockIdx.x * 256 + threadIdx.x;   // index of a group of four columns
+  const int per_row = F / 4;
+  if (i >= rows * per_row) return;
+  const int r = i / per_row, c = (i - r * per_row) * 4;
+  const size_t slice = static_cast<size_t>(rows) * 2 * F;
+  *reinterpret_cast<uint2*>(H + static_cast<size_t>(r) * F + c) =
+      swiglu_from_partials(P + static_cast<size_t>(r) * 2 * F + c, slice, F, split);
 }
 
 // O[z, row0 + r, n0 + j] = sum over k in slice z of H[row0 + r, k] * W_down[n0 + j, k];
 // grid (d / (16 * DEC_NT), max active experts, split).
-template <int NTILE, bool PACKED>   // 16-row tiles of W_down per workgroup (4 or 8; 8 when packed)
+// SWIGLU: H is not materialised; the prologue builds the workgroup's H rows of slice z in LDS
+// from the gate/up partial sums P with the arithmetic of decode_swiglu_kernel, so the bits are
+// the same. The host takes this path when every group's rows of one slice fit in
+// kFusedSwigluLds and take at most kFusedItems four-column groups per thread.
+template <int NTILE, bool PACKED, bool SWIGLU = false>   // NTILE: 16-row W_down tiles per workgroup (4 or 8)
 __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeArgs p) {
   static_assert(!PACKED || 16 * NTILE == kPackRows, "a workgroup's rows are one packed group");
   constexpr int TPW = (NTILE + 3) / 4;
@@ -606,11 +639,32 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_down_kernel(const DecodeAr
   auto wrow = [=](int r) {
     return PACKED ? wd + static_cast<size_t>(n0) * F + r * kPackCols : wd + static_cast<size_t>(n0 + r) * F;
   };
-  const uint16_t* arow = p.H + static_cast<size_t>(row0 + min(lane & 15, nrows - 1)) * p.F;
   f32x4 acc[TPW];
 #pragma unroll
   for (int q = 0; q < TPW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  stream_rows<NTILE, PACKED ? kPackBlock : DEC_CK>(wrow, arow, z * klen, klen, lds, acc);
+  if (SWIGLU) {
+    __shared__ __attribute__((aligned(16))) uint16_t hs[kFusedSwigluLds / 2];
+    const int pitch = klen + 8;   // 16 bytes past a multiple of 128: rows start on different banks
+    const RowOperand<true> aop{hs + min(lane & 15, nrows - 1) * pitch + (lane >> 4) * 8};
+    auto prologue = [&] {
+      const int per_row = klen / 4, items = nrows * per_row;
+      const size_t slice = static_cast<size_t>(p.rows) * 2 * F;
+#pragma unroll
+      for (int i = 0; i < kFusedItems; ++i) {
+        const int it = threadIdx.x + i * DEC_THREADS;
+        if (it < items) {
+          const int r = it / per_row, c = (it - r * per_row) * 4;
+          *reinterpret_cast<uint2*>(hs + r * pitch + c) = swiglu_from_partials(
+              p.P + static_cast<size_t>(row0 + r) * 2 * F + z * klen + c, slice, F, p.split_gu);
+        }
+      }
+    };
+    stream_rows<NTILE, PACKED ? kPackBlock : DEC_CK>(wrow, aop, z * klen, klen, lds, acc, prologue);
+  } else {
+    const uint16_t* arow = p.H + static_cast<size_t>(row0 + min(lane & 15, nrows - 1)) * p.F;
+    const RowOperand<false> aop{arow + z * klen + (lane >> 4) * 8};
+    stream_rows<NTILE, PACKED ? kPackBlock : DEC_CK>(wrow, aop, z * klen, klen, lds, acc, [] {});
+  }
   // wave w holds tiles w, w + 4: rows 4*(lane>>4)+i, column lane & 15
 #pragma unroll
   for (int q = 0; q < TPW; ++q)
@@ -864,22 +918,30 @@ hipError_t launch_experts_bf16_decode(const ExpertArgs& a, const PermBuffers& pb
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 0, stream);
-  if (p.split_gu > 1) {  // timed with the down stage
+  // A group holds at most T rows (a token picks an expert once; a shared expert takes all T).
+  const int klen_down = p.F / p.split;
+  const bool fuse = p.split_gu > 1 && a.T * (klen_down + 8) * 2 <= kFusedSwigluLds &&
+                    a.T * (klen_down / 4) <= kFusedItems * DEC_THREADS;
+  if (p.split_gu > 1 && !fuse) {  // timed with the down stage
     const int groups = p.rows * (p.F / 4);   // rows <= 16 (K + n_shared): no overflow
     const unsigned blocks = static_cast<unsigned>((groups + 255) / 256);
     hipLaunchKernelGGL(decode_swiglu_kernel, dim3(blocks), dim3(256), 0, stream, P, H, p.rows, p.F, p.split_gu);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
-  if (a.packed)   // d % kPackRows == 0, so decode_down_tiles(d) == 8
-    hipLaunchKernelGGL((decode_down_kernel<8, true>), dim3(a.d / 128, max_active, p.split), dim3(DEC_THREADS), 0,
-                       stream, p);
+  const dim3 dn_grid8(a.d / 128, max_active, p.split), dn_grid4(a.d / (16 * DEC_NT), max_active, p.split);
+  if (a.packed && fuse)   // d % kPackRows == 0, so decode_down_tiles(d) == 8
+    hipLaunchKernelGGL((decode_down_kernel<8, true, true>), dn_grid8, dim3(DEC_THREADS), 0, stream, p);
+  else if (a.packed)
+    hipLaunchKernelGGL((decode_down_kernel<8, true>), dn_grid8, dim3(DEC_THREADS), 0, stream, p);
+  else if (decode_down_tiles(a.d) == 8 && fuse)
+    hipLaunchKernelGGL((decode_down_kernel<8, false, true>), dn_grid8, dim3(DEC_THREADS), 0, stream, p);
   else if (decode_down_tiles(a.d) == 8)
-    hipLaunchKernelGGL((decode_down_kernel<8, false>), dim3(a.d / 128, max_active, p.split), dim3(DEC_THREADS), 0,
-                       stream, p);
+    hipLaunchKernelGGL((decode_down_kernel<8, false>), dn_grid8, dim3(DEC_THREADS), 0, stream, p);
+  else if (fuse)
+    hipLaunchKernelGGL((decode_down_kernel<DEC_NT, false, true>), dn_grid4, dim3(DEC_THREADS), 0, stream, p);
   else
-    hipLaunchKernelGGL((decode_down_kernel<DEC_NT, false>), dim3(a.d / (16 * DEC_NT), max_active, p.split),
-                       dim3(DEC_THREADS), 0, stream, p);
+    hipLaunchKernelGGL((decode_down_kernel<DEC_NT, false>), dn_grid4, dim3(DEC_THREADS), 0, stream, p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   record_mark(marks, 1, stream);

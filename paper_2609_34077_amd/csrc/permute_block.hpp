@@ -98,4 +98,54 @@ __device__ inline void permute_block(const int32_t* idx, int T, int K, int E, in
   }
 }
 
+// The same layout computed by one wavefront, for n = T*K <= 64 entries and G = E + n_shared < 64
+// groups: lane j holds entry j and lane g group g. Group sizes come from a pass over the
+// entries, first rows and row-tiles from lane prefix sums, the rank of an entry among equal
+// experts from ballots on the expert id bits; no LDS passes and no barriers. Same outputs as
+// permute_block (and the same contract for `idx`).
+__device__ inline void permute_wave(const int32_t* idx, int T, int K, int E, int n_shared, int tile_rows,
+                                    const PermBuffers& pb) {
+  const int lane = threadIdx.x & 63;
+  const int n = T * K, G = E + n_shared;
+  const int e = lane < n ? idx[lane] : -1;
+  const bool valid = e >= 0 && e < E;
+  uint64_t same = __ballot(valid);   // lanes holding the same expert (E < 64: six id bits)
+#pragma unroll
+  for (int b = 0; b < 6; ++b) {
+    const uint64_t bb = __ballot(valid && ((e >> b) & 1));
+    same &= ((e >> b) & 1) ? bb : ~bb;
+  }
+  int c = 0;   // entries of expert `lane` (an invalid entry matches no lane below E)
+  for (int j = 0; j < n; ++j) c += __builtin_amdgcn_readlane(e, j) == lane ? 1 : 0;
+  if (lane >= E) c = lane < G ? T : 0;   // shared groups hold every token; none past G
+  const int tiles = (c + tile_rows - 1) / tile_rows;
+  int off = c, toff = tiles;   // inclusive prefix sums over the lanes
+#pragma unroll
+  for (int dl = 1; dl < 64; dl <<= 1) {
+    const int o = __shfl_up(off, dl), q = __shfl_up(toff, dl);
+    if (lane >= dl) {
+      off += o;
+      toff += q;
+    }
+  }
+  off -= c;   // first row and row-tile of group `lane`; lane G: the totals
+  toff -= tiles;
+  if (lane <= G) {
+    pb.offsets[lane] = off;
+    pb.tile_off[lane] = toff;
+  }
+  const uint64_t act = __ballot(lane < G && c > 0);
+  if (lane < G && c > 0) pb.active[__popcll(act & lanemask_lt(lane))] = lane;
+  if (lane == 0) pb.n_active[0] = __popcll(act);
+  // shared-expert rows: token t of shared expert s sits at row n + s*T + t
+  for (int r = lane; r < n_shared * T; r += kWave) pb.row_tok[n + r] = r % T;
+  const int first = __shfl(off, valid ? e : 0);
+  if (valid) {
+    const int pos = first + __popcll(same & lanemask_lt(lane));
+    pb.perm[pos] = lane;
+    pb.inv[lane] = pos;
+    pb.row_tok[pos] = lane / K;
+  }
+}
+
 }  // namespace maskmoe

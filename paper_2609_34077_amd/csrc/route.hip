@@ -369,8 +369,77 @@ __device__ void route_finalize_wave(const RouteParams& p, const float* logits, i
   }
 }
 
+// E <= 16 experts, tokens 0..TT-1 of the single-workgroup launch: token t is selected by
+// 16-lane row t % 4 of wavefront t / 4, lane e of the row holding expert e. An expert's rank
+// (the number of valid keys larger, or equal with a lower index; -inf and NaN keys are not
+// valid) comes from the row's other keys, and the j-th pick is the expert of rank j, as in the
+// successive picks of select_pair; with fewer than K valid keys the lowest experts not taken
+// follow. Margin, gates and normalisers are formed in select_pair's order (picks in order for
+// the renormalised rule, experts in order for the softmax), so both give the same bits. The
+// picks are also left in sel_lds [T, K] for the permutation.
+__device__ void route_select_rows(const RouteParams& p, const float* logits, int ld, const float* lo, int TT,
+                                  int32_t* sel_lds, int nwaves) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int E = p.E, K = p.K;
+  const int row = lane >> 4, e = lane & 15, rb = lane & 48;
+  for (int t0 = 4 * wave; t0 < TT && t0 < p.T; t0 += 4 * nwaves) {
+    const int t = t0 + row;
+    const bool live = t < p.T;
+    const bool in = live && e < E;
+    const float z = in ? logits[t * ld + e] : 0.0f;
+    const float key = in ? z + lo[e] : -INFINITY;
+    const bool valid = key > -INFINITY;   // false for NaN too
+    int rank = 0;
+#pragma unroll
+    for (int r = 1; r < 16; ++r) {
+      const int f = (e + r) & 15;
+      const float kf = __shfl(key, rb + f);
+      rank += (kf > -INFINITY && (kf > key || (kf == key && f < e))) ? 1 : 0;
+    }
+    const uint32_t emask = E >= 16 ? 0xffffu : (1u << E) - 1u;
+    uint32_t taken = 0;
+    int my_sel = 0;
+    float my_selz = 0.0f, kth = -INFINITY;
+    for (int j = 0; j < K; ++j) {
+      const uint32_t m = static_cast<uint32_t>(__ballot(valid && rank == j) >> rb) & 0xffffu;
+      const uint32_t fr = ~taken & emask;   // m == 0: fewer than j + 1 valid keys
+      const int ej = m ? __builtin_ctz(m) : (fr ? __builtin_ctz(fr) : 0);
+      taken |= 1u << ej;
+      const float zj = __shfl(z, rb + ej), kj = __shfl(key, rb + ej);
+      if (e == j) {
+        my_sel = ej;
+        my_selz = zj;
+      }
+      kth = m ? kj : -INFINITY;
+    }
+    const uint32_t mk = static_cast<uint32_t>(__ballot(valid && rank == K) >> rb) & 0xffffu;
+    const float kn = __shfl(key, rb + (mk ? __builtin_ctz(mk) : 0));
+    const float nxt = mk ? kn : -INFINITY;
+    float zref, norm = 0.0f;
+    if (p.gate_mode == 0) {   // g = p_i: softmax over all E experts, normaliser in expert order
+      zref = __shfl(z, rb);
+      for (int f = 1; f < E; ++f) zref = fmaxf(zref, __shfl(z, rb + f));
+      const float ex = e < E ? expf(z - zref) : 0.0f;
+      for (int f = 0; f < E; ++f) norm += __shfl(ex, rb + f);
+    } else {   // g = p_i / sum_{j in A} p_j, in pick order
+      zref = __shfl(my_selz, rb);
+      for (int j = 1; j < K; ++j) zref = fmaxf(zref, __shfl(my_selz, rb + j));
+      for (int j = 0; j < K; ++j) norm += expf(__shfl(my_selz, rb + j) - zref);
+    }
+    const float inv = 1.0f / norm;
+    if (live && e < K) {
+      p.idx[static_cast<size_t>(t) * K + e] = my_sel;
+      p.gate[static_cast<size_t>(t) * K + e] = expf(my_selz - zref) * inv;
+      sel_lds[t * K + e] = my_sel;
+    }
+    if (live && e == 0 && p.margin) p.margin[t] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+    if (in && p.logits) p.logits[static_cast<size_t>(t) * E + e] = z;
+  }
+}
+
 // FUSE: the grid is one workgroup holding every token of one layer; after the selection it
-// also groups the (token, slot) pairs by expert (permute_block).
+// also groups the (token, slot) pairs by expert (permute_wave for few entries, else
+// permute_block).
 // SPLIT (not with FUSE): the tile's logits go to p.logits and route_select_kernel selects.
 // Kernel parameters not needed before the epilogue, read at the start so that their loads
 // share the first memory round trip: the argument block is fetched from memory at each
@@ -508,9 +577,16 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
   } else if (FUSE) {
     __shared__ PermLds plds;
     __shared__ int32_t sel_lds[kRouteOneBlockT * kMaxK];
-    route_finalize_wave(p, red, NO, lo, TT, sel_lds, NT / 64);
+    if (NO <= 16)   // E <= 16
+      route_select_rows(p, red, NO, lo, TT, sel_lds, NT / 64);
+    else
+      route_finalize_wave(p, red, NO, lo, TT, sel_lds, NT / 64);
     lds_sync();   // the selections left in sel_lds are read by other threads
-    permute_block(sel_lds, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb, plds, NT);
+    if (p.T * p.K <= kWave && p.E + p.n_shared < kWave) {
+      if (wave == 0) permute_wave(sel_lds, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb);
+    } else {
+      permute_block(sel_lds, p.T, p.K, p.E, p.n_shared, p.tile_rows, p.pb, plds, NT);
+    }
   } else {
     route_finalize(p, red, NO, lo, t0, TT, lg0, nl, NT);
   }

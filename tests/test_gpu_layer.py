@@ -150,6 +150,38 @@ def test_decode_path_small(cfg):
     check_layer(cfg)
 
 
+# Few tokens (T <= 16): one workgroup routes and groups the tokens. E <= 16 selects one token
+# per 16-lane row, larger E one token per wavefront; T*K <= 64 entries with fewer than 64
+# groups are grouped by one wavefront, more by the whole workgroup. Each case must give the
+# bits of maskmoe_route's idx and gates, and the output is checked against the oracle.
+# (T, E, K, shared, mode, gate, kept experts)
+FEW_TOKEN_ROUTING = [
+    (1, 8, 2, 0, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, (0, 2, 5, 7)),
+    (3, 5, 3, 0, L.ROUTE_PLAIN, L.GATE_P, None),
+    (2, 1, 1, 0, L.ROUTE_PLAIN, L.GATE_RENORM, None),
+    (16, 16, 4, 2, L.ROUTE_HARD_MASK, L.GATE_P, tuple(range(0, 16, 2))),    # 64 entries, shared groups
+    (16, 16, 5, 0, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM, (1, 3, 5, 7, 9, 11)),  # 80 entries: workgroup grouping
+    (4, 8, 3, 0, L.ROUTE_HARD_MASK, L.GATE_RENORM, (1, 4, 6)),              # exactly K eligible
+    (4, 16, 16, 0, L.ROUTE_PLAIN, L.GATE_P, None),                          # K = E = 16
+    (7, 24, 4, 1, L.ROUTE_SOFT_PRIOR, L.GATE_P, (0, 5, 9, 13, 20)),         # E > 16: one token per wavefront
+    (16, 64, 6, 2, L.ROUTE_HARD_MASK, L.GATE_P, tuple(synth.deepseek_mask_set())),
+]
+
+
+@pytest.mark.parametrize("T,E,K,ns,mode,gmode,keep", FEW_TOKEN_ROUTING,
+                         ids=lambda v: str(v) if not isinstance(v, tuple) else "keep%d" % len(v))
+def test_few_token_routing_matches_route(T, E, K, ns, mode, gmode, keep):
+    cfg = synth.LayerConfig(f"few_t{T}_e{E}_k{K}", T=T, d=128, F=128, E=E, K=K, n_shared=ns, route_mode=mode,
+                            gate_mode=gmode, mask_set=keep, seed=30 + T + E + K)
+    inp = _inputs(cfg)
+    dd = _upload(inp, cfg)
+    y, idx, gate = run_gpu(cfg, inp, dd)
+    i2, g2, _ = L.maskmoe_route(dd["x"], dd["w_router"], K, mode, gmode, **_mp(cfg, inp))
+    assert torch.equal(idx, i2)
+    assert torch.equal(gate.view(torch.int32), g2.view(torch.int32))
+    check_layer(cfg)
+
+
 def test_empty_tokens():
     cfg = synth.LayerConfig("empty", T=0, d=64, F=64, E=8, K=2, route_mode=L.ROUTE_PLAIN)
     inp = synth.make_layer(cfg)
