@@ -98,6 +98,20 @@ __device__ inline void permute_block(const int32_t* idx, int T, int K, int E, in
   }
 }
 
+// Inclusive prefix sum over the 64 lanes with DPP lane shifts: within each 16-lane row by
+// shifts of 1, 2, 4, 8 (lanes shifted in from outside the row add 0), then the last lane of
+// rows 0 and 2 is added to rows 1 and 3 (row_bcast:15) and lane 31 to rows 2 and 3
+// (row_bcast:31).
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);   // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);   // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);   // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);   // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);   // row_bcast:15 into rows 1, 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);   // row_bcast:31 into rows 2, 3
+  return v;
+}
+
 // The same layout computed by one wavefront, for n = T*K <= 64 entries and G = E + n_shared < 64
 // groups: lane j holds entry j and lane g group g. Group sizes come from a pass over the
 // entries, first rows and row-tiles from lane prefix sums, the rank of an entry among equal
@@ -119,15 +133,7 @@ __device__ inline void permute_wave(const int32_t* idx, int T, int K, int E, int
   for (int j = 0; j < n; ++j) c += __builtin_amdgcn_readlane(e, j) == lane ? 1 : 0;
   if (lane >= E) c = lane < G ? T : 0;   // shared groups hold every token; none past G
   const int tiles = (c + tile_rows - 1) / tile_rows;
-  int off = c, toff = tiles;   // inclusive prefix sums over the lanes
-#pragma unroll
-  for (int dl = 1; dl < 64; dl <<= 1) {
-    const int o = __shfl_up(off, dl), q = __shfl_up(toff, dl);
-    if (lane >= dl) {
-      off += o;
-      toff += q;
-    }
-  }
+  int off = wave_inclusive_sum(c), toff = wave_inclusive_sum(tiles);
   off -= c;   // first row and row-tile of group `lane`; lane G: the totals
   toff -= tiles;
   if (lane <= G) {

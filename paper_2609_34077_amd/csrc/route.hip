@@ -369,72 +369,85 @@ __device__ void route_finalize_wave(const RouteParams& p, const float* logits, i
   }
 }
 
-// E <= 16 experts, tokens 0..TT-1 of the single-workgroup launch: token t is selected by
-// 16-lane row t % 4 of wavefront t / 4, lane e of the row holding expert e. An expert's rank
-// (the number of valid keys larger, or equal with a lower index; -inf and NaN keys are not
-// valid) comes from the row's other keys, and the j-th pick is the expert of rank j, as in the
-// successive picks of select_pair; with fewer than K valid keys the lowest experts not taken
-// follow. Margin, gates and normalisers are formed in select_pair's order (picks in order for
-// the renormalised rule, experts in order for the softmax), so both give the same bits. The
-// picks are also left in sel_lds [T, K] for the permutation.
-__device__ void route_select_rows(const RouteParams& p, const float* logits, int ld, const float* lo, int TT,
-                                  int32_t* sel_lds, int nwaves) {
+// Lane exchanges within a 16-lane row (DPP): lane e of the row receives lane (e - R) mod 16.
+template <int R>
+__device__ __forceinline__ int row_ror(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x120 + R, 0xF, 0xF, false);
+}
+
+// Rank of each lane's key among the row's valid keys (larger, or equal with a lower index).
+template <int R>
+__device__ __forceinline__ void row_rank_step(float key, int e, int& rank) {
+  if constexpr (R < 16) {
+    const float kf = __int_as_float(row_ror<R>(__float_as_int(key)));
+    const int f = row_ror<R>(e);
+    rank += static_cast<int>(kf > -INFINITY) & (static_cast<int>(kf > key) | (static_cast<int>(kf == key) & static_cast<int>(f < e)));
+    row_rank_step<R + 1>(key, e, rank);
+  }
+}
+
+// fmaxf over the 16 lanes of the row, in every lane. fmaxf drops NaN operands, so any order
+// of the reduction gives the same value (the largest non-NaN, NaN if all are NaN).
+__device__ __forceinline__ float row_max(float v) {
+  v = fmaxf(v, __int_as_float(row_ror<8>(__float_as_int(v))));
+  v = fmaxf(v, __int_as_float(row_ror<4>(__float_as_int(v))));
+  v = fmaxf(v, __int_as_float(row_ror<2>(__float_as_int(v))));
+  v = fmaxf(v, __int_as_float(row_ror<1>(__float_as_int(v))));
+  return v;
+}
+
+// E <= 16 experts, the tokens of the single-workgroup launch (4 per wavefront, every wavefront
+// calls this: it holds a barrier): token t is selected by 16-lane row t % 4 of wavefront t / 4,
+// lane e of the row holding expert e. An expert's rank among the valid keys (larger, or equal
+// with a lower index; -inf and NaN keys are not valid) is its position in select_pair's
+// successive picks; with fewer than K valid keys the lowest other experts follow in index
+// order. Each picked lane writes its own outputs. The maxima are order-free; the normalisers
+// are summed through LDS (`sc`, [16 tokens][16]) in select_pair's order (picks for the
+// renormalised rule, experts for the softmax), so both give the same bits. The picks are also
+// left in sel_lds [T, K] for the permutation.
+__device__ void route_select_rows(const RouteParams& p, const float* logits, int ld, const float* lo, float* sc,
+                                  int32_t* sel_lds) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int E = p.E, K = p.K;
-  const int row = lane >> 4, e = lane & 15, rb = lane & 48;
-  for (int t0 = 4 * wave; t0 < TT && t0 < p.T; t0 += 4 * nwaves) {
-    const int t = t0 + row;
-    const bool live = t < p.T;
-    const bool in = live && e < E;
-    const float z = in ? logits[t * ld + e] : 0.0f;
-    const float key = in ? z + lo[e] : -INFINITY;
+  const int E = p.E, K = p.K, rb = lane & 48, e = lane & 15;
+  const int t = 4 * wave + (lane >> 4);
+  const bool act = 4 * wave < p.T;   // wavefronts without tokens only take part in the barrier
+  const bool live = t < p.T;         // p.T <= 16
+  const bool in = live && e < E;
+  const bool soft_all = p.gate_mode == 0;   // g = p_i (softmax over all E), else renormalised over the picks
+  float z = 0.0f, key = -INFINITY, ex = 0.0f, zref = 0.0f, kth = -INFINITY, nxt = -INFINITY;
+  int pos = 0;
+  bool pick = false;
+  if (act) {
+    z = in ? logits[t * ld + e] : 0.0f;
+    key = in ? z + lo[e] : -INFINITY;
     const bool valid = key > -INFINITY;   // false for NaN too
     int rank = 0;
-#pragma unroll
-    for (int r = 1; r < 16; ++r) {
-      const int f = (e + r) & 15;
-      const float kf = __shfl(key, rb + f);
-      rank += (kf > -INFINITY && (kf > key || (kf == key && f < e))) ? 1 : 0;
-    }
-    const uint32_t emask = E >= 16 ? 0xffffu : (1u << E) - 1u;
-    uint32_t taken = 0;
-    int my_sel = 0;
-    float my_selz = 0.0f, kth = -INFINITY;
-    for (int j = 0; j < K; ++j) {
-      const uint32_t m = static_cast<uint32_t>(__ballot(valid && rank == j) >> rb) & 0xffffu;
-      const uint32_t fr = ~taken & emask;   // m == 0: fewer than j + 1 valid keys
-      const int ej = m ? __builtin_ctz(m) : (fr ? __builtin_ctz(fr) : 0);
-      taken |= 1u << ej;
-      const float zj = __shfl(z, rb + ej), kj = __shfl(key, rb + ej);
-      if (e == j) {
-        my_sel = ej;
-        my_selz = zj;
-      }
-      kth = m ? kj : -INFINITY;
-    }
-    const uint32_t mk = static_cast<uint32_t>(__ballot(valid && rank == K) >> rb) & 0xffffu;
-    const float kn = __shfl(key, rb + (mk ? __builtin_ctz(mk) : 0));
-    const float nxt = mk ? kn : -INFINITY;
-    float zref, norm = 0.0f;
-    if (p.gate_mode == 0) {   // g = p_i: softmax over all E experts, normaliser in expert order
-      zref = __shfl(z, rb);
-      for (int f = 1; f < E; ++f) zref = fmaxf(zref, __shfl(z, rb + f));
-      const float ex = e < E ? expf(z - zref) : 0.0f;
-      for (int f = 0; f < E; ++f) norm += __shfl(ex, rb + f);
-    } else {   // g = p_i / sum_{j in A} p_j, in pick order
-      zref = __shfl(my_selz, rb);
-      for (int j = 1; j < K; ++j) zref = fmaxf(zref, __shfl(my_selz, rb + j));
-      for (int j = 0; j < K; ++j) norm += expf(__shfl(my_selz, rb + j) - zref);
-    }
-    const float inv = 1.0f / norm;
-    if (live && e < K) {
-      p.idx[static_cast<size_t>(t) * K + e] = my_sel;
-      p.gate[static_cast<size_t>(t) * K + e] = expf(my_selz - zref) * inv;
-      sel_lds[t * K + e] = my_sel;
-    }
-    if (live && e == 0 && p.margin) p.margin[t] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
-    if (in && p.logits) p.logits[static_cast<size_t>(t) * E + e] = z;
+    row_rank_step<1>(key, e, rank);
+    const uint32_t vbits = static_cast<uint32_t>(__ballot(valid) >> rb) & 0xffffu;
+    const uint32_t ibits = static_cast<uint32_t>(__ballot(in && !valid) >> rb) & 0xffffu;
+    pos = valid ? rank : __popc(vbits) + __popc(ibits & ((1u << e) - 1u));
+    pick = in && pos < K;
+    kth = row_max(pick && valid && pos == K - 1 ? key : -INFINITY);
+    nxt = row_max(valid && rank == K ? key : -INFINITY);
+    const bool term = soft_all ? in : pick;
+    zref = row_max(term ? z : __builtin_nanf(""));
+    ex = expf(z - zref);
+    if (term) sc[t * 16 + (soft_all ? e : pos)] = ex;
   }
+  lds_sync();
+  if (!act) return;
+  float norm = 0.0f;
+  const int nterms = soft_all ? E : K;
+  if (live)
+    for (int i = 0; i < nterms; ++i) norm += sc[t * 16 + i];
+  const float inv = 1.0f / norm;
+  if (pick) {
+    p.idx[static_cast<size_t>(t) * K + pos] = e;
+    p.gate[static_cast<size_t>(t) * K + pos] = ex * inv;
+    sel_lds[t * K + pos] = e;
+  }
+  if (live && e == 0 && p.margin) p.margin[t] = (nxt == -INFINITY) ? INFINITY : (kth - nxt);
+  if (in && p.logits) p.logits[static_cast<size_t>(t) * E + e] = z;
 }
 
 // FUSE: the grid is one workgroup holding every token of one layer; after the selection it
@@ -506,9 +519,48 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // k-steps wk, wk+WK, ...; groups of U steps are loaded before any is multiplied.
+  // k-steps wk, wk+WK, ...; groups of U steps are loaded before any is multiplied. Each wave
+  // accumulates its steps in increasing order on every path below.
   constexpr int U = (MB + NB) <= 2 ? 8 : 4;
   int s = wk;
+  // Few tokens in the fused launch: their rows are read once into LDS (all lanes of a row
+  // tile share them) and the A operands come from there, which halves the load instructions;
+  // the first group's weight loads are issued before the rows are stored.
+  constexpr bool kStageX = FUSE && NO <= 16 && MB == 1 && NB == 1;
+  constexpr int kXsUnits = kStageX ? 2 * NT : 1;   // 16-byte units: 32 KB
+  __shared__ u32x4 xs[kXsUnits];
+  if (kStageX && p.T * p.d <= kXsUnits * 8) {
+    const int units = p.T * p.d / 8;
+    const int tr = lane & 15;   // token row of this lane's A operand (loaded when tr < T)
+    u32x4 xr[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + i * NT;
+      xr[i] = c < units ? reinterpret_cast<const u32x4*>(x)[c] : zero4;
+    }
+    u32x4 bv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int st = s + u * WK;
+      bv[u] = brow[0] && st < ksteps ? *reinterpret_cast<const u32x4*>(bp[0] + (st << 5)) : zero4;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + i * NT;
+      if (c < units) xs[c] = xr[i];
+    }
+    lds_sync();
+    const u32x4* xa = xs + (tr * p.d + kg) / 8;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int st = s + u * WK;
+      if (st < ksteps) acc[0][0] = mfma_16x16x32(arow[0] ? xa[st * 4] : zero4, bv[u], acc[0][0]);
+    }
+    for (s += U * WK; s < ksteps; s += WK) {
+      const u32x4 b = brow[0] ? *reinterpret_cast<const u32x4*>(bp[0] + (s << 5)) : zero4;
+      acc[0][0] = mfma_16x16x32(arow[0] ? xa[s * 4] : zero4, b, acc[0][0]);
+    }
+  }
   for (; s + (U - 1) * WK < ksteps; s += U * WK) {
     u32x4 av[U][MB], bv[U][NB];
 #pragma unroll
@@ -577,9 +629,11 @@ __global__ __launch_bounds__(64 * WN * WK) void route_bf16_kernel(const RoutePar
   } else if (FUSE) {
     __shared__ PermLds plds;
     __shared__ int32_t sel_lds[kRouteOneBlockT * kMaxK];
-    if (NO <= 16)   // E <= 16
-      route_select_rows(p, red, NO, lo, TT, sel_lds, NT / 64);
-    else
+    if (NO <= 16) {   // E <= 16
+      static_assert(!FUSE || NO > 16 || (TT == 16 && NT >= 4 * 64), "four wavefronts of 4 rows hold the 16 tokens");
+      __shared__ float sc[16 * 16];
+      route_select_rows(p, red, NO, lo, sc, sel_lds);
+    } else
       route_finalize_wave(p, red, NO, lo, TT, sel_lds, NT / 64);
     lds_sync();   // the selections left in sel_lds are read by other threads
     if (p.T * p.K <= kWave && p.E + p.n_shared < kWave) {
