@@ -56,35 +56,40 @@ __global__ __launch_bounds__(64 * kCacheWavesPerBlock) void cache_kernel(
   int clock = 0;
   bool bad = false;
 
-  if (POLICY == 1 && counts && lane < E) count = counts[stream * E + lane];
-  if (state) {  // slots are listed oldest first
-    const int32_t* st = state + stream * B;
-    for (int s = 0; s < B; ++s) {
-      const int e = st[s];  // wave-uniform
-      if (e < 0) continue;
-      const bool dup = e < E && ((__ballot(cached) >> e) & 1ull);
-      if (e >= E || dup) {
-        bad = true;
-        continue;
-      }
-      if (lane == e) {
-        cached = true;
-        stamp = s;
-      }
-      ++ncached;
-    }
-    clock = B;
-  }
-
-  long tot_f = 0, tot_h = 0;
   const int chunk = 64 / K;  // steps per 64-entry load
   // entries of the steps n0 .. n0 + ns - 1 in lanes 0 .. ns K - 1; the next chunk's load is
-  // issued before the current chunk is replayed
+  // issued before the current chunk is replayed (the first one before the state is read)
   auto load_chunk = [&](int n0) {
     const int ns = min(chunk, N - n0);
     return (n0 < N && lane < ns * K) ? tr[static_cast<long>(n0) * K + lane] : -1;
   };
   int v_next = load_chunk(0);
+
+  if (POLICY == 1 && counts && lane < E) count = counts[stream * E + lane];
+  if (state) {  // slots are listed oldest first; 64 slots per load, taken in order from the lanes
+    const int32_t* st = state + stream * B;
+    for (int s0 = 0; s0 < B; s0 += 64) {
+      const int sv = s0 + lane < B ? st[s0 + lane] : -1;
+      const int ns = min(64, B - s0);
+      for (int i = 0; i < ns; ++i) {
+        const int e = __builtin_amdgcn_readlane(sv, i);   // slot s0 + i
+        if (e < 0) continue;
+        const bool dup = e < E && ((__ballot(cached) >> e) & 1ull);
+        if (e >= E || dup) {
+          bad = true;
+          continue;
+        }
+        if (lane == e) {
+          cached = true;
+          stamp = s0 + i;
+        }
+        ++ncached;
+      }
+    }
+    clock = B;
+  }
+
+  long tot_f = 0, tot_h = 0;
   for (int n0 = 0; n0 < N; n0 += chunk) {
     const int ns = min(chunk, N - n0);
     const int v = v_next;
