@@ -48,7 +48,7 @@ struct GemmArgs {
   const uint16_t* ws;       // shared weights, same layout with n_shared experts
   const int32_t* offsets;   // [G+1]
   const int32_t* tile_off;  // [G+1]
-  void* out;                // EPI 0: H bf16 [rows, F]; EPI 1: O f32 [rows, d]
+  void* out;                // EPI 0: H bf16 [rows, F]; EPI 1: O bf16 [rows, d]
   uint16_t* ab;             // EPI 0, training: gate / up pre-activations bf16 [rows, 2F], or null
   const uint16_t* lora_u;   // LORA: rank-r projections of this GEMM's A rows, bf16 [rows, 64]
   const uint16_t* lora_b;   // LORA: (alpha / r) B rows matching the B operand, bf16 [G, N rows, 64]
@@ -76,8 +76,9 @@ __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt
 
 // Epilogue of a finished tile: rows [row0, row_end) of one group, columns from n0. EPI 0:
 // SwiGLU of the gate / up column pairs into H (bf16; the pre-activations into ab when given);
-// EPI 1: O (fp32). acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column
-// (lane & 31) of fragment j.
+// EPI 1: O, each expert output rounded to bf16 (the layer's dtype; the combine adds them in
+// fp32). acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column (lane & 31)
+// of fragment j.
 template <int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&acc)[kTileTM][kTileTN], int row0,
                                               int row_end, int n0) {
@@ -85,7 +86,6 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int Ndim = EPI == 0 ? p.F : p.d;
-  float* out_f32 = static_cast<float*>(p.out);
   const int col_in = lane & 31;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -110,7 +110,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int col = n0 + wn * 64 + j * 32 + col_in;
-            if (col < Ndim) out_f32[static_cast<size_t>(row) * Ndim + col] = acc[i][j][r];
+            if (col < Ndim) static_cast<uint16_t*>(p.out)[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(acc[i][j][r]);
           }
         }
       }
@@ -227,15 +227,16 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_tail_fixup(const GemmArg
   const int row0 = p.offsets[g] + (mt - p.tile_off[g]) * BM, row_end = p.offsets[g + 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave / 4, wn = wave % 4;
   const int c0 = nt * BN + wn * 64 + (lane & 31);
-  float* out = static_cast<float*>(p.out);
+  uint16_t* out = static_cast<uint16_t*>(p.out);
   tail_fixup_part(p.part, xcd * kTailSlotsPerXcd + t * x.s, x.s, part, [&](int i, int q, float4 a0, float4 a1) {
     const float v0[4] = {a0.x, a0.y, a0.z, a0.w}, v1[4] = {a1.x, a1.y, a1.z, a1.w};
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int row = row0 + wm * 128 + i * 32 + 8 * q + 4 * (lane >> 5) + u;
       if (row >= row_end) continue;
-      if (c0 < p.d) out[static_cast<size_t>(row) * p.d + c0] = v0[u];
-      if (c0 + 32 < p.d) out[static_cast<size_t>(row) * p.d + c0 + 32] = v1[u];
+      const size_t o = static_cast<size_t>(row) * p.d + c0;
+      if (c0 < p.d) out[o] = f32_to_bf16(v0[u]);
+      if (c0 + 32 < p.d) out[o + 32] = f32_to_bf16(v1[u]);
     }
   });
 }
@@ -243,6 +244,24 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_tail_fixup(const GemmArg
 // y_t = sum_k gate[t,k] * O[inv[t*K+k]] + sum_s O[T*K + s*T + t]; fp32 sum in k order, one
 // rounding at the end. O holds `split` partial slices [split, rows, d] that are added first,
 // in slice order. One workgroup per token.
+// Each expert output of a bf16 layer is rounded to bf16 (the layer's dtype) before the gated
+// sum: the grouped path stores O in bf16; the few-token path rounds its fp32 slice sums.
+__device__ __forceinline__ float4 round_bf16x4(float4 v) {
+  return make_float4(bf16_to_f32(f32_to_bf16(v.x)), bf16_to_f32(f32_to_bf16(v.y)), bf16_to_f32(f32_to_bf16(v.z)),
+                     bf16_to_f32(f32_to_bf16(v.w)));
+}
+
+// Four consecutive expert-output values at element offset off of O: fp32, or (OB) bf16.
+template <bool OB>
+__device__ __forceinline__ float4 load_o4(const void* O, size_t off) {
+  if (OB) {
+    const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(O) + off);
+    return make_float4(bf16_to_f32(static_cast<uint16_t>(u.x & 0xffffu)), bf16_to_f32(static_cast<uint16_t>(u.x >> 16)),
+                       bf16_to_f32(static_cast<uint16_t>(u.y & 0xffffu)), bf16_to_f32(static_cast<uint16_t>(u.y >> 16)));
+  }
+  return *reinterpret_cast<const float4*>(static_cast<const float*>(O) + off);
+}
+
 // Sum of the `split` slices at offset off, added in slice order; groups of four loads are
 // issued together so that a long split costs a few memory round trips, not one per slice.
 __device__ __forceinline__ float4 sum_slices(const float* O, int split, size_t slice, size_t off) {
@@ -272,13 +291,15 @@ constexpr int kCombineCols = 1024;
 constexpr int kMaxSharedCombine = 8;   // the API's limit on shared experts
 
 // KC: K known at compile time with one slice (the grouped path): every row's index, gate and
-// O values are loaded before any is added (same additions, same order).
-template <bool BF16, int KC = 0>
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
+// O values are loaded before any is added (same additions, same order). OB: O holds bf16
+// values (one slice, no expert outputs requested); the sums are still formed in fp32.
+template <bool BF16, int KC = 0, bool OB = false>
+__global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ Ov,
                                                        const int32_t* __restrict__ inv,
                                                        const float* __restrict__ gate, int T, int K,
                                                        int n_shared, int d, void* y, int split,
                                                        float* __restrict__ eo) {
+  const float* O = static_cast<const float*>(Ov);
   const int nb = (d + kCombineCols - 1) / kCombineCols;
   const int t = blockIdx.x / nb, cb = blockIdx.x % nb;
   if (BF16 && KC > 0) {  // d % 4 == 0, split == 1, K == KC, n_shared <= kMaxSharedCombine
@@ -294,11 +315,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     }
     float4 v[KA], vs[kMaxSharedCombine];
 #pragma unroll
-    for (int k = 0; k < KC; ++k) v[k] = *reinterpret_cast<const float4*>(O + static_cast<size_t>(row[k]) * d + c);
+    for (int k = 0; k < KC; ++k) v[k] = load_o4<OB>(Ov, static_cast<size_t>(row[k]) * d + c);
 #pragma unroll
     for (int sh = 0; sh < kMaxSharedCombine; ++sh)
       if (sh < n_shared)
-        vs[sh] = *reinterpret_cast<const float4*>(O + (static_cast<size_t>(T) * KC + static_cast<size_t>(sh) * T + t) * d + c);
+        vs[sh] = load_o4<OB>(Ov, (static_cast<size_t>(T) * KC + static_cast<size_t>(sh) * T + t) * d + c);
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
@@ -321,12 +342,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int k = 0; k < K; ++k) {
       const float gk = gate[t * K + k];
-      const float4 v = sum_slices(O, split, slice, static_cast<size_t>(inv[t * K + k]) * d + c);
+      const size_t off = static_cast<size_t>(inv[t * K + k]) * d + c;
+      const float4 v = OB ? load_o4<true>(Ov, off) : round_bf16x4(sum_slices(O, split, slice, off));
       s.x += gk * v.x; s.y += gk * v.y; s.z += gk * v.z; s.w += gk * v.w;
       if (eo) *reinterpret_cast<float4*>(eo + (static_cast<size_t>(t) * K + k) * d + c) = v;
     }
     for (int sh = 0; sh < n_shared; ++sh) {
-      const float4 v = sum_slices(O, split, slice, (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c);
+      const size_t off = (static_cast<size_t>(T) * K + static_cast<size_t>(sh) * T + t) * d + c;
+      const float4 v = OB ? load_o4<true>(Ov, off) : round_bf16x4(sum_slices(O, split, slice, off));
       s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
     }
     uint2 packed;
@@ -820,15 +843,16 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   }
   record_mark(marks, 1, stream);
 
+  const dim3 cgrid = combine_grid(a.T, a.d), cblk(256);   // O holds bf16 expert outputs
   if (a.K == 2)
-    hipLaunchKernelGGL((combine_kernel<true, 2>), combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate,
-                       a.T, a.K, a.n_shared, a.d, y, 1, a.expert_out);
+    hipLaunchKernelGGL((combine_kernel<true, 2, true>), cgrid, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
+                       a.n_shared, a.d, y, 1, a.expert_out);
   else if (a.K == 6)
-    hipLaunchKernelGGL((combine_kernel<true, 6>), combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate,
-                       a.T, a.K, a.n_shared, a.d, y, 1, a.expert_out);
+    hipLaunchKernelGGL((combine_kernel<true, 6, true>), cgrid, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
+                       a.n_shared, a.d, y, 1, a.expert_out);
   else
-    hipLaunchKernelGGL(combine_kernel<true>, combine_grid(a.T, a.d), dim3(256), 0, stream, O, pb.inv, a.gate, a.T,
-                       a.K, a.n_shared, a.d, y, 1, a.expert_out);
+    hipLaunchKernelGGL((combine_kernel<true, 0, true>), cgrid, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
+                       a.n_shared, a.d, y, 1, a.expert_out);
   err = hipGetLastError();
   record_mark(marks, 2, stream);
   return err;
