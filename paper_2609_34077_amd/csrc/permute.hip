@@ -52,19 +52,32 @@ __global__ __launch_bounds__(kPermThreads) void permute_scan_kernel(int32_t* __r
     total[g] = run;
   }
   lds_sync();
-  if (tid == 0) {
-    int off = 0, toff = 0, na = 0;
-    for (int g = 0; g < G; ++g) {
-      const int cnt = g < E ? total[g] : T;
-      pb.offsets[g] = off;
-      pb.tile_off[g] = toff;
-      if (cnt > 0) pb.active[na++] = g;
-      off += cnt;
-      toff += (cnt + tile_rows - 1) / tile_rows;
+  if (tid < kWave) {   // one wavefront: lane l takes groups l*PG .. l*PG + PG - 1 in order
+    constexpr int PG = (kPermMaxGroups + kWave - 1) / kWave;
+    const int g0 = tid * PG;
+    int cnt[PG], til[PG], sc = 0, st = 0, sa = 0;
+#pragma unroll
+    for (int i = 0; i < PG; ++i) {
+      const int g = g0 + i;
+      cnt[i] = g < G ? (g < E ? total[g] : T) : 0;
+      til[i] = (cnt[i] + tile_rows - 1) / tile_rows;
+      sc += cnt[i];
+      st += til[i];
+      sa += cnt[i] > 0 ? 1 : 0;
     }
-    pb.offsets[G] = off;
-    pb.tile_off[G] = toff;
-    pb.n_active[0] = na;
+    int off = wave_inclusive_sum(sc) - sc, toff = wave_inclusive_sum(st) - st, na = wave_inclusive_sum(sa) - sa;
+#pragma unroll
+    for (int i = 0; i < PG; ++i) {
+      const int g = g0 + i;
+      if (g <= G) {   // offsets[G], tile_off[G]: the totals
+        pb.offsets[g] = off;
+        pb.tile_off[g] = toff;
+      }
+      if (g < G && cnt[i] > 0) pb.active[na++] = g;
+      off += cnt[i];
+      toff += til[i];
+    }
+    if (tid == kWave - 1) pb.n_active[0] = na;
   }
 }
 
