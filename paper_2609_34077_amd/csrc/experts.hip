@@ -265,6 +265,19 @@ __device__ __forceinline__ float4 load_o4(const void* O, size_t off) {
 // Sum of the `split` slices at offset off, added in slice order; groups of four loads are
 // issued together so that a long split costs a few memory round trips, not one per slice.
 __device__ __forceinline__ float4 sum_slices(const float* O, int split, size_t slice, size_t off) {
+  if (split <= kDecodeMaxSplit) {   // every slice's load in flight at once
+    float4 u[kDecodeMaxSplit];
+#pragma unroll
+    for (int z = 0; z < kDecodeMaxSplit; ++z)
+      if (z < split) u[z] = *reinterpret_cast<const float4*>(O + z * slice + off);
+    float4 v = u[0];
+#pragma unroll
+    for (int z = 1; z < kDecodeMaxSplit; ++z)
+      if (z < split) {
+        v.x += u[z].x; v.y += u[z].y; v.z += u[z].z; v.w += u[z].w;
+      }
+    return v;
+  }
   float4 v = *reinterpret_cast<const float4*>(O + off);
   int z = 1;
   for (; z + 3 < split; z += 4) {
