@@ -78,43 +78,75 @@ __device__ __forceinline__ int find_group(const int32_t* tile_off, int G, int mt
 // SwiGLU of the gate / up column pairs into H (bf16; the pre-activations into ab when given);
 // EPI 1: O, each expert output rounded to bf16 (the layer's dtype; the combine adds them in
 // fp32). acc[i][j][4*jj+ii] is row wm*128 + i*32 + 8*jj + 4*(lane>>5) + ii, column (lane & 31)
-// of fragment j.
+// of fragment j. The bf16 tile is staged in LDS (free after the k-loop; rows padded by 16
+// bytes, conflict-free) and stored eight columns per 16-byte access: a lane holds one column
+// of each row it owns, and 2-byte stores kept the texture-address path busy for several
+// percent of a tile.
+template <int COLS>   // columns of the staged tile: LDS row pitch COLS + 8 elements
+__device__ __forceinline__ void store_staged(const uint16_t* stg, uint16_t* out, size_t ld, int row0, int row_end,
+                                             int col0, int ncol) {
+  constexpr int G = COLS / 8;   // 8-column groups per row
+  for (int u = threadIdx.x; u < 256 * G; u += kTileThreads) {
+    const int lr = u / G, cg = (u % G) * 8;
+    const int row = row0 + lr, col = col0 + cg;
+    if (row >= row_end || col >= ncol) continue;
+    const uint16_t* src = stg + lr * (COLS + 8) + cg;
+    uint16_t* dst = out + static_cast<size_t>(row) * ld + col;
+    if (col + 8 <= ncol) {   // ld and col are multiples of 8: 16-byte aligned
+      *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+    } else {
+      for (int e = 0; e < ncol - col; ++e) dst[e] = src[e];
+    }
+  }
+}
+
 template <int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&acc)[kTileTM][kTileTN], int row0,
-                                              int row_end, int n0) {
+                                              int row_end, int n0, TileLds& L) {
   constexpr int WN = 4, TM = kTileTM, TN = kTileTN;
+  constexpr int COLS = EPI == 0 ? BN / 2 : BN, PITCH = COLS + 8;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int Ndim = EPI == 0 ? p.F : p.d;
-  const int col_in = lane & 31;
+  uint16_t* stg = reinterpret_cast<uint16_t*>(&L);
+  static_assert((EPI == 0 ? 2 : 1) * 256 * PITCH * 2 <= sizeof(TileLds), "the staged tiles fit in LDS");
+  wait_lgkmcnt0();
+  tile_barrier();   // every wave is past the k-loop's LDS reads and DMA writes
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
+    for (int r = 0; r < 16; ++r) {
+      const int lr = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (EPI == 0) {   // H, and the gate pre-activations when kept (the up ones follow)
+        const int c = wn * 32 + (lane & 31);
+        stg[lr * PITCH + c] = f32_to_bf16(silu(acc[i][0][r]) * acc[i][1][r]);
+        if (p.ab) stg[256 * PITCH + lr * PITCH + c] = f32_to_bf16(acc[i][0][r]);
+      } else {
 #pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int row = row0 + wm * 128 + i * 32 + 8 * jj + 4 * (lane >> 5) + ii;
-        if (row >= row_end) continue;
-        const int r = 4 * jj + ii;
-        if (EPI == 0) {
-          const int col = n0 + wn * 32 + col_in;
-          if (col < Ndim) {
-            const float h = silu(acc[i][0][r]) * acc[i][1][r];
-            static_cast<uint16_t*>(p.out)[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(h);
-            if (p.ab) {
-              p.ab[static_cast<size_t>(row) * 2 * Ndim + col] = f32_to_bf16(acc[i][0][r]);
-              p.ab[static_cast<size_t>(row) * 2 * Ndim + Ndim + col] = f32_to_bf16(acc[i][1][r]);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wn * 64 + j * 32 + col_in;
-            if (col < Ndim) static_cast<uint16_t*>(p.out)[static_cast<size_t>(row) * Ndim + col] = f32_to_bf16(acc[i][j][r]);
-          }
-        }
+        for (int j = 0; j < TN; ++j) stg[lr * PITCH + wn * 64 + j * 32 + (lane & 31)] = f32_to_bf16(acc[i][j][r]);
       }
     }
+  }
+  wait_lgkmcnt0();
+  tile_barrier();
+  uint16_t* out = static_cast<uint16_t*>(p.out);
+  if (EPI == 0) {
+    store_staged<COLS>(stg, out, p.F, row0, row_end, n0, p.F);
+    if (p.ab) {
+      store_staged<COLS>(stg + 256 * PITCH, p.ab, 2 * static_cast<size_t>(p.F), row0, row_end, n0, p.F);
+      wait_lgkmcnt0();
+      tile_barrier();   // the staged tiles are read: stage the up pre-activations
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          stg[(wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * PITCH + wn * 32 + (lane & 31)] =
+              f32_to_bf16(acc[i][1][r]);
+      wait_lgkmcnt0();
+      tile_barrier();
+      store_staged<COLS>(stg, p.ab + p.F, 2 * static_cast<size_t>(p.F), row0, row_end, n0, p.F);
+    }
+  } else {
+    store_staged<COLS>(stg, out, p.d, row0, row_end, n0, p.d);
   }
 }
 
@@ -208,7 +240,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_bf16(const GemmArgs
     tail_store_partial(p.part, job.slot, acc);
     return;
   }
-  gemm_epilogue<EPI>(p, acc, row0, row_end, n0);
+  gemm_epilogue<EPI>(p, acc, row0, row_end, n0, lds);
 }
 
 // Adds the slices of each split tail tile of the down GEMM (grouped_gemm_bf16<1>) in slice order
