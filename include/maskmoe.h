@@ -184,8 +184,9 @@ size_t maskmoe_layer_workspace_bytes(const maskmoe_layer_desc* desc);
  *  workspace    device, at least maskmoe_layer_workspace_bytes(desc) bytes, 256-byte
  *               aligned; its contents on entry do not matter and are clobbered.
  *  Rounding (bf16): fp32 accumulation; the SwiGLU activation is rounded to bf16 before the
- *  down projection; the combine sums the gate-weighted fp32 expert outputs in fp32 and
- *  rounds once to bf16. f32: no intermediate rounding beyond fp32 arithmetic.
+ *  down projection; each expert's output is rounded to bf16 (the layer's dtype); the combine
+ *  sums the gate-weighted expert outputs in fp32 and rounds once to bf16. f32: no
+ *  intermediate rounding beyond fp32 arithmetic.
  *  Errors: as maskmoe_route, plus E_INVAL for F < 1 or n_shared outside 0..8 or a NULL
  *  shared-weight pointer with n_shared > 0; E_WORKSPACE when the workspace is too small;
  *  E_UNSUPPORTED for bf16 with d % 64 != 0 or F % 64 != 0, or with T*d, T*(K+n_shared)*F or
@@ -321,8 +322,9 @@ int maskmoe_sample_mask(const float* mask_logits, const double* uniforms, int32_
  *
  *  topk_idx      device [T, K] int32, required.   topk_gate device [T, K] float, required.
  *  router_logits device [T, E] float, required: z = W x in fp32.
- *  expert_out    device [T, K, d] float, required, 16-byte aligned: F_{A_t[k]}(x_t) in fp32
- *                (for bf16 layers: from the bf16-rounded SwiGLU activation, as in y).
+ *  expert_out    device [T, K, d] float, required, 16-byte aligned: F_{A_t[k]}(x_t) as the
+ *                combine used it (for bf16 layers: from the bf16-rounded SwiGLU activation,
+ *                and itself rounded to bf16, as in y).
  *  workspace     at least maskmoe_layer_train_workspace_bytes(desc) bytes; for bf16 layers it
  *                keeps what maskmoe_layer_backward reads (the permutation, the SwiGLU
  *                activations and the gate / up pre-activations, bf16).

@@ -189,6 +189,26 @@ __global__ __launch_bounds__(kSelThreads) void route_select_kernel(const RoutePa
   select_pair<EC>(p, zs + threadIdx.x * (E + 1), lo + l * E, q, false);
 }
 
+// Lane exchanges within a 16-lane row (DPP): lane e of the row receives lane (e - R) mod 16.
+template <int R>
+__device__ __forceinline__ int row_ror(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x120 + R, 0xF, 0xF, false);
+}
+
+// Adds to `rank` the number of the row's keys src_key (of experts src_idx, one per lane,
+// rotated by R .. 15 lanes within the row; R = 0 is the lane's own source) that rank above
+// (key, idx): valid (above -inf, not NaN) and larger, or equal with a lower index. Branch-free.
+template <int R>
+__device__ __forceinline__ void rank_from_row(float src_key, int src_idx, float key, int idx, int& rank) {
+  if constexpr (R < 16) {
+    const float kf = R == 0 ? src_key : __int_as_float(row_ror<R == 0 ? 1 : R>(__float_as_int(src_key)));
+    const int f = R == 0 ? src_idx : row_ror<R == 0 ? 1 : R>(src_idx);
+    rank += static_cast<int>(kf > -INFINITY) &
+            (static_cast<int>(kf > key) | (static_cast<int>(kf == key) & static_cast<int>(f < idx)));
+    rank_from_row<R + 1>(src_key, src_idx, key, idx, rank);
+  }
+}
+
 // One (token, layer) pair on one wavefront, lane e holding expert e (E <= 64): z its logit,
 // key its log-domain key (z + offset). Each expert's rank (the number of valid keys larger, or
 // equal with a lower index; -inf and NaN keys are not valid) is its position in the successive
@@ -199,11 +219,12 @@ __device__ __forceinline__ int wave_select_pair(const RouteParams& p, float z, f
   const int lane = threadIdx.x & 63;
   const int E = p.E, K = p.K;
   const bool valid = in && key > -INFINITY;   // false for NaN too
+  // rank over the 64 lanes (lanes past E hold -inf): the lane's own row by DPP rotations, the
+  // other three rows through one lane exchange each
   int rank = 0;
-  for (int f = 0; f < E; ++f) {
-    const float kf = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key), f));
-    if (kf > -INFINITY && (kf > key || (kf == key && f < lane))) ++rank;
-  }
+  rank_from_row<1>(key, lane, key, lane, rank);
+#pragma unroll
+  for (int ro = 16; ro < 64; ro += 16) rank_from_row<0>(__shfl_xor(key, ro, kWave), lane ^ ro, key, lane, rank);
   const uint64_t vmask = __ballot(valid);
   const int n_valid = __popcll(vmask);
   // picks in order: valid experts by rank, then (fewer than K valid keys) the lowest others
@@ -369,23 +390,6 @@ __device__ void route_finalize_wave(const RouteParams& p, const float* logits, i
   }
 }
 
-// Lane exchanges within a 16-lane row (DPP): lane e of the row receives lane (e - R) mod 16.
-template <int R>
-__device__ __forceinline__ int row_ror(int v) {
-  return __builtin_amdgcn_update_dpp(v, v, 0x120 + R, 0xF, 0xF, false);
-}
-
-// Rank of each lane's key among the row's valid keys (larger, or equal with a lower index).
-template <int R>
-__device__ __forceinline__ void row_rank_step(float key, int e, int& rank) {
-  if constexpr (R < 16) {
-    const float kf = __int_as_float(row_ror<R>(__float_as_int(key)));
-    const int f = row_ror<R>(e);
-    rank += static_cast<int>(kf > -INFINITY) & (static_cast<int>(kf > key) | (static_cast<int>(kf == key) & static_cast<int>(f < e)));
-    row_rank_step<R + 1>(key, e, rank);
-  }
-}
-
 // fmaxf over the 16 lanes of the row, in every lane. fmaxf drops NaN operands, so any order
 // of the reduction gives the same value (the largest non-NaN, NaN if all are NaN).
 __device__ __forceinline__ float row_max(float v) {
@@ -422,7 +426,7 @@ __device__ void route_select_rows(const RouteParams& p, const float* logits, int
     key = in ? z + lo[e] : -INFINITY;
     const bool valid = key > -INFINITY;   // false for NaN too
     int rank = 0;
-    row_rank_step<1>(key, e, rank);
+    rank_from_row<1>(key, e, key, e, rank);
     const uint32_t vbits = static_cast<uint32_t>(__ballot(valid) >> rb) & 0xffffu;
     const uint32_t ibits = static_cast<uint32_t>(__ballot(in && !valid) >> rb) & 0xffffu;
     pos = valid ? rank : __popc(vbits) + __popc(ibits & ((1u << e) - 1u));
