@@ -13,11 +13,14 @@
  * Conventions shared by every entry point
  *  - Every pointer marked "device" must point to device memory of the current HIP device;
  *    pointers marked "host" are read synchronously during the call and not kept.
- *  - The caller owns every buffer. The library allocates nothing, keeps no global state and
- *    is reentrant, with one exception: maskmoe_layer_forward_noalloc uses a device array of
- *    the library (one per device) and remembers its address per device. All work is enqueued
- *    asynchronously on `stream` (0 = the null stream); nothing is synchronised. Outputs are
- *    valid once the stream reaches that point.
+ *  - The caller owns every buffer. The library allocates no device memory, keeps no global
+ *    state and is reentrant, with two exceptions: maskmoe_layer_forward_noalloc uses a device
+ *    array of the library (one per device) and remembers its address per device, and
+ *    maskmoe_layer_backward creates one extra stream per device on first use (kept until the
+ *    process ends) for the zero gradients of unchosen experts, ordered with `stream` by
+ *    events created and released per call. All work is enqueued asynchronously on `stream`
+ *    (0 = the null stream); nothing is synchronised. Outputs are valid once the stream
+ *    reaches that point.
  *  - Every argument is validated before anything is enqueued: a non-zero status means that
  *    nothing was written. MASKMOE_E_HIP reports a failed launch (work enqueued before the
  *    failing launch may still run).

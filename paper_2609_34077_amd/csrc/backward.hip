@@ -19,6 +19,8 @@
 // Rounding (bf16 layers): dO = g dy and [da db] are rounded to bf16 before their GEMMs;
 // accumulation is fp32; dX, dW are fp32.
 
+#include <mutex>
+
 #include "common.hpp"
 #include "gemm_tile.hpp"
 #include "kernels.hpp"
@@ -347,6 +349,24 @@ __global__ __launch_bounds__(kBwdThreads) void zero_unused_kernel(const int32_t*
     if (e_ != hipSuccess) return e_; \
   } while (0)
 
+// A second stream per device (default priority, created on first use and kept until the
+// process ends) on which the backward writes the zero gradients of unchosen experts while the
+// weight-gradient GEMMs run on the caller's stream: the fill is bound by HBM writes, the GEMMs
+// by the matrix units, so side by side the fill costs almost nothing. Ordered with the
+// caller's stream by two events created per call.
+constexpr int kMaxDevices = 64;
+hipError_t side_stream(hipStream_t* out) {
+  static std::mutex mu;
+  static hipStream_t streams[kMaxDevices] = {};
+  int dev = 0;
+  MASKMOE_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!streams[dev]) MASKMOE_TRY(hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking));
+  *out = streams[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 BwdLayout backward_layout(int T, int d, int F, int E, int K, int S) {
@@ -373,7 +393,42 @@ static dim3 rows_grid(int mt_max, int n_tiles) {
   return dim3(static_cast<unsigned>(8 * ((static_cast<long>(mt_max) * n_tiles + 7) / 8 + kTailSlotsPerXcd)));
 }
 
+static hipError_t launch_backward_products(const BwdArgs& a, hipStream_t s);
+
 hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
+  const int G = a.E + a.S;
+  const size_t FD = static_cast<size_t>(a.F) * a.d;
+
+  // The zero gradients of the experts no token chose depend on nothing but the routing: they
+  // are written on the side stream from the start, beside everything below.
+  hipStream_t side;
+  MASKMOE_TRY(side_stream(&side));
+  hipEvent_t fork, join;
+  MASKMOE_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+  MASKMOE_TRY(hipEventCreateWithFlags(&join, hipEventDisableTiming));
+  hipError_t fe = hipEventRecord(fork, s);
+  if (fe == hipSuccess) fe = hipStreamWaitEvent(side, fork, 0);
+  if (fe == hipSuccess) {
+    hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, side, a.pb.offsets, a.E, FD,
+                       a.d_w_down, a.d_ws_down);
+    hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, side, a.pb.offsets, a.E, 2 * FD,
+                       a.d_w_gate_up, a.d_ws_gate_up);
+    fe = hipGetLastError();
+  }
+  if (fe == hipSuccess) fe = hipEventRecord(join, side);
+  (void)hipEventDestroy(fork);   // released once recorded and waited on
+  if (fe != hipSuccess) {
+    (void)hipEventDestroy(join);
+    return fe;
+  }
+  const hipError_t e = launch_backward_products(a, s);
+  const hipError_t je = hipStreamWaitEvent(s, join, 0);   // the caller's stream sees the fill done
+  (void)hipEventDestroy(join);
+  return e != hipSuccess ? e : je;
+}
+
+// Everything of the backward but the zero fill, on the caller's stream.
+static hipError_t launch_backward_products(const BwdArgs& a, hipStream_t s) {
   const int G = a.E + a.S, T = a.T, d = a.d, F = a.F, K = a.K;
   const int R = T * (K + a.S);
   const BwdLayout& w = a.lay;
@@ -382,7 +437,6 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   uint16_t* dab = reinterpret_cast<uint16_t*>(ws + w.dab);
   float* dxr = reinterpret_cast<float*>(ws + w.dxr);
   uint16_t* xg = reinterpret_cast<uint16_t*>(ws + w.xg);
-  const size_t FD = static_cast<size_t>(F) * d;
 
   // dO and the gathered tokens, then dgrad of the down projection with the SwiGLU backward:
   // [da db] (bf16)
@@ -434,9 +488,6 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
                      m);
   MASKMOE_TRY(hipGetLastError());
-  hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, s, a.pb.offsets, a.E, FD, a.d_w_down,
-                     a.d_ws_down);
-  MASKMOE_TRY(hipGetLastError());
   // dW_gate_up [2F, d] = [da db]^T x
   m.a = dab; m.lda = 2 * F; m.b = xg; m.ldb = d; m.M = 2 * F; m.N = d;
   m.c = a.d_w_gate_up; m.cs = a.d_ws_gate_up;
@@ -444,9 +495,6 @@ hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
   m.n_tiles = (d + kTileN - 1) / kTileN;
   hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
                      m);
-  MASKMOE_TRY(hipGetLastError());
-  hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, s, a.pb.offsets, a.E, 2 * FD,
-                     a.d_w_gate_up, a.d_ws_gate_up);
   return hipGetLastError();
 }
 
