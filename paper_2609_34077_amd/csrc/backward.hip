@@ -90,23 +90,50 @@ __host__ __device__ constexpr bool nt_tail_split(int mode, int epi, int nk) {
 }
 
 // Stores a finished ROWS tile of fp32 output: rows [row0, row_end), columns from n0.
-__device__ __forceinline__ void nt_store_rows(const NtArgs& p, const f32x16 (&acc)[kTileTM][kTileTN], int row0,
-                                              int row_end, int n0) {
-  constexpr int WN = 4;
+// Staged fp32 tiles: 128 rows x 256 columns at a pitch of 264 floats (the two 32-lane halves of
+// a wavefront, four rows apart, then write different banks).
+constexpr int kStgPitch = 264;
+static_assert(128 * kStgPitch * 4 <= sizeof(TileLds), "a staged half tile fits in LDS");
+
+// Half h (0, 1) of the tile into LDS: acc[2h + ii] of every wave, as staged row
+// wm*64 + ii*32 + (row within the 32-row block). Staged row pr is tile row
+// (pr >> 6) * 128 + 64 h + (pr & 63).
+__device__ __forceinline__ void stage_half(float* stg, const f32x16 (&acc)[kTileTM][kTileTN], int h) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  const int wm = wave / 4, wn = wave % 4;
 #pragma unroll
-  for (int i = 0; i < kTileTM; ++i)
+  for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = row0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if (row >= row_end) continue;
+    for (int r = 0; r < 16; ++r)
 #pragma unroll
-      for (int j = 0; j < kTileTN; ++j) {
-        const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (col < p.N) static_cast<float*>(p.c)[static_cast<size_t>(row) * p.ldc + col] = acc[i][j][r];
-      }
+      for (int j = 0; j < kTileTN; ++j)
+        stg[(wm * 64 + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * kStgPitch + wn * 64 + j * 32 +
+            (lane & 31)] = (h == 0 ? acc[ii][j][r] : acc[2 + ii][j][r]);
+}
+
+// The fp32 tile (rows row0.., columns n0..) into out (row stride ld), through LDS in two halves
+// so that it leaves in 16-byte stores: one 4-byte store per value and lane kept the
+// texture-address path busy for ~10 us at the end of every tile. ncol % 4 == 0.
+__device__ __forceinline__ void nt_store_staged(const f32x16 (&acc)[kTileTM][kTileTN], float* out, size_t ld, int row0,
+                                                int row_end, int n0, int ncol, TileLds& L) {
+  float* stg = reinterpret_cast<float*>(&L);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    wait_lgkmcnt0();
+    tile_barrier();   // the k-loop's (or the previous half's) LDS reads are done
+    stage_half(stg, acc, h);
+    wait_lgkmcnt0();
+    tile_barrier();
+#pragma unroll 4
+    for (int q = 0; q < 16; ++q) {   // 8192 float4 per half: 64 per staged row
+      const int u = static_cast<int>(threadIdx.x) + kTileThreads * q;
+      const int pr = u >> 6, c = (u & 63) * 4;
+      const int row = row0 + (pr >> 6) * 128 + 64 * h + (pr & 63), col = n0 + c;
+      if (row < row_end && col < ncol)
+        *reinterpret_cast<float4*>(out + static_cast<size_t>(row) * ld + col) =
+            *reinterpret_cast<const float4*>(&stg[pr * kStgPitch + c]);
     }
+  }
 }
 
 enum { kNtRows = 0, kNtKSplit = 1 };
@@ -122,7 +149,7 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
   constexpr int TM = kTileTM, TN = kTileTN, WN = 4;
   __shared__ TileLds lds;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  const int wn = wave % WN;
   int mt, nt, g, row0, row_end, nk;
   TileJob job{0, 0, 1, -1};
   TileOps ops{};
@@ -187,7 +214,7 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
   gemm_tile_mainloop<false, MODE == kNtKSplit, true>(ops, nk, bfrag, acc, lds, nullptr, &akm, &bkm);
   if (MODE == kNtRows && EPI == kEpiF32) {
     if (job.s > 1) tail_store_partial(p.part, job.slot, acc);   // a slice of a split tail tile
-    else nt_store_rows(p, acc, row0, row_end, nt * kTileN);
+    else nt_store_staged(acc, static_cast<float*>(p.c), p.ldc, row0, row_end, nt * kTileN, p.N, lds);
     return;
   }
 
@@ -197,88 +224,59 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
     // v = dh; da, db (bf16) into [rows, 2N]. The tile goes through LDS (free after the k-loop)
     // in two halves of 128 rows x 256 columns, so that each thread then reads a, b and writes
     // da, db eight columns at a time: 16-byte accesses instead of one 2-byte access per value
-    // and operand, which kept the texture-address path busy for a fifth of the kernel.
+    // and operand, which kept the texture-address path busy for a fifth of the kernel. A half's
+    // a and b are loaded before it is staged, all in flight together. N % 64 == 0 (checked by
+    // the host), so a group of eight columns is either whole or past N.
     float* stg = reinterpret_cast<float*>(&lds);
     uint16_t* o = static_cast<uint16_t*>(p.c);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
+      u32x4 a8[8], b8[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {   // 4096 groups of 8 columns: 32 per staged row
+        const int u = tid + kTileThreads * q;
+        const int pr = u >> 5, col = n0 + (u & 31) * 8;
+        const int row = row0 + (pr >> 6) * 128 + 64 * h + (pr & 63);
+        if (row < row_end && col < p.N) {
+          const uint16_t* src = p.ab + static_cast<size_t>(row) * 2 * p.N + col;
+          a8[q] = *reinterpret_cast<const u32x4*>(src);
+          b8[q] = *reinterpret_cast<const u32x4*>(src + p.N);
+        }
+      }
       wait_lgkmcnt0();
       tile_barrier();   // the k-loop's (or the previous half's) LDS reads are done
-#pragma unroll
-      for (int ii = 0; ii < 2; ++ii)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            stg[(wm * 64 + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * 256 + wn * 64 + j * 32 + (lane & 31)] =
-                acc[2 * h + ii][j][r];
+      stage_half(stg, acc, h);
       wait_lgkmcnt0();
       tile_barrier();
-#pragma unroll 2
+#pragma unroll
       for (int q = 0; q < 8; ++q) {
-        const int u = tid + kTileThreads * q;   // 4096 groups of 8 columns: 32 per staged row
-        const int prow = u >> 5, cg = (u & 31) * 8;
-        const int row = row0 + (prow >> 6) * 128 + 64 * h + (prow & 63);
-        const int col = n0 + cg;
+        const int u = tid + kTileThreads * q;
+        const int pr = u >> 5, cg = (u & 31) * 8, col = n0 + cg;
+        const int row = row0 + (pr >> 6) * 128 + 64 * h + (pr & 63);
         if (row >= row_end || col >= p.N) continue;
         float v[8];
-        *reinterpret_cast<float4*>(&v[0]) = *reinterpret_cast<const float4*>(&stg[prow * 256 + cg]);
-        *reinterpret_cast<float4*>(&v[4]) = *reinterpret_cast<const float4*>(&stg[prow * 256 + cg + 4]);
-        const size_t base = static_cast<size_t>(row) * 2 * p.N;
-        const int nv = min(8, p.N - col);
-        uint16_t a8[8], b8[8], da8[8], db8[8];
-        if (nv == 8) {   // N % 4 == 0: 16-byte aligned
-          *reinterpret_cast<u32x4*>(a8) = *reinterpret_cast<const u32x4*>(p.ab + base + col);
-          *reinterpret_cast<u32x4*>(b8) = *reinterpret_cast<const u32x4*>(p.ab + base + p.N + col);
-        } else {
-          for (int e = 0; e < nv; ++e) {
-            a8[e] = p.ab[base + col + e];
-            b8[e] = p.ab[base + p.N + col + e];
-          }
-        }
+        *reinterpret_cast<float4*>(&v[0]) = *reinterpret_cast<const float4*>(&stg[pr * kStgPitch + cg]);
+        *reinterpret_cast<float4*>(&v[4]) = *reinterpret_cast<const float4*>(&stg[pr * kStgPitch + cg + 4]);
+        const uint16_t* av8 = reinterpret_cast<const uint16_t*>(&a8[q]);
+        const uint16_t* bv8 = reinterpret_cast<const uint16_t*>(&b8[q]);
+        uint16_t da8[8], db8[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float av = bf16_to_f32(a8[e]), bv = bf16_to_f32(b8[e]);
+          const float av = bf16_to_f32(av8[e]), bv = bf16_to_f32(bv8[e]);
           const float s = 1.0f / (1.0f + __expf(-av));
           da8[e] = f32_to_bf16(v[e] * bv * (s * (1.0f + av * (1.0f - s))));
           db8[e] = f32_to_bf16(v[e] * av * s);
         }
-        if (nv == 8) {
-          *reinterpret_cast<u32x4*>(o + base + col) = *reinterpret_cast<const u32x4*>(da8);
-          *reinterpret_cast<u32x4*>(o + base + p.N + col) = *reinterpret_cast<const u32x4*>(db8);
-        } else {
-          for (int e = 0; e < nv; ++e) {
-            o[base + col + e] = da8[e];
-            o[base + p.N + col + e] = db8[e];
-          }
-        }
+        uint16_t* dst = o + static_cast<size_t>(row) * 2 * p.N + col;
+        *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(da8);
+        *reinterpret_cast<u32x4*>(dst + p.N) = *reinterpret_cast<const u32x4*>(db8);
       }
     }
     return;
   }
-  float* cf = nullptr;
-  if (MODE == kNtKSplit)
-    cf = g < p.E ? static_cast<float*>(p.c) + static_cast<size_t>(g) * p.M * p.N
-                 : static_cast<float*>(p.cs) + static_cast<size_t>(g - p.E) * p.M * p.N;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = row0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if (row >= row_end) continue;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (col >= p.N) continue;
-        const float v = acc[i][j][r];
-        if (MODE == kNtRows) {
-          static_cast<float*>(p.c)[static_cast<size_t>(row) * p.ldc + col] = v;
-        } else {
-          cf[static_cast<size_t>(row) * p.N + col] = v;
-        }
-      }
-    }
-  }
+  float* cf = g < p.E ? static_cast<float*>(p.c) + static_cast<size_t>(g) * p.M * p.N
+                      : static_cast<float*>(p.cs) + static_cast<size_t>(g - p.E) * p.M * p.N;
+  nt_store_staged(acc, cf, p.N, row0, row_end, n0, p.N, lds);
 }
 
 // Adds the slices of each split tail tile of the ROWS fp32 product in slice order and stores
@@ -351,9 +349,8 @@ __global__ __launch_bounds__(kBwdThreads) void zero_unused_kernel(const int32_t*
 
 // A second stream per device (default priority, created on first use and kept until the
 // process ends) on which the backward writes the zero gradients of unchosen experts while the
-// weight-gradient GEMMs run on the caller's stream: the fill is bound by HBM writes, the GEMMs
-// by the matrix units, so side by side the fill costs almost nothing. Ordered with the
-// caller's stream by two events created per call.
+// GEMMs run on the caller's stream. Ordered with the caller's stream by two events created per
+// call.
 constexpr int kMaxDevices = 64;
 hipError_t side_stream(hipStream_t* out) {
   static std::mutex mu;
@@ -393,44 +390,14 @@ static dim3 rows_grid(int mt_max, int n_tiles) {
   return dim3(static_cast<unsigned>(8 * ((static_cast<long>(mt_max) * n_tiles + 7) / 8 + kTailSlotsPerXcd)));
 }
 
-static hipError_t launch_backward_products(const BwdArgs& a, hipStream_t s);
-
+// The zero gradients of the experts no token chose depend on nothing but the routing; they are
+// written on a second stream beside the GEMMs, forked after the row gathers: the fill is bound
+// by HBM writes like the gathers, and next to them it slowed both (gathers 0.08 -> 0.66 ms on
+// the Mixtral fine-tuning layer).
 hipError_t launch_layer_backward(const BwdArgs& a, hipStream_t s) {
-  const int G = a.E + a.S;
-  const size_t FD = static_cast<size_t>(a.F) * a.d;
-
-  // The zero gradients of the experts no token chose depend on nothing but the routing: they
-  // are written on the side stream from the start, beside everything below.
-  hipStream_t side;
-  MASKMOE_TRY(side_stream(&side));
-  hipEvent_t fork, join;
-  MASKMOE_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
-  MASKMOE_TRY(hipEventCreateWithFlags(&join, hipEventDisableTiming));
-  hipError_t fe = hipEventRecord(fork, s);
-  if (fe == hipSuccess) fe = hipStreamWaitEvent(side, fork, 0);
-  if (fe == hipSuccess) {
-    hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, side, a.pb.offsets, a.E, FD,
-                       a.d_w_down, a.d_ws_down);
-    hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, side, a.pb.offsets, a.E, 2 * FD,
-                       a.d_w_gate_up, a.d_ws_gate_up);
-    fe = hipGetLastError();
-  }
-  if (fe == hipSuccess) fe = hipEventRecord(join, side);
-  (void)hipEventDestroy(fork);   // released once recorded and waited on
-  if (fe != hipSuccess) {
-    (void)hipEventDestroy(join);
-    return fe;
-  }
-  const hipError_t e = launch_backward_products(a, s);
-  const hipError_t je = hipStreamWaitEvent(s, join, 0);   // the caller's stream sees the fill done
-  (void)hipEventDestroy(join);
-  return e != hipSuccess ? e : je;
-}
-
-// Everything of the backward but the zero fill, on the caller's stream.
-static hipError_t launch_backward_products(const BwdArgs& a, hipStream_t s) {
   const int G = a.E + a.S, T = a.T, d = a.d, F = a.F, K = a.K;
   const int R = T * (K + a.S);
+  const size_t FD = static_cast<size_t>(F) * d;
   const BwdLayout& w = a.lay;
   char* ws = static_cast<char*>(a.workspace);
   uint16_t* dout = reinterpret_cast<uint16_t*>(ws + w.dout);
@@ -438,13 +405,39 @@ static hipError_t launch_backward_products(const BwdArgs& a, hipStream_t s) {
   float* dxr = reinterpret_cast<float*>(ws + w.dxr);
   uint16_t* xg = reinterpret_cast<uint16_t*>(ws + w.xg);
 
-  // dO and the gathered tokens, then dgrad of the down projection with the SwiGLU backward:
-  // [da db] (bf16)
+  hipStream_t side;
+  MASKMOE_TRY(side_stream(&side));
+  hipEvent_t fork, join;
+  MASKMOE_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+  hipError_t e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    (void)hipEventDestroy(fork);
+    return e;
+  }
+  bool forked = false;
+  auto fill = [&]() {   // fork the zero fill off the caller's stream
+    if (e == hipSuccess) e = hipEventRecord(fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
+    if (e != hipSuccess) return;
+    hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, side, a.pb.offsets, a.E, FD,
+                       a.d_w_down, a.d_ws_down);
+    hipLaunchKernelGGL(zero_unused_kernel, dim3(G, 512), dim3(kBwdThreads), 0, side, a.pb.offsets, a.E, 2 * FD,
+                       a.d_w_gate_up, a.d_ws_gate_up);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipEventRecord(join, side);
+    forked = e == hipSuccess;
+  };
+  auto check = [&]() {
+    if (e == hipSuccess) e = hipGetLastError();
+  };
+
+  // dO and the gathered tokens
   hipLaunchKernelGGL(build_dout_kernel, dim3(R), dim3(kBwdThreads), 0, s, a.dy, a.gate, a.pb.perm, a.pb.row_tok, T * K,
                      d, dout);
-  MASKMOE_TRY(hipGetLastError());
   hipLaunchKernelGGL(gather_rows_kernel, dim3(R), dim3(kBwdThreads), 0, s, a.x, a.pb.row_tok, d, xg);
-  MASKMOE_TRY(hipGetLastError());
+  check();
+  fill();
+  // dgrad of the down projection with the SwiGLU backward: [da db] (bf16)
   NtArgs n{};
   n.offsets = a.pb.offsets;
   n.tile_off = a.pb.tile_off;
@@ -457,45 +450,56 @@ static hipError_t launch_backward_products(const BwdArgs& a, hipStream_t s) {
   n.n_tiles = (F + kTileN - 1) / kTileN;
   n.cu_xcd = device_cus_per_xcd();
   n.part = reinterpret_cast<float*>(ws + w.part);
-  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiSwigluBwd>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads), 0,
-                     s, n);
-  MASKMOE_TRY(hipGetLastError());
-  // dgrad of gate/up: dX rows = [da db] W_gate_up, then the token sums
-  n.a = dab; n.lda = 2 * F;
-  n.b = a.w_gate_up; n.bs = a.ws_gate_up; n.N = d; n.K = 2 * F; n.ldb = d;   // W_gate_up [2F, d]: K-major
-  n.ab = nullptr;
-  n.c = dxr; n.ldc = d;
-  n.n_tiles = (d + kTileN - 1) / kTileN;
-  hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiF32>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads), 0, s, n);
-  MASKMOE_TRY(hipGetLastError());
-  if (nt_tail_split(kNtRows, kEpiF32, n.K / kTileK)) {
-    hipLaunchKernelGGL(nt_tail_fixup, dim3(8 * kTailSlotsPerXcd * kTailFixParts), dim3(kTileThreads), 0, s, n);
-    MASKMOE_TRY(hipGetLastError());
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiSwigluBwd>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads),
+                       0, s, n);
+    check();
   }
-  hipLaunchKernelGGL(dx_combine_kernel, dim3(T), dim3(kBwdThreads), 0, s, dxr, a.pb.inv, T, K, a.S, d, a.d_x);
-  MASKMOE_TRY(hipGetLastError());
+  // dgrad of gate/up: dX rows = [da db] W_gate_up, then the token sums
+  if (e == hipSuccess) {
+    n.a = dab; n.lda = 2 * F;
+    n.b = a.w_gate_up; n.bs = a.ws_gate_up; n.N = d; n.K = 2 * F; n.ldb = d;   // W_gate_up [2F, d]: K-major
+    n.ab = nullptr;
+    n.c = dxr; n.ldc = d;
+    n.n_tiles = (d + kTileN - 1) / kTileN;
+    hipLaunchKernelGGL((gemm_nt_kernel<kNtRows, kEpiF32>), rows_grid(n.mt_max, n.n_tiles), dim3(kTileThreads), 0, s,
+                       n);
+    if (nt_tail_split(kNtRows, kEpiF32, n.K / kTileK))
+      hipLaunchKernelGGL(nt_tail_fixup, dim3(8 * kTailSlotsPerXcd * kTailFixParts), dim3(kTileThreads), 0, s, n);
+    hipLaunchKernelGGL(dx_combine_kernel, dim3(T), dim3(kBwdThreads), 0, s, dxr, a.pb.inv, T, K, a.S, d, a.d_x);
+    check();
+  }
   // weight gradients over each expert's own rows
   NtArgs m{};
   m.offsets = a.pb.offsets;
   m.active = a.pb.active;
   m.n_active = a.pb.n_active;
   m.G = G; m.E = a.E;
-  // dW_down [d, F] = dO^T h
-  m.a = dout; m.lda = d; m.b = a.h; m.ldb = F; m.M = d; m.N = F;
-  m.c = a.d_w_down; m.cs = a.d_ws_down;
-  m.mt_max = (d + kTileM - 1) / kTileM;
-  m.n_tiles = (F + kTileN - 1) / kTileN;
-  hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
-                     m);
-  MASKMOE_TRY(hipGetLastError());
-  // dW_gate_up [2F, d] = [da db]^T x
-  m.a = dab; m.lda = 2 * F; m.b = xg; m.ldb = d; m.M = 2 * F; m.N = d;
-  m.c = a.d_w_gate_up; m.cs = a.d_ws_gate_up;
-  m.mt_max = (2 * F + kTileM - 1) / kTileM;
-  m.n_tiles = (d + kTileN - 1) / kTileN;
-  hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
-                     m);
-  return hipGetLastError();
+  if (e == hipSuccess) {   // dW_down [d, F] = dO^T h
+    m.a = dout; m.lda = d; m.b = a.h; m.ldb = F; m.M = d; m.N = F;
+    m.c = a.d_w_down; m.cs = a.d_ws_down;
+    m.mt_max = (d + kTileM - 1) / kTileM;
+    m.n_tiles = (F + kTileN - 1) / kTileN;
+    hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
+                       m);
+    check();
+  }
+  if (e == hipSuccess) {   // dW_gate_up [2F, d] = [da db]^T x
+    m.a = dab; m.lda = 2 * F; m.b = xg; m.ldb = d; m.M = 2 * F; m.N = d;
+    m.c = a.d_w_gate_up; m.cs = a.d_ws_gate_up;
+    m.mt_max = (2 * F + kTileM - 1) / kTileM;
+    m.n_tiles = (d + kTileN - 1) / kTileN;
+    hipLaunchKernelGGL((gemm_nt_kernel<kNtKSplit, kEpiF32>), dim3(G * m.mt_max * m.n_tiles), dim3(kTileThreads), 0, s,
+                       m);
+    check();
+  }
+  if (forked) {   // the caller's stream sees the fill done
+    const hipError_t je = hipStreamWaitEvent(s, join, 0);
+    if (e == hipSuccess) e = je;
+  }
+  (void)hipEventDestroy(fork);   // released once their waits are done
+  (void)hipEventDestroy(join);
+  return e;
 }
 
 }  // namespace maskmoe
