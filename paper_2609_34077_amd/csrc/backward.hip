@@ -33,7 +33,7 @@ constexpr int kBwdThreads = 256;
 __device__ __forceinline__ uint32_t scale_pair(uint32_t v, float w) {
   const float lo = bf16_to_f32(static_cast<uint16_t>(v & 0xffffu)) * w;
   const float hi = bf16_to_f32(static_cast<uint16_t>(v >> 16)) * w;
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  return f32x2_to_bf16x2(lo, hi);
 }
 
 // dO[r, :] = bf16(w_r dy[row_tok[r], :]): w_r the gate of the (token, slot) entry at routed row
@@ -263,7 +263,7 @@ __global__ __launch_bounds__(kTileThreads) void gemm_nt_kernel(const NtArgs p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float av = bf16_to_f32(av8[e]), bv = bf16_to_f32(bv8[e]);
-          const float s = 1.0f / (1.0f + __expf(-av));
+          const float s = sigmoid(av);
           da8[e] = f32_to_bf16(v[e] * bv * (s * (1.0f + av * (1.0f - s))));
           db8[e] = f32_to_bf16(v[e] * av * s);
         }

@@ -17,12 +17,18 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// float -> bf16 bits, round to nearest even (NaN stays NaN).
+// float -> bf16 bits, round to nearest even; a NaN keeps its sign and upper payload bits and
+// becomes quiet. gfx950 converts in one instruction (v_cvt_pk_bf16_f32, two values at a
+// time); it matches the bit-level rounding (add 0x7fff plus the kept lsb, NaN -> bits | 0x40)
+// on all 2^32 inputs, and takes no branch for the NaN case.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
 // D = A(16x32) * B(32x16) + C on bf16 operands, fp32 accumulate.
@@ -43,7 +49,11 @@ __device__ __forceinline__ f32x16 mfma_32x32x16(const u32x4& a, const u32x4& b, 
                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float silu(float u) { return u / (1.0f + __expf(-u)); }
+// silu(u) = u sigmoid(u); the hardware reciprocal (1 ulp) instead of an IEEE division: the
+// result is rounded to bf16 next, and the division's scale-and-fix-up sequence was most of
+// the gate/up epilogue's arithmetic.
+__device__ __forceinline__ float sigmoid(float u) { return __builtin_amdgcn_rcpf(1.0f + __expf(-u)); }
+__device__ __forceinline__ float silu(float u) { return u * sigmoid(u); }
 
 __device__ __forceinline__ int wave_min_int(int v) {
 #pragma unroll

@@ -111,20 +111,26 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&
   static_assert((EPI == 0 ? 2 : 1) * 256 * PITCH * 2 <= sizeof(TileLds), "the staged tiles fit in LDS");
   wait_lgkmcnt0();
   tile_barrier();   // every wave is past the k-loop's LDS reads and DMA writes
+  // this lane's rows of the tile: row_of(i, r)
+  auto row_of = [&](int i, int r) { return wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); };
+  if (EPI == 0) {   // H, and the gate pre-activations when kept (the up ones follow)
+    const int c = wn * 32 + (lane & 31);
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int lr = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if (EPI == 0) {   // H, and the gate pre-activations when kept (the up ones follow)
-        const int c = wn * 32 + (lane & 31);
-        stg[lr * PITCH + c] = f32_to_bf16(silu(acc[i][0][r]) * acc[i][1][r]);
-        if (p.ab) stg[256 * PITCH + lr * PITCH + c] = f32_to_bf16(acc[i][0][r]);
-      } else {
+      for (int r = 0; r < 16; ++r) stg[row_of(i, r) * PITCH + c] = f32_to_bf16(silu(acc[i][0][r]) * acc[i][1][r]);
+    if (p.ab)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) stg[lr * PITCH + wn * 64 + j * 32 + (lane & 31)] = f32_to_bf16(acc[i][j][r]);
-      }
-    }
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) stg[256 * PITCH + row_of(i, r) * PITCH + c] = f32_to_bf16(acc[i][0][r]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) stg[row_of(i, r) * PITCH + wn * 64 + j * 32 + (lane & 31)] = f32_to_bf16(acc[i][j][r]);
   }
   wait_lgkmcnt0();
   tile_barrier();
@@ -138,9 +144,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, const f32x16 (&
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          stg[(wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * PITCH + wn * 32 + (lane & 31)] =
-              f32_to_bf16(acc[i][1][r]);
+        for (int r = 0; r < 16; ++r) stg[row_of(i, r) * PITCH + wn * 32 + (lane & 31)] = f32_to_bf16(acc[i][1][r]);
       wait_lgkmcnt0();
       tile_barrier();
       store_staged<COLS>(stg, p.ab + p.F, 2 * static_cast<size_t>(p.F), row0, row_end, n0, p.F);
@@ -377,8 +381,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ O
         s.x += vs[sh].x; s.y += vs[sh].y; s.z += vs[sh].z; s.w += vs[sh].w;
       }
     uint2 packed;
-    packed.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
-    packed.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
+    packed.x = f32x2_to_bf16x2(s.x, s.y);
+    packed.y = f32x2_to_bf16x2(s.z, s.w);
     *reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d + c) = packed;
   } else if (BF16) {  // d % 4 == 0
     const size_t slice = static_cast<size_t>(T) * (K + n_shared) * d;
@@ -398,8 +402,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ O
       s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
     }
     uint2 packed;
-    packed.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
-    packed.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
+    packed.x = f32x2_to_bf16x2(s.x, s.y);
+    packed.y = f32x2_to_bf16x2(s.z, s.w);
     *reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d + c) = packed;
   } else {
     for (int c = cb * kCombineCols + threadIdx.x; c < d && c < (cb + 1) * kCombineCols; c += 256) {
@@ -661,10 +665,8 @@ __device__ __forceinline__ uint2 swiglu_from_partials(const float* src, size_t s
     }
   }
   uint2 packed;
-  packed.x = static_cast<uint32_t>(f32_to_bf16(silu(gs.x) * us.x)) |
-             (static_cast<uint32_t>(f32_to_bf16(silu(gs.y) * us.y)) << 16);
-  packed.y = static_cast<uint32_t>(f32_to_bf16(silu(gs.z) * us.z)) |
-             (static_cast<uint32_t>(f32_to_bf16(silu(gs.w) * us.w)) << 16);
+  packed.x = f32x2_to_bf16x2(silu(gs.x) * us.x, silu(gs.y) * us.y);
+  packed.y = f32x2_to_bf16x2(silu(gs.z) * us.z, silu(gs.w) * us.w);
   return packed;
 }
 
