@@ -330,8 +330,11 @@ def run_layer(args, base=None):
     st = layer_setup(args, base)
     cfg = st["cfg"]
     work = layer_work(st)
-    steps = args.steps if args.steps is not None else (1000 if args.workload == "decode" else 20)
-    warmup = args.warmup if args.warmup is not None else (300 if args.workload == "decode" else 3)
+    # Defaults: 1000 timed steps after 300 warmup steps at decode shapes, 200 after 20 for the
+    # many-token layers (measured, 20 steps after 3 warmup steps gave a DeepSeek-shaped step
+    # ~10% longer than 200 after 20, and the Mixtral fine-tuning step ~0.5% longer).
+    steps = args.steps if args.steps is not None else (1000 if args.workload == "decode" else 200)
+    warmup = args.warmup if args.warmup is not None else (300 if args.workload == "decode" else 20)
     for i in range(warmup):
         layer_step(st, i)
     nev = L.NUM_STAGES + 1
