@@ -31,6 +31,14 @@ namespace {
 
 constexpr int kMaxK = 16;
 constexpr int kMaxModeParams = 512;
+// Selection by one thread per (token, layer) pair up to this many experts, by one wavefront
+// (a lane per expert) above it when E <= 64. The softmax normaliser over all E experts (g = p)
+// is summed in expert order for E <= kSelThreadE and E > 64; for kSelThreadE < E <= 64 in the
+// order of a 64-lane butterfly: lane e with lane e ^ 32, then ^ 16, ..., ^ 1, experts past E
+// counting as 0. The wavefront selection sums that way in six steps (a serial sum over the
+// lanes took ~5 us of the 4096-token selection kernel), the per-thread selection replays the
+// same tree, so every path gives the same bits.
+constexpr int kSelThreadE = 16;
 // The LDS-tiled router GEMM (route_gemm_kernel) pays off once a launch has many tokens and
 // enough router outputs to fill its 256-wide tile.
 constexpr int kRouteGemmMinT = 1024;
@@ -102,7 +110,19 @@ __device__ __forceinline__ void select_pair(const RouteParams& p, const float* z
   if (p.gate_mode == 0) {  // g = p_i: full softmax over all E experts
     zref = z[0];
     for (int e = 1; e < E; ++e) zref = fmaxf(zref, z[e]);
-    for (int e = 0; e < E; ++e) norm += expf(z[e] - zref);
+    if (E > kSelThreadE && E <= kWave) {   // the butterfly's tree (kSelThreadE)
+      float a[kWave / 2];
+#pragma unroll
+      for (int i = 0; i < kWave / 2; ++i)
+        a[i] = (i < E ? expf(z[i] - zref) : 0.0f) + (i + kWave / 2 < E ? expf(z[i + kWave / 2] - zref) : 0.0f);
+#pragma unroll
+      for (int w = kWave / 4; w >= 1; w >>= 1)
+#pragma unroll
+        for (int i = 0; i < w; ++i) a[i] = a[i] + a[i + w];
+      norm = a[0];
+    } else {
+      for (int e = 0; e < E; ++e) norm += expf(z[e] - zref);
+    }
   } else {  // g = p_i / sum_{j in A} p_j
     zref = selz[0];
 #pragma unroll
@@ -154,7 +174,6 @@ constexpr int kSelThreads = 256;
 
 // E <= kSelThreadE: one thread per pair, the block's logits staged in LDS (odd row stride) so
 // the per-pair selection reads them without bank conflicts.
-constexpr int kSelThreadE = 16;
 template <int EC>
 __global__ __launch_bounds__(kSelThreads) void route_select_kernel(const RouteParams p) {
   constexpr int EMAX = EC ? EC : kSelThreadE;
@@ -252,11 +271,20 @@ __device__ __forceinline__ int wave_select_pair(const RouteParams& p, float z, f
     nxt = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(key), e));
   }
   float zref, norm = 0.0f;
-  if (p.gate_mode == 0) {   // softmax over all E, normaliser in expert order
-    zref = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(z), 0));
-    for (int e = 1; e < E; ++e) zref = fmaxf(zref, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(z), e)));
-    const float ex = in ? expf(z - zref) : 0.0f;
-    for (int e = 0; e < E; ++e) norm += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), e));
+  if (p.gate_mode == 0) {   // softmax over all E
+    // the largest logit: fmaxf drops NaN operands (lanes past E hold NaN), so the reduction
+    // order does not change the value (the largest non-NaN logit, NaN if all are NaN)
+    zref = in ? z : __builtin_nanf("");
+#pragma unroll
+    for (int m = kWave / 2; m >= 1; m >>= 1) zref = fmaxf(zref, __shfl_xor(zref, m, kWave));
+    float ex = in ? expf(z - zref) : 0.0f;
+    if (E > kSelThreadE) {   // the butterfly's tree (kSelThreadE)
+#pragma unroll
+      for (int m = kWave / 2; m >= 1; m >>= 1) ex += __shfl_xor(ex, m, kWave);
+      norm = ex;
+    } else {   // expert order, as the per-thread selection for E <= kSelThreadE
+      for (int e = 0; e < E; ++e) norm += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), e));
+    }
   } else {   // renormalised over the picks, in pick order
     zref = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_selz), 0));
     for (int j = 1; j < K; ++j) zref = fmaxf(zref, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_selz), j)));
