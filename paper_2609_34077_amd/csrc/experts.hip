@@ -337,11 +337,13 @@ __device__ __forceinline__ float4 sum_slices(const float* O, int split, size_t s
 // inv[t K + k] (the selected expert's output before gating). One workgroup of 256 threads
 // per (token, block of kCombineCols columns), token-major in a 1-D grid.
 constexpr int kCombineCols = 1024;
+constexpr int kCombineColsOB = 2048;   // the bf16-O instances with K known: 8 columns per thread
 constexpr int kMaxSharedCombine = 8;   // the API's limit on shared experts
 
 // KC: K known at compile time with one slice (the grouped path): every row's index, gate and
 // O values are loaded before any is added (same additions, same order). OB: O holds bf16
-// values (one slice, no expert outputs requested); the sums are still formed in fp32.
+// values (one slice); the sums are still formed in fp32. KC and OB together: a thread takes
+// eight columns (16-byte loads of every row, grid by kCombineColsOB).
 template <bool BF16, int KC = 0, bool OB = false>
 __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ Ov,
                                                        const int32_t* __restrict__ inv,
@@ -349,6 +351,56 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ O
                                                        int n_shared, int d, void* y, int split,
                                                        float* __restrict__ eo) {
   const float* O = static_cast<const float*>(Ov);
+  if (BF16 && KC > 0 && OB) {   // eight columns per thread: 16-byte loads of every bf16 row; d % 8 == 0
+    constexpr int KA = KC > 0 ? KC : 1;
+    const int nb8 = (d + kCombineColsOB - 1) / kCombineColsOB;
+    const int t = blockIdx.x / nb8, c = (blockIdx.x % nb8) * kCombineColsOB + threadIdx.x * 8;
+    if (c >= d) return;
+    int row[KA];
+    float gk[KA];
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      row[k] = inv[t * KC + k];
+      gk[k] = gate[t * KC + k];
+    }
+    const uint16_t* O16 = static_cast<const uint16_t*>(Ov);
+    u32x4 v[KA], vs[kMaxSharedCombine];
+#pragma unroll
+    for (int k = 0; k < KC; ++k) v[k] = *reinterpret_cast<const u32x4*>(O16 + static_cast<size_t>(row[k]) * d + c);
+#pragma unroll
+    for (int sh = 0; sh < kMaxSharedCombine; ++sh)
+      if (sh < n_shared)
+        vs[sh] = *reinterpret_cast<const u32x4*>(
+            O16 + (static_cast<size_t>(T) * KC + static_cast<size_t>(sh) * T + t) * d + c);
+    // element e of a 16-byte piece: bf16 number e (little-endian halves of the four words)
+    auto el = [](const u32x4& u, int e) {
+      const uint32_t w = u[e >> 1];
+      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    };
+    float s[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = 0.0f;
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += gk[k] * el(v[k], e);
+      if (eo) {
+        float* dst = eo + (static_cast<size_t>(t) * KC + k) * d + c;
+        *reinterpret_cast<float4*>(dst) = make_float4(el(v[k], 0), el(v[k], 1), el(v[k], 2), el(v[k], 3));
+        *reinterpret_cast<float4*>(dst + 4) = make_float4(el(v[k], 4), el(v[k], 5), el(v[k], 6), el(v[k], 7));
+      }
+    }
+#pragma unroll
+    for (int sh = 0; sh < kMaxSharedCombine; ++sh)
+      if (sh < n_shared)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] += el(vs[sh], e);
+    u32x4 packed;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) packed[q] = f32x2_to_bf16x2(s[2 * q], s[2 * q + 1]);
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d + c) = packed;
+    return;
+  }
   const int nb = (d + kCombineCols - 1) / kCombineCols;
   const int t = blockIdx.x / nb, cb = blockIdx.x % nb;
   if (BF16 && KC > 0) {  // d % 4 == 0, split == 1, K == KC, n_shared <= kMaxSharedCombine
@@ -419,7 +471,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ O
   }
 }
 
-static dim3 combine_grid(int T, int d) { return dim3(T * ((d + kCombineCols - 1) / kCombineCols)); }
+static dim3 combine_grid(int T, int d, int cols = kCombineCols) { return dim3(T * ((d + cols - 1) / cols)); }
 
 // ------------------------------------------------------------------ bf16 decode kernels
 //
@@ -890,12 +942,13 @@ hipError_t launch_experts_bf16(const ExpertArgs& a, const PermBuffers& pb, uint1
   }
   record_mark(marks, 1, stream);
 
-  const dim3 cgrid = combine_grid(a.T, a.d), cblk(256);   // O holds bf16 expert outputs
+  // O holds bf16 expert outputs; with K known, eight columns per thread
+  const dim3 cgrid = combine_grid(a.T, a.d), cgrid8 = combine_grid(a.T, a.d, kCombineColsOB), cblk(256);
   if (a.K == 2)
-    hipLaunchKernelGGL((combine_kernel<true, 2, true>), cgrid, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
+    hipLaunchKernelGGL((combine_kernel<true, 2, true>), cgrid8, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
                        a.n_shared, a.d, y, 1, a.expert_out);
   else if (a.K == 6)
-    hipLaunchKernelGGL((combine_kernel<true, 6, true>), cgrid, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
+    hipLaunchKernelGGL((combine_kernel<true, 6, true>), cgrid8, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
                        a.n_shared, a.d, y, 1, a.expert_out);
   else
     hipLaunchKernelGGL((combine_kernel<true, 0, true>), cgrid, cblk, 0, stream, O, pb.inv, a.gate, a.T, a.K,
