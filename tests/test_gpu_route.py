@@ -191,6 +191,11 @@ SPLIT_CASES = [
     (700, 256, 17, 3, 1, L.ROUTE_SOFT_PRIOR, L.GATE_RENORM),
     (515, 128, 5, 3, 3, L.ROUTE_HARD_MASK, L.GATE_P),
     (512, 64, 64, 16, 1, L.ROUTE_PLAIN, L.GATE_RENORM),
+    # softmax over all E (g = p) with 16 < E < 64: the normaliser's pairwise tree with experts
+    # past E counting as 0, on both the wavefront and the per-thread selection
+    (640, 256, 17, 2, 1, L.ROUTE_SOFT_PRIOR, L.GATE_P),
+    (520, 128, 48, 6, 2, L.ROUTE_PLAIN, L.GATE_P),
+    (1030, 192, 40, 4, 3, L.ROUTE_HARD_MASK, L.GATE_P),
 ]
 
 
